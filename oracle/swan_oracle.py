@@ -1,0 +1,290 @@
+"""Plain CPU oracle for SWAN decode attention (TEST INFRASTRUCTURE ONLY).
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this module.  The product path (``libswan.so`` and its
+Python binding) never calls it and shares no code with it.
+
+Everything is computed in float64 with numpy, step by step in the order the
+paper states the method (SWAN: Sparse Winnowed Attention, arXiv 2511.18936):
+
+* ``calibrate``            Sec. 4.1.2: the projection is the right singular
+                           matrix of the joint activation matrix S, columns in
+                           descending singular value.
+* ``rotate`` / ``to_storage``  Algorithm 1 (project the key; the value arrives
+                           projected): x_hat = x . P, rounded once to the
+                           storage type T when it enters the dense buffer.
+* ``topk_indices``         Algorithm 1 (arg TopK of |x_hat_old|) and Sec. 4.3
+                           (magnitude pruning), ranking the stored T values,
+                           ties to the lower index.
+* ``UnitCache.append``     Algorithm 1: append to the buffer, and while the
+                           buffer holds more than b vectors pop the oldest, prune
+                           it and append the (index, value) pairs to the sparse
+                           cache (Sec. 5.1: values plus int8 indices).
+* ``UnitCache.attend``     Algorithm 1 (scores over Concat(sparse, buffer),
+                           softmax with 1/sqrt(d_h), weighted sum of values) and
+                           Sec. 4.2 / Lemma 2: the rotated output is mapped back
+                           with P_VO^T.
+* ``space_bytes`` / ``flops_swan`` / ``break_even_length``  Sec. 5.1 and Sec. 5.2
+                           with Appendix A.2.
+
+Readings of the paper used here (where it is silent or ambiguous):
+  1. top-k ranks the stored (T-rounded) buffer value, because Algorithm 1 pops
+     the vector from the buffer;
+  2. equal magnitudes go to the lower index; +0 and -0 tie;
+  3. pairs are kept in ascending index order (the CSR convention of Sec. 5.1);
+  4. the current token is appended before attention, so it attends to itself;
+  5. with b = 0 every token, the current one included, is pruned at once;
+  6. the scale is 1/sqrt(d_h) for the full head dimension, whatever k is;
+  7. q_hat, scores, probabilities and the accumulator are never rounded to T;
+  8. the output is returned un-rotated: o = o_hat . P_VO^T.
+
+Parity status: every function above is pinned by tests/test_oracle_pins.py;
+nothing here is "parity unpinned" except the end-task accuracy of Tables 1-3,
+which needs models and datasets and is not computed.
+"""
+from __future__ import annotations
+
+import collections
+import math
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+F64 = np.float64
+
+
+# --------------------------------------------------------------------------- #
+# Sec. 4.1.2: projection matrices from the SVD of the joint matrix S
+# --------------------------------------------------------------------------- #
+def canonical_signs(P: np.ndarray) -> np.ndarray:
+    """Make the largest-magnitude entry of every column positive (ties: lowest row).
+
+    Singular vectors are defined up to sign; this only makes them reproducible.
+    The attention output does not depend on the choice (|-x| = |x|).
+    """
+    P = np.array(P, dtype=F64, copy=True)
+    for j in range(P.shape[1]):
+        col = P[:, j]
+        r = int(np.argmax(np.abs(col)))  # argmax returns the first (lowest) row on ties
+        if col[r] < 0:
+            P[:, j] = -col
+    return P
+
+
+def calibrate(S: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """P = right singular matrix of S (columns = basis vectors, descending sigma).
+
+    S is the n x d joint matrix (rows stacked along the sequence axis, Sec. 4.1.2);
+    no mean is removed.  Returns (P [d][d] float64, sigma [d] float64).
+    """
+    S = np.asarray(S, dtype=F64)
+    d = S.shape[1]
+    _, sig, vt = np.linalg.svd(S, full_matrices=True)
+    sigma = np.zeros(d, dtype=F64)
+    sigma[: sig.shape[0]] = sig
+    P = vt.T  # columns are the right singular vectors, already in descending sigma
+    return canonical_signs(P), sigma
+
+
+def calibrate_f32(S: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """The fp32 rotation that both the oracle and the GPU path then consume."""
+    P, sigma = calibrate(S)
+    return P.astype(np.float32), sigma.astype(np.float32)
+
+
+# --------------------------------------------------------------------------- #
+# Algorithm 1: rotation, rounding to storage, magnitude top-k
+# --------------------------------------------------------------------------- #
+def rotate(x: np.ndarray, P: np.ndarray) -> np.ndarray:
+    """x_hat = x . P for row vectors x (float64, not rounded)."""
+    return np.asarray(x, dtype=F64) @ np.asarray(P, dtype=F64)
+
+
+def to_storage(y: np.ndarray, dtype) -> np.ndarray:
+    """Round once, to nearest-even, to the storage type T (the buffer's type)."""
+    return np.asarray(y, dtype=F64).astype(dtype)
+
+
+def topk_indices(y: np.ndarray, k: int) -> np.ndarray:
+    """arg TopK(|y|, k): the k largest magnitudes, lower index first on ties.
+
+    Returned in ascending index order (the order in which pairs are stored).
+    """
+    mag = np.abs(np.asarray(y, dtype=F64))
+    d = mag.shape[0]
+    order = np.lexsort((np.arange(d), -mag))  # primary key -|y|, secondary key index
+    return np.sort(order[:k])
+
+
+def topk_indices_rows(Y: np.ndarray, k: int) -> np.ndarray:
+    """Row-wise ``topk_indices`` for a [n][d] block (stable sort keeps index order on ties)."""
+    mag = np.abs(np.asarray(Y, dtype=F64))
+    order = np.argsort(-mag, axis=1, kind="stable")[:, :k]
+    return np.sort(order, axis=1)
+
+
+# --------------------------------------------------------------------------- #
+# Algorithm 1: hybrid cache of one (sequence, kv head) unit
+# --------------------------------------------------------------------------- #
+class UnitCache:
+    """Sparse cache + dense FIFO buffer of one (sequence, KV head), as in Algorithm 1.
+
+    The buffer holds rotated vectors already rounded to T.  The sparse cache
+    holds, per pruned token, k ascending indices and the T values at them,
+    separately for keys and values.
+    """
+
+    def __init__(self, P_qk: np.ndarray, P_vo: np.ndarray, buffer_tokens: int,
+                 k_active: int, dtype=np.float16):
+        self.P_qk = np.asarray(P_qk, dtype=F64)
+        self.P_vo = np.asarray(P_vo, dtype=F64)
+        self.b = int(buffer_tokens)
+        self.k = int(k_active)
+        self.dtype = dtype
+        self.k_buf: collections.deque = collections.deque()
+        self.v_buf: collections.deque = collections.deque()
+        self.k_idx: List[np.ndarray] = []
+        self.k_val: List[np.ndarray] = []
+        self.v_idx: List[np.ndarray] = []
+        self.v_val: List[np.ndarray] = []
+
+    def __len__(self) -> int:
+        return len(self.k_idx) + len(self.k_buf)
+
+    def append(self, k_row: np.ndarray, v_row: np.ndarray) -> None:
+        """One token of Algorithm 1: project, append to the buffer, evict-and-prune if > b."""
+        k_hat = to_storage(rotate(k_row, self.P_qk), self.dtype)
+        v_hat = to_storage(rotate(v_row, self.P_vo), self.dtype)
+        self.k_buf.append(k_hat)
+        self.v_buf.append(v_hat)
+        while len(self.k_buf) > self.b:
+            k_old = self.k_buf.popleft()
+            v_old = self.v_buf.popleft()
+            i_k = topk_indices(k_old, self.k)
+            self.k_idx.append(i_k)
+            self.k_val.append(k_old[i_k])
+            i_v = topk_indices(v_old, self.k)
+            self.v_idx.append(i_v)
+            self.v_val.append(v_old[i_v])
+
+    def sparse_arrays(self) -> Dict[str, np.ndarray]:
+        d = self.P_qk.shape[0]
+        n = len(self.k_idx)
+        def stack(lst, dt, width):
+            return np.stack(lst) if lst else np.zeros((0, width), dtype=dt)
+        return {
+            "k_idx": stack(self.k_idx, np.int64, self.k),
+            "k_val": stack(self.k_val, self.dtype, self.k),
+            "v_idx": stack(self.v_idx, np.int64, self.k),
+            "v_val": stack(self.v_val, self.dtype, self.k),
+            "k_buf": np.stack(list(self.k_buf)) if self.k_buf else np.zeros((0, d), self.dtype),
+            "v_buf": np.stack(list(self.v_buf)) if self.v_buf else np.zeros((0, d), self.dtype),
+            "n_sparse": n,
+        }
+
+    def attend(self, q: np.ndarray, scale: Optional[float] = None) -> np.ndarray:
+        return attend_arrays(q, self.P_qk, self.P_vo, self.sparse_arrays(), scale)
+
+
+def compress_block(K_rows: np.ndarray, V_rows: np.ndarray, P_qk: np.ndarray,
+                   P_vo: np.ndarray, buffer_tokens: int, k_active: int,
+                   dtype=np.float16) -> Dict[str, np.ndarray]:
+    """Algorithm 1 applied to n tokens of an empty unit, all at once.
+
+    Equal, bit for bit, to n successive ``UnitCache.append`` calls (tested):
+    the first max(n - b, 0) tokens end up pruned, the last min(n, b) stay dense.
+    """
+    n = K_rows.shape[0]
+    b = int(buffer_tokens)
+    k_hat = to_storage(rotate(K_rows, P_qk), dtype)
+    v_hat = to_storage(rotate(V_rows, P_vo), dtype)
+    n_sparse = max(n - b, 0)
+    k_idx = topk_indices_rows(k_hat[:n_sparse], k_active)
+    v_idx = topk_indices_rows(v_hat[:n_sparse], k_active)
+    return {
+        "k_idx": k_idx,
+        "k_val": np.take_along_axis(k_hat[:n_sparse], k_idx, axis=1),
+        "v_idx": v_idx,
+        "v_val": np.take_along_axis(v_hat[:n_sparse], v_idx, axis=1),
+        "k_buf": k_hat[n_sparse:],
+        "v_buf": v_hat[n_sparse:],
+        "n_sparse": n_sparse,
+    }
+
+
+def attend_arrays(q: np.ndarray, P_qk: np.ndarray, P_vo: np.ndarray,
+                  cache: Dict[str, np.ndarray], scale: Optional[float] = None) -> np.ndarray:
+    """Algorithm 1, attention part, for one query head on one unit's cache.
+
+    q_hat = q . P_QK; scores = q_hat . K_cache^T over the sparse pairs and the
+    dense buffer; softmax of scores / sqrt(d_h); o_hat = p . V_cache; and the
+    output is returned to the model's coordinates with P_VO^T (Lemma 2).
+    """
+    P_qk = np.asarray(P_qk, dtype=F64)
+    P_vo = np.asarray(P_vo, dtype=F64)
+    d = P_qk.shape[0]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    q_hat = rotate(q, P_qk)
+    k_idx, k_val = cache["k_idx"], np.asarray(cache["k_val"], dtype=F64)
+    v_idx, v_val = cache["v_idx"], np.asarray(cache["v_val"], dtype=F64)
+    k_buf = np.asarray(cache["k_buf"], dtype=F64)
+    v_buf = np.asarray(cache["v_buf"], dtype=F64)
+    # sparse-dense mat-vec: only the kept components of each key contribute
+    s_sparse = scale * np.sum(q_hat[k_idx] * k_val, axis=1) if k_idx.shape[0] else np.zeros(0)
+    s_buf = scale * (k_buf @ q_hat)
+    s = np.concatenate([s_sparse, s_buf])
+    if s.shape[0] == 0:
+        raise ValueError("attention over an empty cache")
+    m = np.max(s)
+    w = np.exp(s - m)
+    p = w / np.sum(w)
+    p_sparse, p_buf = p[: s_sparse.shape[0]], p[s_sparse.shape[0]:]
+    o_hat = np.zeros(d, dtype=F64)
+    if v_idx.shape[0]:
+        np.add.at(o_hat, v_idx.ravel(), (p_sparse[:, None] * v_val).ravel())
+    o_hat += p_buf @ v_buf
+    return o_hat @ P_vo.T
+
+
+def decode_batch(q: np.ndarray, P_qk: np.ndarray, P_vo: np.ndarray,
+                 caches: Sequence[Sequence[Dict[str, np.ndarray]]],
+                 scale: Optional[float] = None) -> np.ndarray:
+    """o[b][h_q] for q [B][H_q][d]; caches[b][h_kv]; P [H_kv][d][d].  GQA: h_kv = h_q // G."""
+    B, Hq, d = q.shape
+    Hkv = len(caches[0])
+    G = Hq // Hkv
+    out = np.zeros((B, Hq, d), dtype=F64)
+    for b in range(B):
+        for hq in range(Hq):
+            g = hq // G
+            out[b, hq] = attend_arrays(q[b, hq], P_qk[g], P_vo[g], caches[b][g], scale)
+    return out
+
+
+# --------------------------------------------------------------------------- #
+# Sec. 5.1 space model and Sec. 5.2 / Appendix A.2 FLOP model
+# --------------------------------------------------------------------------- #
+def space_bytes_per_vector(k_active: int, value_bytes: int = 2, index_bytes: int = 1,
+                           offset_bytes: int = 2) -> int:
+    """M_sparse = k (sizeof(value) + sizeof(index)) + the 2-byte CSR offset."""
+    return k_active * (value_bytes + index_bytes) + offset_bytes
+
+
+def dense_bytes_per_vector(d_h: int = 128, value_bytes: int = 2) -> int:
+    return d_h * value_bytes
+
+
+def flops_standard(L: int, d_h: int) -> int:
+    """C_std ~ 4 L d_h: two mat-vecs over the whole cache."""
+    return 4 * L * d_h
+
+
+def flops_swan(L: int, d_h: int, b: int, k_active: int) -> int:
+    """C_SWAN ~ 4 d_h^2 + 4 (L - b) k + 4 b d_h (projections, sparse part, buffer part)."""
+    return 4 * d_h * d_h + 4 * (L - b) * k_active + 4 * b * d_h
+
+
+def break_even_length(d_h: int, k_active: int, b: int) -> float:
+    """SWAN is cheaper than standard attention once L exceeds d_h^2 / (d_h - k) + b."""
+    return d_h * d_h / (d_h - k_active) + b

@@ -1,0 +1,355 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these tests retypes the oracle's own formula: each checks it against an
+independent route (exact rational arithmetic, a constructed SVD, brute-force
+loops over a dense masked formulation, Lemma 1 / Lemma 2 of Appendix A.1, or
+numbers printed in the paper), chosen so that a dropped term, a wrong sign or
+index, a transposed operand or a wrong tie rule fails at least one of them.
+"""
+import fractions
+import math
+import os
+
+import numpy as np
+import pytest
+
+import swan_inputs as si
+from oracle import swan_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# --------------------------------------------------------------------------- #
+# Rounding to the storage type: exact nearest-even by rational arithmetic
+# --------------------------------------------------------------------------- #
+def _fp16_grid_neighbors(x: float):
+    """All fp16 values as exact fractions around x (finite range only)."""
+    h = np.float16(x)
+    cands = set()
+    bits = np.array([h], dtype=np.float16).view(np.uint16)[0]
+    for dlt in (-2, -1, 0, 1, 2):
+        b = (int(bits) + dlt) & 0xFFFF
+        v = np.array([b], dtype=np.uint16).view(np.float16)[0]
+        if np.isfinite(v):
+            cands.add(float(v))
+    return sorted(cands)
+
+
+def _exact_nearest_even_fp16(x: float) -> float:
+    fx = fractions.Fraction(x)
+    best = None
+    for c in _fp16_grid_neighbors(x):
+        fc = fractions.Fraction(c)
+        dist = abs(fc - fx)
+        if best is None or dist < best[0]:
+            best = (dist, [c])
+        elif dist == best[0]:
+            best[1].append(c)
+    cands = best[1]
+    if len(cands) == 1:
+        return cands[0]
+    # tie: pick the one with an even mantissa (last bit 0)
+    for c in cands:
+        if int(np.array([c], dtype=np.float16).view(np.uint16)[0]) % 2 == 0:
+            return c
+    raise AssertionError("no even candidate")
+
+
+def test_to_storage_fp16_is_round_to_nearest_even():
+    r = np.random.default_rng(1)
+    xs = list(r.standard_normal(3000) * np.exp(r.uniform(-12, 8, 3000)))
+    # exact midpoints between consecutive fp16 values, and doubles one ulp off them
+    grid = np.array(r.integers(0x0400, 0x7B00, 400), dtype=np.uint16).view(np.float16)
+    for g in grid.astype(np.float64):
+        up = float(np.nextafter(np.float16(g), np.float16(np.inf)))
+        mid = (g + up) / 2.0
+        xs += [mid, -mid, np.nextafter(mid, 0.0), np.nextafter(mid, np.inf)]
+    got = O.to_storage(np.array(xs), np.float16).astype(np.float64)
+    want = np.array([_exact_nearest_even_fp16(x) for x in xs])
+    assert np.array_equal(got, want)
+
+
+# --------------------------------------------------------------------------- #
+# Sec. 4.1.2 calibration: right singular vectors, descending sigma
+# --------------------------------------------------------------------------- #
+def test_calibrate_recovers_a_constructed_svd():
+    d, n = 16, 40
+    V = si.random_orthogonal(3, d)
+    U = si.random_orthogonal(4, n)[:, :d]
+    sig = np.linspace(9.0, 1.0, d) ** 1.5  # distinct, descending
+    perm = si.rng_for(77).permutation(d)  # hand the SVD its columns shuffled
+    S = (U[:, perm] * sig[perm]) @ V[:, perm].T
+    P, sigma = O.calibrate(S)
+    assert np.allclose(sigma, sig, rtol=1e-12, atol=0)
+    # every column of P is +/- the matching column of V
+    assert np.allclose(np.abs(np.sum(P * V, axis=0)), 1.0, atol=1e-12)
+    # canonical sign: the largest-magnitude entry of each column is positive
+    for j in range(d):
+        assert P[np.argmax(np.abs(P[:, j])), j] > 0
+
+
+def test_calibrate_orthogonal_columns_give_a_sorted_permutation():
+    # S with orthogonal columns of distinct norms: the basis is the identity, sorted by norm
+    norms = np.array([2.0, 7.0, 3.0, 5.0, 1.0, 4.0])
+    S = np.zeros((10, 6))
+    for j, nj in enumerate(norms):
+        S[j, j] = -nj if j % 2 else nj
+    P, sigma = O.calibrate(S)
+    order = np.argsort(-norms)
+    want = np.zeros((6, 6))
+    want[order, np.arange(6)] = 1.0
+    assert np.array_equal(P, want)
+    assert np.allclose(sigma, norms[order])
+
+
+def test_calibrate_on_the_synthetic_recipe():
+    S = si.calibration_rows(0, 0, si.ROLE_K).astype(np.float64)
+    P, sigma = O.calibrate(S)
+    d = S.shape[1]
+    assert np.max(np.abs(P.T @ P - np.eye(d))) < 1e-12
+    # eigen-equation of the Gram matrix, checked column by column
+    G = S.T @ S
+    resid = np.linalg.norm(G @ P - P * sigma**2, axis=0) / sigma[0] ** 2
+    assert np.max(resid) < 1e-12
+    assert np.all(np.diff(sigma) <= 0)
+    # closed form of the recipe: sigma_j ~ sqrt(n) s_j for the leading directions
+    s = si.spectrum(d)
+    ratio = sigma[:5] / (math.sqrt(S.shape[0]) * s[:5])
+    assert np.all(np.abs(ratio - 1) < 0.05)
+    # fp32 copy stays orthogonal to fp32 precision
+    P32, _ = O.calibrate_f32(S)
+    P32 = P32.astype(np.float64)
+    assert np.max(np.abs(P32.T @ P32 - np.eye(d))) < 1e-6
+
+
+# --------------------------------------------------------------------------- #
+# Algorithm 1 arg TopK: brute force and special cases
+# --------------------------------------------------------------------------- #
+def _brute_topk(y, k):
+    order = sorted(range(len(y)), key=lambda j: (-abs(float(y[j])), j))
+    return sorted(order[:k])
+
+
+@pytest.mark.parametrize("d", [4, 8, 16, 128])
+def test_topk_brute_force_with_many_ties(d):
+    r = si.rng_for(11, d)
+    for trial in range(200):
+        y = r.integers(-3, 4, d).astype(np.float64) * (0.5 if trial % 2 else 1.0)
+        if trial % 3 == 0:
+            y[r.integers(0, d, 2)] = -0.0
+        for k in sorted({1, 2, d // 2, d - 1, d}):
+            assert list(O.topk_indices(y, k)) == _brute_topk(y, k)
+        Y = np.stack([y, -y, y[::-1]])
+        for k in (1, d // 2, d):
+            rows = O.topk_indices_rows(Y, k)
+            for i in range(3):
+                assert list(rows[i]) == _brute_topk(Y[i], k)
+
+
+def test_topk_special_cases():
+    y = np.array([1.0, -1.0] * 8)
+    assert list(O.topk_indices(y, 5)) == [0, 1, 2, 3, 4]
+    y = np.array([0.0, -0.0, 0.0, -0.0])
+    assert list(O.topk_indices(y, 2)) == [0, 1]
+    y = np.array([0.1, -0.7, 0.7, 0.2])
+    assert list(O.topk_indices(y, 1)) == [1]  # argmax of |y|, lowest index on the tie
+    assert list(O.topk_indices(y, 4)) == [0, 1, 2, 3]
+    y = np.float16(np.array([3.0, -5.0, 1.0, 5.0, -2.0]))
+    assert list(O.topk_indices(y, 3)) == [0, 1, 3]
+
+
+# --------------------------------------------------------------------------- #
+# Algorithm 1 end to end: brute force over a dense masked formulation
+# --------------------------------------------------------------------------- #
+def _brute_swan(q, K, V, Pqk, Pvo, b, k, dtype):
+    """Independent restatement with Python loops.
+
+    Token t (0-based) of L is dense if t >= L - b, else pruned to its k
+    largest-magnitude rotated components (ties: lower index), the rest zeroed.
+    """
+    d = len(q)
+    L = len(K)
+    def rot(x, P):
+        return [sum(float(x[i]) * float(P[i][j]) for i in range(d)) for j in range(d)]
+    def rnd(v):
+        return [float(np.asarray(x).astype(dtype)) for x in v]
+    qh = rot(q, Pqk)
+    scores, vrows = [], []
+    for t in range(L):
+        kh = rnd(rot(K[t], Pqk))
+        vh = rnd(rot(V[t], Pvo))
+        if t < L - b:
+            for vec in (kh, vh):
+                keep = sorted(range(d), key=lambda j: (-abs(vec[j]), j))[:k]
+                for j in range(d):
+                    if j not in keep:
+                        vec[j] = 0.0
+        scores.append(sum(qh[j] * kh[j] for j in range(d)) / math.sqrt(d))
+        vrows.append(vh)
+    m = max(scores)
+    w = [math.exp(s - m) for s in scores]
+    z = sum(w)
+    oh = [sum(w[t] / z * vrows[t][j] for t in range(L)) for j in range(d)]
+    return [sum(oh[j] * float(Pvo[i][j]) for j in range(d)) for i in range(d)]
+
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float16])
+@pytest.mark.parametrize("d", [4, 8])
+def test_attention_brute_force_tiny(d, dtype):
+    for L in (1, 2, 5, 12):
+        q, K, V = si.tiny_case(L * 10 + d, d, L)
+        Pqk = si.random_orthogonal(L + 1, d)
+        Pvo = si.random_orthogonal(L + 2, d)
+        for k in range(1, d + 1):
+            for b in range(0, L + 2):
+                uc = O.UnitCache(Pqk, Pvo, b, k, dtype)
+                for t in range(L):
+                    uc.append(K[0, t], V[0, t])
+                got = uc.attend(q[0])
+                want = _brute_swan(q[0], K[0], V[0], Pqk, Pvo, b, k, dtype)
+                assert np.allclose(got, want, rtol=1e-12, atol=1e-12), (L, k, b)
+
+
+# --------------------------------------------------------------------------- #
+# Appendix A.1, Lemma 1 and Lemma 2: the rotation itself is lossless
+# --------------------------------------------------------------------------- #
+def _textbook_attention(q, K, V):
+    s = K @ q / math.sqrt(len(q))
+    w = np.exp(s - s.max())
+    return (w / w.sum()) @ V
+
+
+@pytest.mark.parametrize("d,L", [(8, 30), (128, 300)])
+def test_full_retention_equals_dense_attention(d, L):
+    q, K, V = si.tiny_case(5, d, L)
+    Pqk = si.random_orthogonal(6, d)
+    Pvo = si.random_orthogonal(7, d)
+    want = _textbook_attention(q[0], K[0], V[0])
+    for b in (0, 3, L, L + 5):
+        c = O.compress_block(K[0], V[0], Pqk, Pvo, b, d, np.float64)
+        got = O.attend_arrays(q[0], Pqk, Pvo, c)
+        assert np.allclose(got, want, rtol=0, atol=1e-12 * np.abs(want).max())
+    # buffer covering the whole context: dense whatever k is
+    c = O.compress_block(K[0], V[0], Pqk, Pvo, L, 1, np.float64)
+    assert np.allclose(O.attend_arrays(q[0], Pqk, Pvo, c), want, atol=1e-12)
+    # identity rotation, full retention
+    I = np.eye(d)
+    c = O.compress_block(K[0], V[0], I, I, 0, d, np.float64)
+    assert np.allclose(O.attend_arrays(q[0], I, I, c), want, atol=1e-12)
+
+
+def test_full_retention_fp16_equals_dense_on_rounded_rotated_rows():
+    d, L = 128, 200
+    q, K, V = si.tiny_case(8, d, L)
+    Pqk = si.random_orthogonal(9, d)
+    Pvo = si.random_orthogonal(10, d)
+    c = O.compress_block(K[0], V[0], Pqk, Pvo, 16, d, np.float16)
+    got = O.attend_arrays(q[0], Pqk, Pvo, c)
+    Kh = (K[0] @ Pqk).astype(np.float16).astype(np.float64)
+    Vh = (V[0] @ Pvo).astype(np.float16).astype(np.float64)
+    want = _textbook_attention(q[0] @ Pqk, Kh, Vh) @ Pvo.T
+    assert np.allclose(got, want, rtol=0, atol=1e-13)
+
+
+# --------------------------------------------------------------------------- #
+# Invariances
+# --------------------------------------------------------------------------- #
+@pytest.mark.parametrize("b,k", [(0, 5), (4, 3), (16, 64), (0, 128)])
+def test_prefill_equals_token_by_token_appends(b, k):
+    d = 128 if k > 8 else 8
+    L = 70
+    q, K, V = si.tiny_case(12 + b + k, d, L)
+    K16, V16 = K.astype(np.float16), V.astype(np.float16)
+    Pqk = si.random_orthogonal(13, d)
+    Pvo = si.random_orthogonal(14, d)
+    uc = O.UnitCache(Pqk, Pvo, b, k, np.float16)
+    for t in range(L):
+        uc.append(K16[0, t], V16[0, t])
+    a = uc.sparse_arrays()
+    c = O.compress_block(K16[0], V16[0], Pqk, Pvo, b, k, np.float16)
+    for key in ("k_idx", "k_val", "v_idx", "v_val", "k_buf", "v_buf"):
+        assert np.array_equal(a[key], c[key]), key
+    assert a["n_sparse"] == c["n_sparse"] == max(L - b, 0)
+    assert np.array_equal(uc.attend(q[0]), O.attend_arrays(q[0], Pqk, Pvo, c))
+
+
+def test_column_sign_flip_changes_nothing_but_signs():
+    d, L, b, k = 128, 90, 8, 40
+    q, K, V = si.tiny_case(15, d, L)
+    K16, V16 = K.astype(np.float16), V.astype(np.float16)
+    Pqk = si.random_orthogonal(16, d)
+    Pvo = si.random_orthogonal(17, d)
+    flip = np.where(si.rng_for(18).random(d) < 0.5, -1.0, 1.0)
+    c1 = O.compress_block(K16[0], V16[0], Pqk, Pvo, b, k, np.float16)
+    c2 = O.compress_block(K16[0], V16[0], Pqk * flip, Pvo * flip, b, k, np.float16)
+    assert np.array_equal(c1["k_idx"], c2["k_idx"])
+    assert np.array_equal(c1["v_idx"], c2["v_idx"])
+    assert np.array_equal(np.abs(c1["k_val"]), np.abs(c2["k_val"]))
+    o1 = O.attend_arrays(q[0], Pqk, Pvo, c1)
+    o2 = O.attend_arrays(q[0], Pqk * flip, Pvo * flip, c2)
+    assert np.allclose(o1, o2, rtol=0, atol=1e-14)
+
+
+def test_gqa_query_heads_map_to_their_kv_head():
+    d, L, b, k = 16, 40, 4, 6
+    Hq, Hkv = 8, 2
+    q, K, V = si.tiny_case(19, d, L, n_q=Hq, n_kv=Hkv)
+    Pqk = np.stack([si.random_orthogonal(20 + h, d) for h in range(Hkv)])
+    Pvo = np.stack([si.random_orthogonal(30 + h, d) for h in range(Hkv)])
+    caches = [[O.compress_block(K[h], V[h], Pqk[h], Pvo[h], b, k, np.float16)
+               for h in range(Hkv)]]
+    out = O.decode_batch(q[None], Pqk, Pvo, caches)[0]
+    for hq in range(Hq):
+        g = hq // (Hq // Hkv)
+        assert np.array_equal(out[hq], O.attend_arrays(q[hq], Pqk[g], Pvo[g], caches[0][g]))
+    # permuting query heads inside a group permutes the outputs
+    perm = np.array([1, 3, 0, 2, 6, 4, 7, 5])
+    out_p = O.decode_batch(q[perm][None], Pqk, Pvo, caches)[0]
+    assert np.array_equal(out_p, out[perm])
+    # a query head of the other group gives a different answer
+    assert not np.allclose(out[0], O.attend_arrays(q[0], Pqk[1], Pvo[1], caches[0][1]))
+
+
+# --------------------------------------------------------------------------- #
+# Sec. 5.1 space model, Sec. 5.2 / Appendix A.2 FLOP model, Sec. 1 sizes
+# --------------------------------------------------------------------------- #
+def _rows(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return [ln.split() for ln in f if ln.strip() and not ln.startswith("#")]
+
+
+def test_break_even_examples_match_the_paper():
+    for d_h, k, b, printed in _rows("break_even.txt"):
+        d_h, k, b, printed = int(d_h), int(k), int(b), int(printed)
+        L = O.break_even_length(d_h, k, b)
+        assert round(L) == printed
+        # the bound is where the FLOP model of C_SWAN crosses C_std
+        Lc = int(math.floor(L)) + 1
+        assert O.flops_swan(Lc, d_h, b, k) < O.flops_standard(Lc, d_h)
+        assert O.flops_swan(int(math.floor(L)) - 1, d_h, b, k) > O.flops_standard(
+            int(math.floor(L)) - 1, d_h)
+
+
+def test_space_model_matches_the_paper():
+    g = {k: float(v) for k, v in _rows("space_model.txt")}
+    assert O.dense_bytes_per_vector(128, 2) == g["dense_fp16_bytes_d128"]
+    assert O.space_bytes_per_vector(1) == g["sparse_fp16_formula_k1"]
+    assert O.space_bytes_per_vector(64) == g["sparse_fp16_formula_k64"]
+    assert O.space_bytes_per_vector(64, value_bytes=1) == g["sparse_fp8_formula_k64"]
+    # largest retention ratio that still saves memory with 16-bit values
+    kmax = max(k for k in range(1, 129) if O.space_bytes_per_vector(k) < 256)
+    assert round((kmax + 1) / 128, 2) == g["fp16_break_even_retention"] or \
+        round(kmax / 128, 2) == g["fp16_break_even_retention"]
+
+
+def test_motivating_kv_size_matches_the_paper():
+    (layers, heads, d_h, nbytes, seq, batch, printed), = _rows("motivating_size.txt")
+    total = 2 * int(layers) * int(heads) * int(d_h) * int(nbytes) * int(seq) * int(batch)
+    assert round(total / 2**30) == int(printed)
+
+
+def test_flops_swan_terms():
+    # each term of C_SWAN checked separately: projections, sparse part, buffer part
+    assert O.flops_swan(0, 128, 0, 48) == 4 * 128 * 128
+    assert O.flops_swan(1000, 128, 0, 48) - O.flops_swan(999, 128, 0, 48) == 4 * 48
+    assert O.flops_swan(1000, 128, 10, 48) - O.flops_swan(1000, 128, 9, 48) == 4 * (128 - 48)
