@@ -1,0 +1,186 @@
+/*
+ * swan.h -- C ABI of libswan, a gfx950 (MI355X) implementation of the decode
+ * hot path of SWAN (Sparse Winnowed Attention, arXiv 2511.18936).
+ *
+ * The method, in the paper's terms: keys and values are rotated by an offline
+ * per-head orthogonal matrix obtained from an SVD (Sec. 4.1.2), the most recent
+ * b rotated vectors stay dense in a FIFO buffer, and each vector evicted from
+ * the buffer is pruned to its k largest-magnitude components, stored as
+ * (value, uint8 index) pairs (Algorithm 1; Sec. 4.3; Sec. 5.1).  A decode query
+ * is rotated once and scored directly against the sparse pairs and the dense
+ * buffer; softmax and the weighted sum of values stay in the rotated space and
+ * one inverse rotation per head maps the output back (Sec. 4.2, Lemma 2).
+ *
+ * Conventions for every entry point:
+ *  - Pointers are DEVICE pointers unless the name ends in _host.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Work is enqueued on it and the call returns without waiting, except
+ *    swan_calibrate_rotation, which waits for its result.
+ *  - The library never allocates memory.  The caller owns every buffer and
+ *    sizes it with the *_bytes queries below.
+ *  - All arguments are validated on the host before anything is enqueued, so
+ *    a non-OK status means nothing was written.  Errors never abort, throw or
+ *    exit; swan_last_error() returns a message for the calling thread.
+ *  - Faults inside enqueued kernels surface at the caller's next
+ *    synchronisation, as for any HIP work.
+ *  - The GPU path supports head_dim == 128 only; batch <= SWAN_MAX_BATCH.
+ */
+#ifndef SWAN_H
+#define SWAN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum swan_status {
+  SWAN_OK = 0,
+  SWAN_ERR_INVALID_ARG = 1,    /* null pointer, bad size, out-of-range k, ... */
+  SWAN_ERR_UNSUPPORTED = 2,    /* valid request outside what this build supports */
+  SWAN_ERR_CAPACITY = 3,       /* sparse_capacity would be exceeded */
+  SWAN_ERR_WORKSPACE = 4,      /* workspace missing or smaller than the query says */
+  SWAN_ERR_HIP = 5,            /* a HIP runtime call failed (message has details) */
+  SWAN_ERR_NO_CONVERGENCE = 6  /* the eigensolver hit its sweep limit */
+} swan_status;
+
+typedef enum swan_dtype {
+  SWAN_F32 = 0,  /* float32 storage */
+  SWAN_F16 = 1   /* IEEE binary16 storage */
+} swan_dtype;
+
+#define SWAN_MAX_BATCH 64
+#define SWAN_HEAD_DIM 128
+#define SWAN_PAGE_TOKENS 64
+
+/*
+ * The hybrid KV cache of Algorithm 1 for one attention layer: per (sequence,
+ * KV head) a dense FIFO buffer of the last b rotated tokens (the "ring") and a
+ * sparse cache of pruned tokens (the "pages").  The caller allocates the four
+ * arrays (sizes from swan_cache_bytes) and keeps, on the host, the number of
+ * tokens cached per sequence and each sequence's k_active.
+ *
+ * Ring layout: [batch][n_kv_heads][buffer_tokens][head_dim] of the storage
+ * type; the token at position pos (0-based, pos >= L - b) is in slot pos % b.
+ *
+ * Page layout.  Sparse token p of sequence s and KV head h (p < L - b) is in
+ * page p / 64, slot t = p % 64.  With T the storage type, k_pad = k rounded up
+ * to a multiple of 8 and GV = 16 / sizeof(T) values per 16-byte chunk, a page is
+ *     values : k_pad / GV chunks, each [64 slots][16 bytes]
+ *     indices: k_pad / 8  chunks, each [64 slots][8 bytes] (uint8)
+ * so entry e of slot t has its value at byte (e / GV) * 1024 + t * 16 +
+ * (e % GV) * sizeof(T) and its index at byte 64 * k_pad * sizeof(T) +
+ * (e / 8) * 512 + t * 8 + (e % 8).  A page is 64 * k_pad * (sizeof(T) + 1)
+ * bytes.  Entries are in ascending index order; entries k..k_pad-1 are padding
+ * (value +0, index 0).  Sequence s owns n_kv_heads * ceil(sparse_capacity / 64)
+ * pages of its own k, stored after those of sequences 0..s-1; within it, head h
+ * owns the consecutive pages [h * ceil(sparse_capacity / 64), ...).  The keys'
+ * pages live in k_pages, the values' in v_pages, with identical layouts.
+ */
+typedef struct swan_cache {
+  int32_t batch;            /* sequences, 1..SWAN_MAX_BATCH */
+  int32_t n_q_heads;        /* query heads; a multiple of n_kv_heads (GQA group G = n_q / n_kv) */
+  int32_t n_kv_heads;       /* KV heads */
+  int32_t head_dim;         /* d_h; must be 128 */
+  int32_t buffer_tokens;    /* b >= 0, dense buffer size of Algorithm 1 */
+  int32_t sparse_capacity;  /* max pruned tokens per (sequence, KV head) */
+  int32_t dtype;            /* swan_dtype of keys, values, queries and outputs */
+  int32_t reserved;         /* must be 0 */
+  void* k_pages;            /* sparse keys (see page layout) */
+  void* v_pages;            /* sparse values */
+  void* k_ring;             /* dense rotated keys, [B][H_kv][b][d] */
+  void* v_ring;             /* dense rotated values, same layout */
+} swan_cache;
+
+/* Message describing the last non-OK status returned on this thread. */
+const char* swan_last_error(void);
+
+/* Library ABI version (major * 100 + minor). */
+int32_t swan_version(void);
+
+/*
+ * Bytes of one page for storage type `dtype` and `k_active`: the Sec. 5.1 space
+ * model of 64 vectors (k values + k uint8 indices each, k padded to 8; the
+ * 2-byte row offsets are implicit because k is fixed per sequence).
+ */
+swan_status swan_page_bytes(int32_t dtype, int32_t k_active, size_t* bytes);
+
+/*
+ * Sizes of the cache arrays: *page_bytes for each of k_pages / v_pages and
+ * *ring_bytes for each of k_ring / v_ring.  k_active_host[batch] is each
+ * sequence's k (1..head_dim); it fixes the page layout, so every later call on
+ * this cache must pass the same values.  The array pointers in `c` are ignored.
+ */
+swan_status swan_cache_bytes(const swan_cache* c, const int32_t* k_active_host,
+                             size_t* page_bytes, size_t* ring_bytes);
+
+/* Device workspace needed by swan_calibrate_rotation for head dimension d. */
+swan_status swan_calibrate_workspace_bytes(int32_t d, size_t* bytes);
+
+/*
+ * Offline calibration, Sec. 4.1.2: P = the right singular matrix of the joint
+ * matrix S (`rows`, n_rows x d, row-major float32, device), i.e. the
+ * eigenvectors of S^T S, with columns ordered by descending singular value and
+ * each column's largest-magnitude entry made positive (ties: lowest row).  No
+ * mean is removed.  Writes P_out[i * d + j] = component i of basis vector j
+ * (float32, device; x_hat = x . P) and, if sigma_out is not NULL, the singular
+ * values sigma_out[j] (float32, device).  The caller forms S, e.g. keys for
+ * P_QK and values for P_VO.  Needs d == 128, n_rows >= 1.  Runs on `stream` and
+ * waits for it, because convergence is reported through the status
+ * (SWAN_ERR_NO_CONVERGENCE).
+ */
+swan_status swan_calibrate_rotation(const float* rows, int64_t n_rows, int32_t d,
+                                    float* P_out, float* sigma_out, void* workspace,
+                                    size_t workspace_bytes, void* stream);
+
+/*
+ * Algorithm 1, compress part, for up to n_new tokens per sequence.
+ *  seq_len_host[batch]  tokens already cached per sequence (before this call);
+ *  k_active_host[batch] k of each sequence (1..head_dim), as in swan_cache_bytes;
+ *  k_new, v_new         [batch][n_kv_heads][n_new][head_dim] storage type, the
+ *                       un-rotated (post-RoPE) keys and values;
+ *  n_new_host[batch]    tokens to append per sequence, 0..n_new (the first ones
+ *                       of its rows); NULL means n_new for every sequence;
+ *  P_qk, P_vo           [n_kv_heads][head_dim][head_dim] float32 rotations.
+ * Each new token is rotated (k_hat = k . P_qk, v_hat = v . P_vo, accumulated in
+ * float64 and rounded once to the storage type) and appended to the buffer;
+ * every token that leaves the buffer (position < L_new - b) is pruned to the
+ * top-k magnitudes of its stored values (ties: lower index), separately for
+ * keys and values, and packed into its page slot.  With b == 0 every token is
+ * pruned on arrival.  Appending n tokens at once gives the same bytes as n
+ * single appends.  The caller then adds each sequence's count to its seq_len.
+ * Errors: SWAN_ERR_CAPACITY if L_new - b > sparse_capacity for a sequence.
+ */
+swan_status swan_compress_append(const swan_cache* c, const int32_t* seq_len_host,
+                                 const int32_t* k_active_host, const void* k_new,
+                                 const void* v_new, int32_t n_new, const int32_t* n_new_host,
+                                 const float* P_qk, const float* P_vo, void* stream);
+
+/* Device workspace needed by swan_decode_attention for these lengths and k. */
+swan_status swan_decode_workspace_bytes(const swan_cache* c, const int32_t* seq_len_host,
+                                        const int32_t* k_active_host, size_t* bytes);
+
+/*
+ * Algorithm 1, attention part, one decode query per (sequence, query head):
+ *  seq_len_host[batch]  L >= 1, tokens in the cache with the current one
+ *                       already appended by swan_compress_append;
+ *  q                    [batch][n_q_heads][head_dim] storage type (post-RoPE);
+ *  scale                softmax scale; <= 0 means 1 / sqrt(head_dim);
+ *  out                  [batch][n_q_heads][head_dim] storage type.
+ * Computes q_hat = q . P_qk[g] (g = h_q / G), scores q_hat . k over the sparse
+ * pairs and the dense buffer, softmax, o_hat = sum_t p_t v_hat_t, and returns
+ * out = o_hat . P_vo[g]^T (the inverse rotation of Sec. 4.2), rounded once to
+ * the storage type.  Scores, probabilities and accumulators are float32.
+ */
+swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_host,
+                                  const int32_t* k_active_host, const void* q,
+                                  const float* P_qk, const float* P_vo, float scale,
+                                  void* out, void* workspace, size_t workspace_bytes,
+                                  void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SWAN_H */

@@ -1,0 +1,194 @@
+// Compress-append (Algorithm 1, lines that project, append, evict and prune).
+//
+// Two launches on the caller's stream, so that every vector leaving the ring
+// is read before a new token overwrites its slot:
+//   evict_kernel   one wave per ring vector that leaves the buffer: top-k of
+//                  its stored values, packed into its page slot
+//   insert_kernel  one wave per group of kTPW new tokens of one (sequence, kv
+//                  head, role): rotation x . P accumulated in float64 and rounded
+//                  once to the storage type; tokens still inside the buffer go to
+//                  their ring slot, the others are pruned and packed at once
+//
+// Top-k (Sec. 4.3, ranking the stored values, ties to the lower index): each
+// lane holds dims 2l and 2l+1; the key (|x| bits << 8) | (255 - dim) is unique
+// and orders by magnitude, then by lower index.  A binary search over the key
+// bits with wave ballots finds the k-th largest key; the selected entries are
+// then numbered in ascending dim order with mbcnt and written to the page.
+#include "swan_device.h"
+#include "swan_internal.h"
+
+namespace swan {
+
+constexpr int kTPW = 8;  // new tokens per insert wave
+
+// Write the top-k of a 128-vector (lane holds elements 2l, 2l+1) into page
+// slot `slot` of the page at `page`.
+template <typename T>
+__device__ __forceinline__ void select_and_pack(typename Store<T>::Bits x0,
+                                                typename Store<T>::Bits x1, int k, char* page,
+                                                int slot, int lane) {
+  using St = Store<T>;
+  using Key = typename std::conditional<(St::kMagBits + 8 > 32), uint64_t, uint32_t>::type;
+  constexpr int kKeyBits = St::kMagBits + 8;
+  const Key key0 = ((Key)St::mag(x0) << 8) | (Key)(255 - 2 * lane);
+  const Key key1 = ((Key)St::mag(x1) << 8) | (Key)(255 - (2 * lane + 1));
+  Key thr = 0;
+  for (int bit = kKeyBits - 1; bit >= 0; --bit) {
+    const Key cand = thr | ((Key)1 << bit);
+    const int cnt = __popcll(__ballot(key0 >= cand)) + __popcll(__ballot(key1 >= cand));
+    if (cnt >= k) thr = cand;
+  }
+  const bool s0 = key0 >= thr;
+  const bool s1 = key1 >= thr;
+  const uint64_t m0 = __ballot(s0);
+  const uint64_t m1 = __ballot(s1);
+  const int e0 = popc_below(m0) + popc_below(m1);
+  const int e1 = e0 + (s0 ? 1 : 0);
+  constexpr int GV = 16 / St::kBytes;
+  const int kp = kpad_of(k);
+  char* vals = page + slot * 16;
+  char* idxs = page + (int64_t)kPage * kp * St::kBytes + slot * 8;
+  if (s0) {
+    *(typename St::Bits*)(vals + (e0 / GV) * 1024 + (e0 % GV) * St::kBytes) = x0;
+    idxs[(e0 / 8) * 512 + (e0 % 8)] = (char)(2 * lane);
+  }
+  if (s1) {
+    *(typename St::Bits*)(vals + (e1 / GV) * 1024 + (e1 % GV) * St::kBytes) = x1;
+    idxs[(e1 / 8) * 512 + (e1 % 8)] = (char)(2 * lane + 1);
+  }
+  const int e = k + lane;  // padding entries k .. kp-1: value +0, index 0
+  if (e < kp) {
+    *(typename St::Bits*)(vals + (e / GV) * 1024 + (e % GV) * St::kBytes) = 0;
+    idxs[(e / 8) * 512 + (e % 8)] = 0;
+  }
+}
+
+__device__ __forceinline__ int evict_begin(int len_old, int bb) {
+  return len_old > bb ? len_old - bb : 0;
+}
+
+// tokens that leave the ring in this call: positions [begin, end)
+__device__ __forceinline__ int evict_end(int len_old, int n_new, int bb) {
+  const int lim = len_old + n_new - bb;
+  return len_old < lim ? len_old : lim;
+}
+
+template <typename T>
+__global__ __launch_bounds__(64) void evict_kernel(CompressLaunch a) {
+  using St = Store<T>;
+  const int lane = threadIdx.x;
+  int w = blockIdx.x;
+  const int e = w % a.max_evict;
+  w /= a.max_evict;
+  const int role = w & 1;
+  w >>= 1;
+  const int h = w % a.Hkv;
+  const int b = w / a.Hkv;
+  const int len_old = a.tab.len[b];
+  const int p0 = evict_begin(len_old, a.bb);
+  const int p1 = evict_end(len_old, a.tab.nnew[b], a.bb);
+  const int p = p0 + e;
+  if (p >= p1) return;
+  const typename St::Bits* ring =
+      (const typename St::Bits*)(role ? a.v_ring : a.k_ring) +
+      (((int64_t)b * a.Hkv + h) * a.bb + (p % a.bb)) * kD;
+  const typename St::Bits x0 = ring[2 * lane];
+  const typename St::Bits x1 = ring[2 * lane + 1];
+  const int k = a.tab.kact[b];
+  const int64_t pbytes = page_bytes_of(St::kBytes, k);
+  char* page = (char*)(role ? a.v_pages : a.k_pages) + a.tab.page_off[b] +
+               ((int64_t)h * a.n_pages_cap + p / kPage) * pbytes;
+  select_and_pack<T>(x0, x1, k, page, p % kPage, lane);
+}
+
+template <typename T>
+__global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
+  using St = Store<T>;
+  __shared__ __attribute__((aligned(16))) double xs[kD][kTPW];
+  const int lane = threadIdx.x;
+  const int ngroups = (a.n_new + kTPW - 1) / kTPW;
+  int w = blockIdx.x;
+  const int grp = w % ngroups;
+  w /= ngroups;
+  const int role = w & 1;
+  w >>= 1;
+  const int h = w % a.Hkv;
+  const int b = w / a.Hkv;
+  const int t0 = grp * kTPW;
+  const int nnew = a.tab.nnew[b];
+  if (t0 >= nnew) return;
+  const int nt = (nnew - t0) < kTPW ? (nnew - t0) : kTPW;
+  const T* x = (const T*)(role ? a.v_new : a.k_new) +
+               (((int64_t)b * a.Hkv + h) * a.n_new + t0) * kD;
+  for (int t = 0; t < kTPW; ++t) {
+    double v0 = 0.0, v1 = 0.0;
+    if (t < nt) {
+      v0 = (double)(float)x[(int64_t)t * kD + 2 * lane];
+      v1 = (double)(float)x[(int64_t)t * kD + 2 * lane + 1];
+    }
+    xs[2 * lane][t] = v0;
+    xs[2 * lane + 1][t] = v1;
+  }
+  __syncthreads();
+  const float2* P = (const float2*)((role ? a.P_vo : a.P_qk) + (int64_t)h * kD * kD) + lane;
+  double acc0[kTPW], acc1[kTPW];
+#pragma unroll
+  for (int t = 0; t < kTPW; ++t) acc0[t] = acc1[t] = 0.0;
+#pragma unroll 4
+  for (int i = 0; i < kD; ++i) {
+    const float2 pr = P[i * (kD / 2)];
+    const double p0 = (double)pr.x, p1 = (double)pr.y;
+#pragma unroll
+    for (int t = 0; t < kTPW; ++t) {
+      const double xv = xs[i][t];
+      acc0[t] = fma(xv, p0, acc0[t]);
+      acc1[t] = fma(xv, p1, acc1[t]);
+    }
+  }
+  const int len_old = a.tab.len[b];
+  const int len_new = len_old + nnew;
+  const int k = a.tab.kact[b];
+  const int64_t pbytes = page_bytes_of(St::kBytes, k);
+  char* pages = (char*)(role ? a.v_pages : a.k_pages) + a.tab.page_off[b] +
+                (int64_t)h * a.n_pages_cap * pbytes;
+  typename St::Bits* ring = (typename St::Bits*)(role ? a.v_ring : a.k_ring) +
+                            ((int64_t)b * a.Hkv + h) * a.bb * kD;
+#pragma unroll
+  for (int t = 0; t < kTPW; ++t) {
+    if (t >= nt) break;
+    const typename St::Bits y0 = St::from_f64(acc0[t]);
+    const typename St::Bits y1 = St::from_f64(acc1[t]);
+    const int pos = len_old + t0 + t;
+    if (pos >= len_new - a.bb) {  // stays dense: ring slot pos % b
+      typename St::Bits* r = ring + (int64_t)(pos % a.bb) * kD;
+      r[2 * lane] = y0;
+      r[2 * lane + 1] = y1;
+    } else {  // pruned on arrival
+      select_and_pack<T>(y0, y1, k, pages + (int64_t)(pos / kPage) * pbytes, pos % kPage, lane);
+    }
+  }
+}
+
+template <typename T>
+static hipError_t launch_compress_t(const CompressLaunch& a) {
+  const int units = a.B * a.Hkv * 2;
+  if (a.max_evict > 0) {
+    hipLaunchKernelGGL(evict_kernel<T>, dim3(units * a.max_evict), dim3(64), 0, a.stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (a.n_new > 0) {
+    const int ngroups = (a.n_new + kTPW - 1) / kTPW;
+    hipLaunchKernelGGL(insert_kernel<T>, dim3((int64_t)units * ngroups), dim3(64), 0, a.stream,
+                       a);
+    return hipGetLastError();
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_compress(const CompressLaunch& a) {
+  if (a.dtype == SWAN_F16) return launch_compress_t<_Float16>(a);
+  return launch_compress_t<float>(a);
+}
+
+}  // namespace swan

@@ -1,0 +1,430 @@
+// Decode attention on the hybrid SWAN cache (Algorithm 1, attention part).
+//
+// Three launches on the caller's stream:
+//   qrot_kernel    q_hat = q . P_QK[g], pre-multiplied by scale * log2(e)
+//   attn_kernel    one wave per (sequence, query head, token split) over the
+//                  sparse pages, plus one wave per (sequence, query head) over
+//                  the dense buffer; each writes a partial (m, l, acc[128]) in
+//                  the rotated space
+//   merge_kernel   log-sum-exp merge of the partials, then o = o_hat . P_VO^T
+//                  (the inverse rotation that Sec. 4.2 absorbs into W_O)
+//
+// Sparse wave: one token per lane.  The rotated query is replicated 32 times
+// in LDS (q_rep[dim][32]) so that the per-lane gathers q_hat[idx] of a half
+// wave never share a bank; the value accumulator is acc[dim][32] in LDS,
+// shared by lanes l and l+32 and updated with LDS float atomics.  Pages of
+// keys and values are streamed with 16-byte coalesced loads, the next page in
+// flight while the current one is consumed.  The softmax reference m is the
+// first page's maximum and is only raised (with a rescale of acc) when a page
+// maximum exceeds it by more than kTau in log2 units, so exponentials stay
+// bounded by 2^kTau while rescales are rare.
+#include "swan_device.h"
+#include "swan_internal.h"
+
+namespace swan {
+
+constexpr float kTau = 8.0f;
+
+// ---------------------------------------------------------------------------
+// q rotation: q_hat[b][h][j] = mult * sum_i q[b][h][i] * P_qk[g][i][j]
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(128) void qrot_kernel(const T* __restrict__ q,
+                                                   const float* __restrict__ Pqk,
+                                                   float* __restrict__ qhat, int Hq, int G,
+                                                   float mult) {
+  __shared__ float qs[kD];
+  const int bh = blockIdx.x;
+  const int g = (bh % Hq) / G;
+  const int j = threadIdx.x;
+  qs[j] = (float)q[(int64_t)bh * kD + j];
+  __syncthreads();
+  const float* P = Pqk + (int64_t)g * kD * kD;
+  float acc = 0.f;
+#pragma unroll 8
+  for (int i = 0; i < kD; ++i) acc = fmaf(qs[i], P[i * kD + j], acc);
+  qhat[(int64_t)bh * kD + j] = acc * mult;
+}
+
+// ---------------------------------------------------------------------------
+// page registers: KP8 groups of 8 entries; VCH 16-byte value chunks per group
+// ---------------------------------------------------------------------------
+template <typename T, int KP8>
+struct PageRegs {
+  static constexpr int VCH = (int)sizeof(T) / 2;
+  u32x4 val[KP8 * VCH];
+  u32x2 idx[KP8];
+};
+
+template <typename T, int KP8>
+__device__ __forceinline__ void load_page(PageRegs<T, KP8>& r, const char* page, int lane) {
+  constexpr int VCH = PageRegs<T, KP8>::VCH;
+  const char* vp = page + lane * 16;
+#pragma unroll
+  for (int c = 0; c < KP8 * VCH; ++c)
+    r.val[c] = __builtin_nontemporal_load((const u32x4*)(vp + c * 1024));
+  const char* ip = page + KP8 * VCH * 1024 + lane * 8;
+#pragma unroll
+  for (int g = 0; g < KP8; ++g)
+    r.idx[g] = __builtin_nontemporal_load((const u32x2*)(ip + g * 512));
+}
+
+// value of entry u (0..7) of group g, as float
+template <typename T, int KP8>
+struct EntryVal {
+  __device__ static __forceinline__ float get(const PageRegs<T, KP8>& r, int g, int u) {
+    if constexpr (sizeof(T) == 2) {
+      const u32x4 c = r.val[g];
+      const uint32_t w = (u < 2) ? c.x : (u < 4) ? c.y : (u < 6) ? c.z : c.w;
+      return f16_bits_to_f32((u & 1) ? (w >> 16) : (w & 0xFFFFu));
+    } else {
+      const u32x4 c = r.val[g * 2 + (u >> 2)];
+      const int v = u & 3;
+      const uint32_t w = (v == 0) ? c.x : (v == 1) ? c.y : (v == 2) ? c.z : c.w;
+      return __uint_as_float(w);
+    }
+  }
+};
+
+template <typename T, int KP8>
+__device__ __forceinline__ int entry_idx(const PageRegs<T, KP8>& r, int g, int u) {
+  const uint32_t w = (u < 4) ? r.idx[g].x : r.idx[g].y;
+  return (int)((w >> (8 * (u & 3))) & 0xFFu);
+}
+
+template <typename T, int KP8>
+__device__ __forceinline__ float page_score(const PageRegs<T, KP8>& r, const float* qrep) {
+  float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+  for (int g = 0; g < KP8; ++g) {
+#pragma unroll
+    for (int u = 0; u < 8; u += 2) {
+      s0 = fmaf(qrep[entry_idx(r, g, u) * 32], EntryVal<T, KP8>::get(r, g, u), s0);
+      s1 = fmaf(qrep[entry_idx(r, g, u + 1) * 32], EntryVal<T, KP8>::get(r, g, u + 1), s1);
+    }
+  }
+  return s0 + s1;
+}
+
+template <typename T, int KP8>
+__device__ __forceinline__ void page_accumulate(const PageRegs<T, KP8>& r, float* accl, float p) {
+#pragma unroll
+  for (int g = 0; g < KP8; ++g) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      __hip_atomic_fetch_add(accl + entry_idx(r, g, u) * 32, p * EntryVal<T, KP8>::get(r, g, u),
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+  }
+}
+
+struct SoftmaxState {
+  float m;     // reference maximum (log2 units), wave-uniform
+  float l;     // per-lane sum of exp2(s - m)
+  bool first;
+};
+
+__device__ __forceinline__ void rescale_acc(float* acc, int lane, float f) {
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < 16; ++c) {
+    float4* p = (float4*)acc + c * 64 + lane;
+    float4 v = *p;
+    v.x *= f; v.y *= f; v.z *= f; v.w *= f;
+    *p = v;
+  }
+  __syncthreads();
+}
+
+template <typename T, int KP8>
+__device__ __forceinline__ void process_page(const PageRegs<T, KP8>& kr, const PageRegs<T, KP8>& vr,
+                                             bool valid, const float* qrep_l, float* acc_l,
+                                             float* acc, int lane, SoftmaxState& st) {
+  float s = valid ? page_score(kr, qrep_l) : -INFINITY;
+  const float pm = wave_max(s);
+  if (st.first) {
+    st.m = pm;
+    st.first = false;
+  } else if (pm > st.m + kTau) {
+    const float f = exp2f(st.m - pm);
+    rescale_acc(acc, lane, f);
+    st.l *= f;
+    st.m = pm;
+  }
+  if (valid) {
+    const float p = exp2f(s - st.m);
+    st.l += p;
+    page_accumulate(vr, acc_l, p);
+  }
+}
+
+// One wave: pages [pbeg, pend) of one (sequence, kv head), for one query head.
+template <typename T, int KP8>
+__device__ void sparse_split(const char* kbase, const char* vbase, int64_t pbytes, int pbeg,
+                             int pend, int S, float* qrep, float* acc, int lane,
+                             float* __restrict__ part) {
+  const int l32 = lane & 31;
+  const float* qrep_l = qrep + l32;
+  float* acc_l = acc + l32;
+  SoftmaxState st{0.f, 0.f, true};
+  PageRegs<T, KP8> ka, va, kb, vb;
+  load_page<T, KP8>(ka, kbase + pbeg * pbytes, lane);
+  load_page<T, KP8>(va, vbase + pbeg * pbytes, lane);
+  for (int p = pbeg; p < pend; p += 2) {
+    const bool has_b = p + 1 < pend;
+    if (has_b) {
+      load_page<T, KP8>(kb, kbase + (p + 1) * pbytes, lane);
+      load_page<T, KP8>(vb, vbase + (p + 1) * pbytes, lane);
+    }
+    process_page<T, KP8>(ka, va, p * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
+    if (!has_b) break;
+    if (p + 2 < pend) {
+      load_page<T, KP8>(ka, kbase + (p + 2) * pbytes, lane);
+      load_page<T, KP8>(va, vbase + (p + 2) * pbytes, lane);
+    }
+    process_page<T, KP8>(kb, vb, (p + 1) * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
+  }
+  const float ltot = wave_sum(st.l);
+  __syncthreads();
+  // reduce acc[dim][32] over its 32 columns: lane owns dims lane and lane + 64
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int r = lane + 64 * h;
+    const float4* row = (const float4*)(acc + r * 32);
+    float sum = 0.f;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const float4 v = row[(c + lane) & 7];
+      sum += (v.x + v.y) + (v.z + v.w);
+    }
+    part[4 + r] = sum;
+  }
+  if (lane == 0) {
+    part[0] = st.m;
+    part[1] = ltot;
+  }
+}
+
+// One wave: the dense buffer of one (sequence, kv head), for one query head.
+// Lane t scores buffer token t (a dense 128-dim dot product), then lane l
+// accumulates output dims 2l and 2l+1 over all buffer tokens.
+template <typename T>
+__device__ void buffer_part(const T* kring, const T* vring, int nb, const float* qh, float* qs,
+                            float* pb, int lane, float* __restrict__ part) {
+  constexpr int E = 16 / (int)sizeof(T);  // elements per 16-byte load
+  qs[lane] = qh[lane];
+  qs[lane + 64] = qh[lane + 64];
+  __syncthreads();
+  float mloc = -INFINITY;
+  for (int t0 = 0; t0 < nb; t0 += 64) {
+    const int t = t0 + lane;
+    if (t < nb) {
+      const u32x4* kr = (const u32x4*)(kring + (int64_t)t * kD);
+      float s0 = 0.f, s1 = 0.f;
+#pragma unroll 4
+      for (int c = 0; c < kD / E; ++c) {
+        const u32x4 w = kr[c];
+#pragma unroll
+        for (int e = 0; e < E; e += 2) {
+          const int j = c * E + e;
+          if constexpr (sizeof(T) == 2) {
+            const uint32_t x = w[e / 2];
+            s0 = fmaf(qs[j], f16_bits_to_f32(x & 0xFFFFu), s0);
+            s1 = fmaf(qs[j + 1], f16_bits_to_f32(x >> 16), s1);
+          } else {
+            s0 = fmaf(qs[j], __uint_as_float(w[e]), s0);
+            s1 = fmaf(qs[j + 1], __uint_as_float(w[e + 1]), s1);
+          }
+        }
+      }
+      const float s = s0 + s1;
+      pb[t] = s;
+      mloc = fmaxf(mloc, s);
+    }
+  }
+  const float m = wave_max(mloc);
+  float lloc = 0.f;
+  for (int t0 = 0; t0 < nb; t0 += 64) {
+    const int t = t0 + lane;
+    if (t < nb) {
+      const float p = exp2f(pb[t] - m);
+      pb[t] = p;
+      lloc += p;
+    }
+  }
+  const float l = wave_sum(lloc);
+  __syncthreads();
+  float a0 = 0.f, a1 = 0.f;
+  for (int t = 0; t < nb; ++t) {
+    const float p = pb[t];
+    const T* vr = vring + (int64_t)t * kD + 2 * lane;
+    a0 = fmaf(p, (float)vr[0], a0);
+    a1 = fmaf(p, (float)vr[1], a1);
+  }
+  part[4 + 2 * lane] = a0;
+  part[4 + 2 * lane + 1] = a1;
+  if (lane == 0) {
+    part[0] = m;
+    part[1] = l;
+  }
+}
+
+// Grid: the dense-buffer waves of the launch's sequences first, then their
+// sparse waves.  One launch per distinct k_pad (KP8 = k_pad / 8) in the batch;
+// a.seq lists the sequences of this launch.
+template <typename T, int KP8>
+__global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup grp) {
+  __shared__ __attribute__((aligned(16))) float qrep[kD * 32];
+  __shared__ __attribute__((aligned(16))) float acc[kD * 32];
+  const int lane = threadIdx.x;
+  const int GH = grp.n * a.Hq;
+  const int G = a.Hq / a.Hkv;
+  int w = blockIdx.x;
+  if (w < GH) {  // dense-buffer wave
+    const int b = grp.seq[w / a.Hq], hq = w % a.Hq, h = hq / G;
+    const int bhq = b * a.Hq + hq;
+    const int L = a.tab.len[b];
+    const int nb = L < a.bb ? L : a.bb;
+    if (nb == 0) return;
+    const int64_t ring_off = ((int64_t)b * a.Hkv + h) * a.bb * kD;
+    float* part = a.part + ((int64_t)bhq * (a.n_splits + 1) + a.n_splits) * kPartFloats;
+    buffer_part<T>((const T*)a.k_ring + ring_off, (const T*)a.v_ring + ring_off, nb,
+                   a.qhat + (int64_t)bhq * kD, acc, qrep, lane, part);
+    return;
+  }
+  w -= GH;
+  const int split = w / GH;
+  const int gi = w % GH;
+  const int b = grp.seq[gi / a.Hq], hq = gi % a.Hq, h = hq / G;
+  const int bhq = b * a.Hq + hq;
+  const int L = a.tab.len[b];
+  const int S = L > a.bb ? L - a.bb : 0;
+  const int np = pages_for(S);
+  const int ns = np < a.n_splits ? np : a.n_splits;
+  if (split >= ns) return;
+  const int pbeg = (int)((int64_t)split * np / ns);
+  const int pend = (int)((int64_t)(split + 1) * np / ns);
+  const int k = a.tab.kact[b];
+  const int64_t pbytes = page_bytes_of((int)sizeof(T), k);
+  const int64_t unit_off = a.tab.page_off[b] + (int64_t)h * a.n_pages_cap * pbytes;
+  const char* kbase = (const char*)a.k_pages + unit_off;
+  const char* vbase = (const char*)a.v_pages + unit_off;
+  float* part = a.part + ((int64_t)bhq * (a.n_splits + 1) + split) * kPartFloats;
+
+  // replicate q_hat: q_rep[dim][32]; lane writes dims lane and lane + 64
+  const float* qh = a.qhat + (int64_t)bhq * kD;
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const int r = lane + 64 * hh;
+    const float v = qh[r];
+    float4* row = (float4*)(qrep + r * 32);
+#pragma unroll
+    for (int c = 0; c < 8; ++c) row[(c + lane) & 7] = make_float4(v, v, v, v);
+  }
+#pragma unroll
+  for (int c = 0; c < 16; ++c) ((float4*)acc)[c * 64 + lane] = make_float4(0.f, 0.f, 0.f, 0.f);
+  __syncthreads();
+  sparse_split<T, KP8>(kbase, vbase, pbytes, pbeg, pend, S, qrep, acc, lane, part);
+}
+
+// ---------------------------------------------------------------------------
+// merge partials (log-sum-exp, fixed order) and rotate back: o = o_hat . P_vo^T
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(128) void merge_kernel(DecodeLaunch a) {
+  __shared__ float oh[kD];
+  __shared__ float wts[kMaxSplits + 1];
+  __shared__ float red[2];
+  const int bhq = blockIdx.x;
+  const int b = bhq / a.Hq, hq = bhq % a.Hq, h = hq / (a.Hq / a.Hkv);
+  const int t = threadIdx.x;
+  const int L = a.tab.len[b];
+  const int S = L > a.bb ? L - a.bb : 0;
+  const int np = pages_for(S);
+  const int ns = np < a.n_splits ? np : a.n_splits;
+  const bool has_buf = (L < a.bb ? L : a.bb) > 0;
+  const float* part = a.part + (int64_t)bhq * (a.n_splits + 1) * kPartFloats;
+
+  if (t == 0) {
+    float m = -INFINITY;
+    for (int i = 0; i < ns; ++i) m = fmaxf(m, part[i * kPartFloats]);
+    if (has_buf) m = fmaxf(m, part[a.n_splits * kPartFloats]);
+    float lsum = 0.f;
+    for (int i = 0; i < ns; ++i) {
+      const float wgt = exp2f(part[i * kPartFloats] - m);
+      wts[i] = wgt;
+      lsum += wgt * part[i * kPartFloats + 1];
+    }
+    if (has_buf) {
+      const float wgt = exp2f(part[a.n_splits * kPartFloats] - m);
+      wts[a.n_splits] = wgt;
+      lsum += wgt * part[a.n_splits * kPartFloats + 1];
+    }
+    red[0] = 1.f / lsum;
+  }
+  __syncthreads();
+  float o = 0.f;
+  for (int i = 0; i < ns; ++i) o = fmaf(wts[i], part[i * kPartFloats + 4 + t], o);
+  if (has_buf) o = fmaf(wts[a.n_splits], part[a.n_splits * kPartFloats + 4 + t], o);
+  oh[t] = o * red[0];
+  __syncthreads();
+  const float4* P = (const float4*)(a.P_vo + ((int64_t)h * kD + t) * kD);
+  float r = 0.f;
+#pragma unroll 8
+  for (int j4 = 0; j4 < kD / 4; ++j4) {
+    const float4 p = P[j4];
+    r = fmaf(p.x, oh[4 * j4], r);
+    r = fmaf(p.y, oh[4 * j4 + 1], r);
+    r = fmaf(p.z, oh[4 * j4 + 2], r);
+    r = fmaf(p.w, oh[4 * j4 + 3], r);
+  }
+  ((T*)a.out)[(int64_t)bhq * kD + t] = (T)r;
+}
+
+template <typename T, int KP8>
+static hipError_t launch_attn(const DecodeLaunch& a, const SeqGroup& g) {
+  const int GH = g.n * a.Hq;
+  hipLaunchKernelGGL((attn_kernel<T, KP8>), dim3(GH * (a.n_splits + 1)), dim3(64), 0, a.stream,
+                     a, g);
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t launch_decode_t(const DecodeLaunch& a) {
+  const int BH = a.B * a.Hq;
+  hipLaunchKernelGGL(qrot_kernel<T>, dim3(BH), dim3(128), 0, a.stream, (const T*)a.q, a.P_qk,
+                     a.qhat, a.Hq, a.Hq / a.Hkv, a.qmult);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // group sequences by k_pad: one attention launch per group
+  for (int kp8 = 1; kp8 <= kD / 8; ++kp8) {
+    SeqGroup g;
+    g.n = 0;
+    for (int b = 0; b < a.B; ++b)
+      if (kpad_of(a.tab.kact[b]) / 8 == kp8) g.seq[g.n++] = b;
+    if (g.n == 0) continue;
+    switch (kp8) {
+#define SWAN_KP8_CASE(n) \
+  case n:                \
+    e = launch_attn<T, n>(a, g); \
+    break;
+      SWAN_KP8_CASE(1) SWAN_KP8_CASE(2) SWAN_KP8_CASE(3) SWAN_KP8_CASE(4)
+      SWAN_KP8_CASE(5) SWAN_KP8_CASE(6) SWAN_KP8_CASE(7) SWAN_KP8_CASE(8)
+      SWAN_KP8_CASE(9) SWAN_KP8_CASE(10) SWAN_KP8_CASE(11) SWAN_KP8_CASE(12)
+      SWAN_KP8_CASE(13) SWAN_KP8_CASE(14) SWAN_KP8_CASE(15) SWAN_KP8_CASE(16)
+#undef SWAN_KP8_CASE
+      default:
+        break;
+    }
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(merge_kernel<T>, dim3(BH), dim3(128), 0, a.stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode(const DecodeLaunch& a) {
+  if (a.dtype == SWAN_F16) return launch_decode_t<_Float16>(a);
+  return launch_decode_t<float>(a);
+}
+
+}  // namespace swan

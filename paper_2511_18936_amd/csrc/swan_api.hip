@@ -1,0 +1,326 @@
+// Host side of the C ABI declared in include/swan.h: argument validation
+// (always before anything is enqueued), workspace sizing, split planning and
+// kernel launches.  No allocation, no host arithmetic on the data path.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "swan.h"
+#include "swan_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+swan_status fail(swan_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+swan_status ok() {
+  g_last_error.clear();
+  return SWAN_OK;
+}
+
+int elem_bytes(int32_t dtype) { return dtype == SWAN_F16 ? 2 : 4; }
+
+swan_status check_cache_shape(const swan_cache* c) {
+  if (!c) return fail(SWAN_ERR_INVALID_ARG, "cache descriptor is NULL");
+  if (c->batch < 1 || c->batch > SWAN_MAX_BATCH)
+    return fail(SWAN_ERR_INVALID_ARG, "batch %d outside 1..%d", c->batch, SWAN_MAX_BATCH);
+  if (c->n_kv_heads < 1 || c->n_q_heads < 1)
+    return fail(SWAN_ERR_INVALID_ARG, "head counts must be >= 1 (q %d, kv %d)", c->n_q_heads,
+                c->n_kv_heads);
+  if (c->n_q_heads % c->n_kv_heads != 0)
+    return fail(SWAN_ERR_INVALID_ARG, "n_q_heads %d is not a multiple of n_kv_heads %d",
+                c->n_q_heads, c->n_kv_heads);
+  if (c->head_dim != SWAN_HEAD_DIM)
+    return fail(SWAN_ERR_UNSUPPORTED, "head_dim %d: the GPU path supports %d only", c->head_dim,
+                SWAN_HEAD_DIM);
+  if (c->buffer_tokens < 0)
+    return fail(SWAN_ERR_INVALID_ARG, "buffer_tokens %d < 0", c->buffer_tokens);
+  if (c->buffer_tokens > swan::kMaxRing)
+    return fail(SWAN_ERR_UNSUPPORTED, "buffer_tokens %d above %d", c->buffer_tokens,
+                swan::kMaxRing);
+  if (c->sparse_capacity < 0)
+    return fail(SWAN_ERR_INVALID_ARG, "sparse_capacity %d < 0", c->sparse_capacity);
+  if (c->dtype != SWAN_F16 && c->dtype != SWAN_F32)
+    return fail(SWAN_ERR_UNSUPPORTED, "dtype %d not supported", c->dtype);
+  if (c->reserved != 0) return fail(SWAN_ERR_INVALID_ARG, "reserved field must be 0");
+  return SWAN_OK;
+}
+
+swan_status check_k(const swan_cache* c, const int32_t* k_active_host) {
+  if (!k_active_host) return fail(SWAN_ERR_INVALID_ARG, "k_active_host is NULL");
+  for (int b = 0; b < c->batch; ++b) {
+    const int k = k_active_host[b];
+    if (k < 1 || k > c->head_dim)
+      return fail(SWAN_ERR_INVALID_ARG, "k_active[%d] = %d outside 1..%d", b, k, c->head_dim);
+  }
+  return SWAN_OK;
+}
+
+swan_status check_cache_ptrs(const swan_cache* c) {
+  if (c->sparse_capacity > 0 && (!c->k_pages || !c->v_pages))
+    return fail(SWAN_ERR_INVALID_ARG, "k_pages / v_pages is NULL");
+  if (c->buffer_tokens > 0 && (!c->k_ring || !c->v_ring))
+    return fail(SWAN_ERR_INVALID_ARG, "k_ring / v_ring is NULL");
+  const void* ptrs[4] = {c->k_pages, c->v_pages, c->k_ring, c->v_ring};
+  for (const void* p : ptrs)
+    if (((uintptr_t)p & 15) != 0)
+      return fail(SWAN_ERR_INVALID_ARG, "cache arrays must be 16-byte aligned");
+  return SWAN_OK;
+}
+
+// fills tab.kact and tab.page_off; returns total page bytes per role
+int64_t fill_layout(const swan_cache* c, const int32_t* k_active_host, swan::SeqTab& tab) {
+  const int npc = swan::pages_for(c->sparse_capacity);
+  int64_t off = 0;
+  for (int b = 0; b < SWAN_MAX_BATCH; ++b) {
+    tab.kact[b] = 0;
+    tab.page_off[b] = 0;
+    tab.len[b] = 0;
+    tab.nnew[b] = 0;
+  }
+  for (int b = 0; b < c->batch; ++b) {
+    tab.kact[b] = k_active_host[b];
+    tab.page_off[b] = off;
+    off += (int64_t)c->n_kv_heads * npc * swan::page_bytes_of(elem_bytes(c->dtype), k_active_host[b]);
+  }
+  return off;
+}
+
+int plan_splits(const swan_cache* c, const int32_t* seq_len_host) {
+  int max_pages = 0;
+  for (int b = 0; b < c->batch; ++b) {
+    const int S = seq_len_host[b] > c->buffer_tokens ? seq_len_host[b] - c->buffer_tokens : 0;
+    const int np = swan::pages_for(S);
+    if (np > max_pages) max_pages = np;
+  }
+  if (max_pages == 0) return 1;
+  // enough waves to cover the 256 CUs several times over
+  const int64_t units = (int64_t)c->batch * c->n_q_heads;
+  const int64_t target_waves = 256 * 5 * 6;
+  int ns = (int)((target_waves + units - 1) / units);
+  if (ns < 1) ns = 1;
+  if (ns > max_pages) ns = max_pages;
+  if (ns > swan::kMaxSplits) ns = swan::kMaxSplits;
+  return ns;
+}
+
+size_t decode_ws_bytes(const swan_cache* c, int ns) {
+  const size_t units = (size_t)c->batch * c->n_q_heads;
+  const size_t qhat = units * swan::kD * sizeof(float);
+  const size_t part = units * (size_t)(ns + 1) * swan::kPartFloats * sizeof(float);
+  return ((qhat + 255) & ~(size_t)255) + part;
+}
+
+swan_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(SWAN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* swan_last_error(void) { return g_last_error.c_str(); }
+
+int32_t swan_version(void) { return 100; }
+
+swan_status swan_page_bytes(int32_t dtype, int32_t k_active, size_t* bytes) {
+  if (!bytes) return fail(SWAN_ERR_INVALID_ARG, "bytes is NULL");
+  if (dtype != SWAN_F16 && dtype != SWAN_F32)
+    return fail(SWAN_ERR_UNSUPPORTED, "dtype %d not supported", dtype);
+  if (k_active < 1 || k_active > SWAN_HEAD_DIM)
+    return fail(SWAN_ERR_INVALID_ARG, "k_active %d outside 1..%d", k_active, SWAN_HEAD_DIM);
+  *bytes = (size_t)swan::page_bytes_of(elem_bytes(dtype), k_active);
+  return ok();
+}
+
+swan_status swan_cache_bytes(const swan_cache* c, const int32_t* k_active_host, size_t* page_bytes,
+                             size_t* ring_bytes) {
+  swan_status st = check_cache_shape(c);
+  if (st != SWAN_OK) return st;
+  if ((st = check_k(c, k_active_host)) != SWAN_OK) return st;
+  if (!page_bytes || !ring_bytes) return fail(SWAN_ERR_INVALID_ARG, "output pointer is NULL");
+  swan::SeqTab tab;
+  *page_bytes = (size_t)fill_layout(c, k_active_host, tab);
+  *ring_bytes = (size_t)c->batch * c->n_kv_heads * c->buffer_tokens * c->head_dim *
+                elem_bytes(c->dtype);
+  return ok();
+}
+
+swan_status swan_calibrate_workspace_bytes(int32_t d, size_t* bytes) {
+  if (!bytes) return fail(SWAN_ERR_INVALID_ARG, "bytes is NULL");
+  if (d != SWAN_HEAD_DIM)
+    return fail(SWAN_ERR_UNSUPPORTED, "d %d: the GPU path supports %d only", d, SWAN_HEAD_DIM);
+  *bytes = swan::kCalibWorkspace;
+  return ok();
+}
+
+swan_status swan_calibrate_rotation(const float* rows, int64_t n_rows, int32_t d, float* P_out,
+                                    float* sigma_out, void* workspace, size_t workspace_bytes,
+                                    void* stream) {
+  if (d != SWAN_HEAD_DIM)
+    return fail(SWAN_ERR_UNSUPPORTED, "d %d: the GPU path supports %d only", d, SWAN_HEAD_DIM);
+  if (!rows || !P_out) return fail(SWAN_ERR_INVALID_ARG, "rows / P_out is NULL");
+  if (n_rows < 1) return fail(SWAN_ERR_INVALID_ARG, "n_rows %lld < 1", (long long)n_rows);
+  if (!workspace || workspace_bytes < swan::kCalibWorkspace)
+    return fail(SWAN_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes,
+                swan::kCalibWorkspace);
+  if (((uintptr_t)workspace & 15) != 0)
+    return fail(SWAN_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+  char* ws = (char*)workspace;
+  swan::CalibLaunch a;
+  a.rows = rows;
+  a.n_rows = n_rows;
+  a.P_out = P_out;
+  a.sigma_out = sigma_out;
+  a.gram = (double*)ws;
+  a.vecs = (double*)(ws + sizeof(double) * swan::kD * swan::kD);
+  a.status = (int32_t*)(ws + 2 * sizeof(double) * swan::kD * swan::kD);
+  a.stream = (hipStream_t)stream;
+  hipError_t e = swan::launch_calibrate(a);
+  if (e != hipSuccess) return hip_status(e, "calibrate launch");
+  int32_t st_host[2] = {0, 0};
+  e = hipMemcpyAsync(st_host, a.status, sizeof(st_host), hipMemcpyDeviceToHost, a.stream);
+  if (e != hipSuccess) return hip_status(e, "calibrate status copy");
+  e = hipStreamSynchronize(a.stream);
+  if (e != hipSuccess) return hip_status(e, "calibrate synchronize");
+  if (!st_host[0])
+    return fail(SWAN_ERR_NO_CONVERGENCE, "Jacobi eigensolver did not converge in %d sweeps",
+                st_host[1]);
+  return ok();
+}
+
+swan_status swan_compress_append(const swan_cache* c, const int32_t* seq_len_host,
+                                 const int32_t* k_active_host, const void* k_new, const void* v_new,
+                                 int32_t n_new, const int32_t* n_new_host, const float* P_qk,
+                                 const float* P_vo, void* stream) {
+  swan_status st = check_cache_shape(c);
+  if (st != SWAN_OK) return st;
+  if ((st = check_k(c, k_active_host)) != SWAN_OK) return st;
+  if ((st = check_cache_ptrs(c)) != SWAN_OK) return st;
+  if (!seq_len_host) return fail(SWAN_ERR_INVALID_ARG, "seq_len_host is NULL");
+  if (n_new < 0) return fail(SWAN_ERR_INVALID_ARG, "n_new %d < 0", n_new);
+  if (n_new > 0 && (!k_new || !v_new)) return fail(SWAN_ERR_INVALID_ARG, "k_new / v_new is NULL");
+  if (!P_qk || !P_vo) return fail(SWAN_ERR_INVALID_ARG, "P_qk / P_vo is NULL");
+  if ((((uintptr_t)P_qk | (uintptr_t)P_vo) & 15) != 0)
+    return fail(SWAN_ERR_INVALID_ARG, "P_qk / P_vo must be 16-byte aligned");
+  int max_evict = 0, any_new = 0;
+  for (int b = 0; b < c->batch; ++b) {
+    const int64_t L0 = seq_len_host[b];
+    if (L0 < 0) return fail(SWAN_ERR_INVALID_ARG, "seq_len[%d] = %lld < 0", b, (long long)L0);
+    const int nb_new = n_new_host ? n_new_host[b] : n_new;
+    if (nb_new < 0 || nb_new > n_new)
+      return fail(SWAN_ERR_INVALID_ARG, "n_new_host[%d] = %d outside 0..%d", b, nb_new, n_new);
+    any_new |= nb_new;
+    const int64_t L1 = L0 + nb_new;
+    if (L1 > INT32_MAX / 2)
+      return fail(SWAN_ERR_INVALID_ARG, "seq_len[%d] + n_new too large", b);
+    if (L1 - c->buffer_tokens > c->sparse_capacity)
+      return fail(SWAN_ERR_CAPACITY, "sequence %d needs %lld sparse tokens, capacity %d", b,
+                  (long long)(L1 - c->buffer_tokens), c->sparse_capacity);
+    const int64_t p0 = L0 > c->buffer_tokens ? L0 - c->buffer_tokens : 0;
+    const int64_t p1 = L0 < L1 - c->buffer_tokens ? L0 : L1 - c->buffer_tokens;
+    if (p1 - p0 > max_evict) max_evict = (int)(p1 - p0);
+  }
+  swan::CompressLaunch a;
+  fill_layout(c, k_active_host, a.tab);
+  for (int b = 0; b < c->batch; ++b) {
+    a.tab.len[b] = seq_len_host[b];
+    a.tab.nnew[b] = n_new_host ? n_new_host[b] : n_new;
+  }
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.P_qk = P_qk;
+  a.P_vo = P_vo;
+  a.k_pages = c->k_pages;
+  a.v_pages = c->v_pages;
+  a.k_ring = c->k_ring;
+  a.v_ring = c->v_ring;
+  a.B = c->batch;
+  a.Hkv = c->n_kv_heads;
+  a.bb = c->buffer_tokens;
+  a.n_pages_cap = swan::pages_for(c->sparse_capacity);
+  a.n_new = n_new;
+  a.max_evict = max_evict;
+  a.dtype = c->dtype;
+  a.stream = (hipStream_t)stream;
+  if (!any_new) return ok();
+  return hip_status(swan::launch_compress(a), "compress launch");
+}
+
+swan_status swan_decode_workspace_bytes(const swan_cache* c, const int32_t* seq_len_host,
+                                        const int32_t* k_active_host, size_t* bytes) {
+  swan_status st = check_cache_shape(c);
+  if (st != SWAN_OK) return st;
+  if ((st = check_k(c, k_active_host)) != SWAN_OK) return st;
+  if (!seq_len_host || !bytes) return fail(SWAN_ERR_INVALID_ARG, "NULL argument");
+  *bytes = decode_ws_bytes(c, plan_splits(c, seq_len_host));
+  return ok();
+}
+
+swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_host,
+                                  const int32_t* k_active_host, const void* q, const float* P_qk,
+                                  const float* P_vo, float scale, void* out, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  swan_status st = check_cache_shape(c);
+  if (st != SWAN_OK) return st;
+  if ((st = check_k(c, k_active_host)) != SWAN_OK) return st;
+  if ((st = check_cache_ptrs(c)) != SWAN_OK) return st;
+  if (!seq_len_host) return fail(SWAN_ERR_INVALID_ARG, "seq_len_host is NULL");
+  if (!q || !out || !P_qk || !P_vo) return fail(SWAN_ERR_INVALID_ARG, "q / out / P is NULL");
+  if ((((uintptr_t)P_qk | (uintptr_t)P_vo) & 15) != 0)
+    return fail(SWAN_ERR_INVALID_ARG, "P_qk / P_vo must be 16-byte aligned");
+  for (int b = 0; b < c->batch; ++b) {
+    const int64_t L = seq_len_host[b];
+    if (L < 1) return fail(SWAN_ERR_INVALID_ARG, "seq_len[%d] = %lld: need L >= 1", b, (long long)L);
+    if (L - c->buffer_tokens > c->sparse_capacity)
+      return fail(SWAN_ERR_CAPACITY, "sequence %d has %lld sparse tokens, capacity %d", b,
+                  (long long)(L - c->buffer_tokens), c->sparse_capacity);
+  }
+  if (!(scale == scale) || isinf(scale)) return fail(SWAN_ERR_INVALID_ARG, "scale is not finite");
+  const int ns = plan_splits(c, seq_len_host);
+  const size_t need = decode_ws_bytes(c, ns);
+  if (!workspace || workspace_bytes < need)
+    return fail(SWAN_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, need);
+  if (((uintptr_t)workspace & 255) != 0)
+    return fail(SWAN_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  swan::DecodeLaunch a;
+  fill_layout(c, k_active_host, a.tab);
+  for (int b = 0; b < c->batch; ++b) a.tab.len[b] = seq_len_host[b];
+  const float sc = scale > 0.f ? scale : 1.0f / sqrtf((float)c->head_dim);
+  a.q = q;
+  a.P_qk = P_qk;
+  a.P_vo = P_vo;
+  a.out = out;
+  a.k_pages = c->k_pages;
+  a.v_pages = c->v_pages;
+  a.k_ring = c->k_ring;
+  a.v_ring = c->v_ring;
+  const size_t units = (size_t)c->batch * c->n_q_heads;
+  a.qhat = (float*)workspace;
+  a.part = (float*)((char*)workspace + ((units * swan::kD * sizeof(float) + 255) & ~(size_t)255));
+  a.B = c->batch;
+  a.Hq = c->n_q_heads;
+  a.Hkv = c->n_kv_heads;
+  a.bb = c->buffer_tokens;
+  a.n_pages_cap = swan::pages_for(c->sparse_capacity);
+  a.n_splits = ns;
+  a.qmult = sc * 1.4426950408889634f;
+  a.dtype = c->dtype;
+  a.stream = (hipStream_t)stream;
+  return hip_status(swan::launch_decode(a), "decode launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,97 @@
+// Device helpers for the gfx950 kernels: storage-type traits, correctly
+// rounded float64 -> storage conversion, wave64 reductions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace swan {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// ---------------------------------------------------------------------------
+// float64 -> IEEE binary16, round to nearest, ties to even, from the bit
+// pattern (one rounding step; converting through float32 would round twice).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint16_t f64_to_f16_bits(double x) {
+  const uint64_t bits = (uint64_t)__double_as_longlong(x);
+  const uint32_t sign = (uint32_t)(bits >> 48) & 0x8000u;
+  const uint64_t a = bits & 0x7FFFFFFFFFFFFFFFull;
+  if (a >= 0x7FF0000000000000ull) {  // inf or NaN
+    return (uint16_t)(sign | 0x7C00u | (a > 0x7FF0000000000000ull ? 0x0200u : 0u));
+  }
+  const int e = (int)(a >> 52) - 1023;            // unbiased exponent
+  if (e > 15) return (uint16_t)(sign | 0x7C00u);  // >= 65536: overflow to inf
+  if (a == 0) return (uint16_t)sign;
+  uint64_t m = (a & 0x000FFFFFFFFFFFFFull);
+  int shift;
+  if ((a >> 52) == 0) {  // float64 subnormal: far below the binary16 range
+    return (uint16_t)sign;
+  }
+  m |= 0x0010000000000000ull;                 // 53-bit significand
+  shift = 42 + (e < -14 ? (-14 - e) : 0);     // 52 - 10, plus denormalisation
+  if (shift > 63) return (uint16_t)sign;
+  const uint64_t q = m >> shift;
+  const uint64_t rem = m & ((1ull << shift) - 1);
+  const uint64_t half = 1ull << (shift - 1);
+  uint64_t r = q + ((rem > half || (rem == half && (q & 1))) ? 1 : 0);
+  // normal: exponent field (e + 15) with the implicit bit folded into q
+  uint32_t h = (e >= -14) ? (uint32_t)(((e + 14) << 10) + r) : (uint32_t)r;
+  if (h >= 0x7C00u) h = 0x7C00u;
+  return (uint16_t)(sign | h);
+}
+
+__device__ __forceinline__ float f16_bits_to_f32(uint32_t h) {
+  _Float16 v = __builtin_bit_cast(_Float16, (uint16_t)h);
+  return (float)v;
+}
+
+// Storage traits.  `Bits` is the raw integer of one stored element.
+template <typename T>
+struct Store;
+
+template <>
+struct Store<_Float16> {
+  using Bits = uint16_t;
+  static constexpr int kBytes = 2;
+  static constexpr int kMagBits = 15;  // |x| as the low 15 bits, order-preserving
+  __device__ static Bits from_f64(double x) { return f64_to_f16_bits(x); }
+  __device__ static float to_f32(Bits b) { return f16_bits_to_f32(b); }
+  __device__ static uint32_t mag(Bits b) { return (uint32_t)b & 0x7FFFu; }
+};
+
+template <>
+struct Store<float> {
+  using Bits = uint32_t;
+  static constexpr int kBytes = 4;
+  static constexpr int kMagBits = 31;
+  __device__ static Bits from_f64(double x) { return __float_as_uint(__double2float_rn(x)); }
+  __device__ static float to_f32(Bits b) { return __uint_as_float(b); }
+  __device__ static uint32_t mag(Bits b) { return b & 0x7FFFFFFFu; }
+};
+
+// ---------------------------------------------------------------------------
+// wave64 helpers
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
+
+// number of set bits of `mask` in lanes strictly below this one
+__device__ __forceinline__ int popc_below(uint64_t mask) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+}  // namespace swan

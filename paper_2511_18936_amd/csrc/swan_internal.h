@@ -1,0 +1,91 @@
+// Internal declarations shared by the libswan translation units (host + device).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "swan.h"
+
+namespace swan {
+
+constexpr int kD = 128;        // head dimension of the GPU path
+constexpr int kPage = 64;      // tokens per page (one token per lane of a wave64)
+constexpr int kMaxSplits = 256;
+constexpr int kMaxRing = 4096; // largest dense buffer the decode kernel stages in LDS
+constexpr int kPartFloats = 132;  // m, l, 2 pad, acc[128]
+
+// Per-sequence parameters passed by value to every kernel (batch <= 64).
+struct SeqTab {
+  int32_t len[SWAN_MAX_BATCH];       // tokens cached (compress: before the call; decode: L)
+  int32_t kact[SWAN_MAX_BATCH];      // k_active
+  int64_t page_off[SWAN_MAX_BATCH];  // byte offset of the sequence's first page
+  int32_t nnew[SWAN_MAX_BATCH];      // compress: tokens appended to the sequence
+};
+
+__host__ __device__ inline int kpad_of(int k) { return (k + 7) & ~7; }
+
+__host__ __device__ inline int64_t page_bytes_of(int elem_bytes, int k) {
+  return int64_t(kPage) * kpad_of(k) * (elem_bytes + 1);
+}
+
+__host__ __device__ inline int pages_for(int tokens) { return (tokens + kPage - 1) / kPage; }
+
+// Host-side launchers (defined in the .hip files).  All return hipSuccess or the
+// error of the launch.
+struct DecodeLaunch {
+  const void* q;
+  const float* P_qk;
+  const float* P_vo;
+  void* out;
+  const void* k_pages;
+  const void* v_pages;
+  const void* k_ring;
+  const void* v_ring;
+  float* qhat;   // [B][Hq][128] workspace
+  float* part;   // [B][Hq][NS + 1][kPartFloats] workspace
+  int B, Hq, Hkv, bb, n_pages_cap, n_splits;
+  float qmult;   // scale * log2(e)
+  int dtype;
+  SeqTab tab;
+  hipStream_t stream;
+};
+hipError_t launch_decode(const DecodeLaunch& a);
+
+// sequences of one attention launch (those sharing a page format)
+struct SeqGroup {
+  int32_t n;
+  int32_t seq[SWAN_MAX_BATCH];
+};
+
+struct CompressLaunch {
+  const void* k_new;
+  const void* v_new;
+  const float* P_qk;
+  const float* P_vo;
+  void* k_pages;
+  void* v_pages;
+  void* k_ring;
+  void* v_ring;
+  int B, Hkv, bb, n_pages_cap, n_new;  // n_new: token stride of k_new / v_new
+  int max_evict;  // largest per-sequence eviction count
+  int dtype;
+  SeqTab tab;     // len = tokens cached before the call
+  hipStream_t stream;
+};
+hipError_t launch_compress(const CompressLaunch& a);
+
+struct CalibLaunch {
+  const float* rows;
+  int64_t n_rows;
+  float* P_out;
+  float* sigma_out;
+  double* gram;    // [128][128]
+  double* vecs;    // [128][128]
+  int32_t* status; // [4]: converged flag, sweeps
+  hipStream_t stream;
+};
+hipError_t launch_calibrate(const CalibLaunch& a);
+constexpr size_t kCalibWorkspace = 2 * sizeof(double) * kD * kD + 256;
+constexpr int kJacobiMaxSweeps = 40;
+
+}  // namespace swan

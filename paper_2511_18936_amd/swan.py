@@ -1,0 +1,256 @@
+"""ctypes binding of libswan (include/swan.h), plus a small cache holder.
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels.  PyTorch provides device memory and the current stream.  If the
+library is missing the import fails loudly; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.environ.get("SWAN_LIB", os.path.join(_HERE, "libswan.so"))
+
+SWAN_OK = 0
+SWAN_ERR_INVALID_ARG = 1
+SWAN_ERR_UNSUPPORTED = 2
+SWAN_ERR_CAPACITY = 3
+SWAN_ERR_WORKSPACE = 4
+SWAN_ERR_HIP = 5
+SWAN_ERR_NO_CONVERGENCE = 6
+SWAN_F32 = 0
+SWAN_F16 = 1
+MAX_BATCH = 64
+HEAD_DIM = 128
+PAGE_TOKENS = 64
+
+EXPORTED = (
+    "swan_last_error", "swan_version", "swan_page_bytes", "swan_cache_bytes",
+    "swan_calibrate_workspace_bytes", "swan_calibrate_rotation", "swan_compress_append",
+    "swan_decode_workspace_bytes", "swan_decode_attention",
+)
+
+
+class SwanError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"swan status {status}: {message}")
+        self.status = status
+
+
+class CacheDesc(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("buffer_tokens", ctypes.c_int32),
+        ("sparse_capacity", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+        ("k_pages", ctypes.c_void_p),
+        ("v_pages", ctypes.c_void_p),
+        ("k_ring", ctypes.c_void_p),
+        ("v_ring", ctypes.c_void_p),
+    ]
+
+
+def _load() -> ctypes.CDLL:
+    # torch first: its HIP runtime (soname libamdhip64.so.7) then also serves
+    # libswan, so the process holds a single runtime and a single device context
+    import torch  # noqa: F401
+
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"libswan.so not found at {LIB_PATH}; build it with "
+            "`python -m paper_2511_18936_amd.build` (there is no fallback path)")
+    lib = ctypes.CDLL(LIB_PATH)
+    i32, i64, sz, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p
+    pi32, psz, pdesc = ctypes.POINTER(i32), ctypes.POINTER(sz), ctypes.POINTER(CacheDesc)
+    lib.swan_last_error.restype = ctypes.c_char_p
+    lib.swan_last_error.argtypes = []
+    lib.swan_version.restype = i32
+    lib.swan_version.argtypes = []
+    sigs = {
+        "swan_page_bytes": [i32, i32, psz],
+        "swan_cache_bytes": [pdesc, pi32, psz, psz],
+        "swan_calibrate_workspace_bytes": [i32, psz],
+        "swan_calibrate_rotation": [vp, i64, i32, vp, vp, vp, sz, vp],
+        "swan_compress_append": [pdesc, pi32, pi32, vp, vp, i32, pi32, vp, vp, vp],
+        "swan_decode_workspace_bytes": [pdesc, pi32, pi32, psz],
+        "swan_decode_attention": [pdesc, pi32, pi32, vp, vp, vp, ctypes.c_float, vp, vp, sz, vp],
+    }
+    for name, args in sigs.items():
+        f = getattr(lib, name)
+        f.restype = i32
+        f.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+def lib() -> ctypes.CDLL:
+    return _lib
+
+
+def last_error() -> str:
+    return _lib.swan_last_error().decode()
+
+
+def _check(status: int) -> None:
+    if status != SWAN_OK:
+        raise SwanError(status, last_error())
+
+
+def _i32_array(values: Sequence[int]):
+    arr = (ctypes.c_int32 * len(values))(*[int(v) for v in values])
+    return arr
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def dtype_code(torch_dtype) -> int:
+    import torch
+
+    if torch_dtype == torch.float16:
+        return SWAN_F16
+    if torch_dtype == torch.float32:
+        return SWAN_F32
+    raise SwanError(SWAN_ERR_UNSUPPORTED, f"dtype {torch_dtype} not supported")
+
+
+def page_bytes(dtype: int, k_active: int) -> int:
+    out = ctypes.c_size_t()
+    _check(_lib.swan_page_bytes(dtype, k_active, ctypes.byref(out)))
+    return out.value
+
+
+def cache_bytes(desc: CacheDesc, k_active: Sequence[int]):
+    pb, rb = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(_lib.swan_cache_bytes(ctypes.byref(desc), _i32_array(k_active), ctypes.byref(pb),
+                                 ctypes.byref(rb)))
+    return pb.value, rb.value
+
+
+def calibrate_workspace_bytes(d: int = HEAD_DIM) -> int:
+    out = ctypes.c_size_t()
+    _check(_lib.swan_calibrate_workspace_bytes(d, ctypes.byref(out)))
+    return out.value
+
+
+def calibrate_rotation(rows, P_out, sigma_out=None, workspace=None, stream=None) -> None:
+    """Sec. 4.1.2 basis of `rows` ([n][d] float32, cuda) into P_out ([d][d] float32)."""
+    import torch
+
+    n, d = rows.shape
+    if workspace is None:
+        workspace = torch.empty(calibrate_workspace_bytes(d), dtype=torch.uint8,
+                                device=rows.device)
+    _check(_lib.swan_calibrate_rotation(_ptr(rows), n, d, _ptr(P_out), _ptr(sigma_out),
+                                        _ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+def compress_append(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence[int], k_new,
+                    v_new, P_qk, P_vo, n_new_per_seq: Optional[Sequence[int]] = None,
+                    stream=None) -> None:
+    n_new = 0 if k_new is None else int(k_new.shape[2])
+    per = None if n_new_per_seq is None else _i32_array(n_new_per_seq)
+    _check(_lib.swan_compress_append(ctypes.byref(desc), _i32_array(seq_len),
+                                     _i32_array(k_active), _ptr(k_new), _ptr(v_new), n_new, per,
+                                     _ptr(P_qk), _ptr(P_vo), _stream(stream)))
+
+
+def decode_workspace_bytes(desc: CacheDesc, seq_len: Sequence[int],
+                           k_active: Sequence[int]) -> int:
+    out = ctypes.c_size_t()
+    _check(_lib.swan_decode_workspace_bytes(ctypes.byref(desc), _i32_array(seq_len),
+                                            _i32_array(k_active), ctypes.byref(out)))
+    return out.value
+
+
+def decode_attention(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence[int], q,
+                     P_qk, P_vo, out, workspace, scale: float = 0.0, stream=None) -> None:
+    _check(_lib.swan_decode_attention(ctypes.byref(desc), _i32_array(seq_len),
+                                      _i32_array(k_active), _ptr(q), _ptr(P_qk), _ptr(P_vo),
+                                      float(scale), _ptr(out), _ptr(workspace),
+                                      workspace.numel(), _stream(stream)))
+
+
+class SwanCache:
+    """Owns the device arrays of one layer's hybrid cache and the host-side lengths.
+
+    The arrays are plain torch tensors (uint8 pages, storage-typed ring); the
+    library only ever receives their device pointers.
+    """
+
+    def __init__(self, batch: int, n_q_heads: int, n_kv_heads: int, buffer_tokens: int,
+                 sparse_capacity: int, k_active: Sequence[int], dtype, device,
+                 head_dim: int = HEAD_DIM):
+        import torch
+
+        self.dtype = dtype
+        self.device = torch.device(device)
+        self.k_active = [int(k) for k in k_active]
+        if len(self.k_active) != batch:
+            raise ValueError("k_active needs one entry per sequence")
+        self.seq_len = [0] * batch
+        self.desc = CacheDesc(batch, n_q_heads, n_kv_heads, head_dim, buffer_tokens,
+                              sparse_capacity, dtype_code(dtype), 0, None, None, None, None)
+        pb, rb = cache_bytes(self.desc, self.k_active)
+        # torch's caching allocator returns 256-byte aligned blocks
+        self.k_pages = torch.zeros(max(pb, 16), dtype=torch.uint8, device=self.device)
+        self.v_pages = torch.zeros(max(pb, 16), dtype=torch.uint8, device=self.device)
+        shape = (batch, n_kv_heads, buffer_tokens, head_dim)
+        self.k_ring = torch.zeros(shape, dtype=dtype, device=self.device)
+        self.v_ring = torch.zeros(shape, dtype=dtype, device=self.device)
+        self.desc.k_pages = self.k_pages.data_ptr()
+        self.desc.v_pages = self.v_pages.data_ptr()
+        self.desc.k_ring = self.k_ring.data_ptr() if buffer_tokens > 0 else None
+        self.desc.v_ring = self.v_ring.data_ptr() if buffer_tokens > 0 else None
+        self._ws = None
+
+    @property
+    def batch(self) -> int:
+        return self.desc.batch
+
+    def append(self, k_new, v_new, P_qk, P_vo, n_new_per_seq=None, stream=None) -> None:
+        """Compress-append k_new / v_new ([B][H_kv][n][d]) and advance the lengths.
+
+        n_new_per_seq optionally appends only the first n_b rows of sequence b.
+        """
+        compress_append(self.desc, self.seq_len, self.k_active, k_new, v_new, P_qk, P_vo,
+                        n_new_per_seq, stream)
+        n = int(k_new.shape[2])
+        per = [n] * self.batch if n_new_per_seq is None else [int(x) for x in n_new_per_seq]
+        self.seq_len = [L + m for L, m in zip(self.seq_len, per)]
+
+    def workspace(self):
+        import torch
+
+        need = decode_workspace_bytes(self.desc, self.seq_len, self.k_active)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(need, dtype=torch.uint8, device=self.device)
+        return self._ws
+
+    def decode(self, q, P_qk, P_vo, out=None, scale: float = 0.0, stream=None):
+        import torch
+
+        if out is None:
+            out = torch.empty_like(q)
+        decode_attention(self.desc, self.seq_len, self.k_active, q, P_qk, P_vo, out,
+                         self.workspace(), scale, stream)
+        return out

@@ -1,0 +1,87 @@
+"""Shared set-up for the GPU parity tests: build caches on the GPU through the
+C ABI and the same caches with the oracle, from the same seeded input bytes."""
+import numpy as np
+
+import swan_inputs as si
+from oracle import swan_oracle as O
+from tests import swan_layout as lay
+
+
+def torch_dtype(dtype: str):
+    import torch
+
+    return {"f16": torch.float16, "f32": torch.float32}[dtype]
+
+
+def gpu_calibrate(rows_np, device):
+    """P (float32 numpy) computed by swan_calibrate_rotation on the GPU."""
+    import torch
+
+    from paper_2511_18936_amd import swan
+
+    rows = torch.tensor(np.ascontiguousarray(rows_np, dtype=np.float32), device=device)
+    P = torch.empty((128, 128), dtype=torch.float32, device=device)
+    sig = torch.empty(128, dtype=torch.float32, device=device)
+    swan.calibrate_rotation(rows, P, sig)
+    return P.cpu().numpy(), sig.cpu().numpy()
+
+
+def rotations(wid: int, n_kv: int, device, use_gpu: bool = True):
+    """P_qk, P_vo [n_kv][128][128] float32 from the recipe's calibration rows."""
+    Pqk, Pvo = [], []
+    for h in range(n_kv):
+        for role, dst in ((si.ROLE_K, Pqk), (si.ROLE_V, Pvo)):
+            rows = si.calibration_rows(wid, h, role)
+            if use_gpu:
+                P, _ = gpu_calibrate(rows, device)
+            else:
+                P, _ = O.calibrate_f32(rows)
+            dst.append(P)
+    return np.stack(Pqk), np.stack(Pvo)
+
+
+def max_rel_err(got: np.ndarray, ref: np.ndarray) -> float:
+    """max_j |got - ref| / max_j |ref| per output row, maximised over rows."""
+    got = np.asarray(got, dtype=np.float64).reshape(-1, ref.shape[-1])
+    ref = np.asarray(ref, dtype=np.float64).reshape(-1, ref.shape[-1])
+    num = np.max(np.abs(got - ref), axis=1)
+    den = np.max(np.abs(ref), axis=1)
+    return float(np.max(num / den))
+
+
+def unit_pages(cache, b, h, role, n_tokens, dtype_np):
+    """(idx, val, pad_idx, pad_val) of one unit's sparse tokens read back from the GPU."""
+    esize = np.dtype(dtype_np).itemsize
+    s, e = lay.unit_slice(cache.k_active, cache.desc.n_kv_heads, cache.desc.sparse_capacity,
+                          esize, b, h)
+    pages = cache.k_pages if role == 0 else cache.v_pages
+    raw = pages[s:e].cpu().numpy()
+    return lay.unpack(raw, dtype_np, cache.k_active[b], n_tokens)
+
+
+def ring_rows(cache, b, h, role, L):
+    """The dense buffer rows of one unit in position order (oldest first)."""
+    bb = cache.desc.buffer_tokens
+    ring = (cache.k_ring if role == 0 else cache.v_ring)[b, h].cpu().numpy()
+    nb = min(L, bb)
+    pos = np.arange(L - nb, L)
+    return ring[pos % bb] if bb else ring[:0]
+
+
+def compare_unit(cache, oc, b, h, L, dtype_np):
+    """Bit-exact comparison of one unit's GPU cache with the oracle's cache dict."""
+    S = oc["n_sparse"]
+    assert S == max(L - cache.desc.buffer_tokens, 0)
+    k = cache.k_active[b]
+    for role, (ik, iv) in enumerate((("k_idx", "k_val"), ("v_idx", "v_val"))):
+        idx, val, pidx, pval = unit_pages(cache, b, h, role, S, dtype_np)
+        bad = np.nonzero(np.any(idx != oc[ik], axis=1))[0]
+        assert bad.size == 0, f"role {role}: {bad.size} of {S} tokens select other indices"
+        assert np.array_equal(val.view(np.uint8), np.asarray(oc[iv], dtype_np).view(np.uint8)), \
+            f"role {role}: values differ"
+        if pidx.size:
+            assert np.all(pidx == 0) and np.all(pval.astype(np.float64) == 0)
+        buf = ring_rows(cache, b, h, role, L)
+        want = oc["k_buf" if role == 0 else "v_buf"]
+        assert np.array_equal(np.asarray(buf).view(np.uint8),
+                              np.asarray(want, dtype_np).view(np.uint8)), f"role {role}: ring"

@@ -1,0 +1,151 @@
+"""Host-only checks of the C ABI: the library loads, exports every declared entry
+point, and rejects bad arguments before touching the GPU (no compute calls)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+swan = pytest.importorskip("paper_2511_18936_amd.swan")
+
+FAKE = 0x10000  # never dereferenced: every call below fails validation first
+
+
+def _declared_functions():
+    with open(os.path.join(ROOT, "include", "swan.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:swan_status|const char\*|int32_t)\s+(swan_\w+)\(",
+                                 text, re.M)))
+
+
+def test_header_and_binding_agree_on_exports():
+    declared = _declared_functions()
+    assert len(declared) == 9
+    assert sorted(swan.EXPORTED) == declared
+    lib = swan.lib()
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_nm_shows_exported_symbols():
+    import subprocess
+
+    out = subprocess.run(["nm", "-D", "--defined-only", swan.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    for name in _declared_functions():
+        assert re.search(rf"\bT {name}\b", out), name
+
+
+def _desc(**kw):
+    d = dict(batch=2, n_q_heads=8, n_kv_heads=2, head_dim=128, buffer_tokens=16,
+             sparse_capacity=1000, dtype=swan.SWAN_F16, reserved=0,
+             k_pages=FAKE, v_pages=FAKE, k_ring=FAKE, v_ring=FAKE)
+    d.update(kw)
+    return swan.CacheDesc(**d)
+
+
+def test_page_and_cache_sizes():
+    assert swan.page_bytes(swan.SWAN_F16, 48) == 64 * 48 * 3
+    assert swan.page_bytes(swan.SWAN_F16, 45) == 64 * 48 * 3  # k padded to 8
+    assert swan.page_bytes(swan.SWAN_F32, 64) == 64 * 64 * 5
+    pb, rb = swan.cache_bytes(_desc(), [48, 64])
+    npc = (1000 + 63) // 64
+    assert pb == 2 * npc * 64 * 3 * (48 + 64)
+    assert rb == 2 * 2 * 16 * 128 * 2
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(batch=0), swan.SWAN_ERR_INVALID_ARG),
+    (dict(batch=65), swan.SWAN_ERR_INVALID_ARG),
+    (dict(n_q_heads=6, n_kv_heads=4), swan.SWAN_ERR_INVALID_ARG),
+    (dict(head_dim=64), swan.SWAN_ERR_UNSUPPORTED),
+    (dict(buffer_tokens=-1), swan.SWAN_ERR_INVALID_ARG),
+    (dict(buffer_tokens=5000), swan.SWAN_ERR_UNSUPPORTED),
+    (dict(dtype=7), swan.SWAN_ERR_UNSUPPORTED),
+    (dict(reserved=1), swan.SWAN_ERR_INVALID_ARG),
+    (dict(k_pages=None), swan.SWAN_ERR_INVALID_ARG),
+    (dict(v_ring=FAKE + 4), swan.SWAN_ERR_INVALID_ARG),
+])
+def test_compress_rejects_bad_descriptors(kw, status):
+    lib = swan.lib()
+    d = _desc(**kw)
+    n = max(1, min(d.batch, 64))
+    seq = swan._i32_array([0] * n)
+    kk = swan._i32_array([48] * n)
+    st = lib.swan_compress_append(ctypes.byref(d), seq, kk, FAKE, FAKE, 1, None, FAKE, FAKE, None)
+    assert st == status, swan.last_error()
+    assert swan.last_error()
+
+
+def test_compress_rejects_bad_arguments():
+    lib = swan.lib()
+    d = _desc()
+    ok_seq = swan._i32_array([10, 20])
+    ok_k = swan._i32_array([48, 64])
+    E = swan.SWAN_ERR_INVALID_ARG
+    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, swan._i32_array([0, 48]), FAKE,
+                                    FAKE, 1, None, FAKE, FAKE, None) == E
+    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, swan._i32_array([48, 129]), FAKE,
+                                    FAKE, 1, None, FAKE, FAKE, None) == E
+    assert lib.swan_compress_append(ctypes.byref(d), None, ok_k, FAKE, FAKE, 1, None, FAKE,
+                                    FAKE, None) == E
+    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, FAKE, FAKE, 2,
+                                    swan._i32_array([1, 3]), FAKE, FAKE, None) == E
+    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, FAKE, FAKE, -1, None, FAKE,
+                                    FAKE, None) == E
+    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, None, FAKE, 1, None, FAKE,
+                                    FAKE, None) == E
+    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, FAKE, FAKE, 1, None, None,
+                                    FAKE, None) == E
+    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, FAKE, FAKE, 1, None, FAKE + 8,
+                                    FAKE, None) == E
+    assert lib.swan_compress_append(ctypes.byref(d), swan._i32_array([-1, 0]), ok_k, FAKE, FAKE,
+                                    1, None, FAKE, FAKE, None) == E
+    # capacity: 1000 + 16 tokens fit, one more does not
+    st = lib.swan_compress_append(ctypes.byref(d), swan._i32_array([1016, 0]), ok_k, FAKE, FAKE,
+                                  1, None, FAKE, FAKE, None)
+    assert st == swan.SWAN_ERR_CAPACITY
+
+
+def test_decode_rejects_bad_arguments():
+    lib = swan.lib()
+    d = _desc()
+    ok_k = swan._i32_array([48, 64])
+    seq = swan._i32_array([100, 200])
+    need = swan.decode_workspace_bytes(d, [100, 200], [48, 64])
+    assert need > 0
+    E = swan.SWAN_ERR_INVALID_ARG
+    args = lambda seq_, ws, wsb, scale=0.0: (ctypes.byref(d), seq_, ok_k, FAKE, FAKE, FAKE,
+                                            scale, FAKE, ws, wsb, None)
+    assert lib.swan_decode_attention(*args(swan._i32_array([0, 5]), FAKE, need)) == E
+    assert lib.swan_decode_attention(*args(seq, None, need)) == swan.SWAN_ERR_WORKSPACE
+    assert lib.swan_decode_attention(*args(seq, FAKE, need - 1)) == swan.SWAN_ERR_WORKSPACE
+    assert lib.swan_decode_attention(*args(seq, FAKE + 16, need)) == E  # misaligned
+    assert lib.swan_decode_attention(*args(seq, FAKE, need, float("nan"))) == E
+    assert lib.swan_decode_attention(*args(swan._i32_array([1017, 5]), FAKE, 1 << 30)) == \
+        swan.SWAN_ERR_CAPACITY
+    assert lib.swan_decode_attention(ctypes.byref(d), seq, ok_k, None, FAKE, FAKE, 0.0, FAKE,
+                                     FAKE, need, None) == E
+
+
+def test_calibrate_rejects_bad_arguments():
+    lib = swan.lib()
+    need = swan.calibrate_workspace_bytes(128)
+    assert need >= 2 * 8 * 128 * 128
+    assert lib.swan_calibrate_rotation(FAKE, 100, 64, FAKE, None, FAKE, need, None) == \
+        swan.SWAN_ERR_UNSUPPORTED
+    assert lib.swan_calibrate_rotation(FAKE, 0, 128, FAKE, None, FAKE, need, None) == \
+        swan.SWAN_ERR_INVALID_ARG
+    assert lib.swan_calibrate_rotation(None, 10, 128, FAKE, None, FAKE, need, None) == \
+        swan.SWAN_ERR_INVALID_ARG
+    assert lib.swan_calibrate_rotation(FAKE, 10, 128, FAKE, None, FAKE, need - 1, None) == \
+        swan.SWAN_ERR_WORKSPACE
+
+
+def test_workspace_grows_with_splits():
+    d = _desc(batch=1, n_q_heads=1, n_kv_heads=1, sparse_capacity=1 << 20)
+    small = swan.decode_workspace_bytes(d, [100], [48])
+    large = swan.decode_workspace_bytes(d, [1 << 19], [48])
+    assert large > small > 0
