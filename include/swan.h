@@ -72,8 +72,10 @@ typedef enum swan_dtype {
  * so entry e of slot t has its value at byte (e / GV) * 1024 + t * 16 +
  * (e % GV) * sizeof(T) and its index at byte 64 * k_pad * sizeof(T) +
  * (e / 8) * 512 + t * 8 + (e % 8).  A page is 64 * k_pad * (sizeof(T) + 1)
- * bytes.  Entries are in ascending index order; entries k..k_pad-1 are padding
- * (value +0, index 0).  Sequence s owns n_kv_heads * ceil(sparse_capacity / 64)
+ * bytes.  Entries 0..k-1 are the kept components in ascending index order;
+ * entries k..k_pad-1 are padding with value +0 at the lowest dims that were not
+ * kept, so the k_pad indices of a token are distinct (the decode kernel relies
+ * on it).  Sequence s owns n_kv_heads * ceil(sparse_capacity / 64)
  * pages of its own k, stored after those of sequences 0..s-1; within it, head h
  * owns the consecutive pages [h * ceil(sparse_capacity / 64), ...).  The keys'
  * pages live in k_pages, the values' in v_pages, with identical layouts.
@@ -178,6 +180,15 @@ swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_ho
                                   const float* P_qk, const float* P_vo, float scale,
                                   void* out, void* workspace, size_t workspace_bytes,
                                   void* stream);
+
+/*
+ * Profiling hook.  While both are non-NULL, swan_decode_attention on this
+ * thread records start_event (a hipEvent_t) on its stream right before its
+ * sparse/buffer attention launches and stop_event right after them, so that
+ * hipEventElapsedTime gives the duration of that kernel alone.  NULL, NULL
+ * (the default) disables it.  The events stay owned by the caller.
+ */
+swan_status swan_set_profile_events(void* start_event, void* stop_event);
 
 #ifdef __cplusplus
 }

@@ -56,10 +56,24 @@ __device__ __forceinline__ void select_and_pack(typename Store<T>::Bits x0,
     *(typename St::Bits*)(vals + (e1 / GV) * 1024 + (e1 % GV) * St::kBytes) = x1;
     idxs[(e1 / 8) * 512 + (e1 % 8)] = (char)(2 * lane + 1);
   }
-  const int e = k + lane;  // padding entries k .. kp-1: value +0, index 0
-  if (e < kp) {
-    *(typename St::Bits*)(vals + (e / GV) * 1024 + (e % GV) * St::kBytes) = 0;
-    idxs[(e / 8) * 512 + (e % 8)] = 0;
+  // padding entries k .. kp-1: value +0 at the lowest unselected dims, so that
+  // the indices of a token stay distinct
+  const int npad = kp - k;
+  if (npad > 0) {
+    const uint64_t n0 = __ballot(!s0);
+    const uint64_t n1 = __ballot(!s1);
+    const int r0 = popc_below(n0) + popc_below(n1);
+    const int r1 = r0 + (s0 ? 0 : 1);
+    if (!s0 && r0 < npad) {
+      const int e = k + r0;
+      *(typename St::Bits*)(vals + (e / GV) * 1024 + (e % GV) * St::kBytes) = 0;
+      idxs[(e / 8) * 512 + (e % 8)] = (char)(2 * lane);
+    }
+    if (!s1 && r1 < npad) {
+      const int e = k + r1;
+      *(typename St::Bits*)(vals + (e / GV) * 1024 + (e % GV) * St::kBytes) = 0;
+      idxs[(e / 8) * 512 + (e % 8)] = (char)(2 * lane + 1);
+    }
   }
 }
 

@@ -92,30 +92,44 @@ __device__ __forceinline__ int entry_idx(const PageRegs<T, KP8>& r, int g, int u
   return (int)((w >> (8 * (u & 3))) & 0xFFu);
 }
 
+// LDS layouts of one wave (a workgroup is one wave):
+//   qrep[dim][8]   the rotated query, 8 copies so that lanes l, l+8, ... of a
+//                  half wave spread over the banks
+//   acc[dim][64]   lane-private accumulators: lane t owns column t, so the
+//                  read-modify-write of one entry never meets another lane's
+constexpr int kQRep = 8;
+
 template <typename T, int KP8>
-__device__ __forceinline__ float page_score(const PageRegs<T, KP8>& r, const float* qrep) {
+__device__ __forceinline__ float page_score(const PageRegs<T, KP8>& r, const float* qrep_l) {
   float s0 = 0.f, s1 = 0.f;
 #pragma unroll
   for (int g = 0; g < KP8; ++g) {
 #pragma unroll
     for (int u = 0; u < 8; u += 2) {
-      s0 = fmaf(qrep[entry_idx(r, g, u) * 32], EntryVal<T, KP8>::get(r, g, u), s0);
-      s1 = fmaf(qrep[entry_idx(r, g, u + 1) * 32], EntryVal<T, KP8>::get(r, g, u + 1), s1);
+      s0 = fmaf(qrep_l[entry_idx(r, g, u) * kQRep], EntryVal<T, KP8>::get(r, g, u), s0);
+      s1 = fmaf(qrep_l[entry_idx(r, g, u + 1) * kQRep], EntryVal<T, KP8>::get(r, g, u + 1), s1);
     }
   }
   return s0 + s1;
 }
 
+// acc[idx][lane] += p * v for the k entries of this lane's token.  A token's
+// indices are distinct, so all reads can be issued before the writes.
 template <typename T, int KP8>
-__device__ __forceinline__ void page_accumulate(const PageRegs<T, KP8>& r, float* accl, float p) {
+__device__ __forceinline__ void page_accumulate(const PageRegs<T, KP8>& r, float* acc_l, float p) {
+  float a[KP8 * 8];
 #pragma unroll
-  for (int g = 0; g < KP8; ++g) {
+  for (int g = 0; g < KP8; ++g)
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      __hip_atomic_fetch_add(accl + entry_idx(r, g, u) * 32, p * EntryVal<T, KP8>::get(r, g, u),
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    }
-  }
+    for (int u = 0; u < 8; ++u) a[g * 8 + u] = acc_l[entry_idx(r, g, u) * 64];
+#pragma unroll
+  for (int g = 0; g < KP8; ++g)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) a[g * 8 + u] = fmaf(p, EntryVal<T, KP8>::get(r, g, u), a[g * 8 + u]);
+#pragma unroll
+  for (int g = 0; g < KP8; ++g)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc_l[entry_idx(r, g, u) * 64] = a[g * 8 + u];
 }
 
 struct SoftmaxState {
@@ -126,8 +140,8 @@ struct SoftmaxState {
 
 __device__ __forceinline__ void rescale_acc(float* acc, int lane, float f) {
   __syncthreads();
-#pragma unroll
-  for (int c = 0; c < 16; ++c) {
+#pragma unroll 8
+  for (int c = 0; c < 32; ++c) {
     float4* p = (float4*)acc + c * 64 + lane;
     float4 v = *p;
     v.x *= f; v.y *= f; v.z *= f; v.w *= f;
@@ -159,42 +173,42 @@ __device__ __forceinline__ void process_page(const PageRegs<T, KP8>& kr, const P
 }
 
 // One wave: pages [pbeg, pend) of one (sequence, kv head), for one query head.
+// The next page is always loaded (clamped to the last page) so that no load
+// sits under a branch and the compiler can keep one page in flight.
 template <typename T, int KP8>
 __device__ void sparse_split(const char* kbase, const char* vbase, int64_t pbytes, int pbeg,
                              int pend, int S, float* qrep, float* acc, int lane,
                              float* __restrict__ part) {
-  const int l32 = lane & 31;
-  const float* qrep_l = qrep + l32;
-  float* acc_l = acc + l32;
+  const float* qrep_l = qrep + (lane & (kQRep - 1));
+  float* acc_l = acc + lane;
   SoftmaxState st{0.f, 0.f, true};
   PageRegs<T, KP8> ka, va, kb, vb;
+  const int plast = pend - 1;
   load_page<T, KP8>(ka, kbase + pbeg * pbytes, lane);
   load_page<T, KP8>(va, vbase + pbeg * pbytes, lane);
   for (int p = pbeg; p < pend; p += 2) {
-    const bool has_b = p + 1 < pend;
-    if (has_b) {
-      load_page<T, KP8>(kb, kbase + (p + 1) * pbytes, lane);
-      load_page<T, KP8>(vb, vbase + (p + 1) * pbytes, lane);
-    }
+    const int p1 = p + 1 < plast ? p + 1 : plast;
+    load_page<T, KP8>(kb, kbase + p1 * pbytes, lane);
+    load_page<T, KP8>(vb, vbase + p1 * pbytes, lane);
     process_page<T, KP8>(ka, va, p * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
-    if (!has_b) break;
-    if (p + 2 < pend) {
-      load_page<T, KP8>(ka, kbase + (p + 2) * pbytes, lane);
-      load_page<T, KP8>(va, vbase + (p + 2) * pbytes, lane);
-    }
-    process_page<T, KP8>(kb, vb, (p + 1) * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
+    const int p2 = p + 2 < plast ? p + 2 : plast;
+    load_page<T, KP8>(ka, kbase + p2 * pbytes, lane);
+    load_page<T, KP8>(va, vbase + p2 * pbytes, lane);
+    if (p + 1 < pend)
+      process_page<T, KP8>(kb, vb, (p + 1) * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
   }
   const float ltot = wave_sum(st.l);
   __syncthreads();
-  // reduce acc[dim][32] over its 32 columns: lane owns dims lane and lane + 64
+  // reduce acc[dim][64] over its 64 columns: lane owns dims lane and lane + 64;
+  // the starting chunk is staggered per lane to spread the banks
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int r = lane + 64 * h;
-    const float4* row = (const float4*)(acc + r * 32);
+    const float4* row = (const float4*)(acc + r * 64);
     float sum = 0.f;
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const float4 v = row[(c + lane) & 7];
+    for (int c = 0; c < 16; ++c) {
+      const float4 v = row[(c + lane) & 15];
       sum += (v.x + v.y) + (v.z + v.w);
     }
     part[4 + r] = sum;
@@ -274,8 +288,8 @@ __device__ void buffer_part(const T* kring, const T* vring, int nb, const float*
 // a.seq lists the sequences of this launch.
 template <typename T, int KP8>
 __global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup grp) {
-  __shared__ __attribute__((aligned(16))) float qrep[kD * 32];
-  __shared__ __attribute__((aligned(16))) float acc[kD * 32];
+  __shared__ __attribute__((aligned(16))) float qrep[kD * kQRep];
+  __shared__ __attribute__((aligned(16))) float acc[kD * 64];
   const int lane = threadIdx.x;
   const int GH = grp.n * a.Hq;
   const int G = a.Hq / a.Hkv;
@@ -289,7 +303,7 @@ __global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup grp) 
     const int64_t ring_off = ((int64_t)b * a.Hkv + h) * a.bb * kD;
     float* part = a.part + ((int64_t)bhq * (a.n_splits + 1) + a.n_splits) * kPartFloats;
     buffer_part<T>((const T*)a.k_ring + ring_off, (const T*)a.v_ring + ring_off, nb,
-                   a.qhat + (int64_t)bhq * kD, acc, qrep, lane, part);
+                   a.qhat + (int64_t)bhq * kD, qrep, acc, lane, part);
     return;
   }
   w -= GH;
@@ -311,18 +325,18 @@ __global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup grp) 
   const char* vbase = (const char*)a.v_pages + unit_off;
   float* part = a.part + ((int64_t)bhq * (a.n_splits + 1) + split) * kPartFloats;
 
-  // replicate q_hat: q_rep[dim][32]; lane writes dims lane and lane + 64
+  // replicate q_hat: q_rep[dim][8]; lane writes dims lane and lane + 64
   const float* qh = a.qhat + (int64_t)bhq * kD;
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh) {
     const int r = lane + 64 * hh;
     const float v = qh[r];
-    float4* row = (float4*)(qrep + r * 32);
-#pragma unroll
-    for (int c = 0; c < 8; ++c) row[(c + lane) & 7] = make_float4(v, v, v, v);
+    float4* row = (float4*)(qrep + r * kQRep);
+    row[0] = make_float4(v, v, v, v);
+    row[1] = make_float4(v, v, v, v);
   }
-#pragma unroll
-  for (int c = 0; c < 16; ++c) ((float4*)acc)[c * 64 + lane] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8
+  for (int c = 0; c < 32; ++c) ((float4*)acc)[c * 64 + lane] = make_float4(0.f, 0.f, 0.f, 0.f);
   __syncthreads();
   sparse_split<T, KP8>(kbase, vbase, pbytes, pbeg, pend, S, qrep, acc, lane, part);
 }
@@ -396,6 +410,10 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
                      a.qhat, a.Hq, a.Hq / a.Hkv, a.qmult);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (a.prof_start) {
+    e = hipEventRecord(a.prof_start, a.stream);
+    if (e != hipSuccess) return e;
+  }
   // group sequences by k_pad: one attention launch per group
   for (int kp8 = 1; kp8 <= kD / 8; ++kp8) {
     SeqGroup g;
@@ -416,6 +434,10 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
       default:
         break;
     }
+    if (e != hipSuccess) return e;
+  }
+  if (a.prof_stop) {
+    e = hipEventRecord(a.prof_stop, a.stream);
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(merge_kernel<T>, dim3(BH), dim3(128), 0, a.stream, a);

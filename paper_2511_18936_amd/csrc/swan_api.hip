@@ -14,6 +14,8 @@
 namespace {
 
 thread_local std::string g_last_error;
+thread_local hipEvent_t g_prof_start = nullptr;
+thread_local hipEvent_t g_prof_stop = nullptr;
 
 swan_status fail(swan_status st, const char* fmt, ...) {
   char buf[512];
@@ -320,7 +322,17 @@ swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_ho
   a.qmult = sc * 1.4426950408889634f;
   a.dtype = c->dtype;
   a.stream = (hipStream_t)stream;
+  a.prof_start = g_prof_start;
+  a.prof_stop = g_prof_stop;
   return hip_status(swan::launch_decode(a), "decode launch");
+}
+
+swan_status swan_set_profile_events(void* start_event, void* stop_event) {
+  if ((start_event == nullptr) != (stop_event == nullptr))
+    return fail(SWAN_ERR_INVALID_ARG, "pass both events or neither");
+  g_prof_start = (hipEvent_t)start_event;
+  g_prof_stop = (hipEvent_t)stop_event;
+  return ok();
 }
 
 }  // extern "C"

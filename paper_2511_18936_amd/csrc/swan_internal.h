@@ -48,6 +48,8 @@ struct DecodeLaunch {
   int dtype;
   SeqTab tab;
   hipStream_t stream;
+  hipEvent_t prof_start;  // optional events around the attention launches
+  hipEvent_t prof_stop;
 };
 hipError_t launch_decode(const DecodeLaunch& a);
 

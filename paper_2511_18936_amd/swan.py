@@ -31,7 +31,7 @@ PAGE_TOKENS = 64
 EXPORTED = (
     "swan_last_error", "swan_version", "swan_page_bytes", "swan_cache_bytes",
     "swan_calibrate_workspace_bytes", "swan_calibrate_rotation", "swan_compress_append",
-    "swan_decode_workspace_bytes", "swan_decode_attention",
+    "swan_decode_workspace_bytes", "swan_decode_attention", "swan_set_profile_events",
 )
 
 
@@ -82,6 +82,7 @@ def _load() -> ctypes.CDLL:
         "swan_compress_append": [pdesc, pi32, pi32, vp, vp, i32, pi32, vp, vp, vp],
         "swan_decode_workspace_bytes": [pdesc, pi32, pi32, psz],
         "swan_decode_attention": [pdesc, pi32, pi32, vp, vp, vp, ctypes.c_float, vp, vp, sz, vp],
+        "swan_set_profile_events": [vp, vp],
     }
     for name, args in sigs.items():
         f = getattr(lib, name)
@@ -188,6 +189,13 @@ def decode_attention(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence
                                       _i32_array(k_active), _ptr(q), _ptr(P_qk), _ptr(P_vo),
                                       float(scale), _ptr(out), _ptr(workspace),
                                       workspace.numel(), _stream(stream)))
+
+
+def set_profile_events(start=None, stop=None) -> None:
+    """Record torch.cuda.Event start/stop around the attention kernels of the next
+    decode calls on this thread (None, None disables)."""
+    _check(_lib.swan_set_profile_events(None if start is None else start.cuda_event,
+                                        None if stop is None else stop.cuda_event))
 
 
 class SwanCache:

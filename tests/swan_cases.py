@@ -79,8 +79,11 @@ def compare_unit(cache, oc, b, h, L, dtype_np):
         assert bad.size == 0, f"role {role}: {bad.size} of {S} tokens select other indices"
         assert np.array_equal(val.view(np.uint8), np.asarray(oc[iv], dtype_np).view(np.uint8)), \
             f"role {role}: values differ"
-        if pidx.size:
-            assert np.all(pidx == 0) and np.all(pval.astype(np.float64) == 0)
+        if pidx.size:  # padding: value +0 at the lowest dims not kept
+            assert np.all(pval.astype(np.float64) == 0)
+            for t in range(S):
+                free = np.setdiff1d(np.arange(128), oc[ik][t])[: pidx.shape[1]]
+                assert np.array_equal(pidx[t], free), f"role {role}: padding of token {t}"
         buf = ring_rows(cache, b, h, role, L)
         want = oc["k_buf" if role == 0 else "v_buf"]
         assert np.array_equal(np.asarray(buf).view(np.uint8),

@@ -60,6 +60,10 @@ def pack(idx: np.ndarray, val: np.ndarray, dtype, k: int, n_pages: int) -> np.nd
     ifull = np.zeros((n_pages * 64, kp), dtype=np.uint8)
     vfull[:n, :k] = val
     ifull[:n, :k] = idx
+    for t in range(n):  # padding: value 0 at the lowest dims not kept
+        if kp > k:
+            free = np.setdiff1d(np.arange(128), idx[t])[: kp - k]
+            ifull[t, k:] = free
     vb = vfull.view(np.uint8).reshape(n_pages, 64, kp // gv, 16).transpose(0, 2, 1, 3)
     ib = ifull.reshape(n_pages, 64, kp // 8, 8).transpose(0, 2, 1, 3)
     out = np.concatenate([vb.reshape(n_pages, -1), ib.reshape(n_pages, -1)], axis=1)

@@ -22,7 +22,7 @@ def _declared_functions():
 
 def test_header_and_binding_agree_on_exports():
     declared = _declared_functions()
-    assert len(declared) == 9
+    assert len(declared) == 10
     assert sorted(swan.EXPORTED) == declared
     lib = swan.lib()
     for name in declared:
@@ -142,6 +142,12 @@ def test_calibrate_rejects_bad_arguments():
         swan.SWAN_ERR_INVALID_ARG
     assert lib.swan_calibrate_rotation(FAKE, 10, 128, FAKE, None, FAKE, need - 1, None) == \
         swan.SWAN_ERR_WORKSPACE
+
+
+def test_profile_hook_needs_both_events():
+    lib = swan.lib()
+    assert lib.swan_set_profile_events(FAKE, None) == swan.SWAN_ERR_INVALID_ARG
+    assert lib.swan_set_profile_events(None, None) == swan.SWAN_OK
 
 
 def test_workspace_grows_with_splits():
