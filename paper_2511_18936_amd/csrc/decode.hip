@@ -56,6 +56,7 @@ struct PageRegs {
   u32x2 idx[KP8];
 };
 
+// Loads one page into registers (nontemporal: the pages are streamed once).
 template <typename T, int KP8>
 __device__ __forceinline__ void load_page(PageRegs<T, KP8>& r, const char* page, int lane) {
   constexpr int VCH = PageRegs<T, KP8>::VCH;
@@ -95,9 +96,12 @@ __device__ __forceinline__ int entry_idx(const PageRegs<T, KP8>& r, int g, int u
 // LDS layouts of one wave (a workgroup is one wave):
 //   qrep[dim][8]   the rotated query, 8 copies so that lanes l, l+8, ... of a
 //                  half wave spread over the banks
-//   acc[dim][64]   lane-private accumulators: lane t owns column t, so the
-//                  read-modify-write of one entry never meets another lane's
+//   acc[dim][C]    accumulators: lane t owns column t % C (C = kAccCols), so
+//                  within one pass no two lanes update the same word
 constexpr int kQRep = 8;
+// accumulator columns: 64 = one per lane; 32 = lanes l and l+32 share column
+// l, updated in two half-wave passes (half the LDS, twice the waves per CU)
+constexpr int kAccCols = 64;
 
 template <typename T, int KP8>
 __device__ __forceinline__ float page_score(const PageRegs<T, KP8>& r, const float* qrep_l) {
@@ -114,22 +118,58 @@ __device__ __forceinline__ float page_score(const PageRegs<T, KP8>& r, const flo
 }
 
 // acc[idx][lane] += p * v for the k entries of this lane's token.  A token's
-// indices are distinct, so all reads can be issued before the writes.
+// indices are distinct, so the reads of a chunk can all be issued before its
+// writes; chunks of 16 entries bound the live registers.
+template <typename T, int KP8, int G0, int NG>
+__device__ __forceinline__ void accumulate_groups(const PageRegs<T, KP8>& r, float* acc_l,
+                                                  float p) {
+  float a[NG * 8];
+#pragma unroll
+  for (int g = 0; g < NG; ++g)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) a[g * 8 + u] = acc_l[entry_idx(r, G0 + g, u) * kAccCols];
+#pragma unroll
+  for (int g = 0; g < NG; ++g)
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      a[g * 8 + u] = fmaf(p, EntryVal<T, KP8>::get(r, G0 + g, u), a[g * 8 + u]);
+#pragma unroll
+  for (int g = 0; g < NG; ++g)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc_l[entry_idx(r, G0 + g, u) * kAccCols] = a[g * 8 + u];
+}
+
+// acc[idx][lane] += p * v for the k entries of this lane's token.  A token's
+// indices are distinct, so every read of a chunk is issued before its writes
+// (one LDS round trip per chunk); up to 64 entries form one chunk.
 template <typename T, int KP8>
-__device__ __forceinline__ void page_accumulate(const PageRegs<T, KP8>& r, float* acc_l, float p) {
-  float a[KP8 * 8];
+__device__ __forceinline__ void page_accumulate_lanes(const PageRegs<T, KP8>& r, float* acc_l,
+                                                      float p) {
+  if constexpr (KP8 <= 8) {
+    accumulate_groups<T, KP8, 0, KP8>(r, acc_l, p);
+  } else {
+    accumulate_groups<T, KP8, 0, 8>(r, acc_l, p);
+    accumulate_groups<T, KP8, 8, KP8 - 8>(r, acc_l, p);
+  }
+}
+
+__device__ __forceinline__ void wave_lds_fence();
+
+template <typename T, int KP8>
+__device__ __forceinline__ void page_accumulate(const PageRegs<T, KP8>& r, float* acc_l, float p,
+                                                bool valid, int lane) {
+  if constexpr (kAccCols == 64) {
+    if (valid) page_accumulate_lanes<T, KP8>(r, acc_l, p);
+  } else {
+    // two half-wave passes: within a pass every lane owns its column; the
+    // fence keeps the passes in program order (LDS executes a wave's
+    // accesses in that order)
 #pragma unroll
-  for (int g = 0; g < KP8; ++g)
-#pragma unroll
-    for (int u = 0; u < 8; ++u) a[g * 8 + u] = acc_l[entry_idx(r, g, u) * 64];
-#pragma unroll
-  for (int g = 0; g < KP8; ++g)
-#pragma unroll
-    for (int u = 0; u < 8; ++u) a[g * 8 + u] = fmaf(p, EntryVal<T, KP8>::get(r, g, u), a[g * 8 + u]);
-#pragma unroll
-  for (int g = 0; g < KP8; ++g)
-#pragma unroll
-    for (int u = 0; u < 8; ++u) acc_l[entry_idx(r, g, u) * 64] = a[g * 8 + u];
+    for (int half = 0; half < 2; ++half) {
+      if (valid && (lane >> 5) == half) page_accumulate_lanes<T, KP8>(r, acc_l, p);
+      wave_lds_fence();
+    }
+  }
 }
 
 struct SoftmaxState {
@@ -138,38 +178,46 @@ struct SoftmaxState {
   bool first;
 };
 
+// LDS accesses of one wave execute in program order; this keeps the compiler
+// from moving them across the point (no workgroup barrier: waves of one
+// workgroup may take different branches).
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
 __device__ __forceinline__ void rescale_acc(float* acc, int lane, float f) {
-  __syncthreads();
+  wave_lds_fence();
 #pragma unroll 8
-  for (int c = 0; c < 32; ++c) {
+  for (int c = 0; c < kAccCols / 2; ++c) {
     float4* p = (float4*)acc + c * 64 + lane;
     float4 v = *p;
     v.x *= f; v.y *= f; v.z *= f; v.w *= f;
     *p = v;
   }
-  __syncthreads();
+  wave_lds_fence();
 }
 
 template <typename T, int KP8>
 __device__ __forceinline__ void process_page(const PageRegs<T, KP8>& kr, const PageRegs<T, KP8>& vr,
                                              bool valid, const float* qrep_l, float* acc_l,
                                              float* acc, int lane, SoftmaxState& st) {
-  float s = valid ? page_score(kr, qrep_l) : -INFINITY;
-  const float pm = wave_max(s);
+  const float s = valid ? page_score<T, KP8>(kr, qrep_l) : -INFINITY;
+  // the reference m only moves when a score passes m + kTau: one ballot per
+  // page, a wave max only on the first page and on the rare raise
   if (st.first) {
-    st.m = pm;
+    st.m = wave_max(s);
     st.first = false;
-  } else if (pm > st.m + kTau) {
+  } else if (__ballot(s > st.m + kTau) != 0) {
+    const float pm = wave_max(s);
     const float f = exp2f(st.m - pm);
     rescale_acc(acc, lane, f);
     st.l *= f;
     st.m = pm;
   }
-  if (valid) {
-    const float p = exp2f(s - st.m);
-    st.l += p;
-    page_accumulate(vr, acc_l, p);
-  }
+  const float p = valid ? exp2f(s - st.m) : 0.f;
+  st.l += p;
+  page_accumulate<T, KP8>(vr, acc_l, p, valid, lane);
 }
 
 // One wave: pages [pbeg, pend) of one (sequence, kv head), for one query head.
@@ -180,35 +228,47 @@ __device__ void sparse_split(const char* kbase, const char* vbase, int64_t pbyte
                              int pend, int S, float* qrep, float* acc, int lane,
                              float* __restrict__ part) {
   const float* qrep_l = qrep + (lane & (kQRep - 1));
-  float* acc_l = acc + lane;
+  float* acc_l = acc + (lane & (kAccCols - 1));
   SoftmaxState st{0.f, 0.f, true};
-  PageRegs<T, KP8> ka, va, kb, vb;
-  const int plast = pend - 1;
-  load_page<T, KP8>(ka, kbase + pbeg * pbytes, lane);
-  load_page<T, KP8>(va, vbase + pbeg * pbytes, lane);
-  for (int p = pbeg; p < pend; p += 2) {
-    const int p1 = p + 1 < plast ? p + 1 : plast;
-    load_page<T, KP8>(kb, kbase + p1 * pbytes, lane);
-    load_page<T, KP8>(vb, vbase + p1 * pbytes, lane);
-    process_page<T, KP8>(ka, va, p * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
-    const int p2 = p + 2 < plast ? p + 2 : plast;
-    load_page<T, KP8>(ka, kbase + p2 * pbytes, lane);
-    load_page<T, KP8>(va, vbase + p2 * pbytes, lane);
-    if (p + 1 < pend)
-      process_page<T, KP8>(kb, vb, (p + 1) * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
+  // pipeline depth by the register footprint of a page (16-byte chunks per lane)
+  constexpr int kChunks = KP8 * PageRegs<T, KP8>::VCH;
+  if constexpr (kChunks <= 12) {  // two register sets: one page in flight
+    PageRegs<T, KP8> ka, va, kb, vb;
+    const int plast = pend - 1;
+    load_page<T, KP8>(ka, kbase + pbeg * pbytes, lane);
+    load_page<T, KP8>(va, vbase + pbeg * pbytes, lane);
+    for (int p = pbeg; p < pend; p += 2) {
+      const int p1 = p + 1 < plast ? p + 1 : plast;
+      load_page<T, KP8>(kb, kbase + p1 * pbytes, lane);
+      load_page<T, KP8>(vb, vbase + p1 * pbytes, lane);
+      process_page<T, KP8>(ka, va, p * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
+      const int p2 = p + 2 < plast ? p + 2 : plast;
+      load_page<T, KP8>(ka, kbase + p2 * pbytes, lane);
+      load_page<T, KP8>(va, vbase + p2 * pbytes, lane);
+      if (p + 1 < pend)
+        process_page<T, KP8>(kb, vb, (p + 1) * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
+    }
+  } else {  // large pages: one page at a time
+    PageRegs<T, KP8> ka, va;
+    for (int p = pbeg; p < pend; ++p) {
+      load_page<T, KP8>(ka, kbase + p * pbytes, lane);
+      load_page<T, KP8>(va, vbase + p * pbytes, lane);
+      process_page<T, KP8>(ka, va, p * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
+    }
   }
   const float ltot = wave_sum(st.l);
-  __syncthreads();
-  // reduce acc[dim][64] over its 64 columns: lane owns dims lane and lane + 64;
+  wave_lds_fence();
+  // reduce acc[dim][cols] over its columns: lane owns dims lane and lane + 64;
   // the starting chunk is staggered per lane to spread the banks
+  constexpr int kRowChunks = kAccCols / 4;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int r = lane + 64 * h;
-    const float4* row = (const float4*)(acc + r * 64);
+    const float4* row = (const float4*)(acc + r * kAccCols);
     float sum = 0.f;
 #pragma unroll
-    for (int c = 0; c < 16; ++c) {
-      const float4 v = row[(c + lane) & 15];
+    for (int c = 0; c < kRowChunks; ++c) {
+      const float4 v = row[(c + lane) & (kRowChunks - 1)];
       sum += (v.x + v.y) + (v.z + v.w);
     }
     part[4 + r] = sum;
@@ -228,7 +288,7 @@ __device__ void buffer_part(const T* kring, const T* vring, int nb, const float*
   constexpr int E = 16 / (int)sizeof(T);  // elements per 16-byte load
   qs[lane] = qh[lane];
   qs[lane + 64] = qh[lane + 64];
-  __syncthreads();
+  wave_lds_fence();
   float mloc = -INFINITY;
   for (int t0 = 0; t0 < nb; t0 += 64) {
     const int t = t0 + lane;
@@ -267,7 +327,7 @@ __device__ void buffer_part(const T* kring, const T* vring, int nb, const float*
     }
   }
   const float l = wave_sum(lloc);
-  __syncthreads();
+  wave_lds_fence();
   float a0 = 0.f, a1 = 0.f;
   for (int t = 0; t < nb; ++t) {
     const float p = pb[t];
@@ -283,25 +343,26 @@ __device__ void buffer_part(const T* kring, const T* vring, int nb, const float*
   }
 }
 
-// Grid: the dense-buffer waves of the launch's sequences first, then their
-// sparse waves.  One launch per distinct k_pad (KP8 = k_pad / 8) in the batch;
-// a.seq lists the sequences of this launch.
+// One launch per distinct k_pad of the batch (KP8 = k_pad / 8), over the
+// sequences g.seq[0..g.n) that use it.  Grid: n * Hq dense-buffer waves first,
+// then n * Hq * g.n_splits sparse waves.
 template <typename T, int KP8>
-__global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup grp) {
+__global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup g) {
   __shared__ __attribute__((aligned(16))) float qrep[kD * kQRep];
-  __shared__ __attribute__((aligned(16))) float acc[kD * 64];
+  __shared__ __attribute__((aligned(16))) float acc[kD * kAccCols];
   const int lane = threadIdx.x;
-  const int GH = grp.n * a.Hq;
+  const int GH = g.n * a.Hq;
   const int G = a.Hq / a.Hkv;
+  const int pstride = a.n_splits + 1;  // partial slots per (sequence, q-head)
   int w = blockIdx.x;
   if (w < GH) {  // dense-buffer wave
-    const int b = grp.seq[w / a.Hq], hq = w % a.Hq, h = hq / G;
+    const int b = g.seq[w / a.Hq], hq = w % a.Hq, h = hq / G;
     const int bhq = b * a.Hq + hq;
     const int L = a.tab.len[b];
     const int nb = L < a.bb ? L : a.bb;
     if (nb == 0) return;
     const int64_t ring_off = ((int64_t)b * a.Hkv + h) * a.bb * kD;
-    float* part = a.part + ((int64_t)bhq * (a.n_splits + 1) + a.n_splits) * kPartFloats;
+    float* part = a.part + ((int64_t)bhq * pstride + a.n_splits) * kPartFloats;
     buffer_part<T>((const T*)a.k_ring + ring_off, (const T*)a.v_ring + ring_off, nb,
                    a.qhat + (int64_t)bhq * kD, qrep, acc, lane, part);
     return;
@@ -309,12 +370,13 @@ __global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup grp) 
   w -= GH;
   const int split = w / GH;
   const int gi = w % GH;
-  const int b = grp.seq[gi / a.Hq], hq = gi % a.Hq, h = hq / G;
+  const int b = g.seq[gi / a.Hq], hq = gi % a.Hq, h = hq / G;
   const int bhq = b * a.Hq + hq;
   const int L = a.tab.len[b];
   const int S = L > a.bb ? L - a.bb : 0;
   const int np = pages_for(S);
-  const int ns = np < a.n_splits ? np : a.n_splits;
+  const int nsb = a.tab.nsplit[b];
+  const int ns = np < nsb ? np : nsb;
   if (split >= ns) return;
   const int pbeg = (int)((int64_t)split * np / ns);
   const int pend = (int)((int64_t)(split + 1) * np / ns);
@@ -323,7 +385,7 @@ __global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup grp) 
   const int64_t unit_off = a.tab.page_off[b] + (int64_t)h * a.n_pages_cap * pbytes;
   const char* kbase = (const char*)a.k_pages + unit_off;
   const char* vbase = (const char*)a.v_pages + unit_off;
-  float* part = a.part + ((int64_t)bhq * (a.n_splits + 1) + split) * kPartFloats;
+  float* part = a.part + ((int64_t)bhq * pstride + split) * kPartFloats;
 
   // replicate q_hat: q_rep[dim][8]; lane writes dims lane and lane + 64
   const float* qh = a.qhat + (int64_t)bhq * kD;
@@ -336,8 +398,9 @@ __global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup grp) 
     row[1] = make_float4(v, v, v, v);
   }
 #pragma unroll 8
-  for (int c = 0; c < 32; ++c) ((float4*)acc)[c * 64 + lane] = make_float4(0.f, 0.f, 0.f, 0.f);
-  __syncthreads();
+  for (int c = 0; c < kAccCols / 2; ++c)
+    ((float4*)acc)[c * 64 + lane] = make_float4(0.f, 0.f, 0.f, 0.f);
+  wave_lds_fence();
   sparse_split<T, KP8>(kbase, vbase, pbytes, pbeg, pend, S, qrep, acc, lane, part);
 }
 
@@ -348,39 +411,40 @@ template <typename T>
 __global__ __launch_bounds__(128) void merge_kernel(DecodeLaunch a) {
   __shared__ float oh[kD];
   __shared__ float wts[kMaxSplits + 1];
-  __shared__ float red[2];
+  __shared__ float red[4];
   const int bhq = blockIdx.x;
   const int b = bhq / a.Hq, hq = bhq % a.Hq, h = hq / (a.Hq / a.Hkv);
   const int t = threadIdx.x;
   const int L = a.tab.len[b];
   const int S = L > a.bb ? L - a.bb : 0;
   const int np = pages_for(S);
-  const int ns = np < a.n_splits ? np : a.n_splits;
+  const int nsg = a.tab.nsplit[b];
+  const int ns = np < nsg ? np : nsg;
   const bool has_buf = (L < a.bb ? L : a.bb) > 0;
   const float* part = a.part + (int64_t)bhq * (a.n_splits + 1) * kPartFloats;
-
-  if (t == 0) {
-    float m = -INFINITY;
-    for (int i = 0; i < ns; ++i) m = fmaxf(m, part[i * kPartFloats]);
-    if (has_buf) m = fmaxf(m, part[a.n_splits * kPartFloats]);
-    float lsum = 0.f;
-    for (int i = 0; i < ns; ++i) {
-      const float wgt = exp2f(part[i * kPartFloats] - m);
-      wts[i] = wgt;
-      lsum += wgt * part[i * kPartFloats + 1];
-    }
-    if (has_buf) {
-      const float wgt = exp2f(part[a.n_splits * kPartFloats] - m);
-      wts[a.n_splits] = wgt;
-      lsum += wgt * part[a.n_splits * kPartFloats + 1];
-    }
-    red[0] = 1.f / lsum;
-  }
+  // partial i < ns is split i; partial ns stands for the buffer (slot n_splits)
+  const int np_all = ns + (has_buf ? 1 : 0);
+  auto slot = [&](int i) { return i < ns ? i : a.n_splits; };
+  float mloc = -INFINITY;
+  for (int i = t; i < np_all; i += 128) mloc = fmaxf(mloc, part[slot(i) * kPartFloats]);
+  mloc = wave_max(mloc);
+  if ((t & 63) == 0) red[t >> 6] = mloc;
   __syncthreads();
+  const float m = fmaxf(red[0], red[1]);
+  float lloc = 0.f;
+  for (int i = t; i < np_all; i += 128) {
+    const float* pi = part + slot(i) * kPartFloats;
+    const float wgt = exp2f(pi[0] - m);
+    wts[i] = wgt;
+    lloc += wgt * pi[1];
+  }
+  lloc = wave_sum(lloc);
+  if ((t & 63) == 0) red[2 + (t >> 6)] = lloc;
+  __syncthreads();
+  const float inv = 1.f / (red[2] + red[3]);
   float o = 0.f;
-  for (int i = 0; i < ns; ++i) o = fmaf(wts[i], part[i * kPartFloats + 4 + t], o);
-  if (has_buf) o = fmaf(wts[a.n_splits], part[a.n_splits * kPartFloats + 4 + t], o);
-  oh[t] = o * red[0];
+  for (int i = 0; i < np_all; ++i) o = fmaf(wts[i], part[slot(i) * kPartFloats + 4 + t], o);
+  oh[t] = o * inv;
   __syncthreads();
   const float4* P = (const float4*)(a.P_vo + ((int64_t)h * kD + t) * kD);
   float r = 0.f;
@@ -397,9 +461,8 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeLaunch a) {
 
 template <typename T, int KP8>
 static hipError_t launch_attn(const DecodeLaunch& a, const SeqGroup& g) {
-  const int GH = g.n * a.Hq;
-  hipLaunchKernelGGL((attn_kernel<T, KP8>), dim3(GH * (a.n_splits + 1)), dim3(64), 0, a.stream,
-                     a, g);
+  const dim3 grid(g.n * a.Hq * (g.n_splits + 1));
+  hipLaunchKernelGGL((attn_kernel<T, KP8>), grid, dim3(64), 0, a.stream, a, g);
   return hipGetLastError();
 }
 
@@ -414,17 +477,22 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
     e = hipEventRecord(a.prof_start, a.stream);
     if (e != hipSuccess) return e;
   }
-  // group sequences by k_pad: one attention launch per group
-  for (int kp8 = 1; kp8 <= kD / 8; ++kp8) {
+  // sequences grouped by k_pad: one launch per group, each specialised on its
+  // exact k_pad (launches of one call run back to back on the stream)
+  for (int kp8 = kD / 8; kp8 >= 1; --kp8) {
     SeqGroup g;
     g.n = 0;
+    g.n_splits = 0;
     for (int b = 0; b < a.B; ++b)
-      if (kpad_of(a.tab.kact[b]) / 8 == kp8) g.seq[g.n++] = b;
+      if (kpad_of(a.tab.kact[b]) / 8 == kp8) {
+        g.seq[g.n++] = b;
+        g.n_splits = a.tab.nsplit[b] > g.n_splits ? a.tab.nsplit[b] : g.n_splits;
+      }
     if (g.n == 0) continue;
     switch (kp8) {
-#define SWAN_KP8_CASE(n) \
-  case n:                \
-    e = launch_attn<T, n>(a, g); \
+#define SWAN_KP8_CASE(n)                \
+  case n:                               \
+    e = launch_attn<T, n>(a, g);        \
     break;
       SWAN_KP8_CASE(1) SWAN_KP8_CASE(2) SWAN_KP8_CASE(3) SWAN_KP8_CASE(4)
       SWAN_KP8_CASE(5) SWAN_KP8_CASE(6) SWAN_KP8_CASE(7) SWAN_KP8_CASE(8)

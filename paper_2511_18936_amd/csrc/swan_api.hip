@@ -4,6 +4,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <string>
@@ -91,6 +92,7 @@ int64_t fill_layout(const swan_cache* c, const int32_t* k_active_host, swan::Seq
     tab.page_off[b] = 0;
     tab.len[b] = 0;
     tab.nnew[b] = 0;
+    tab.nsplit[b] = 1;
   }
   for (int b = 0; b < c->batch; ++b) {
     tab.kact[b] = k_active_host[b];
@@ -100,22 +102,38 @@ int64_t fill_layout(const swan_cache* c, const int32_t* k_active_host, swan::Seq
   return off;
 }
 
-int plan_splits(const swan_cache* c, const int32_t* seq_len_host) {
-  int max_pages = 0;
+// Token splits per (sequence, query head): about two waves per CU slot in total
+// (measured best for long contexts; SWAN_DECODE_WAVES overrides the target),
+// each sequence cut into equal page ranges carrying about the same bytes (a
+// page weighs k_pad), never more splits than pages.  Fills nsplit[b] (may be
+// NULL); returns the largest.
+int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t* k_active_host,
+                int32_t* nsplit) {
+  int64_t total = 0;
+  for (int b = 0; b < c->batch; ++b) {
+    const int S = seq_len_host[b] > c->buffer_tokens ? seq_len_host[b] - c->buffer_tokens : 0;
+    total += (int64_t)swan::pages_for(S) * swan::kpad_of(k_active_host[b]) * c->n_q_heads;
+  }
+  static const int64_t target_waves = [] {
+    const char* s = getenv("SWAN_DECODE_WAVES");  // tuning override
+    const long v = s ? atol(s) : 0;
+    return (int64_t)(v > 0 ? v : 256 * 4 * 2);
+  }();
+  int64_t per_wave = (total + target_waves - 1) / target_waves;
+  if (per_wave < 1) per_wave = 1;
+  int ns_max = 1;
   for (int b = 0; b < c->batch; ++b) {
     const int S = seq_len_host[b] > c->buffer_tokens ? seq_len_host[b] - c->buffer_tokens : 0;
     const int np = swan::pages_for(S);
-    if (np > max_pages) max_pages = np;
+    const int64_t work = (int64_t)np * swan::kpad_of(k_active_host[b]);
+    int ns = (int)((work + per_wave - 1) / per_wave);
+    if (ns > np) ns = np;
+    if (ns > swan::kMaxSplits) ns = swan::kMaxSplits;
+    if (ns < 1) ns = 1;
+    if (nsplit) nsplit[b] = ns;
+    if (ns > ns_max) ns_max = ns;
   }
-  if (max_pages == 0) return 1;
-  // enough waves to cover the 256 CUs several times over
-  const int64_t units = (int64_t)c->batch * c->n_q_heads;
-  const int64_t target_waves = 256 * 5 * 6;
-  int ns = (int)((target_waves + units - 1) / units);
-  if (ns < 1) ns = 1;
-  if (ns > max_pages) ns = max_pages;
-  if (ns > swan::kMaxSplits) ns = swan::kMaxSplits;
-  return ns;
+  return ns_max;
 }
 
 size_t decode_ws_bytes(const swan_cache* c, int ns) {
@@ -268,7 +286,7 @@ swan_status swan_decode_workspace_bytes(const swan_cache* c, const int32_t* seq_
   if (st != SWAN_OK) return st;
   if ((st = check_k(c, k_active_host)) != SWAN_OK) return st;
   if (!seq_len_host || !bytes) return fail(SWAN_ERR_INVALID_ARG, "NULL argument");
-  *bytes = decode_ws_bytes(c, plan_splits(c, seq_len_host));
+  *bytes = decode_ws_bytes(c, plan_splits(c, seq_len_host, k_active_host, nullptr));
   return ok();
 }
 
@@ -292,14 +310,14 @@ swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_ho
                   (long long)(L - c->buffer_tokens), c->sparse_capacity);
   }
   if (!(scale == scale) || isinf(scale)) return fail(SWAN_ERR_INVALID_ARG, "scale is not finite");
-  const int ns = plan_splits(c, seq_len_host);
+  swan::DecodeLaunch a;
+  fill_layout(c, k_active_host, a.tab);
+  const int ns = plan_splits(c, seq_len_host, k_active_host, a.tab.nsplit);
   const size_t need = decode_ws_bytes(c, ns);
   if (!workspace || workspace_bytes < need)
     return fail(SWAN_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, need);
   if (((uintptr_t)workspace & 255) != 0)
     return fail(SWAN_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
-  swan::DecodeLaunch a;
-  fill_layout(c, k_active_host, a.tab);
   for (int b = 0; b < c->batch; ++b) a.tab.len[b] = seq_len_host[b];
   const float sc = scale > 0.f ? scale : 1.0f / sqrtf((float)c->head_dim);
   a.q = q;

@@ -74,16 +74,39 @@ struct Store<float> {
 // ---------------------------------------------------------------------------
 // wave64 helpers
 // ---------------------------------------------------------------------------
+// wave64 reductions with DPP row shifts and row broadcasts (no LDS traffic);
+// the result is read from lane 63 and returned to every lane
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  // identity -inf for lanes whose DPP source is out of the row
+  auto mx = [](float x, float y) { return fmaxf(x, y); };
+  v = mx(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(-INFINITY),
+                                                       __float_as_int(v), 0x111, 0xF, 0xF, false)));
+  v = mx(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(-INFINITY),
+                                                       __float_as_int(v), 0x112, 0xF, 0xF, false)));
+  v = mx(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(-INFINITY),
+                                                       __float_as_int(v), 0x114, 0xF, 0xF, false)));
+  v = mx(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(-INFINITY),
+                                                       __float_as_int(v), 0x118, 0xF, 0xF, false)));
+  v = mx(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(-INFINITY),
+                                                       __float_as_int(v), 0x142, 0xA, 0xF, false)));
+  v = mx(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(-INFINITY),
+                                                       __float_as_int(v), 0x143, 0xC, 0xF, false)));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x111, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x112, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x114, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x118, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x142, 0xA, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x143, 0xC, 0xF, false));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 
 __device__ __forceinline__ int lane_id() { return (int)__lane_id(); }

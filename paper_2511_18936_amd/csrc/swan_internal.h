@@ -20,6 +20,7 @@ struct SeqTab {
   int32_t kact[SWAN_MAX_BATCH];      // k_active
   int64_t page_off[SWAN_MAX_BATCH];  // byte offset of the sequence's first page
   int32_t nnew[SWAN_MAX_BATCH];      // compress: tokens appended to the sequence
+  int32_t nsplit[SWAN_MAX_BATCH];    // decode: token splits of the sequence's launch
 };
 
 __host__ __device__ inline int kpad_of(int k) { return (k + 7) & ~7; }
@@ -43,7 +44,8 @@ struct DecodeLaunch {
   const void* v_ring;
   float* qhat;   // [B][Hq][128] workspace
   float* part;   // [B][Hq][NS + 1][kPartFloats] workspace
-  int B, Hq, Hkv, bb, n_pages_cap, n_splits;
+  int B, Hq, Hkv, bb, n_pages_cap;
+  int n_splits;  // NS: largest split count of any launch (slot NS holds the buffer partial)
   float qmult;   // scale * log2(e)
   int dtype;
   SeqTab tab;
@@ -56,8 +58,10 @@ hipError_t launch_decode(const DecodeLaunch& a);
 // sequences of one attention launch (those sharing a page format)
 struct SeqGroup {
   int32_t n;
+  int32_t n_splits;
   int32_t seq[SWAN_MAX_BATCH];
 };
+
 
 struct CompressLaunch {
   const void* k_new;
