@@ -18,12 +18,9 @@
 // first page's maximum and is only raised (with a rescale of acc) when a page
 // maximum exceeds it by more than kTau in log2 units, so exponentials stay
 // bounded by 2^kTau while rescales are rare.
-#include "swan_device.h"
-#include "swan_internal.h"
+#include "decode_common.h"
 
 namespace swan {
-
-constexpr float kTau = 8.0f;
 
 // ---------------------------------------------------------------------------
 // q rotation: q_hat[b][h][j] = mult * sum_i q[b][h][i] * P_qk[g][i][j]
@@ -44,53 +41,6 @@ __global__ __launch_bounds__(128) void qrot_kernel(const T* __restrict__ q,
 #pragma unroll 8
   for (int i = 0; i < kD; ++i) acc = fmaf(qs[i], P[i * kD + j], acc);
   qhat[(int64_t)bh * kD + j] = acc * mult;
-}
-
-// ---------------------------------------------------------------------------
-// page registers: KP8 groups of 8 entries; VCH 16-byte value chunks per group
-// ---------------------------------------------------------------------------
-template <typename T, int KP8>
-struct PageRegs {
-  static constexpr int VCH = (int)sizeof(T) / 2;
-  u32x4 val[KP8 * VCH];
-  u32x2 idx[KP8];
-};
-
-// Loads one page into registers (nontemporal: the pages are streamed once).
-template <typename T, int KP8>
-__device__ __forceinline__ void load_page(PageRegs<T, KP8>& r, const char* page, int lane) {
-  constexpr int VCH = PageRegs<T, KP8>::VCH;
-  const char* vp = page + lane * 16;
-#pragma unroll
-  for (int c = 0; c < KP8 * VCH; ++c)
-    r.val[c] = __builtin_nontemporal_load((const u32x4*)(vp + c * 1024));
-  const char* ip = page + KP8 * VCH * 1024 + lane * 8;
-#pragma unroll
-  for (int g = 0; g < KP8; ++g)
-    r.idx[g] = __builtin_nontemporal_load((const u32x2*)(ip + g * 512));
-}
-
-// value of entry u (0..7) of group g, as float
-template <typename T, int KP8>
-struct EntryVal {
-  __device__ static __forceinline__ float get(const PageRegs<T, KP8>& r, int g, int u) {
-    if constexpr (sizeof(T) == 2) {
-      const u32x4 c = r.val[g];
-      const uint32_t w = (u < 2) ? c.x : (u < 4) ? c.y : (u < 6) ? c.z : c.w;
-      return f16_bits_to_f32((u & 1) ? (w >> 16) : (w & 0xFFFFu));
-    } else {
-      const u32x4 c = r.val[g * 2 + (u >> 2)];
-      const int v = u & 3;
-      const uint32_t w = (v == 0) ? c.x : (v == 1) ? c.y : (v == 2) ? c.z : c.w;
-      return __uint_as_float(w);
-    }
-  }
-};
-
-template <typename T, int KP8>
-__device__ __forceinline__ int entry_idx(const PageRegs<T, KP8>& r, int g, int u) {
-  const uint32_t w = (u < 4) ? r.idx[g].x : r.idx[g].y;
-  return (int)((w >> (8 * (u & 3))) & 0xFFu);
 }
 
 // LDS layouts of one wave (a workgroup is one wave):
@@ -153,8 +103,6 @@ __device__ __forceinline__ void page_accumulate_lanes(const PageRegs<T, KP8>& r,
   }
 }
 
-__device__ __forceinline__ void wave_lds_fence();
-
 template <typename T, int KP8>
 __device__ __forceinline__ void page_accumulate(const PageRegs<T, KP8>& r, float* acc_l, float p,
                                                 bool valid, int lane) {
@@ -170,20 +118,6 @@ __device__ __forceinline__ void page_accumulate(const PageRegs<T, KP8>& r, float
       wave_lds_fence();
     }
   }
-}
-
-struct SoftmaxState {
-  float m;     // reference maximum (log2 units), wave-uniform
-  float l;     // per-lane sum of exp2(s - m)
-  bool first;
-};
-
-// LDS accesses of one wave execute in program order; this keeps the compiler
-// from moving them across the point (no workgroup barrier: waves of one
-// workgroup may take different branches).
-__device__ __forceinline__ void wave_lds_fence() {
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  __builtin_amdgcn_wave_barrier();
 }
 
 __device__ __forceinline__ void rescale_acc(float* acc, int lane, float f) {
@@ -276,70 +210,6 @@ __device__ void sparse_split(const char* kbase, const char* vbase, int64_t pbyte
   if (lane == 0) {
     part[0] = st.m;
     part[1] = ltot;
-  }
-}
-
-// One wave: the dense buffer of one (sequence, kv head), for one query head.
-// Lane t scores buffer token t (a dense 128-dim dot product), then lane l
-// accumulates output dims 2l and 2l+1 over all buffer tokens.
-template <typename T>
-__device__ void buffer_part(const T* kring, const T* vring, int nb, const float* qh, float* qs,
-                            float* pb, int lane, float* __restrict__ part) {
-  constexpr int E = 16 / (int)sizeof(T);  // elements per 16-byte load
-  qs[lane] = qh[lane];
-  qs[lane + 64] = qh[lane + 64];
-  wave_lds_fence();
-  float mloc = -INFINITY;
-  for (int t0 = 0; t0 < nb; t0 += 64) {
-    const int t = t0 + lane;
-    if (t < nb) {
-      const u32x4* kr = (const u32x4*)(kring + (int64_t)t * kD);
-      float s0 = 0.f, s1 = 0.f;
-#pragma unroll 4
-      for (int c = 0; c < kD / E; ++c) {
-        const u32x4 w = kr[c];
-#pragma unroll
-        for (int e = 0; e < E; e += 2) {
-          const int j = c * E + e;
-          if constexpr (sizeof(T) == 2) {
-            const uint32_t x = w[e / 2];
-            s0 = fmaf(qs[j], f16_bits_to_f32(x & 0xFFFFu), s0);
-            s1 = fmaf(qs[j + 1], f16_bits_to_f32(x >> 16), s1);
-          } else {
-            s0 = fmaf(qs[j], __uint_as_float(w[e]), s0);
-            s1 = fmaf(qs[j + 1], __uint_as_float(w[e + 1]), s1);
-          }
-        }
-      }
-      const float s = s0 + s1;
-      pb[t] = s;
-      mloc = fmaxf(mloc, s);
-    }
-  }
-  const float m = wave_max(mloc);
-  float lloc = 0.f;
-  for (int t0 = 0; t0 < nb; t0 += 64) {
-    const int t = t0 + lane;
-    if (t < nb) {
-      const float p = exp2f(pb[t] - m);
-      pb[t] = p;
-      lloc += p;
-    }
-  }
-  const float l = wave_sum(lloc);
-  wave_lds_fence();
-  float a0 = 0.f, a1 = 0.f;
-  for (int t = 0; t < nb; ++t) {
-    const float p = pb[t];
-    const T* vr = vring + (int64_t)t * kD + 2 * lane;
-    a0 = fmaf(p, (float)vr[0], a0);
-    a1 = fmaf(p, (float)vr[1], a1);
-  }
-  part[4 + 2 * lane] = a0;
-  part[4 + 2 * lane + 1] = a1;
-  if (lane == 0) {
-    part[0] = m;
-    part[1] = l;
   }
 }
 
@@ -489,6 +359,11 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
         g.n_splits = a.tab.nsplit[b] > g.n_splits ? a.tab.nsplit[b] : g.n_splits;
       }
     if (g.n == 0) continue;
+    if (decode_heads_per_wave(a.dtype, a.Hq, a.Hkv) > 1) {
+      e = launch_attn_gqa(a, g, kp8);
+      if (e != hipSuccess) return e;
+      continue;
+    }
     switch (kp8) {
 #define SWAN_KP8_CASE(n)                \
   case n:                               \

@@ -109,10 +109,14 @@ int64_t fill_layout(const swan_cache* c, const int32_t* k_active_host, swan::Seq
 // NULL); returns the largest.
 int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t* k_active_host,
                 int32_t* nsplit) {
+  // waves per sequence and split: one per query head, or one per GH query
+  // heads of a KV head on the GQA path
+  const int hpw = swan::decode_heads_per_wave(c->dtype, c->n_q_heads, c->n_kv_heads);
+  const int waves_per_seq = c->n_q_heads / hpw;
   int64_t total = 0;
   for (int b = 0; b < c->batch; ++b) {
     const int S = seq_len_host[b] > c->buffer_tokens ? seq_len_host[b] - c->buffer_tokens : 0;
-    total += (int64_t)swan::pages_for(S) * swan::kpad_of(k_active_host[b]) * c->n_q_heads;
+    total += (int64_t)swan::pages_for(S) * swan::kpad_of(k_active_host[b]) * waves_per_seq;
   }
   static const int64_t target_waves = [] {
     const char* s = getenv("SWAN_DECODE_WAVES");  // tuning override

@@ -62,6 +62,15 @@ struct SeqGroup {
   int32_t seq[SWAN_MAX_BATCH];
 };
 
+// GQA path (fp16 storage, G = n_q / n_kv > 1): query heads served by one wave,
+// 1 when the GQA kernel does not apply
+int gqa_heads_per_wave(int G);
+inline int decode_heads_per_wave(int dtype, int n_q, int n_kv) {
+  const int G = n_q / n_kv;
+  return (dtype == SWAN_F16 && G > 1) ? gqa_heads_per_wave(G) : 1;
+}
+hipError_t launch_attn_gqa(const DecodeLaunch& a, const SeqGroup& g, int kp8);
+
 
 struct CompressLaunch {
   const void* k_new;

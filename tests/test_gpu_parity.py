@@ -160,6 +160,10 @@ def _decode_check(swan_mod, torch_mod, device, cache, oc, Pqk, Pvo, tP_qk, tP_vo
     ("f16", 700, 0, 8, 4, 2), ("f16", 700, 128, 48, 4, 4), ("f16", 2049, 128, 64, 8, 2),
     ("f16", 1000, 16, 128, 2, 2), ("f16", 513, 5, 3, 2, 1), ("f32", 512, 16, 64, 1, 1),
     ("f32", 900, 32, 96, 4, 1),
+    # GQA groups of 8 and 16 (MFMA value path, 8 heads per wave) and of 3
+    # (one wave per query head), fp32 GQA (one wave per query head)
+    ("f16", 1500, 64, 48, 16, 2), ("f16", 900, 32, 32, 32, 2), ("f16", 600, 16, 24, 6, 2),
+    ("f32", 700, 16, 40, 8, 2), ("f16", 64, 0, 96, 8, 2),
 ])
 def test_decode_matches_oracle(gpu_device, swan_mod, torch_mod, dtype, L, b, k, Hq, Hkv):
     _log(f"decode dtype={dtype} L={L} b={b} k={k} Hq={Hq} Hkv={Hkv}")
