@@ -4,7 +4,7 @@
 //
 // Per 64-token page (one token per lane):
 //   scores      s_h = q_hat_h . k for the GH heads: one vector gather of the
-//               GH rotated queries per kept component (q_rep[dim][4][GH])
+//               GH rotated queries per kept component (q_rep[dim][8][GH])
 //   softmax     lazy reference per head (as in the MHA kernel), p_h written
 //               to an LDS tile P[16][64] in fp16 as hi + lo parts
 //   values      the page's kept value components are scattered into a zeroed
@@ -22,8 +22,9 @@ namespace swan {
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-constexpr int kGRep = 4;         // replicas of the GH-head query rows
+constexpr int kGRep = 8;         // replicas of the GH-head query rows (lane % 8)
 constexpr int kVtStride = 68;    // halves per row of the value tile (64 + pad)
+constexpr int kPtStride = 68;    // halves per row of the probability tile (64 + pad)
 
 template <int GH>
 struct QVec;
@@ -59,7 +60,7 @@ __device__ __forceinline__ void gqa_page(const PageRegs<_Float16, KP8>& kr,
 #pragma unroll
   for (int h = 0; h < GH; ++h) s[h] = 0.f;
   if (valid) {
-    const float* ql = qrep + (lane & (kGRep - 1)) * GH;
+    const float* ql = qrep + (lane & (kGRep - 1)) * GH;  // replica lane % 8
 #pragma unroll
     for (int g = 0; g < KP8; ++g) {
 #pragma unroll
@@ -106,8 +107,8 @@ __device__ __forceinline__ void gqa_page(const PageRegs<_Float16, KP8>& kr,
     const float p = valid ? exp2f(s[h] - st.m[h]) : 0.f;
     st.l[h] += p;
     const _Float16 hi = (_Float16)p;
-    pt[h * 64 + lane] = hi;
-    pt[16 * 64 + h * 64 + lane] = (_Float16)(p - (float)hi);
+    pt[h * kPtStride + lane] = hi;
+    pt[16 * kPtStride + h * kPtStride + lane] = (_Float16)(p - (float)hi);
   }
   // ---- dense value tile: zero, then scatter this page's kept components ----
   {
@@ -135,8 +136,8 @@ __device__ __forceinline__ void gqa_page(const PageRegs<_Float16, KP8>& kr,
   const int kq = 4 * (lane >> 4);
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
-    const h4 ahi = *(const h4*)(pt + row * 64 + 16 * ks + kq);
-    const h4 alo = *(const h4*)(pt + 16 * 64 + row * 64 + 16 * ks + kq);
+    const h4 ahi = *(const h4*)(pt + row * kPtStride + 16 * ks + kq);
+    const h4 alo = *(const h4*)(pt + 16 * kPtStride + row * kPtStride + 16 * ks + kq);
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt) {
       const h4 b = *(const h4*)(vt + (16 * nt + row) * kVtStride + 16 * ks + kq);
@@ -152,7 +153,7 @@ template <int KP8, int GH>
 __global__ __launch_bounds__(64) void attn_gqa_kernel(DecodeLaunch a, SeqGroup g) {
   __shared__ __attribute__((aligned(16))) float qrep[kD * kGRep * GH];
   __shared__ __attribute__((aligned(16))) _Float16 vt[kD * kVtStride];
-  __shared__ __attribute__((aligned(16))) _Float16 pt[2 * 16 * 64];
+  __shared__ __attribute__((aligned(16))) _Float16 pt[2 * 16 * kPtStride];
   const int lane = threadIdx.x;
   const int G = a.Hq / a.Hkv;
   const int pstride = a.n_splits + 1;
@@ -211,7 +212,7 @@ __global__ __launch_bounds__(64) void attn_gqa_kernel(DecodeLaunch a, SeqGroup g
   {
     u32x4* z = (u32x4*)pt;
 #pragma unroll
-    for (int c = lane; c < 2 * 16 * 64 * 2 / 16; c += 64) z[c] = u32x4{0u, 0u, 0u, 0u};
+    for (int c = lane; c < 2 * 16 * kPtStride * 2 / 16; c += 64) z[c] = u32x4{0u, 0u, 0u, 0u};
   }
   wave_lds_fence();
 
