@@ -191,6 +191,7 @@ static hipError_t launch_compress_t(const CompressLaunch& a) {
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  if (a.n_new >= kPrefillMinTokens && a.dtype == SWAN_F16) return launch_prefill(a);
   if (a.n_new > 0) {
     const int ngroups = (a.n_new + kTPW - 1) / kTPW;
     hipLaunchKernelGGL(insert_kernel<T>, dim3((int64_t)units * ngroups), dim3(64), 0, a.stream,

@@ -1,0 +1,225 @@
+// Compress-append of many tokens at once (prefill), fp16 storage.
+//
+// Same result as token-by-token Algorithm 1 (and as insert_kernel): each new
+// key/value is rotated exactly (float64 products and sums) and rounded once
+// to fp16; tokens that stay in the buffer go to their ring slot, the others
+// are pruned to their top-k magnitudes (ties: lower index) and packed.
+//
+// One wave handles 64-position blocks of one (sequence, kv head, role):
+//   rotation   on MFMA in float64 (v_mfma_f64_16x16x4f64): 16 tokens x 128
+//              output dims per pass, the contraction dim permuted so that a
+//              lane reads 32 contiguous input values of its token row; the
+//              lane's B operands (its 4 x 32 entries of P for one half of the
+//              output dims) are held in registers across the 4 passes
+//   selection  one token per lane on its 128 stored values: a 15-step binary
+//              search for the k-th largest magnitude, counting with packed
+//              16-bit adds, then one in-order pass that emits the kept pairs
+//              (and the padding) into an LDS copy of the page
+//   output     each lane stores its own 16-byte slot chunks of the page (a
+//              wave store is 1 KiB contiguous), or its dense row to the ring
+#include "swan_device.h"
+#include "swan_internal.h"
+
+namespace swan {
+
+typedef double d4 __attribute__((ext_vector_type(4)));
+typedef unsigned short us2 __attribute__((ext_vector_type(2)));
+
+constexpr int kRowHalves = 136;            // LDS row of one token's 128 fp16 values (+ pad)
+constexpr int kPrefillBlocksPerWave = 4;   // 64-position blocks per wave
+constexpr int kStageBytes = 64 * 128 * 3;  // LDS page copy, k_pad <= 128
+
+// count of the 128 fp16 values (64 packed dwords) whose magnitude bits are
+// >= cand, with packed 16-bit adds: (|x| + 0x8000 - cand) has bit 15 set
+// exactly when |x| >= cand
+__device__ __forceinline__ int count_ge(const uint32_t* v, uint32_t cand) {
+  const uint32_t c = 0x8000u - cand;  // cand <= 0x8000: no 16-bit overflow
+  const us2 add = {(unsigned short)c, (unsigned short)c};
+  us2 cnt = {0, 0};
+#pragma unroll
+  for (int w = 0; w < 64; ++w) {
+    const us2 m = __builtin_bit_cast(us2, v[w] & 0x7FFF7FFFu);
+    cnt += (m + add) >> (unsigned short)15;
+  }
+  return (int)cnt.x + (int)cnt.y;
+}
+
+__global__ __launch_bounds__(64) void prefill_kernel(CompressLaunch a) {
+  __shared__ __attribute__((aligned(16))) char lds[kStageBytes];
+  _Float16* rows = (_Float16*)lds;  // [64 tokens][kRowHalves], then reused as the page copy
+  const int lane = threadIdx.x;
+  const int q = lane >> 4, r16 = lane & 15;
+  // grid: (b, h, role, block group)
+  int w = blockIdx.x;
+  const int ngrp = a.prefill_groups;
+  const int grp = w % ngrp;
+  w /= ngrp;
+  const int role = w & 1;
+  w >>= 1;
+  const int h = w % a.Hkv;
+  const int b = w / a.Hkv;
+  const int len_old = a.tab.len[b];
+  const int nnew = a.tab.nnew[b];
+  if (nnew <= 0) return;
+  const int len_new = len_old + nnew;
+  const int blk0 = len_old / kPage;
+  const int blk1 = (len_new - 1) / kPage;  // inclusive
+  const int bbeg = blk0 + grp * kPrefillBlocksPerWave;
+  if (bbeg > blk1) return;
+  const int bend = min(bbeg + kPrefillBlocksPerWave, blk1 + 1);
+
+  const _Float16* x = (const _Float16*)(role ? a.v_new : a.k_new) +
+                      ((int64_t)b * a.Hkv + h) * a.n_new * kD;
+  const float* P = (role ? a.P_vo : a.P_qk) + (int64_t)h * kD * kD;
+
+  const int k = a.tab.kact[b];
+  const int kp = kpad_of(k);
+  const int64_t pbytes = page_bytes_of(2, k);
+  char* pages = (char*)(role ? a.v_pages : a.k_pages) + a.tab.page_off[b] +
+                (int64_t)h * a.n_pages_cap * pbytes;
+  uint16_t* ring = (uint16_t*)(role ? a.v_ring : a.k_ring) + ((int64_t)b * a.Hkv + h) * a.bb * kD;
+
+  for (int blk = bbeg; blk < bend; ++blk) {
+    const int pos0 = blk * kPage;
+    // ---- rotation: two halves of the output dims x 4 passes of 16 tokens,
+    //      results rounded to fp16 into LDS rows ----
+#pragma unroll 1
+    for (int nh = 0; nh < 2; ++nh) {
+      // B operands of this half: pb[nt][ks] = P[32 q + ks][64 nh + 16 nt + r16]
+      float pb[4][32];
+#pragma unroll
+      for (int ks = 0; ks < 32; ++ks)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+          pb[nt][ks] = P[(32 * q + ks) * kD + 64 * nh + 16 * nt + r16];
+#pragma unroll 1
+      for (int mt = 0; mt < 4; ++mt) {
+        const int tp0 = pos0 + 16 * mt - len_old;  // token index of the pass's first row
+        if (tp0 + 15 < 0 || tp0 >= nnew) continue;  // no new token in this pass (uniform)
+        // A operands: lane (q, r16) holds x[token 16 mt + r16][32 q .. 32 q + 31]
+        u32x4 xv[4];
+        {
+          const int t = tp0 + r16;
+          if (t >= 0 && t < nnew) {
+            const u32x4* src = (const u32x4*)(x + (int64_t)t * kD + 32 * q);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) xv[c] = src[c];
+          } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) xv[c] = u32x4{0u, 0u, 0u, 0u};
+          }
+        }
+        d4 acc[4];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) acc[nt] = d4{0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int ks = 0; ks < 32; ++ks) {
+          const uint32_t wv = xv[ks >> 3][(ks >> 1) & 3];
+          const double av = (double)f16_bits_to_f32((ks & 1) ? (wv >> 16) : (wv & 0xFFFFu));
+#pragma unroll
+          for (int nt = 0; nt < 4; ++nt)
+            acc[nt] =
+                __builtin_amdgcn_mfma_f64_16x16x4f64(av, (double)pb[nt][ks], acc[nt], 0, 0, 0);
+        }
+        // f64 MFMA result layout: register v of lane l holds D[l / 16 + 4 v][l % 16],
+        // i.e. token row q + 4 v of the pass, output dim 64 nh + 16 nt + r16
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const uint16_t hb = f64_to_f16_bits_fast(acc[nt][v]);
+            ((uint16_t*)rows)[(16 * mt + q + 4 * v) * kRowHalves + 64 * nh + 16 * nt + r16] = hb;
+          }
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+
+    // ---- one token per lane ----
+    const int pos = pos0 + lane;
+    const int t = pos - len_old;
+    const bool mine = t >= 0 && t < nnew;
+    const bool dense = pos >= len_new - a.bb;
+    uint32_t v[64];
+    if (mine) {
+      const u32x4* rp = (const u32x4*)(rows + lane * kRowHalves);
+#pragma unroll
+      for (int c = 0; c < 16; ++c) {
+        const u32x4 c4 = rp[c];
+        v[4 * c] = c4.x;
+        v[4 * c + 1] = c4.y;
+        v[4 * c + 2] = c4.z;
+        v[4 * c + 3] = c4.w;
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    if (mine && dense) {  // stays in the buffer: ring slot pos % b
+      u32x4* dst = (u32x4*)(ring + (int64_t)(pos % a.bb) * kD);
+#pragma unroll
+      for (int c = 0; c < 16; ++c) dst[c] = u32x4{v[4 * c], v[4 * c + 1], v[4 * c + 2], v[4 * c + 3]};
+    }
+    const bool sparse = mine && !dense;
+    if (sparse) {
+      // k-th largest magnitude
+      uint32_t tau = 0;
+#pragma unroll 1
+      for (int bit = 14; bit >= 0; --bit) {
+        const uint32_t cand = tau | (1u << bit);
+        if (count_ge(v, cand) >= k) tau = cand;
+      }
+      const int need_eq = k - count_ge(v, tau + 1);  // ties at tau taken lowest dim first
+      const int npad = kp - k;
+      // page copy in LDS: values [kp/8][64][16 B], indices [kp/8][64][8 B]
+      uint16_t* sv = (uint16_t*)lds + lane * 8;
+      uint8_t* si = (uint8_t*)lds + 64 * kp * 2 + lane * 8;
+      int e = 0, eq = 0, pad = 0;
+#pragma unroll
+      for (int j = 0; j < kD; ++j) {
+        const uint32_t hb = (v[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu;
+        const uint32_t m = hb & 0x7FFFu;
+        const bool tie = m == tau;
+        const bool sel = m > tau || (tie && eq < need_eq);
+        eq += tie ? 1 : 0;
+        if (sel) {
+          sv[(e >> 3) * 512 + (e & 7)] = (uint16_t)hb;
+          si[(e >> 3) * 512 + (e & 7)] = (uint8_t)j;
+          ++e;
+        } else if (pad < npad) {
+          const int ep = k + pad;
+          sv[(ep >> 3) * 512 + (ep & 7)] = 0;
+          si[(ep >> 3) * 512 + (ep & 7)] = (uint8_t)j;
+          ++pad;
+        }
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    if (sparse) {  // this lane's slot chunks of the page
+      char* page = pages + (int64_t)blk * pbytes;
+      const int nch = kp >> 3;
+      for (int c = 0; c < nch; ++c) {
+        *(u32x4*)(page + c * 1024 + lane * 16) = *(const u32x4*)(lds + c * 1024 + lane * 16);
+        *(u32x2*)(page + 64 * kp * 2 + c * 512 + lane * 8) =
+            *(const u32x2*)(lds + 64 * kp * 2 + c * 512 + lane * 8);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+int prefill_groups(int max_new_tokens, int min_len_old) {
+  (void)min_len_old;
+  const int max_blocks = (max_new_tokens + kPage - 1) / kPage + 1;
+  return (max_blocks + kPrefillBlocksPerWave - 1) / kPrefillBlocksPerWave;
+}
+
+hipError_t launch_prefill(const CompressLaunch& a) {
+  const int units = a.B * a.Hkv * 2;
+  hipLaunchKernelGGL(prefill_kernel, dim3((int64_t)units * a.prefill_groups), dim3(64), 0,
+                     a.stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace swan

@@ -240,6 +240,8 @@ swan_status swan_compress_append(const swan_cache* c, const int32_t* seq_len_hos
   if (!P_qk || !P_vo) return fail(SWAN_ERR_INVALID_ARG, "P_qk / P_vo is NULL");
   if ((((uintptr_t)P_qk | (uintptr_t)P_vo) & 15) != 0)
     return fail(SWAN_ERR_INVALID_ARG, "P_qk / P_vo must be 16-byte aligned");
+  if ((((uintptr_t)k_new | (uintptr_t)v_new) & 15) != 0)
+    return fail(SWAN_ERR_INVALID_ARG, "k_new / v_new must be 16-byte aligned");
   int max_evict = 0, any_new = 0;
   for (int b = 0; b < c->batch; ++b) {
     const int64_t L0 = seq_len_host[b];
@@ -278,6 +280,7 @@ swan_status swan_compress_append(const swan_cache* c, const int32_t* seq_len_hos
   a.n_pages_cap = swan::pages_for(c->sparse_capacity);
   a.n_new = n_new;
   a.max_evict = max_evict;
+  a.prefill_groups = swan::prefill_groups(n_new, 0);
   a.dtype = c->dtype;
   a.stream = (hipStream_t)stream;
   if (!any_new) return ok();

@@ -42,6 +42,28 @@ __device__ __forceinline__ uint16_t f64_to_f16_bits(double x) {
   return (uint16_t)(sign | h);
 }
 
+// float64 -> binary16 with one correct rounding, through float32: the value
+// is first rounded to float32 with round-to-odd (truncate, then set the last
+// bit if anything was cut off), which keeps enough information that the final
+// hardware float32 -> binary16 round-to-nearest-even equals rounding the
+// float64 value directly (float32 has 24 >= 11 + 2 significand bits).
+__device__ __forceinline__ uint16_t f64_to_f16_bits_fast(double x) {
+  // far below half the smallest binary16 subnormal: signed zero (also keeps
+  // float32 denormals, which the hardware may flush, out of the path)
+  if (fabs(x) < 0x1p-30) return (uint16_t)((__double_as_longlong(x) >> 48) & 0x8000);
+  float y = (float)x;  // round to nearest even
+  const double yd = (double)y;
+  if (yd != x && !(x != x)) {
+    uint32_t yb = __float_as_uint(y);
+    // rounded away from zero: step back toward zero (same sign) to truncate
+    if (fabs(yd) > fabs(x)) yb -= 1u;
+    yb |= 1u;  // sticky bit: inexact
+    y = __uint_as_float(yb);
+  }
+  const _Float16 hv = (_Float16)y;
+  return __builtin_bit_cast(uint16_t, hv);
+}
+
 __device__ __forceinline__ float f16_bits_to_f32(uint32_t h) {
   _Float16 v = __builtin_bit_cast(_Float16, (uint16_t)h);
   return (float)v;

@@ -83,11 +83,16 @@ struct CompressLaunch {
   void* v_ring;
   int B, Hkv, bb, n_pages_cap, n_new;  // n_new: token stride of k_new / v_new
   int max_evict;  // largest per-sequence eviction count
+  int prefill_groups;  // waves per (sequence, head, role) of the prefill kernel
   int dtype;
   SeqTab tab;     // len = tokens cached before the call
   hipStream_t stream;
 };
 hipError_t launch_compress(const CompressLaunch& a);
+// prefill path (fp16, many tokens): float64 MFMA rotation + lane-per-token top-k
+constexpr int kPrefillMinTokens = 64;
+int prefill_groups(int max_new_tokens, int min_len_old);
+hipError_t launch_prefill(const CompressLaunch& a);
 
 struct CalibLaunch {
   const float* rows;
