@@ -24,7 +24,9 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic_{wl}.txt")
-ATTN_SOURCE = os.path.join(ROOT, "paper_2511_18936_amd", "csrc", "decode.hip")
+# sources of the decode attention kernels: counter summaries are valid only for these bytes
+ATTN_SOURCES = ("decode.hip", "decode_gqa.hip", "decode_common.h", "swan_device.h",
+                "swan_internal.h")
 
 
 def log(*a):
@@ -47,15 +49,15 @@ def parse_args():
 
 def source_digest() -> str:
     h = hashlib.sha256()
-    for name in ("decode.hip", "swan_device.h", "swan_internal.h"):
+    for name in ATTN_SOURCES:
         with open(os.path.join(ROOT, "paper_2511_18936_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
 def read_traffic(wl: str, digest: str):
-    """HBM bytes per attention launch from the committed counter summary, if it was
-    taken on the current kernel source (else None)."""
+    """HBM bytes of one step's attention launches from the committed counter summary,
+    if it was taken on the current kernel source (else None)."""
     path = TRAFFIC_FILE.format(wl=wl)
     if not os.path.exists(path):
         return None
@@ -68,7 +70,7 @@ def read_traffic(wl: str, digest: str):
     if vals.get("source_digest") != digest:
         return None
     try:
-        return float(vals["hbm_bytes_per_launch"])
+        return float(vals["hbm_bytes_per_step"])
     except (KeyError, ValueError):
         return None
 
@@ -84,6 +86,16 @@ def attention_bytes(w, seq_len, k_active, esize):
         per_head = S * 2 * k_active[b] * (esize + 1) + 2 * nb * w.head_dim * esize
         total += w.n_kv_heads * per_head
     return total
+
+
+def attn_kernel_name(w) -> str:
+    """The decode attention kernel the library launches for this shape (one launch per
+    distinct padded k in the batch)."""
+    g = w.n_q_heads // w.n_kv_heads
+    if w.dtype == "f16" and g > 1 and g % 2 == 0:
+        hpw = 8 if g % 8 == 0 else 4 if g % 4 == 0 else 2
+        return f"attn_gqa_kernel ({hpw} query heads per wave, sparse split-K + dense buffer)"
+    return "attn_kernel (one query head per wave, sparse split-K + dense buffer)"
 
 
 def cpu_model() -> str:
@@ -316,7 +328,10 @@ def main():
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
             "traffic": traffic,
-            "kernel": "attn_kernel (sparse split-K + dense buffer partials)",
+            "kernel": attn_kernel_name(w),
+            # one launch per distinct padded k in the batch; bytes and time cover all of
+            # a step's attention launches together
+            "launches_per_step": len({(k + 7) // 8 for k in ks}),
             "algorithmic_bytes_per_launch": bytes_avg,
             "avg_launch_ms": attn_avg * 1e3,
             "source_digest": digest,
