@@ -18,6 +18,8 @@
 // first page's maximum and is only raised (with a rescale of acc) when a page
 // maximum exceeds it by more than kTau in log2 units, so exponentials stay
 // bounded by 2^kTau while rescales are rare.
+#include <mutex>
+
 #include "decode_common.h"
 
 namespace swan {
@@ -337,6 +339,50 @@ static hipError_t launch_attn(const DecodeLaunch& a, const SeqGroup& g) {
 }
 
 template <typename T>
+static hipError_t launch_group(const DecodeLaunch& a, const SeqGroup& g, int kp8) {
+  if (decode_heads_per_wave(a.dtype, a.Hq, a.Hkv) > 1) return launch_attn_gqa(a, g, kp8);
+  switch (kp8) {
+#define SWAN_KP8_CASE(n) \
+  case n:                \
+    return launch_attn<T, n>(a, g);
+    SWAN_KP8_CASE(1) SWAN_KP8_CASE(2) SWAN_KP8_CASE(3) SWAN_KP8_CASE(4)
+    SWAN_KP8_CASE(5) SWAN_KP8_CASE(6) SWAN_KP8_CASE(7) SWAN_KP8_CASE(8)
+    SWAN_KP8_CASE(9) SWAN_KP8_CASE(10) SWAN_KP8_CASE(11) SWAN_KP8_CASE(12)
+    SWAN_KP8_CASE(13) SWAN_KP8_CASE(14) SWAN_KP8_CASE(15) SWAN_KP8_CASE(16)
+#undef SWAN_KP8_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+// Side streams of one device for the attention launches of a batch that mixes
+// page formats: the launches are independent (disjoint sequences), so running
+// them side by side overlaps each one's ramp-up and tail.  Default priority.
+struct SideStreams {
+  std::mutex mu;  // one fork/join at a time: the events are shared
+  bool tried = false, ok = false;
+  hipStream_t s[kSideStreams];
+  hipEvent_t fork, join[kSideStreams];
+};
+
+static SideStreams* side_streams() {
+  static SideStreams per_device[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  SideStreams* ss = &per_device[dev];
+  std::lock_guard<std::mutex> lk(ss->mu);
+  if (!ss->tried) {
+    ss->tried = true;
+    bool ok = hipEventCreateWithFlags(&ss->fork, hipEventDisableTiming) == hipSuccess;
+    for (int i = 0; ok && i < kSideStreams; ++i)
+      ok = hipStreamCreateWithFlags(&ss->s[i], hipStreamNonBlocking) == hipSuccess &&
+           hipEventCreateWithFlags(&ss->join[i], hipEventDisableTiming) == hipSuccess;
+    ss->ok = ok;
+  }
+  return ss->ok ? ss : nullptr;
+}
+
+template <typename T>
 static hipError_t launch_decode_t(const DecodeLaunch& a) {
   const int BH = a.B * a.Hq;
   hipLaunchKernelGGL(qrot_kernel<T>, dim3(BH), dim3(128), 0, a.stream, (const T*)a.q, a.P_qk,
@@ -348,9 +394,12 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
     if (e != hipSuccess) return e;
   }
   // sequences grouped by k_pad: one launch per group, each specialised on its
-  // exact k_pad (launches of one call run back to back on the stream)
+  // exact k_pad
+  SeqGroup groups[kD / 8];
+  int kp8s[kD / 8];
+  int ng = 0;
   for (int kp8 = kD / 8; kp8 >= 1; --kp8) {
-    SeqGroup g;
+    SeqGroup& g = groups[ng];
     g.n = 0;
     g.n_splits = 0;
     for (int b = 0; b < a.B; ++b)
@@ -358,26 +407,28 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
         g.seq[g.n++] = b;
         g.n_splits = a.tab.nsplit[b] > g.n_splits ? a.tab.nsplit[b] : g.n_splits;
       }
-    if (g.n == 0) continue;
-    if (decode_heads_per_wave(a.dtype, a.Hq, a.Hkv) > 1) {
-      e = launch_attn_gqa(a, g, kp8);
-      if (e != hipSuccess) return e;
-      continue;
+    if (g.n > 0) kp8s[ng++] = kp8;
+  }
+  SideStreams* ss = ng > 1 ? side_streams() : nullptr;
+  if (!ss) {  // one launch, or no side streams: back to back on the caller's stream
+    for (int i = 0; i < ng; ++i)
+      if ((e = launch_group<T>(a, groups[i], kp8s[i])) != hipSuccess) return e;
+  } else {
+    std::lock_guard<std::mutex> lk(ss->mu);
+    const int nside = ng - 1 < kSideStreams ? ng - 1 : kSideStreams;
+    if ((e = hipEventRecord(ss->fork, a.stream)) != hipSuccess) return e;
+    for (int j = 0; j < nside; ++j)
+      if ((e = hipStreamWaitEvent(ss->s[j], ss->fork, 0)) != hipSuccess) return e;
+    for (int i = 0; i < ng; ++i) {
+      DecodeLaunch ai = a;
+      const int lane = i % (nside + 1);  // 0: the caller's stream
+      if (lane > 0) ai.stream = ss->s[lane - 1];
+      if ((e = launch_group<T>(ai, groups[i], kp8s[i])) != hipSuccess) return e;
     }
-    switch (kp8) {
-#define SWAN_KP8_CASE(n)                \
-  case n:                               \
-    e = launch_attn<T, n>(a, g);        \
-    break;
-      SWAN_KP8_CASE(1) SWAN_KP8_CASE(2) SWAN_KP8_CASE(3) SWAN_KP8_CASE(4)
-      SWAN_KP8_CASE(5) SWAN_KP8_CASE(6) SWAN_KP8_CASE(7) SWAN_KP8_CASE(8)
-      SWAN_KP8_CASE(9) SWAN_KP8_CASE(10) SWAN_KP8_CASE(11) SWAN_KP8_CASE(12)
-      SWAN_KP8_CASE(13) SWAN_KP8_CASE(14) SWAN_KP8_CASE(15) SWAN_KP8_CASE(16)
-#undef SWAN_KP8_CASE
-      default:
-        break;
+    for (int j = 0; j < nside; ++j) {
+      if ((e = hipEventRecord(ss->join[j], ss->s[j])) != hipSuccess) return e;
+      if ((e = hipStreamWaitEvent(a.stream, ss->join[j], 0)) != hipSuccess) return e;
     }
-    if (e != hipSuccess) return e;
   }
   if (a.prof_stop) {
     e = hipEventRecord(a.prof_stop, a.stream);

@@ -54,6 +54,8 @@ struct DecodeLaunch {
   hipEvent_t prof_stop;
 };
 hipError_t launch_decode(const DecodeLaunch& a);
+constexpr int kSideStreams = 3;  // extra streams for the launches of a mixed-k batch
+constexpr int kMaxDevices = 16;
 
 // sequences of one attention launch (those sharing a page format)
 struct SeqGroup {
