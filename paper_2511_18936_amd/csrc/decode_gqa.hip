@@ -1,20 +1,24 @@
 // Decode attention for grouped-query attention (GQA, G query heads per KV
-// head), fp16 storage: one wave streams a KV head's pages once for GH of its
-// query heads.
+// head), fp16 storage: one workgroup of two waves streams a KV head's pages
+// once for GH of its query heads.
 //
-// Per 64-token page (one token per lane):
-//   scores      s_h = q_hat_h . k for the GH heads: one vector gather of the
-//               GH rotated queries per kept component (q_rep[dim][8][GH])
-//   softmax     lazy reference per head (as in the MHA kernel), p_h written
-//               to an LDS tile P[16][64] in fp16 as hi + lo parts
-//   values      the page's kept value components are scattered into a zeroed
-//               dense tile V[128 dims][64 tokens] (fp16, exact), and
-//               O[16][128] += P[16][64] . V[64][128] runs on MFMA
+// Per 64-token page (one token per lane in each wave):
+//   score wave  holds the key pages: s_h = q_hat_h . k for the GH heads, one
+//               vector gather of the GH rotated queries per kept component
+//               (q_rep[dim][replica][GH]); lazy softmax reference per head (as
+//               in the MHA kernel); p_h goes to a double-buffered LDS tile
+//               P[GH][64] in fp16 as hi + lo parts, with the rescale factor of
+//               each head's accumulator row
+//   value wave  holds the value pages: scatters the page's kept components
+//               into a zeroed dense tile V[128 dims][64 tokens] (fp16, exact),
+//               then O[16][128] += P[16][64] . V[64][128] on MFMA
 //               (v_mfma_f32_16x16x16f16, fp32 accumulation, once for the hi
 //               and once for the lo part of P, so p keeps ~22 bits)
-// The accumulators stay in registers; rows >= GH of P are zero.  This is
-// the dense contraction of the value update, done once for all heads of the
-// group, instead of GH scatters into LDS accumulators.
+// The waves meet at one workgroup barrier per page: the value wave's MFMA of
+// page p overlaps the score wave's work on page p + 1.  The accumulators stay
+// in the value wave's registers; rows >= GH of the MFMA's A operand are zero.
+// This is the dense contraction of the value update, done once for all heads
+// of the group, instead of GH scatters into LDS accumulators.
 #include "decode_common.h"
 
 namespace swan {
@@ -22,9 +26,15 @@ namespace swan {
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-constexpr int kGRep = 8;         // replicas of the GH-head query rows (lane % 8)
 constexpr int kVtStride = 68;    // halves per row of the value tile (64 + pad)
 constexpr int kPtStride = 68;    // halves per row of the probability tile (64 + pad)
+
+// replicas of the GH-head query rows (lane % R): 8 keep the gathers of 8
+// consecutive lanes on distinct banks; 4 for GH = 8 to bound the LDS
+template <int GH>
+constexpr int qrep_replicas() {
+  return GH >= 8 ? 4 : 8;
+}
 
 template <int GH>
 struct QVec;
@@ -41,32 +51,32 @@ struct QVec<8> {
   typedef float type __attribute__((ext_vector_type(8)));
 };
 
-template <int KP8, int GH>
-struct GqaState {
-  float m[GH];   // reference maxima (log2 units), wave-uniform
-  float l[GH];   // per-lane sums of exp2(s - m)
-  f4 acc[8];     // O tile: n-tile nt, rows 4 * (lane / 16) + r, column 16 nt + lane % 16
-  bool first;
+template <int GH>
+struct GqaLds {
+  float qrep[kD * qrep_replicas<GH>() * GH];
+  _Float16 vt[kD * kVtStride];
+  _Float16 pt[2][2][GH][kPtStride];  // [page parity][hi, lo][head][token]
+  float fr[2][GH];                   // [page parity][head]: accumulator rescale
 };
 
+// score wave, one page: scores, softmax reference, P tile and rescale factors
 template <int KP8, int GH>
-__device__ __forceinline__ void gqa_page(const PageRegs<_Float16, KP8>& kr,
-                                         const PageRegs<_Float16, KP8>& vr, bool valid,
-                                         const float* qrep, _Float16* vt, _Float16* pt, int lane,
-                                         GqaState<KP8, GH>& st) {
+__device__ __forceinline__ void gqa_scores(const PageRegs<_Float16, KP8>& kr, bool valid,
+                                           GqaLds<GH>& sh, int par, int lane, float* m, float* l,
+                                           bool& first) {
   using QV = typename QVec<GH>::type;
-  // ---- scores for the GH heads ----
+  constexpr int R = qrep_replicas<GH>();
   float s[GH];
 #pragma unroll
   for (int h = 0; h < GH; ++h) s[h] = 0.f;
   if (valid) {
-    const float* ql = qrep + (lane & (kGRep - 1)) * GH;  // replica lane % 8
+    const float* ql = sh.qrep + (lane & (R - 1)) * GH;
 #pragma unroll
     for (int g = 0; g < KP8; ++g) {
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const float v = EntryVal<_Float16, KP8>::get(kr, g, u);
-        const QV q = *(const QV*)(ql + entry_idx(kr, g, u) * (kGRep * GH));
+        const QV q = *(const QV*)(ql + entry_idx(kr, g, u) * (R * GH));
 #pragma unroll
         for (int h = 0; h < GH; ++h) s[h] = fmaf(q[h], v, s[h]);
       }
@@ -75,51 +85,45 @@ __device__ __forceinline__ void gqa_page(const PageRegs<_Float16, KP8>& kr,
 #pragma unroll
     for (int h = 0; h < GH; ++h) s[h] = -INFINITY;
   }
-  // ---- lazy softmax reference per head ----
-  float fr[4] = {1.f, 1.f, 1.f, 1.f};  // rescale of this lane's accumulator rows
-  bool raised = false;
+  float frl = 1.f;  // lane h < GH: rescale factor of head h
 #pragma unroll
   for (int h = 0; h < GH; ++h) {
-    if (st.first) {
-      st.m[h] = wave_max(s[h]);
-    } else if (__ballot(s[h] > st.m[h] + kTau) != 0) {
+    if (first) {
+      m[h] = wave_max(s[h]);
+    } else if (__ballot(s[h] > m[h] + kTau) != 0) {
       const float pm = wave_max(s[h]);
-      const float f = exp2f(st.m[h] - pm);
-      st.l[h] *= f;
-      st.m[h] = pm;
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (4 * (lane >> 4) + r == h) fr[r] = f;
-      raised = true;
+      const float f = exp2f(m[h] - pm);
+      l[h] *= f;
+      m[h] = pm;
+      if (lane == h) frl = f;
     }
   }
-  st.first = false;
-  if (raised) {
-#pragma unroll
-    for (int nt = 0; nt < 8; ++nt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) st.acc[nt][r] *= fr[r];
-  }
-  // ---- probability tile P[h][token] = hi + lo ----
-  wave_lds_fence();  // the previous page's tile reads come first
+  first = false;
 #pragma unroll
   for (int h = 0; h < GH; ++h) {
-    const float p = valid ? exp2f(s[h] - st.m[h]) : 0.f;
-    st.l[h] += p;
+    const float p = valid ? exp2f(s[h] - m[h]) : 0.f;
+    l[h] += p;
     const _Float16 hi = (_Float16)p;
-    pt[h * kPtStride + lane] = hi;
-    pt[16 * kPtStride + h * kPtStride + lane] = (_Float16)(p - (float)hi);
+    sh.pt[par][0][h][lane] = hi;
+    sh.pt[par][1][h][lane] = (_Float16)(p - (float)hi);
   }
-  // ---- dense value tile: zero, then scatter this page's kept components ----
+  if (lane < GH) sh.fr[par][lane] = frl;
+}
+
+// value wave, one page: zero the value tile, scatter the kept components
+template <int KP8, int GH>
+__device__ __forceinline__ void gqa_scatter(const PageRegs<_Float16, KP8>& vr, bool valid,
+                                            GqaLds<GH>& sh, int lane) {
+  wave_lds_fence();  // the previous page's tile reads come first
   {
-    u32x4* z = (u32x4*)vt;
+    u32x4* z = (u32x4*)sh.vt;
     constexpr int kChunks = kD * kVtStride * 2 / 16;
 #pragma unroll
     for (int c = lane; c < kChunks; c += 64) z[c] = u32x4{0u, 0u, 0u, 0u};
   }
   wave_lds_fence();
   if (valid) {
-    uint16_t* vt16 = (uint16_t*)vt + lane;
+    uint16_t* vt16 = (uint16_t*)sh.vt + lane;
 #pragma unroll
     for (int g = 0; g < KP8; ++g) {
       const u32x4 c = vr.val[g];
@@ -130,36 +134,61 @@ __device__ __forceinline__ void gqa_page(const PageRegs<_Float16, KP8>& kr,
       }
     }
   }
-  wave_lds_fence();
-  // ---- O += P . V on MFMA (k-steps of 16 tokens, n-tiles of 16 dims) ----
+}
+
+// value wave, after the page barrier: rescale, then O += P . V on MFMA
+// (k-steps of 16 tokens, n-tiles of 16 dims)
+template <int GH>
+__device__ __forceinline__ void gqa_mfma(const GqaLds<GH>& sh, int par, int lane, f4* acc) {
   const int row = lane & 15;
   const int kq = 4 * (lane >> 4);
+  // accumulator rows 4 (lane / 16) + r hold head 4 (lane / 16) + r
+  float fr[4];
+  bool any = false;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int h = 4 * (lane >> 4) + r;
+    fr[r] = h < GH ? sh.fr[par][h < GH ? h : 0] : 1.f;
+  }
+#pragma unroll
+  for (int h = 0; h < GH; ++h) any |= sh.fr[par][h] != 1.f;
+  if (any) {
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[nt][r] *= fr[r];
+  }
+  const bool arow = row < GH;
+  const int rr = arow ? row : 0;
+  const h4 zero = {(_Float16)0.f, (_Float16)0.f, (_Float16)0.f, (_Float16)0.f};
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
-    const h4 ahi = *(const h4*)(pt + row * kPtStride + 16 * ks + kq);
-    const h4 alo = *(const h4*)(pt + 16 * kPtStride + row * kPtStride + 16 * ks + kq);
+    const h4 ahi = arow ? *(const h4*)&sh.pt[par][0][rr][16 * ks + kq] : zero;
+    const h4 alo = arow ? *(const h4*)&sh.pt[par][1][rr][16 * ks + kq] : zero;
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt) {
-      const h4 b = *(const h4*)(vt + (16 * nt + row) * kVtStride + 16 * ks + kq);
-      st.acc[nt] = __builtin_amdgcn_mfma_f32_16x16x16f16(ahi, b, st.acc[nt], 0, 0, 0);
-      st.acc[nt] = __builtin_amdgcn_mfma_f32_16x16x16f16(alo, b, st.acc[nt], 0, 0, 0);
+      const h4 b = *(const h4*)(sh.vt + (16 * nt + row) * kVtStride + 16 * ks + kq);
+      acc[nt] = __builtin_amdgcn_mfma_f32_16x16x16f16(ahi, b, acc[nt], 0, 0, 0);
+      acc[nt] = __builtin_amdgcn_mfma_f32_16x16x16f16(alo, b, acc[nt], 0, 0, 0);
     }
   }
 }
 
-// Grid: n * Hq dense-buffer waves (one per query head), then n * Hkv * (G /
-// GH) * g.n_splits sparse waves, each for GH query heads of one KV head.
+// Grid: n * Hq dense-buffer blocks (wave 0 serves one query head), then
+// n * Hkv * (G / GH) * g.n_splits sparse blocks, each for GH query heads of
+// one KV head.
 template <int KP8, int GH>
-__global__ __launch_bounds__(64) void attn_gqa_kernel(DecodeLaunch a, SeqGroup g) {
-  __shared__ __attribute__((aligned(16))) float qrep[kD * kGRep * GH];
-  __shared__ __attribute__((aligned(16))) _Float16 vt[kD * kVtStride];
-  __shared__ __attribute__((aligned(16))) _Float16 pt[2 * 16 * kPtStride];
-  const int lane = threadIdx.x;
+__global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup g) {
+  constexpr int R = qrep_replicas<GH>();
+  __shared__ __attribute__((aligned(16))) GqaLds<GH> sh;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // 0: scores, 1: values
+  const int lane = threadIdx.x & 63;
   const int G = a.Hq / a.Hkv;
   const int pstride = a.n_splits + 1;
   int w = blockIdx.x;
   const int NB = g.n * a.Hq;
-  if (w < NB) {  // dense-buffer wave, one query head (scratch: the value tile)
+  if (w < NB) {  // dense-buffer block: one wave (scratch: the value tile)
+    if (wave != 0) return;
     const int b = g.seq[w / a.Hq], hq = w % a.Hq, h = hq / G;
     const int bhq = b * a.Hq + hq;
     const int L = a.tab.len[b];
@@ -167,7 +196,7 @@ __global__ __launch_bounds__(64) void attn_gqa_kernel(DecodeLaunch a, SeqGroup g
     if (nb == 0) return;
     const int64_t ring_off = ((int64_t)b * a.Hkv + h) * a.bb * kD;
     float* part = a.part + ((int64_t)bhq * pstride + a.n_splits) * kPartFloats;
-    float* scratch = (float*)vt;  // 128 + up to 4096 floats (the tile holds 4352)
+    float* scratch = (float*)sh.vt;  // 128 + up to 4096 floats (the tile holds 4352)
     buffer_part<_Float16>((const _Float16*)a.k_ring + ring_off,
                           (const _Float16*)a.v_ring + ring_off, nb, a.qhat + (int64_t)bhq * kD,
                           scratch, scratch + kD, lane, part);
@@ -186,78 +215,92 @@ __global__ __launch_bounds__(64) void attn_gqa_kernel(DecodeLaunch a, SeqGroup g
   const int np = pages_for(S);
   const int nsb = a.tab.nsplit[b];
   const int ns = np < nsb ? np : nsb;
-  if (split >= ns) return;
+  if (split >= ns) return;  // uniform over the block
   const int pbeg = (int)((int64_t)split * np / ns);
   const int pend = (int)((int64_t)(split + 1) * np / ns);
   const int k = a.tab.kact[b];
   const int64_t pbytes = page_bytes_of(2, k);
   const int64_t unit_off = a.tab.page_off[b] + (int64_t)h * a.n_pages_cap * pbytes;
-  const char* kbase = (const char*)a.k_pages + unit_off;
-  const char* vbase = (const char*)a.v_pages + unit_off;
 
-  // q_rep[dim][r][head]: lane writes dims lane and lane + 64, all replicas
-  const float* qh = a.qhat + ((int64_t)b * a.Hq + hq0) * kD;
-#pragma unroll
-  for (int hh = 0; hh < 2; ++hh) {
-    const int d = lane + 64 * hh;
+  // q_rep[dim][r][head]: thread t writes dim t, all replicas
+  {
+    const int d = threadIdx.x;
+    const float* qh = a.qhat + ((int64_t)b * a.Hq + hq0) * kD;
     float q[GH];
 #pragma unroll
     for (int j = 0; j < GH; ++j) q[j] = qh[j * kD + d];
 #pragma unroll
-    for (int r = 0; r < kGRep; ++r)
+    for (int r = 0; r < R; ++r)
 #pragma unroll
-      for (int j = 0; j < GH; ++j) qrep[(d * kGRep + r) * GH + j] = q[j];
+      for (int j = 0; j < GH; ++j) sh.qrep[(d * R + r) * GH + j] = q[j];
   }
-  // P tile rows >= GH stay zero
-  {
-    u32x4* z = (u32x4*)pt;
-#pragma unroll
-    for (int c = lane; c < 2 * 16 * kPtStride * 2 / 16; c += 64) z[c] = u32x4{0u, 0u, 0u, 0u};
-  }
-  wave_lds_fence();
+  __syncthreads();
 
-  GqaState<KP8, GH> st;
-  st.first = true;
-#pragma unroll
-  for (int j = 0; j < GH; ++j) {
-    st.m[j] = 0.f;
-    st.l[j] = 0.f;
-  }
-#pragma unroll
-  for (int nt = 0; nt < 8; ++nt) st.acc[nt] = f4{0.f, 0.f, 0.f, 0.f};
-
-  PageRegs<_Float16, KP8> ka, va, kb, vb;
   const int plast = pend - 1;
-  load_page<_Float16, KP8>(ka, kbase + pbeg * pbytes, lane);
-  load_page<_Float16, KP8>(va, vbase + pbeg * pbytes, lane);
-  for (int p = pbeg; p < pend; p += 2) {
-    const int p1 = p + 1 < plast ? p + 1 : plast;
-    load_page<_Float16, KP8>(kb, kbase + p1 * pbytes, lane);
-    load_page<_Float16, KP8>(vb, vbase + p1 * pbytes, lane);
-    gqa_page<KP8, GH>(ka, va, p * kPage + lane < S, qrep, vt, pt, lane, st);
-    const int p2 = p + 2 < plast ? p + 2 : plast;
-    load_page<_Float16, KP8>(ka, kbase + p2 * pbytes, lane);
-    load_page<_Float16, KP8>(va, vbase + p2 * pbytes, lane);
-    if (p + 1 < pend) gqa_page<KP8, GH>(kb, vb, (p + 1) * kPage + lane < S, qrep, vt, pt, lane, st);
-  }
-
-  // partials: rows h < GH of the O tile, with each head's m and l
+  if (wave == 0) {
+    // ---- score wave ----
+    const char* kbase = (const char*)a.k_pages + unit_off;
+    float m[GH], l[GH];
+    bool first = true;
 #pragma unroll
-  for (int j = 0; j < GH; ++j) {
-    const float lt = wave_sum(st.l[j]);
-    if (lane == 0) {
-      float* part = a.part + (((int64_t)b * a.Hq + hq0 + j) * pstride + split) * kPartFloats;
-      part[0] = st.m[j];
-      part[1] = lt;
+    for (int j = 0; j < GH; ++j) {
+      m[j] = 0.f;
+      l[j] = 0.f;
     }
-  }
+    PageRegs<_Float16, KP8> ka, kb;
+    load_page<_Float16, KP8>(ka, kbase + pbeg * pbytes, lane);
+    for (int p = pbeg; p < pend; p += 2) {
+      const int p1 = p + 1 < plast ? p + 1 : plast;
+      load_page<_Float16, KP8>(kb, kbase + p1 * pbytes, lane);
+      gqa_scores<KP8, GH>(ka, p * kPage + lane < S, sh, (p - pbeg) & 1, lane, m, l, first);
+      __syncthreads();
+      const int p2 = p + 2 < plast ? p + 2 : plast;
+      load_page<_Float16, KP8>(ka, kbase + p2 * pbytes, lane);
+      if (p + 1 < pend) {
+        gqa_scores<KP8, GH>(kb, (p + 1) * kPage + lane < S, sh, (p + 1 - pbeg) & 1, lane, m, l,
+                            first);
+        __syncthreads();
+      }
+    }
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int hrow = 4 * (lane >> 4) + r;
-    if (hrow < GH) {
-      float* part = a.part + (((int64_t)b * a.Hq + hq0 + hrow) * pstride + split) * kPartFloats;
+    for (int j = 0; j < GH; ++j) {
+      const float lt = wave_sum(l[j]);
+      if (lane == 0) {
+        float* part = a.part + (((int64_t)b * a.Hq + hq0 + j) * pstride + split) * kPartFloats;
+        part[0] = m[j];
+        part[1] = lt;
+      }
+    }
+  } else {
+    // ---- value wave ----
+    const char* vbase = (const char*)a.v_pages + unit_off;
+    f4 acc[8];
 #pragma unroll
-      for (int nt = 0; nt < 8; ++nt) part[4 + 16 * nt + (lane & 15)] = st.acc[nt][r];
+    for (int nt = 0; nt < 8; ++nt) acc[nt] = f4{0.f, 0.f, 0.f, 0.f};
+    PageRegs<_Float16, KP8> va, vb;
+    load_page<_Float16, KP8>(va, vbase + pbeg * pbytes, lane);
+    for (int p = pbeg; p < pend; p += 2) {
+      const int p1 = p + 1 < plast ? p + 1 : plast;
+      load_page<_Float16, KP8>(vb, vbase + p1 * pbytes, lane);
+      gqa_scatter<KP8, GH>(va, p * kPage + lane < S, sh, lane);
+      __syncthreads();
+      gqa_mfma<GH>(sh, (p - pbeg) & 1, lane, acc);
+      const int p2 = p + 2 < plast ? p + 2 : plast;
+      load_page<_Float16, KP8>(va, vbase + p2 * pbytes, lane);
+      if (p + 1 < pend) {
+        gqa_scatter<KP8, GH>(vb, (p + 1) * kPage + lane < S, sh, lane);
+        __syncthreads();
+        gqa_mfma<GH>(sh, (p + 1 - pbeg) & 1, lane, acc);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int hrow = 4 * (lane >> 4) + r;
+      if (hrow < GH) {
+        float* part = a.part + (((int64_t)b * a.Hq + hq0 + hrow) * pstride + split) * kPartFloats;
+#pragma unroll
+        for (int nt = 0; nt < 8; ++nt) part[4 + 16 * nt + (lane & 15)] = acc[nt][r];
+      }
     }
   }
 }
@@ -266,7 +309,7 @@ template <int KP8, int GH>
 static hipError_t launch_gqa_k(const DecodeLaunch& a, const SeqGroup& g) {
   const int G = a.Hq / a.Hkv;
   const dim3 grid(g.n * a.Hq + g.n * a.Hkv * (G / GH) * g.n_splits);
-  hipLaunchKernelGGL((attn_gqa_kernel<KP8, GH>), grid, dim3(64), 0, a.stream, a, g);
+  hipLaunchKernelGGL((attn_gqa_kernel<KP8, GH>), grid, dim3(128), 0, a.stream, a, g);
   return hipGetLastError();
 }
 
