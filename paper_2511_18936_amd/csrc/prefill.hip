@@ -25,9 +25,11 @@ namespace swan {
 typedef double d4 __attribute__((ext_vector_type(4)));
 typedef unsigned short us2 __attribute__((ext_vector_type(2)));
 
-constexpr int kRowHalves = 136;            // LDS row of one token's 128 fp16 values (+ pad)
-constexpr int kPrefillBlocksPerWave = 4;   // 64-position blocks per wave
-constexpr int kStageBytes = 64 * 128 * 3;  // LDS page copy, k_pad <= 128
+constexpr int kRowHalves = 136;                // LDS row of one token's 128 fp16 values (+ pad)
+constexpr int kPrefillBlocksPerWave = 4;       // 64-position blocks per wave
+constexpr int kStageBytes = 64 * kRowHalves * 2;  // the rows, then the page copy
+// a page (64 * k_pad * 3 bytes) fits the copy up to k_pad 88; above, values and
+// indices are emitted and stored in two rounds
 
 // count of the 128 fp16 values (64 packed dwords) whose magnitude bits are
 // >= cand, with packed 16-bit adds: (|x| + 0x8000 - cand) has bit 15 set
@@ -44,7 +46,35 @@ __device__ __forceinline__ int count_ge(const uint32_t* v, uint32_t cand) {
   return (int)cnt.x + (int)cnt.y;
 }
 
-__global__ __launch_bounds__(64) void prefill_kernel(CompressLaunch a) {
+// One token per lane: its kept (value, index) pairs in ascending index
+// order, then the padding (value +0 at the lowest unselected dims), written
+// into the LDS page copy: values [kp/8][64][16 B] at sv, indices
+// [kp/8][64][8 B] at si.
+template <bool kVals, bool kIdx>
+__device__ __forceinline__ void emit_slots(const uint32_t* v, uint32_t tau, int need_eq, int k,
+                                           int npad, uint16_t* sv, uint8_t* si) {
+  int e = 0, eq = 0, pad = 0;
+#pragma unroll
+  for (int j = 0; j < kD; ++j) {
+    const uint32_t hb = (v[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu;
+    const uint32_t m = hb & 0x7FFFu;
+    const bool tie = m == tau;
+    const bool sel = m > tau || (tie && eq < need_eq);
+    eq += tie ? 1 : 0;
+    if (sel) {
+      if (kVals) sv[(e >> 3) * 512 + (e & 7)] = (uint16_t)hb;
+      if (kIdx) si[(e >> 3) * 512 + (e & 7)] = (uint8_t)j;
+      ++e;
+    } else if (pad < npad) {
+      const int ep = k + pad;
+      if (kVals) sv[(ep >> 3) * 512 + (ep & 7)] = 0;
+      if (kIdx) si[(ep >> 3) * 512 + (ep & 7)] = (uint8_t)j;
+      ++pad;
+    }
+  }
+}
+
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void prefill_kernel(CompressLaunch a) {
   __shared__ __attribute__((aligned(16))) char lds[kStageBytes];
   _Float16* rows = (_Float16*)lds;  // [64 tokens][kRowHalves], then reused as the page copy
   const int lane = threadIdx.x;
@@ -84,14 +114,14 @@ __global__ __launch_bounds__(64) void prefill_kernel(CompressLaunch a) {
     // ---- rotation: two halves of the output dims x 4 passes of 16 tokens,
     //      results rounded to fp16 into LDS rows ----
 #pragma unroll 1
-    for (int nh = 0; nh < 2; ++nh) {
-      // B operands of this half: pb[nt][ks] = P[32 q + ks][64 nh + 16 nt + r16]
-      float pb[4][32];
+    for (int nh = 0; nh < 4; ++nh) {
+      // B operands of this quarter: pb[nt][ks] = P[32 q + ks][32 nh + 16 nt + r16]
+      float pb[2][32];
 #pragma unroll
       for (int ks = 0; ks < 32; ++ks)
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt)
-          pb[nt][ks] = P[(32 * q + ks) * kD + 64 * nh + 16 * nt + r16];
+        for (int nt = 0; nt < 2; ++nt)
+          pb[nt][ks] = P[(32 * q + ks) * kD + 32 * nh + 16 * nt + r16];
 #pragma unroll 1
       for (int mt = 0; mt < 4; ++mt) {
         const int tp0 = pos0 + 16 * mt - len_old;  // token index of the pass's first row
@@ -109,26 +139,29 @@ __global__ __launch_bounds__(64) void prefill_kernel(CompressLaunch a) {
             for (int c = 0; c < 4; ++c) xv[c] = u32x4{0u, 0u, 0u, 0u};
           }
         }
-        d4 acc[4];
+        d4 acc[2];
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) acc[nt] = d4{0.0, 0.0, 0.0, 0.0};
+        for (int nt = 0; nt < 2; ++nt) acc[nt] = d4{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
         for (int ks = 0; ks < 32; ++ks) {
           const uint32_t wv = xv[ks >> 3][(ks >> 1) & 3];
           const double av = (double)f16_bits_to_f32((ks & 1) ? (wv >> 16) : (wv & 0xFFFFu));
 #pragma unroll
-          for (int nt = 0; nt < 4; ++nt)
-            acc[nt] =
-                __builtin_amdgcn_mfma_f64_16x16x4f64(av, (double)pb[nt][ks], acc[nt], 0, 0, 0);
+          for (int nt = 0; nt < 2; ++nt)
+          {
+            float pv = pb[nt][ks];
+            asm volatile("" : "+v"(pv));  // convert per pass: 128 doubles would not fit
+            acc[nt] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, (double)pv, acc[nt], 0, 0, 0);
+          }
         }
         // f64 MFMA result layout: register v of lane l holds D[l / 16 + 4 v][l % 16],
         // i.e. token row q + 4 v of the pass, output dim 64 nh + 16 nt + r16
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt)
+        for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             const uint16_t hb = f64_to_f16_bits_fast(acc[nt][v]);
-            ((uint16_t*)rows)[(16 * mt + q + 4 * v) * kRowHalves + 64 * nh + 16 * nt + r16] = hb;
+            ((uint16_t*)rows)[(16 * mt + q + 4 * v) * kRowHalves + 32 * nh + 16 * nt + r16] = hb;
           }
       }
     }
@@ -160,6 +193,9 @@ __global__ __launch_bounds__(64) void prefill_kernel(CompressLaunch a) {
       for (int c = 0; c < 16; ++c) dst[c] = u32x4{v[4 * c], v[4 * c + 1], v[4 * c + 2], v[4 * c + 3]};
     }
     const bool sparse = mine && !dense;
+    const bool two_rounds = 64 * kp * 3 > kStageBytes;  // uniform
+    uint32_t tau_keep = 0;
+    int need_keep = 0, npad = 0;
     if (sparse) {
       // k-th largest magnitude
       uint32_t tau = 0;
@@ -169,43 +205,42 @@ __global__ __launch_bounds__(64) void prefill_kernel(CompressLaunch a) {
         if (count_ge(v, cand) >= k) tau = cand;
       }
       const int need_eq = k - count_ge(v, tau + 1);  // ties at tau taken lowest dim first
-      const int npad = kp - k;
-      // page copy in LDS: values [kp/8][64][16 B], indices [kp/8][64][8 B]
-      uint16_t* sv = (uint16_t*)lds + lane * 8;
-      uint8_t* si = (uint8_t*)lds + 64 * kp * 2 + lane * 8;
-      int e = 0, eq = 0, pad = 0;
-#pragma unroll
-      for (int j = 0; j < kD; ++j) {
-        const uint32_t hb = (v[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu;
-        const uint32_t m = hb & 0x7FFFu;
-        const bool tie = m == tau;
-        const bool sel = m > tau || (tie && eq < need_eq);
-        eq += tie ? 1 : 0;
-        if (sel) {
-          sv[(e >> 3) * 512 + (e & 7)] = (uint16_t)hb;
-          si[(e >> 3) * 512 + (e & 7)] = (uint8_t)j;
-          ++e;
-        } else if (pad < npad) {
-          const int ep = k + pad;
-          sv[(ep >> 3) * 512 + (ep & 7)] = 0;
-          si[(ep >> 3) * 512 + (ep & 7)] = (uint8_t)j;
-          ++pad;
-        }
-      }
+      npad = kp - k;
+      if (!two_rounds)
+        emit_slots<true, true>(v, tau, need_eq, k, npad, (uint16_t*)lds + lane * 8,
+                               (uint8_t*)lds + 64 * kp * 2 + lane * 8);
+      else
+        emit_slots<true, false>(v, tau, need_eq, k, npad, (uint16_t*)lds + lane * 8, nullptr);
+      tau_keep = tau;
+      need_keep = need_eq;
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
+    char* page = pages + (int64_t)blk * pbytes;
+    const int nch = kp >> 3;
     if (sparse) {  // this lane's slot chunks of the page
-      char* page = pages + (int64_t)blk * pbytes;
-      const int nch = kp >> 3;
-      for (int c = 0; c < nch; ++c) {
+      for (int c = 0; c < nch; ++c)
         *(u32x4*)(page + c * 1024 + lane * 16) = *(const u32x4*)(lds + c * 1024 + lane * 16);
-        *(u32x2*)(page + 64 * kp * 2 + c * 512 + lane * 8) =
-            *(const u32x2*)(lds + 64 * kp * 2 + c * 512 + lane * 8);
-      }
+      if (!two_rounds)
+        for (int c = 0; c < nch; ++c)
+          *(u32x2*)(page + 64 * kp * 2 + c * 512 + lane * 8) =
+              *(const u32x2*)(lds + 64 * kp * 2 + c * 512 + lane * 8);
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
+    if (two_rounds) {  // indices: the same selection again, then their chunks
+      if (sparse)
+        emit_slots<false, true>(v, tau_keep, need_keep, k, npad, nullptr,
+                                (uint8_t*)lds + lane * 8);
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      if (sparse)
+        for (int c = 0; c < nch; ++c)
+          *(u32x2*)(page + 64 * kp * 2 + c * 512 + lane * 8) =
+              *(const u32x2*)(lds + c * 512 + lane * 8);
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+    }
   }
 }
 
