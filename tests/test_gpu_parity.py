@@ -96,7 +96,8 @@ def _build(swan_mod, torch_mod, device, *, B, Hq, Hkv, L, b, k_active, dtype, ch
     cache = swan_mod.SwanCache(B, Hq, Hkv, b, cap, k_active, C.torch_dtype(dtype), device)
     tP_qk = torch.tensor(Pqk, device=device)
     tP_vo = torch.tensor(Pvo, device=device)
-    # sequences of different lengths: append per sequence group by equal length
+    # sequences of different lengths: each chunk appends min(n, what is left)
+    # tokens per sequence
     if chunks is None:
         chunks = [Lmax]
     t0 = 0
@@ -104,10 +105,12 @@ def _build(swan_mod, torch_mod, device, *, B, Hq, Hkv, L, b, k_active, dtype, ch
         n = min(n, Lmax - t0)
         if n <= 0:
             break
+        per = [max(min(n, Lb - t0), 0) for Lb in Ls]
         kn = torch.tensor(K[:, :, t0:t0 + n], device=device)
         vn = torch.tensor(V[:, :, t0:t0 + n], device=device)
-        cache.append(kn, vn, tP_qk, tP_vo)
+        cache.append(kn, vn, tP_qk, tP_vo, n_new_per_seq=per)
         t0 += n
+    assert cache.seq_len == Ls
     torch.cuda.synchronize()
     oc = [[O.compress_block(K[bi, h, :Ls[bi]], V[bi, h, :Ls[bi]], Pqk[h], Pvo[h], b,
                             k_active[bi], np_dt) for h in range(Hkv)] for bi in range(B)]
@@ -118,6 +121,9 @@ def _build(swan_mod, torch_mod, device, *, B, Hq, Hkv, L, b, k_active, dtype, ch
     ("f16", 1, 0, 48), ("f16", 130, 0, 48), ("f16", 200, 16, 1), ("f16", 200, 16, 128),
     ("f16", 333, 64, 13), ("f16", 64, 64, 48), ("f16", 40, 64, 48),
     ("f32", 300, 16, 64), ("f32", 129, 3, 5),
+    # pages that fit the prefill kernel's LDS copy (k_pad 88) and those that
+    # take two rounds (k_pad 96)
+    ("f16", 300, 16, 88), ("f16", 300, 16, 81), ("f16", 300, 16, 89), ("f16", 129, 0, 96),
 ])
 def test_compress_prefill_bit_exact(gpu_device, swan_mod, torch_mod, dtype, L, b, k):
     _log(f"compress prefill dtype={dtype} L={L} b={b} k={k}")
@@ -207,6 +213,33 @@ def test_decode_ragged_lengths_and_per_sequence_k(gpu_device, swan_mod, torch_mo
     for bi in range(B):
         for h in range(Hkv):
             C.compare_unit(cache, oc[bi][h], bi, h, Ls[bi], np.float16)
+    _decode_check(swan_mod, torch_mod, gpu_device, cache, oc, Pqk, Pvo, tqk, tvo, "f16")
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(1, 1), (4, 2)])
+def test_decode_max_batch_many_k(gpu_device, swan_mod, torch_mod, Hq, Hkv):
+    """The largest batch, each sequence with its own length and k: up to 16
+    attention launches, spread over the library's side streams."""
+    B = 64
+    Ls = [1 + (37 * i) % 300 for i in range(B)]
+    ks = [1 + (7 * i) % 128 for i in range(B)]
+    _log(f"decode max batch B={B} Hq={Hq} Hkv={Hkv}, {len({(k + 7) // 8 for k in ks})} k groups")
+    cache, oc, Pqk, Pvo, tqk, tvo, *_ = _build(swan_mod, torch_mod, gpu_device, B=B, Hq=Hq,
+                                                Hkv=Hkv, L=Ls, b=16, k_active=ks, dtype="f16",
+                                                capacity=300)
+    for bi in range(0, B, 7):
+        C.compare_unit(cache, oc[bi][0], bi, 0, Ls[bi], np.float16)
+    _decode_check(swan_mod, torch_mod, gpu_device, cache, oc, Pqk, Pvo, tqk, tvo, "f16")
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(2, 2), (4, 2)])
+def test_decode_largest_buffer(gpu_device, swan_mod, torch_mod, Hq, Hkv):
+    """A dense buffer of 4096 tokens (the ring's maximum) next to sparse pages."""
+    _log(f"decode with b=4096, Hq={Hq} Hkv={Hkv}")
+    cache, oc, Pqk, Pvo, tqk, tvo, *_ = _build(swan_mod, torch_mod, gpu_device, B=1, Hq=Hq,
+                                                Hkv=Hkv, L=4500, b=4096, k_active=[48],
+                                                dtype="f16")
+    C.compare_unit(cache, oc[0][0], 0, 0, 4500, np.float16)
     _decode_check(swan_mod, torch_mod, gpu_device, cache, oc, Pqk, Pvo, tqk, tvo, "f16")
 
 
