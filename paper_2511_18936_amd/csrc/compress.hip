@@ -4,10 +4,11 @@
 // is read before a new token overwrites its slot:
 //   evict_kernel   one wave per ring vector that leaves the buffer: top-k of
 //                  its stored values, packed into its page slot
-//   insert_kernel  one wave per group of kTPW new tokens of one (sequence, kv
-//                  head, role): rotation x . P accumulated in float64 and rounded
-//                  once to the storage type; tokens still inside the buffer go to
-//                  their ring slot, the others are pruned and packed at once
+//   insert_kernel  one wave per group of TPW new tokens of one (sequence, kv
+//                  head, role) (TPW = 1 for a decode step, else 8): rotation
+//                  x . P accumulated in float64 and rounded once to the storage
+//                  type; tokens still inside the buffer go to their ring slot,
+//                  the others are pruned and packed at once
 //
 // Top-k (Sec. 4.3, ranking the stored values, ties to the lower index): each
 // lane holds dims 2l and 2l+1; the key (|x| bits << 8) | (255 - dim) is unique
@@ -19,7 +20,7 @@
 
 namespace swan {
 
-constexpr int kTPW = 8;  // new tokens per insert wave
+constexpr int kTPW = 8;  // new tokens per insert wave (several new tokens per sequence)
 
 // Write the top-k of a 128-vector (lane holds elements 2l, 2l+1) into page
 // slot `slot` of the page at `page`.
@@ -115,12 +116,12 @@ __global__ __launch_bounds__(64) void evict_kernel(CompressLaunch a) {
   select_and_pack<T>(x0, x1, k, page, p % kPage, lane);
 }
 
-template <typename T>
+template <typename T, int TPW>
 __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
   using St = Store<T>;
-  __shared__ __attribute__((aligned(16))) double xs[kD][kTPW];
+  __shared__ __attribute__((aligned(16))) double xs[kD][TPW];
   const int lane = threadIdx.x;
-  const int ngroups = (a.n_new + kTPW - 1) / kTPW;
+  const int ngroups = (a.n_new + TPW - 1) / TPW;
   int w = blockIdx.x;
   const int grp = w % ngroups;
   w /= ngroups;
@@ -128,13 +129,13 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
   w >>= 1;
   const int h = w % a.Hkv;
   const int b = w / a.Hkv;
-  const int t0 = grp * kTPW;
+  const int t0 = grp * TPW;
   const int nnew = a.tab.nnew[b];
   if (t0 >= nnew) return;
-  const int nt = (nnew - t0) < kTPW ? (nnew - t0) : kTPW;
+  const int nt = (nnew - t0) < TPW ? (nnew - t0) : TPW;
   const T* x = (const T*)(role ? a.v_new : a.k_new) +
                (((int64_t)b * a.Hkv + h) * a.n_new + t0) * kD;
-  for (int t = 0; t < kTPW; ++t) {
+  for (int t = 0; t < TPW; ++t) {
     double v0 = 0.0, v1 = 0.0;
     if (t < nt) {
       v0 = (double)(float)x[(int64_t)t * kD + 2 * lane];
@@ -145,15 +146,16 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
   }
   __syncthreads();
   const float2* P = (const float2*)((role ? a.P_vo : a.P_qk) + (int64_t)h * kD * kD) + lane;
-  double acc0[kTPW], acc1[kTPW];
+  double acc0[TPW], acc1[TPW];
 #pragma unroll
-  for (int t = 0; t < kTPW; ++t) acc0[t] = acc1[t] = 0.0;
-#pragma unroll 4
+  for (int t = 0; t < TPW; ++t) acc0[t] = acc1[t] = 0.0;
+  // 32 rows of P in flight per batch: the loads are the latency of this kernel
+#pragma unroll 32
   for (int i = 0; i < kD; ++i) {
     const float2 pr = P[i * (kD / 2)];
     const double p0 = (double)pr.x, p1 = (double)pr.y;
 #pragma unroll
-    for (int t = 0; t < kTPW; ++t) {
+    for (int t = 0; t < TPW; ++t) {
       const double xv = xs[i][t];
       acc0[t] = fma(xv, p0, acc0[t]);
       acc1[t] = fma(xv, p1, acc1[t]);
@@ -168,7 +170,7 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
   typename St::Bits* ring = (typename St::Bits*)(role ? a.v_ring : a.k_ring) +
                             ((int64_t)b * a.Hkv + h) * a.bb * kD;
 #pragma unroll
-  for (int t = 0; t < kTPW; ++t) {
+  for (int t = 0; t < TPW; ++t) {
     if (t >= nt) break;
     const typename St::Bits y0 = St::from_f64(acc0[t]);
     const typename St::Bits y1 = St::from_f64(acc1[t]);
@@ -193,9 +195,13 @@ static hipError_t launch_compress_t(const CompressLaunch& a) {
   }
   if (a.n_new >= kPrefillMinTokens && a.dtype == SWAN_F16) return launch_prefill(a);
   if (a.n_new > 0) {
-    const int ngroups = (a.n_new + kTPW - 1) / kTPW;
-    hipLaunchKernelGGL(insert_kernel<T>, dim3((int64_t)units * ngroups), dim3(64), 0, a.stream,
-                       a);
+    if (a.n_new == 1) {
+      hipLaunchKernelGGL((insert_kernel<T, 1>), dim3(units), dim3(64), 0, a.stream, a);
+    } else {
+      const int ngroups = (a.n_new + kTPW - 1) / kTPW;
+      hipLaunchKernelGGL((insert_kernel<T, kTPW>), dim3((int64_t)units * ngroups), dim3(64), 0,
+                         a.stream, a);
+    }
     return hipGetLastError();
   }
   return hipSuccess;

@@ -40,7 +40,7 @@ __global__ __launch_bounds__(128) void qrot_kernel(const T* __restrict__ q,
   __syncthreads();
   const float* P = Pqk + (int64_t)g * kD * kD;
   float acc = 0.f;
-#pragma unroll 8
+#pragma unroll 32
   for (int i = 0; i < kD; ++i) acc = fmaf(qs[i], P[i * kD + j], acc);
   qhat[(int64_t)bh * kD + j] = acc * mult;
 }
