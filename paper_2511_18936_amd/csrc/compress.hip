@@ -1,11 +1,15 @@
-// Compress-append (Algorithm 1, lines that project, append, evict and prune).
+// Compress-append (Algorithm 1, the steps that project, append, evict and
+// prune).
 //
-// Two launches on the caller's stream, so that every vector leaving the ring
-// is read before a new token overwrites its slot:
+// Several new tokens per sequence: two launches on the caller's stream, so
+// that every vector leaving the ring is read before a new token overwrites its
+// slot.  One new token (a decode step): one launch, insert_kernel<T, 1>, whose
+// wave evicts the slot's old vector before it writes the new one.
 //   evict_kernel   one wave per ring vector that leaves the buffer: top-k of
 //                  its stored values, packed into its page slot
 //   insert_kernel  one wave per group of TPW new tokens of one (sequence, kv
-//                  head, role) (TPW = 1 for a decode step, else 8): rotation
+//                  head, role) (TPW = 1 for a decode step, which also does
+//                  that step's eviction, else 8): rotation
 //                  x . P accumulated in float64 and rounded once to the storage
 //                  type; tokens still inside the buffer go to their ring slot,
 //                  the others are pruned and packed at once
@@ -169,6 +173,18 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
                 (int64_t)h * a.n_pages_cap * pbytes;
   typename St::Bits* ring = (typename St::Bits*)(role ? a.v_ring : a.k_ring) +
                             ((int64_t)b * a.Hkv + h) * a.bb * kD;
+  if constexpr (TPW == 1) {
+    // one new token: the vector that leaves the buffer (if any) sits in the
+    // ring slot the new token takes; prune and pack it first (each lane reads
+    // the two elements it overwrites below)
+    const int p0 = evict_begin(len_old, a.bb);
+    if (p0 < evict_end(len_old, nnew, a.bb)) {
+      const typename St::Bits* old = ring + (int64_t)(p0 % a.bb) * kD;
+      const typename St::Bits o0 = old[2 * lane];
+      const typename St::Bits o1 = old[2 * lane + 1];
+      select_and_pack<T>(o0, o1, k, pages + (int64_t)(p0 / kPage) * pbytes, p0 % kPage, lane);
+    }
+  }
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
     if (t >= nt) break;
@@ -188,6 +204,10 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
 template <typename T>
 static hipError_t launch_compress_t(const CompressLaunch& a) {
   const int units = a.B * a.Hkv * 2;
+  if (a.n_new == 1) {  // a decode step: eviction and insertion in one launch
+    hipLaunchKernelGGL((insert_kernel<T, 1>), dim3(units), dim3(64), 0, a.stream, a);
+    return hipGetLastError();
+  }
   if (a.max_evict > 0) {
     hipLaunchKernelGGL(evict_kernel<T>, dim3(units * a.max_evict), dim3(64), 0, a.stream, a);
     const hipError_t e = hipGetLastError();
@@ -195,13 +215,9 @@ static hipError_t launch_compress_t(const CompressLaunch& a) {
   }
   if (a.n_new >= kPrefillMinTokens && a.dtype == SWAN_F16) return launch_prefill(a);
   if (a.n_new > 0) {
-    if (a.n_new == 1) {
-      hipLaunchKernelGGL((insert_kernel<T, 1>), dim3(units), dim3(64), 0, a.stream, a);
-    } else {
-      const int ngroups = (a.n_new + kTPW - 1) / kTPW;
-      hipLaunchKernelGGL((insert_kernel<T, kTPW>), dim3((int64_t)units * ngroups), dim3(64), 0,
-                         a.stream, a);
-    }
+    const int ngroups = (a.n_new + kTPW - 1) / kTPW;
+    hipLaunchKernelGGL((insert_kernel<T, kTPW>), dim3((int64_t)units * ngroups), dim3(64), 0,
+                       a.stream, a);
     return hipGetLastError();
   }
   return hipSuccess;
