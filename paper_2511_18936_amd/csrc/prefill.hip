@@ -6,15 +6,16 @@
 // are pruned to their top-k magnitudes (ties: lower index) and packed.
 //
 // One wave handles 64-position blocks of one (sequence, kv head, role):
-//   rotation   on MFMA in float64 (v_mfma_f64_16x16x4f64): 16 tokens x 128
+//   rotation   on MFMA in float64 (v_mfma_f64_16x16x4f64): 16 tokens x 32
 //              output dims per pass, the contraction dim permuted so that a
 //              lane reads 32 contiguous input values of its token row; the
-//              lane's B operands (its 4 x 32 entries of P for one half of the
-//              output dims) are held in registers across the 4 passes
-//   selection  one token per lane on its 128 stored values: a 15-step binary
-//              search for the k-th largest magnitude, counting with packed
-//              16-bit adds, then one in-order pass that emits the kept pairs
-//              (and the padding) into an LDS copy of the page
+//              lane's B operands (its 2 x 32 entries of P for one quarter of
+//              the output dims) are held in registers across the block's 4
+//              passes of 16 tokens
+//   selection  one token per lane on its 128 stored values: a radix select
+//              on bit planes of the magnitudes finds the k-th largest, then
+//              one in-order pass emits the kept pairs (and the padding) into
+//              an LDS copy of the page
 //   output     each lane stores its own 16-byte slot chunks of the page (a
 //              wave store is 1 KiB contiguous), or its dense row to the ring
 #include "swan_device.h"
@@ -23,7 +24,6 @@
 namespace swan {
 
 typedef double d4 __attribute__((ext_vector_type(4)));
-typedef unsigned short us2 __attribute__((ext_vector_type(2)));
 
 constexpr int kRowHalves = 136;                // LDS row of one token's 128 fp16 values (+ pad)
 constexpr int kPrefillBlocksPerWave = 4;       // 64-position blocks per wave
@@ -31,19 +31,61 @@ constexpr int kStageBytes = 64 * kRowHalves * 2;  // the rows, then the page cop
 // a page (64 * k_pad * 3 bytes) fits the copy up to k_pad 88; above, values and
 // indices are emitted and stored in two rounds
 
-// count of the 128 fp16 values (64 packed dwords) whose magnitude bits are
-// >= cand, with packed 16-bit adds: (|x| + 0x8000 - cand) has bit 15 set
-// exactly when |x| >= cand
-__device__ __forceinline__ int count_ge(const uint32_t* v, uint32_t cand) {
-  const uint32_t c = 0x8000u - cand;  // cand <= 0x8000: no 16-bit overflow
-  const us2 add = {(unsigned short)c, (unsigned short)c};
-  us2 cnt = {0, 0};
+// One step of a 16x16 bit-matrix transpose applied to both 16-bit halves of
+// 16 words at once (row i of each matrix = half of w[i], column b = bit b):
+// the k x k off-diagonal blocks of every 2k x 2k block trade places.
+template <int K>
+__device__ __forceinline__ void transpose_step(uint32_t* w, uint32_t mask) {
 #pragma unroll
-  for (int w = 0; w < 64; ++w) {
-    const us2 m = __builtin_bit_cast(us2, v[w] & 0x7FFF7FFFu);
-    cnt += (m + add) >> (unsigned short)15;
+  for (int i = 0; i < 16; ++i) {
+    if (i & K) continue;
+    const uint32_t t = ((w[i] >> K) ^ w[i + K]) & mask;
+    w[i + K] ^= t;
+    w[i] ^= t << K;
   }
-  return (int)cnt.x + (int)cnt.y;
+}
+
+// k-th largest of the 128 fp16 magnitudes in v (two per dword), and how many
+// elements equal to it are kept (the rest of the k are strictly larger).
+// Radix select on bit planes: the magnitudes of each 32-element chunk c are
+// transposed so that pl[b][c] holds bit b of each element (bits 0-15: the
+// chunk's even elements, 16-31: its odd ones); from the top bit down, the
+// candidates still equal to the threshold prefix are split by the next bit.
+__device__ __forceinline__ void kth_magnitude(const uint32_t* v, int k, uint32_t& tau,
+                                              int& need_eq) {
+  uint32_t pl[15][4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    uint32_t w[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) w[i] = v[16 * c + i] & 0x7FFF7FFFu;
+    transpose_step<8>(w, 0x00FF00FFu);
+    transpose_step<4>(w, 0x0F0F0F0Fu);
+    transpose_step<2>(w, 0x33333333u);
+    transpose_step<1>(w, 0x55555555u);
+#pragma unroll
+    for (int b = 0; b < 15; ++b) pl[b][c] = w[b];  // plane 15 (the sign) is zero
+  }
+  uint32_t eq[4] = {~0u, ~0u, ~0u, ~0u};
+  int gt = 0;
+  uint32_t t = 0;
+#pragma unroll
+  for (int b = 14; b >= 0; --b) {
+    uint32_t hi[4];
+    int cnt = 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      hi[c] = eq[c] & pl[b][c];
+      cnt += __popc(hi[c]);
+    }
+    const bool one = gt + cnt >= k;  // the k-th largest has this bit set
+    t |= one ? (1u << b) : 0u;
+    gt += one ? 0 : cnt;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) eq[c] = one ? hi[c] : (eq[c] & ~pl[b][c]);
+  }
+  tau = t;
+  need_eq = k - gt;
 }
 
 // One token per lane: its kept (value, index) pairs in ascending index
@@ -197,14 +239,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     uint32_t tau_keep = 0;
     int need_keep = 0, npad = 0;
     if (sparse) {
-      // k-th largest magnitude
-      uint32_t tau = 0;
-#pragma unroll 1
-      for (int bit = 14; bit >= 0; --bit) {
-        const uint32_t cand = tau | (1u << bit);
-        if (count_ge(v, cand) >= k) tau = cand;
-      }
-      const int need_eq = k - count_ge(v, tau + 1);  // ties at tau taken lowest dim first
+      // k-th largest magnitude; ties at it are taken lowest dim first
+      uint32_t tau;
+      int need_eq;
+      kth_magnitude(v, k, tau, need_eq);
       npad = kp - k;
       if (!two_rounds)
         emit_slots<true, true>(v, tau, need_eq, k, npad, (uint16_t*)lds + lane * 8,
