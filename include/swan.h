@@ -17,7 +17,14 @@
  *    Work is enqueued on it and the call returns without waiting, except
  *    swan_calibrate_rotation, which waits for its result.
  *  - The library never allocates memory.  The caller owns every buffer and
- *    sizes it with the *_bytes queries below.
+ *    sizes it with the *_bytes queries below.  The one resource it keeps: for
+ *    a batch whose sequences use different k_pad, swan_decode_attention runs
+ *    those attention launches side by side on up to three HIP streams of its
+ *    own per device (default priority, created on first use with two events
+ *    each, kept until the process ends), forked from and joined back into
+ *    `stream` with events, so the call orders with `stream` like any other.
+ *    Calls are made with the stream's device current; otherwise the launches
+ *    run one after another on `stream`.
  *  - All arguments are validated on the host before anything is enqueued, so
  *    a non-OK status means nothing was written.  Errors never abort, throw or
  *    exit; swan_last_error() returns a message for the calling thread.

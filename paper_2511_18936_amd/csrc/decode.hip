@@ -365,10 +365,16 @@ struct SideStreams {
   hipEvent_t fork, join[kSideStreams];
 };
 
-static SideStreams* side_streams() {
+// The side streams of the current device, or NULL (launch on the caller's
+// stream alone) when they cannot be made or `caller` belongs to another device.
+static SideStreams* side_streams(hipStream_t caller) {
   static SideStreams per_device[kMaxDevices];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  if (caller) {
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice(caller, &sdev) != hipSuccess || sdev != dev) return nullptr;
+  }
   SideStreams* ss = &per_device[dev];
   std::lock_guard<std::mutex> lk(ss->mu);
   if (!ss->tried) {
@@ -409,7 +415,7 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
       }
     if (g.n > 0) kp8s[ng++] = kp8;
   }
-  SideStreams* ss = ng > 1 ? side_streams() : nullptr;
+  SideStreams* ss = ng > 1 ? side_streams(a.stream) : nullptr;
   if (!ss) {  // one launch, or no side streams: back to back on the caller's stream
     for (int i = 0; i < ng; ++i)
       if ((e = launch_group<T>(a, groups[i], kp8s[i])) != hipSuccess) return e;
