@@ -26,6 +26,8 @@ paper states the method (SWAN: Sparse Winnowed Attention, arXiv 2511.18936):
                            with P_VO^T.
 * ``space_bytes`` / ``flops_swan`` / ``break_even_length``  Sec. 5.1 and Sec. 5.2
                            with Appendix A.2.
+* ``to_e4m3_codes``        8-bit sparse values (reading 9), by brute force over
+                           the format's 127 finite magnitudes.
 
 Readings of the paper used here (where it is silent or ambiguous):
   1. top-k ranks the stored (T-rounded) buffer value, because Algorithm 1 pops
@@ -36,7 +38,11 @@ Readings of the paper used here (where it is silent or ambiguous):
   5. with b = 0 every token, the current one included, is pruned at once;
   6. the scale is 1/sqrt(d_h) for the full head dimension, whatever k is;
   7. q_hat, scores, probabilities and the accumulator are never rounded to T;
-  8. the output is returned un-rotated: o = o_hat . P_VO^T.
+  8. the output is returned un-rotated: o = o_hat . P_VO^T;
+  9. 8-bit sparse values (Sec. 4.3, Sec. 5.1 name 8-bit values without a
+     format) are OCP FP8 E4M3 without a scale: the kept T values, rounded to the
+     nearest E4M3 value (ties to the even code, saturating at +-448); the
+     selection still ranks the T values (reading 1) and the buffer stays T.
 
 Parity status: every function above is pinned by tests/test_oracle_pins.py;
 nothing here is "parity unpinned" except the end-task accuracy of Tables 1-3,
@@ -126,6 +132,48 @@ def topk_indices_rows(Y: np.ndarray, k: int) -> np.ndarray:
 # --------------------------------------------------------------------------- #
 # Algorithm 1: hybrid cache of one (sequence, kv head) unit
 # --------------------------------------------------------------------------- #
+# 8-bit sparse values (Sec. 4.3, Sec. 5.1; reading 9: OCP FP8 E4M3, no scale)
+# --------------------------------------------------------------------------- #
+def e4m3_magnitudes() -> np.ndarray:
+    """The 127 finite non-negative E4M3 values, indexed by their 7-bit code:
+    exponent field e = code >> 3 (bias 7), mantissa m = code & 7; e = 0 is
+    subnormal (m * 2^-9); code 127 (all ones) is NaN and not a value."""
+    vals = []
+    for code in range(127):
+        e, m = code >> 3, code & 7
+        vals.append(m * 2.0 ** -9 if e == 0 else (1.0 + m / 8.0) * 2.0 ** (e - 7))
+    return np.array(vals, dtype=F64)
+
+
+def to_e4m3_codes(x: np.ndarray) -> np.ndarray:
+    """Round each value to the nearest E4M3 value, ties to the even code,
+    magnitudes above 448 saturating to 448; returns uint8 codes with the sign in
+    bit 7 (-0 keeps its sign).  Brute force: the distance to every magnitude."""
+    x = np.asarray(x, dtype=F64)
+    flat = x.reshape(-1)
+    tbl = e4m3_magnitudes()
+    codes = np.empty(flat.shape, dtype=np.uint8)
+    step = 1 << 16
+    for s0 in range(0, flat.size, step):
+        a = np.minimum(np.abs(flat[s0:s0 + step]), tbl[-1])
+        dist = np.abs(a[:, None] - tbl[None, :])
+        near = dist == dist.min(axis=1, keepdims=True)
+        first = np.argmax(near, axis=1)  # the lower code of the nearest ones
+        tie = near.sum(axis=1) == 2      # exactly between two codes
+        c = np.where(tie & (first % 2 == 1), first + 1, first)
+        codes[s0:s0 + step] = c.astype(np.uint8) | (np.signbit(flat[s0:s0 + step]) * 0x80).astype(np.uint8)
+    return codes.reshape(x.shape)
+
+
+def e4m3_decode(codes: np.ndarray) -> np.ndarray:
+    """Values of E4M3 codes (sign in bit 7); code 0x7f / 0xff is NaN."""
+    codes = np.asarray(codes, dtype=np.uint8)
+    tbl = np.append(e4m3_magnitudes(), np.nan)
+    mag = tbl[codes & 0x7F]
+    return np.where(codes & 0x80, -mag, mag)
+
+
+# --------------------------------------------------------------------------- #
 class UnitCache:
     """Sparse cache + dense FIFO buffer of one (sequence, KV head), as in Algorithm 1.
 
@@ -135,12 +183,13 @@ class UnitCache:
     """
 
     def __init__(self, P_qk: np.ndarray, P_vo: np.ndarray, buffer_tokens: int,
-                 k_active: int, dtype=np.float16):
+                 k_active: int, dtype=np.float16, values: str = "t"):
         self.P_qk = np.asarray(P_qk, dtype=F64)
         self.P_vo = np.asarray(P_vo, dtype=F64)
         self.b = int(buffer_tokens)
         self.k = int(k_active)
         self.dtype = dtype
+        self.values = values  # "t": sparse values in T; "e4m3": 8-bit (reading 9)
         self.k_buf: collections.deque = collections.deque()
         self.v_buf: collections.deque = collections.deque()
         self.k_idx: List[np.ndarray] = []
@@ -162,21 +211,27 @@ class UnitCache:
             v_old = self.v_buf.popleft()
             i_k = topk_indices(k_old, self.k)
             self.k_idx.append(i_k)
-            self.k_val.append(k_old[i_k])
+            self.k_val.append(self._sparse_value(k_old[i_k]))
             i_v = topk_indices(v_old, self.k)
             self.v_idx.append(i_v)
-            self.v_val.append(v_old[i_v])
+            self.v_val.append(self._sparse_value(v_old[i_v]))
+
+    def _sparse_value(self, kept: np.ndarray) -> np.ndarray:
+        if self.values == "e4m3":
+            return e4m3_decode(to_e4m3_codes(kept))
+        return kept
 
     def sparse_arrays(self) -> Dict[str, np.ndarray]:
         d = self.P_qk.shape[0]
         n = len(self.k_idx)
         def stack(lst, dt, width):
             return np.stack(lst) if lst else np.zeros((0, width), dtype=dt)
+        vdt = F64 if self.values == "e4m3" else self.dtype
         return {
             "k_idx": stack(self.k_idx, np.int64, self.k),
-            "k_val": stack(self.k_val, self.dtype, self.k),
+            "k_val": stack(self.k_val, vdt, self.k),
             "v_idx": stack(self.v_idx, np.int64, self.k),
-            "v_val": stack(self.v_val, self.dtype, self.k),
+            "v_val": stack(self.v_val, vdt, self.k),
             "k_buf": np.stack(list(self.k_buf)) if self.k_buf else np.zeros((0, d), self.dtype),
             "v_buf": np.stack(list(self.v_buf)) if self.v_buf else np.zeros((0, d), self.dtype),
             "n_sparse": n,
@@ -188,11 +243,13 @@ class UnitCache:
 
 def compress_block(K_rows: np.ndarray, V_rows: np.ndarray, P_qk: np.ndarray,
                    P_vo: np.ndarray, buffer_tokens: int, k_active: int,
-                   dtype=np.float16) -> Dict[str, np.ndarray]:
+                   dtype=np.float16, values: str = "t") -> Dict[str, np.ndarray]:
     """Algorithm 1 applied to n tokens of an empty unit, all at once.
 
     Equal, bit for bit, to n successive ``UnitCache.append`` calls (tested):
     the first max(n - b, 0) tokens end up pruned, the last min(n, b) stay dense.
+    With values="e4m3" the kept values are stored as 8-bit codes (reading 9):
+    "k_code"/"v_code" hold the codes and "k_val"/"v_val" their values.
     """
     n = K_rows.shape[0]
     b = int(buffer_tokens)
@@ -201,7 +258,7 @@ def compress_block(K_rows: np.ndarray, V_rows: np.ndarray, P_qk: np.ndarray,
     n_sparse = max(n - b, 0)
     k_idx = topk_indices_rows(k_hat[:n_sparse], k_active)
     v_idx = topk_indices_rows(v_hat[:n_sparse], k_active)
-    return {
+    out = {
         "k_idx": k_idx,
         "k_val": np.take_along_axis(k_hat[:n_sparse], k_idx, axis=1),
         "v_idx": v_idx,
@@ -210,6 +267,11 @@ def compress_block(K_rows: np.ndarray, V_rows: np.ndarray, P_qk: np.ndarray,
         "v_buf": v_hat[n_sparse:],
         "n_sparse": n_sparse,
     }
+    if values == "e4m3":
+        for r in ("k", "v"):
+            out[f"{r}_code"] = to_e4m3_codes(out[f"{r}_val"])
+            out[f"{r}_val"] = e4m3_decode(out[f"{r}_code"])
+    return out
 
 
 def attend_arrays(q: np.ndarray, P_qk: np.ndarray, P_vo: np.ndarray,

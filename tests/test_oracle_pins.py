@@ -353,3 +353,100 @@ def test_flops_swan_terms():
     assert O.flops_swan(0, 128, 0, 48) == 4 * 128 * 128
     assert O.flops_swan(1000, 128, 0, 48) - O.flops_swan(999, 128, 0, 48) == 4 * 48
     assert O.flops_swan(1000, 128, 10, 48) - O.flops_swan(1000, 128, 9, 48) == 4 * (128 - 48)
+
+
+# --------------------------------------------------------------------------- #
+# 8-bit sparse values (reading 9: OCP FP8 E4M3, no scale)
+# --------------------------------------------------------------------------- #
+def _all_finite_fp16():
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    x = bits.view(np.float16)
+    return x[np.isfinite(x)]
+
+
+def test_e4m3_table_is_the_format():
+    """Closed form of E4M3: 2^-9 smallest subnormal, 2^-6 smallest normal, 448 largest,
+    strictly increasing codes, every value exact in fp16 (so fp16 -> E4M3 -> fp16
+    loses nothing more than the rounding)."""
+    t = O.e4m3_magnitudes()
+    assert t.shape == (127,)
+    assert t[0] == 0.0 and t[1] == 2.0 ** -9 and t[7] == 7 * 2.0 ** -9
+    assert t[8] == 2.0 ** -6 and t[126] == 448.0 and t[120] == 256.0
+    assert np.all(np.diff(t) > 0)
+    assert np.array_equal(t.astype(np.float16).astype(np.float64), t)
+    # the spacing doubles at every binade from 2^-6 up
+    for e in range(1, 16):
+        seg = t[8 * e: 8 * e + 8] if e < 15 else t[120:127]
+        assert np.all(np.diff(seg) == 2.0 ** (e - 10))
+
+
+def test_e4m3_rounding_matches_torch_on_every_fp16_value():
+    """A library routine: torch's float8_e4m3fn conversion (nearest, ties to even) on
+    every finite fp16 value up to 464 in magnitude (above, torch gives NaN where the
+    oracle saturates)."""
+    torch = pytest.importorskip("torch")
+    x = _all_finite_fp16()
+    x = x[np.abs(x.astype(np.float64)) <= 464.0]
+    want = torch.tensor(x.astype(np.float32)).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    got = O.to_e4m3_codes(x)
+    assert np.array_equal(got, want)
+
+
+def test_e4m3_ties_saturation_and_signed_zero():
+    assert list(O.to_e4m3_codes(np.array([1.0625, 1.1875, 2.0 ** -10, 3 * 2.0 ** -10]))) == \
+        [56, 58, 0, 2]                                   # ties to the even code
+    assert list(O.to_e4m3_codes(np.array([448.0, 465.0, 1000.0, 65504.0, -1e4]))) == \
+        [126, 126, 126, 126, 254]                        # saturating at +-448
+    assert list(O.to_e4m3_codes(np.array([0.0, -0.0]))) == [0, 128]
+    v = O.e4m3_decode(np.arange(256, dtype=np.uint8))
+    assert np.isnan(v[127]) and np.isnan(v[255]) and v[254] == -448.0
+    # decode(encode(x)) is the nearest value: no other code is strictly closer
+    x = np.random.default_rng(5).uniform(-500, 500, 4000)
+    d_best = np.abs(O.e4m3_decode(O.to_e4m3_codes(x)) - np.clip(x, -448, 448))
+    t = O.e4m3_magnitudes()
+    d_any = np.min(np.abs(np.abs(np.clip(x, -448, 448))[:, None] - t[None, :]), axis=1)
+    assert np.all(d_best <= d_any)
+
+
+def test_e4m3_values_keep_the_fp16_selection():
+    """Reading 9: the indices are those of fp16 storage (selection ranks the stored fp16
+    values), the values are the E4M3 rounding of the kept fp16 values, the buffer is
+    unchanged, and token-by-token appends give the same codes as the block form."""
+    rng = si.rng_for(9100, 0)
+    R = si.haar_orthogonal(rng, 128)
+    K = si.lowrank_rows(si.rng_for(9100, 1), 90, R)
+    V = si.lowrank_rows(si.rng_for(9100, 2), 90, R)
+    Pk, Pv = si.random_orthogonal(91, 128), si.random_orthogonal(92, 128)
+    for k in (1, 13, 48, 128):
+        a = O.compress_block(K, V, Pk, Pv, 16, k, np.float16)
+        e = O.compress_block(K, V, Pk, Pv, 16, k, np.float16, values="e4m3")
+        for r in ("k", "v"):
+            assert np.array_equal(a[f"{r}_idx"], e[f"{r}_idx"])
+            assert np.array_equal(e[f"{r}_code"], O.to_e4m3_codes(a[f"{r}_val"]))
+            assert np.array_equal(a[f"{r}_buf"].view(np.uint16), e[f"{r}_buf"].view(np.uint16))
+        uc = O.UnitCache(Pk, Pv, 16, k, np.float16, values="e4m3")
+        for t in range(90):
+            uc.append(K[t], V[t])
+        sa = uc.sparse_arrays()
+        for r in ("k", "v"):
+            assert np.array_equal(sa[f"{r}_idx"], e[f"{r}_idx"])
+            assert np.array_equal(sa[f"{r}_val"], e[f"{r}_val"])
+
+
+def test_e4m3_values_with_k_equal_d_are_dense_attention_on_rounded_vectors():
+    """k = d, b = 0: every component kept, so attention is textbook softmax attention on
+    the E4M3-rounded rotated keys and values (written out here), rotated back."""
+    rng = si.rng_for(9200, 0)
+    d, L = 8, 12
+    Pk, Pv = si.random_orthogonal(93, d), si.random_orthogonal(94, d)
+    K = rng.standard_normal((L, d))
+    V = rng.standard_normal((L, d))
+    q = rng.standard_normal(d)
+    c = O.compress_block(K, V, Pk, Pv, 0, d, np.float16, values="e4m3")
+    got = O.attend_arrays(q, Pk, Pv, c)
+    kh = O.e4m3_decode(O.to_e4m3_codes((K @ Pk).astype(np.float16)))
+    vh = O.e4m3_decode(O.to_e4m3_codes((V @ Pv).astype(np.float16)))
+    s = (kh @ (q @ Pk)) / math.sqrt(d)
+    p = np.exp(s - s.max())
+    want = (p / p.sum()) @ vh @ Pv.T
+    assert np.allclose(got, want, rtol=1e-12, atol=1e-12)
