@@ -53,8 +53,14 @@ typedef enum swan_status {
 } swan_status;
 
 typedef enum swan_dtype {
-  SWAN_F32 = 0,  /* float32 storage */
-  SWAN_F16 = 1   /* IEEE binary16 storage */
+  SWAN_F32 = 0,      /* float32 storage */
+  SWAN_F16 = 1,      /* IEEE binary16 storage */
+  SWAN_F16_E4M3 = 2  /* binary16 keys, values, queries, outputs and dense buffer; the
+                        sparse values stored as OCP FP8 E4M3 (one byte, no scale): the
+                        kept binary16 values rounded to the nearest E4M3 value, ties to
+                        the even code, magnitudes above 448 to 448 (Sec. 4.3 and
+                        Sec. 5.1 name 8-bit values; the format is this library's
+                        reading).  The top-k still ranks the binary16 values. */
 } swan_dtype;
 
 #define SWAN_MAX_BATCH 64
@@ -72,14 +78,15 @@ typedef enum swan_dtype {
  * type; the token at position pos (0-based, pos >= L - b) is in slot pos % b.
  *
  * Page layout.  Sparse token p of sequence s and KV head h (p < L - b) is in
- * page p / 64, slot t = p % 64.  With T the storage type, k_pad = k rounded up
- * to a multiple of 8 and GV = 16 / sizeof(T) values per 16-byte chunk, a page is
- *     values : k_pad / GV chunks, each [64 slots][16 bytes]
+ * page p / 64, slot t = p % 64.  With VB the bytes of a sparse value (4 for
+ * SWAN_F32, 2 for SWAN_F16, 1 for SWAN_F16_E4M3), CB the value chunk bytes (16,
+ * 16, 8), GV = CB / VB values per chunk and k_pad = k rounded up to a multiple
+ * of 8, a page is
+ *     values : k_pad / GV chunks, each [64 slots][CB bytes]
  *     indices: k_pad / 8  chunks, each [64 slots][8 bytes] (uint8)
- * so entry e of slot t has its value at byte (e / GV) * 1024 + t * 16 +
- * (e % GV) * sizeof(T) and its index at byte 64 * k_pad * sizeof(T) +
- * (e / 8) * 512 + t * 8 + (e % 8).  A page is 64 * k_pad * (sizeof(T) + 1)
- * bytes.  Entries 0..k-1 are the kept components in ascending index order;
+ * so entry e of slot t has its value at byte (e / GV) * 64 * CB + t * CB +
+ * (e % GV) * VB and its index at byte 64 * k_pad * VB + (e / 8) * 512 + t * 8 +
+ * (e % 8).  A page is 64 * k_pad * (VB + 1) bytes.  Entries 0..k-1 are the kept components in ascending index order;
  * entries k..k_pad-1 are padding with value +0 at the lowest dims that were not
  * kept, so the k_pad indices of a token are distinct (the decode kernel relies
  * on it).  Sequence s owns n_kv_heads * ceil(sparse_capacity / 64)

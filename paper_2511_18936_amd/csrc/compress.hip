@@ -3,7 +3,7 @@
 //
 // Several new tokens per sequence: two launches on the caller's stream, so
 // that every vector leaving the ring is read before a new token overwrites its
-// slot.  One new token (a decode step): one launch, insert_kernel<T, 1>, whose
+// slot.  One new token (a decode step): one launch, insert_kernel<F, 1>, whose
 // wave evicts the slot's old vector before it writes the new one.
 //   evict_kernel   one wave per ring vector that leaves the buffer: top-k of
 //                  its stored values, packed into its page slot
@@ -19,6 +19,8 @@
 // and orders by magnitude, then by lower index.  A binary search over the key
 // bits with wave ballots finds the k-th largest key; the selected entries are
 // then numbered in ascending dim order with mbcnt and written to the page.
+#include <type_traits>
+
 #include "swan_device.h"
 #include "swan_internal.h"
 
@@ -26,13 +28,14 @@ namespace swan {
 
 constexpr int kTPW = 8;  // new tokens per insert wave (several new tokens per sequence)
 
-// Write the top-k of a 128-vector (lane holds elements 2l, 2l+1) into page
-// slot `slot` of the page at `page`.
-template <typename T>
-__device__ __forceinline__ void select_and_pack(typename Store<T>::Bits x0,
-                                                typename Store<T>::Bits x1, int k, char* page,
-                                                int slot, int lane) {
-  using St = Store<T>;
+// Write the top-k of a 128-vector of stored values (lane holds elements 2l,
+// 2l+1) into page slot `slot` of the page at `page`, in page format F (the
+// values as stored, or rounded to E4M3; the selection ranks the stored values).
+template <typename F>
+__device__ __forceinline__ void select_and_pack(typename Store<typename Fmt<F>::Elem>::Bits x0,
+                                                typename Store<typename Fmt<F>::Elem>::Bits x1,
+                                                int k, char* page, int slot, int lane) {
+  using St = Store<typename Fmt<F>::Elem>;
   using Key = typename std::conditional<(St::kMagBits + 8 > 32), uint64_t, uint32_t>::type;
   constexpr int kKeyBits = St::kMagBits + 8;
   const Key key0 = ((Key)St::mag(x0) << 8) | (Key)(255 - 2 * lane);
@@ -49,16 +52,23 @@ __device__ __forceinline__ void select_and_pack(typename Store<T>::Bits x0,
   const uint64_t m1 = __ballot(s1);
   const int e0 = popc_below(m0) + popc_below(m1);
   const int e1 = e0 + (s0 ? 1 : 0);
-  constexpr int GV = 16 / St::kBytes;
+  constexpr int VB = Fmt<F>::kValBytes, CB = Fmt<F>::kChunkBytes, GV = CB / VB;
   const int kp = kpad_of(k);
-  char* vals = page + slot * 16;
-  char* idxs = page + (int64_t)kPage * kp * St::kBytes + slot * 8;
+  char* vals = page + slot * CB;
+  char* idxs = page + (int64_t)kPage * kp * VB + slot * 8;
+  auto put = [&](int e, typename St::Bits x) {
+    char* dst = vals + (e / GV) * (kPage * CB) + (e % GV) * VB;
+    if constexpr (std::is_same<F, E4M3V>::value)
+      *(uint8_t*)dst = (uint8_t)f16_bits_to_e4m3(x);
+    else
+      *(typename St::Bits*)dst = x;
+  };
   if (s0) {
-    *(typename St::Bits*)(vals + (e0 / GV) * 1024 + (e0 % GV) * St::kBytes) = x0;
+    put(e0, x0);
     idxs[(e0 / 8) * 512 + (e0 % 8)] = (char)(2 * lane);
   }
   if (s1) {
-    *(typename St::Bits*)(vals + (e1 / GV) * 1024 + (e1 % GV) * St::kBytes) = x1;
+    put(e1, x1);
     idxs[(e1 / 8) * 512 + (e1 % 8)] = (char)(2 * lane + 1);
   }
   // padding entries k .. kp-1: value +0 at the lowest unselected dims, so that
@@ -71,12 +81,12 @@ __device__ __forceinline__ void select_and_pack(typename Store<T>::Bits x0,
     const int r1 = r0 + (s0 ? 0 : 1);
     if (!s0 && r0 < npad) {
       const int e = k + r0;
-      *(typename St::Bits*)(vals + (e / GV) * 1024 + (e % GV) * St::kBytes) = 0;
+      put(e, 0);
       idxs[(e / 8) * 512 + (e % 8)] = (char)(2 * lane);
     }
     if (!s1 && r1 < npad) {
       const int e = k + r1;
-      *(typename St::Bits*)(vals + (e / GV) * 1024 + (e % GV) * St::kBytes) = 0;
+      put(e, 0);
       idxs[(e / 8) * 512 + (e % 8)] = (char)(2 * lane + 1);
     }
   }
@@ -92,9 +102,9 @@ __device__ __forceinline__ int evict_end(int len_old, int n_new, int bb) {
   return len_old < lim ? len_old : lim;
 }
 
-template <typename T>
+template <typename F>
 __global__ __launch_bounds__(64) void evict_kernel(CompressLaunch a) {
-  using St = Store<T>;
+  using St = Store<typename Fmt<F>::Elem>;
   const int lane = threadIdx.x;
   int w = blockIdx.x;
   const int e = w % a.max_evict;
@@ -114,14 +124,15 @@ __global__ __launch_bounds__(64) void evict_kernel(CompressLaunch a) {
   const typename St::Bits x0 = ring[2 * lane];
   const typename St::Bits x1 = ring[2 * lane + 1];
   const int k = a.tab.kact[b];
-  const int64_t pbytes = page_bytes_of(St::kBytes, k);
+  const int64_t pbytes = page_bytes_of(Fmt<F>::kValBytes, k);
   char* page = (char*)(role ? a.v_pages : a.k_pages) + a.tab.page_off[b] +
                ((int64_t)h * a.n_pages_cap + p / kPage) * pbytes;
-  select_and_pack<T>(x0, x1, k, page, p % kPage, lane);
+  select_and_pack<F>(x0, x1, k, page, p % kPage, lane);
 }
 
-template <typename T, int TPW>
+template <typename F, int TPW>
 __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
+  using T = typename Fmt<F>::Elem;
   using St = Store<T>;
   __shared__ __attribute__((aligned(16))) double xs[kD][TPW];
   const int lane = threadIdx.x;
@@ -168,7 +179,7 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
   const int len_old = a.tab.len[b];
   const int len_new = len_old + nnew;
   const int k = a.tab.kact[b];
-  const int64_t pbytes = page_bytes_of(St::kBytes, k);
+  const int64_t pbytes = page_bytes_of(Fmt<F>::kValBytes, k);
   char* pages = (char*)(role ? a.v_pages : a.k_pages) + a.tab.page_off[b] +
                 (int64_t)h * a.n_pages_cap * pbytes;
   typename St::Bits* ring = (typename St::Bits*)(role ? a.v_ring : a.k_ring) +
@@ -182,7 +193,7 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
       const typename St::Bits* old = ring + (int64_t)(p0 % a.bb) * kD;
       const typename St::Bits o0 = old[2 * lane];
       const typename St::Bits o1 = old[2 * lane + 1];
-      select_and_pack<T>(o0, o1, k, pages + (int64_t)(p0 / kPage) * pbytes, p0 % kPage, lane);
+      select_and_pack<F>(o0, o1, k, pages + (int64_t)(p0 / kPage) * pbytes, p0 % kPage, lane);
     }
   }
 #pragma unroll
@@ -196,27 +207,27 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
       r[2 * lane] = y0;
       r[2 * lane + 1] = y1;
     } else {  // pruned on arrival
-      select_and_pack<T>(y0, y1, k, pages + (int64_t)(pos / kPage) * pbytes, pos % kPage, lane);
+      select_and_pack<F>(y0, y1, k, pages + (int64_t)(pos / kPage) * pbytes, pos % kPage, lane);
     }
   }
 }
 
-template <typename T>
+template <typename F>
 static hipError_t launch_compress_t(const CompressLaunch& a) {
   const int units = a.B * a.Hkv * 2;
   if (a.n_new == 1) {  // a decode step: eviction and insertion in one launch
-    hipLaunchKernelGGL((insert_kernel<T, 1>), dim3(units), dim3(64), 0, a.stream, a);
+    hipLaunchKernelGGL((insert_kernel<F, 1>), dim3(units), dim3(64), 0, a.stream, a);
     return hipGetLastError();
   }
   if (a.max_evict > 0) {
-    hipLaunchKernelGGL(evict_kernel<T>, dim3(units * a.max_evict), dim3(64), 0, a.stream, a);
+    hipLaunchKernelGGL(evict_kernel<F>, dim3(units * a.max_evict), dim3(64), 0, a.stream, a);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  if (a.n_new >= kPrefillMinTokens && a.dtype == SWAN_F16) return launch_prefill(a);
+  if (a.n_new >= kPrefillMinTokens && sizeof(typename Fmt<F>::Elem) == 2) return launch_prefill(a);
   if (a.n_new > 0) {
     const int ngroups = (a.n_new + kTPW - 1) / kTPW;
-    hipLaunchKernelGGL((insert_kernel<T, kTPW>), dim3((int64_t)units * ngroups), dim3(64), 0,
+    hipLaunchKernelGGL((insert_kernel<F, kTPW>), dim3((int64_t)units * ngroups), dim3(64), 0,
                        a.stream, a);
     return hipGetLastError();
   }
@@ -225,6 +236,7 @@ static hipError_t launch_compress_t(const CompressLaunch& a) {
 
 hipError_t launch_compress(const CompressLaunch& a) {
   if (a.dtype == SWAN_F16) return launch_compress_t<_Float16>(a);
+  if (a.dtype == SWAN_F16_E4M3) return launch_compress_t<E4M3V>(a);
   return launch_compress_t<float>(a);
 }
 

@@ -235,7 +235,8 @@ __global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup g) {
     if (nb == 0) return;
     const int64_t ring_off = ((int64_t)b * a.Hkv + h) * a.bb * kD;
     float* part = a.part + ((int64_t)bhq * pstride + a.n_splits) * kPartFloats;
-    buffer_part<T>((const T*)a.k_ring + ring_off, (const T*)a.v_ring + ring_off, nb,
+    using E = typename Fmt<T>::Elem;
+    buffer_part<E>((const E*)a.k_ring + ring_off, (const E*)a.v_ring + ring_off, nb,
                    a.qhat + (int64_t)bhq * kD, qrep, acc, lane, part);
     return;
   }
@@ -253,7 +254,7 @@ __global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup g) {
   const int pbeg = (int)((int64_t)split * np / ns);
   const int pend = (int)((int64_t)(split + 1) * np / ns);
   const int k = a.tab.kact[b];
-  const int64_t pbytes = page_bytes_of((int)sizeof(T), k);
+  const int64_t pbytes = page_bytes_of(Fmt<T>::kValBytes, k);
   const int64_t unit_off = a.tab.page_off[b] + (int64_t)h * a.n_pages_cap * pbytes;
   const char* kbase = (const char*)a.k_pages + unit_off;
   const char* vbase = (const char*)a.v_pages + unit_off;
@@ -391,7 +392,8 @@ static SideStreams* side_streams(hipStream_t caller) {
 template <typename T>
 static hipError_t launch_decode_t(const DecodeLaunch& a) {
   const int BH = a.B * a.Hq;
-  hipLaunchKernelGGL(qrot_kernel<T>, dim3(BH), dim3(128), 0, a.stream, (const T*)a.q, a.P_qk,
+  using E = typename Fmt<T>::Elem;
+  hipLaunchKernelGGL(qrot_kernel<E>, dim3(BH), dim3(128), 0, a.stream, (const E*)a.q, a.P_qk,
                      a.qhat, a.Hq, a.Hq / a.Hkv, a.qmult);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -440,12 +442,13 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
     e = hipEventRecord(a.prof_stop, a.stream);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(merge_kernel<T>, dim3(BH), dim3(128), 0, a.stream, a);
+  hipLaunchKernelGGL(merge_kernel<E>, dim3(BH), dim3(128), 0, a.stream, a);
   return hipGetLastError();
 }
 
 hipError_t launch_decode(const DecodeLaunch& a) {
   if (a.dtype == SWAN_F16) return launch_decode_t<_Float16>(a);
+  if (a.dtype == SWAN_F16_E4M3) return launch_decode_t<E4M3V>(a);
   return launch_decode_t<float>(a);
 }
 

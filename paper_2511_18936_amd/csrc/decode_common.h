@@ -2,6 +2,8 @@
 // registers and loads, the lazy-softmax state, and the dense-buffer partial.
 #pragma once
 
+#include <type_traits>
+
 #include "swan_device.h"
 #include "swan_internal.h"
 
@@ -10,34 +12,49 @@ namespace swan {
 constexpr float kTau = 8.0f;
 
 // ---------------------------------------------------------------------------
-// page registers: KP8 groups of 8 entries; VCH 16-byte value chunks per group
+// page registers: KP8 groups of 8 entries; VCH value chunks per group
 // ---------------------------------------------------------------------------
 template <typename T, int KP8>
 struct PageRegs {
-  static constexpr int VCH = (int)sizeof(T) / 2;
-  u32x4 val[KP8 * VCH];
+  static constexpr int CB = Fmt<T>::kChunkBytes;
+  static constexpr int VCH = 8 * Fmt<T>::kValBytes / CB;
+  using VChunk = typename std::conditional<CB == 16, u32x4, u32x2>::type;
+  VChunk val[KP8 * VCH];
   u32x2 idx[KP8];
 };
 
 // Loads one page into registers (nontemporal: the pages are streamed once).
 template <typename T, int KP8>
 __device__ __forceinline__ void load_page(PageRegs<T, KP8>& r, const char* page, int lane) {
-  constexpr int VCH = PageRegs<T, KP8>::VCH;
-  const char* vp = page + lane * 16;
+  using PR = PageRegs<T, KP8>;
+  const char* vp = page + lane * PR::CB;
 #pragma unroll
-  for (int c = 0; c < KP8 * VCH; ++c)
-    r.val[c] = __builtin_nontemporal_load((const u32x4*)(vp + c * 1024));
-  const char* ip = page + KP8 * VCH * 1024 + lane * 8;
+  for (int c = 0; c < KP8 * PR::VCH; ++c)
+    r.val[c] = __builtin_nontemporal_load((const typename PR::VChunk*)(vp + c * 64 * PR::CB));
+  const char* ip = page + KP8 * PR::VCH * 64 * PR::CB + lane * 8;  // 64 * k_pad value bytes
 #pragma unroll
   for (int g = 0; g < KP8; ++g)
     r.idx[g] = __builtin_nontemporal_load((const u32x2*)(ip + g * 512));
+}
+
+// E4M3 byte `sel` (compile-time after unrolling) of w, as float (exact)
+__device__ __forceinline__ float e4m3_byte_to_f32(uint32_t w, int sel) {
+  switch (sel & 3) {
+    case 0: return __builtin_amdgcn_cvt_f32_fp8((int)w, 0);
+    case 1: return __builtin_amdgcn_cvt_f32_fp8((int)w, 1);
+    case 2: return __builtin_amdgcn_cvt_f32_fp8((int)w, 2);
+    default: return __builtin_amdgcn_cvt_f32_fp8((int)w, 3);
+  }
 }
 
 // value of entry u (0..7) of group g, as float
 template <typename T, int KP8>
 struct EntryVal {
   __device__ static __forceinline__ float get(const PageRegs<T, KP8>& r, int g, int u) {
-    if constexpr (sizeof(T) == 2) {
+    if constexpr (std::is_same<T, E4M3V>::value) {
+      const u32x2 c = r.val[g];
+      return e4m3_byte_to_f32(u < 4 ? c.x : c.y, u);
+    } else if constexpr (sizeof(T) == 2) {
       const u32x4 c = r.val[g];
       const uint32_t w = (u < 2) ? c.x : (u < 4) ? c.y : (u < 6) ? c.z : c.w;
       return f16_bits_to_f32((u & 1) ? (w >> 16) : (w & 0xFFFFu));
@@ -49,6 +66,18 @@ struct EntryVal {
     }
   }
 };
+
+// fp16 bits of entry u of group g (fp16 and E4M3 pages; exact either way)
+template <typename T, int KP8>
+__device__ __forceinline__ uint32_t entry_f16_bits(const PageRegs<T, KP8>& r, int g, int u) {
+  if constexpr (std::is_same<T, E4M3V>::value) {
+    const _Float16 h = (_Float16)EntryVal<T, KP8>::get(r, g, u);
+    return (uint32_t)__builtin_bit_cast(uint16_t, h);
+  } else {
+    const uint32_t w = r.val[g][u >> 1];
+    return (u & 1) ? (w >> 16) : (w & 0xFFFFu);
+  }
+}
 
 template <typename T, int KP8>
 __device__ __forceinline__ int entry_idx(const PageRegs<T, KP8>& r, int g, int u) {

@@ -60,8 +60,8 @@ struct GqaLds {
 };
 
 // score wave, one page: scores, softmax reference, P tile and rescale factors
-template <int KP8, int GH>
-__device__ __forceinline__ void gqa_scores(const PageRegs<_Float16, KP8>& kr, bool valid,
+template <typename T, int KP8, int GH>
+__device__ __forceinline__ void gqa_scores(const PageRegs<T, KP8>& kr, bool valid,
                                            GqaLds<GH>& sh, int par, int lane, float* m, float* l,
                                            bool& first) {
   using QV = typename QVec<GH>::type;
@@ -75,7 +75,7 @@ __device__ __forceinline__ void gqa_scores(const PageRegs<_Float16, KP8>& kr, bo
     for (int g = 0; g < KP8; ++g) {
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const float v = EntryVal<_Float16, KP8>::get(kr, g, u);
+        const float v = EntryVal<T, KP8>::get(kr, g, u);
         const QV q = *(const QV*)(ql + entry_idx(kr, g, u) * (R * GH));
 #pragma unroll
         for (int h = 0; h < GH; ++h) s[h] = fmaf(q[h], v, s[h]);
@@ -111,8 +111,8 @@ __device__ __forceinline__ void gqa_scores(const PageRegs<_Float16, KP8>& kr, bo
 }
 
 // value wave, one page: zero the value tile, scatter the kept components
-template <int KP8, int GH>
-__device__ __forceinline__ void gqa_scatter(const PageRegs<_Float16, KP8>& vr, bool valid,
+template <typename T, int KP8, int GH>
+__device__ __forceinline__ void gqa_scatter(const PageRegs<T, KP8>& vr, bool valid,
                                             GqaLds<GH>& sh, int lane) {
   wave_lds_fence();  // the previous page's tile reads come first
   {
@@ -126,12 +126,9 @@ __device__ __forceinline__ void gqa_scatter(const PageRegs<_Float16, KP8>& vr, b
     uint16_t* vt16 = (uint16_t*)sh.vt + lane;
 #pragma unroll
     for (int g = 0; g < KP8; ++g) {
-      const u32x4 c = vr.val[g];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const uint32_t w = c[u >> 1];
-        vt16[entry_idx(vr, g, u) * kVtStride] = (uint16_t)((u & 1) ? (w >> 16) : (w & 0xFFFFu));
-      }
+      for (int u = 0; u < 8; ++u)
+        vt16[entry_idx(vr, g, u) * kVtStride] = (uint16_t)entry_f16_bits<T, KP8>(vr, g, u);
     }
   }
 }
@@ -177,7 +174,7 @@ __device__ __forceinline__ void gqa_mfma(const GqaLds<GH>& sh, int par, int lane
 // Grid: n * Hq dense-buffer blocks (wave 0 serves one query head), then
 // n * Hkv * (G / GH) * g.n_splits sparse blocks, each for GH query heads of
 // one KV head.
-template <int KP8, int GH>
+template <typename T, int KP8, int GH>
 __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup g) {
   constexpr int R = qrep_replicas<GH>();
   __shared__ __attribute__((aligned(16))) GqaLds<GH> sh;
@@ -219,7 +216,7 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
   const int pbeg = (int)((int64_t)split * np / ns);
   const int pend = (int)((int64_t)(split + 1) * np / ns);
   const int k = a.tab.kact[b];
-  const int64_t pbytes = page_bytes_of(2, k);
+  const int64_t pbytes = page_bytes_of(Fmt<T>::kValBytes, k);
   const int64_t unit_off = a.tab.page_off[b] + (int64_t)h * a.n_pages_cap * pbytes;
 
   // q_rep[dim][r][head]: thread t writes dim t, all replicas
@@ -247,17 +244,17 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
       m[j] = 0.f;
       l[j] = 0.f;
     }
-    PageRegs<_Float16, KP8> ka, kb;
-    load_page<_Float16, KP8>(ka, kbase + pbeg * pbytes, lane);
+    PageRegs<T, KP8> ka, kb;
+    load_page<T, KP8>(ka, kbase + pbeg * pbytes, lane);
     for (int p = pbeg; p < pend; p += 2) {
       const int p1 = p + 1 < plast ? p + 1 : plast;
-      load_page<_Float16, KP8>(kb, kbase + p1 * pbytes, lane);
-      gqa_scores<KP8, GH>(ka, p * kPage + lane < S, sh, (p - pbeg) & 1, lane, m, l, first);
+      load_page<T, KP8>(kb, kbase + p1 * pbytes, lane);
+      gqa_scores<T, KP8, GH>(ka, p * kPage + lane < S, sh, (p - pbeg) & 1, lane, m, l, first);
       __syncthreads();
       const int p2 = p + 2 < plast ? p + 2 : plast;
-      load_page<_Float16, KP8>(ka, kbase + p2 * pbytes, lane);
+      load_page<T, KP8>(ka, kbase + p2 * pbytes, lane);
       if (p + 1 < pend) {
-        gqa_scores<KP8, GH>(kb, (p + 1) * kPage + lane < S, sh, (p + 1 - pbeg) & 1, lane, m, l,
+        gqa_scores<T, KP8, GH>(kb, (p + 1) * kPage + lane < S, sh, (p + 1 - pbeg) & 1, lane, m, l,
                             first);
         __syncthreads();
       }
@@ -277,18 +274,18 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
     f4 acc[8];
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt) acc[nt] = f4{0.f, 0.f, 0.f, 0.f};
-    PageRegs<_Float16, KP8> va, vb;
-    load_page<_Float16, KP8>(va, vbase + pbeg * pbytes, lane);
+    PageRegs<T, KP8> va, vb;
+    load_page<T, KP8>(va, vbase + pbeg * pbytes, lane);
     for (int p = pbeg; p < pend; p += 2) {
       const int p1 = p + 1 < plast ? p + 1 : plast;
-      load_page<_Float16, KP8>(vb, vbase + p1 * pbytes, lane);
-      gqa_scatter<KP8, GH>(va, p * kPage + lane < S, sh, lane);
+      load_page<T, KP8>(vb, vbase + p1 * pbytes, lane);
+      gqa_scatter<T, KP8, GH>(va, p * kPage + lane < S, sh, lane);
       __syncthreads();
       gqa_mfma<GH>(sh, (p - pbeg) & 1, lane, acc);
       const int p2 = p + 2 < plast ? p + 2 : plast;
-      load_page<_Float16, KP8>(va, vbase + p2 * pbytes, lane);
+      load_page<T, KP8>(va, vbase + p2 * pbytes, lane);
       if (p + 1 < pend) {
-        gqa_scatter<KP8, GH>(vb, (p + 1) * kPage + lane < S, sh, lane);
+        gqa_scatter<T, KP8, GH>(vb, (p + 1) * kPage + lane < S, sh, lane);
         __syncthreads();
         gqa_mfma<GH>(sh, (p + 1 - pbeg) & 1, lane, acc);
       }
@@ -305,20 +302,20 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
   }
 }
 
-template <int KP8, int GH>
+template <typename T, int KP8, int GH>
 static hipError_t launch_gqa_k(const DecodeLaunch& a, const SeqGroup& g) {
   const int G = a.Hq / a.Hkv;
   const dim3 grid(g.n * a.Hq + g.n * a.Hkv * (G / GH) * g.n_splits);
-  hipLaunchKernelGGL((attn_gqa_kernel<KP8, GH>), grid, dim3(128), 0, a.stream, a, g);
+  hipLaunchKernelGGL((attn_gqa_kernel<T, KP8, GH>), grid, dim3(128), 0, a.stream, a, g);
   return hipGetLastError();
 }
 
-template <int GH>
+template <typename T, int GH>
 static hipError_t launch_gqa_g(const DecodeLaunch& a, const SeqGroup& g, int kp8) {
   switch (kp8) {
 #define SWAN_KP8_CASE(n) \
   case n:                \
-    return launch_gqa_k<n, GH>(a, g);
+    return launch_gqa_k<T, n, GH>(a, g);
     SWAN_KP8_CASE(1) SWAN_KP8_CASE(2) SWAN_KP8_CASE(3) SWAN_KP8_CASE(4)
     SWAN_KP8_CASE(5) SWAN_KP8_CASE(6) SWAN_KP8_CASE(7) SWAN_KP8_CASE(8)
     SWAN_KP8_CASE(9) SWAN_KP8_CASE(10) SWAN_KP8_CASE(11) SWAN_KP8_CASE(12)
@@ -336,17 +333,23 @@ int gqa_heads_per_wave(int G) {
   return 1;
 }
 
-hipError_t launch_attn_gqa(const DecodeLaunch& a, const SeqGroup& g, int kp8) {
+template <typename T>
+static hipError_t launch_gqa_t(const DecodeLaunch& a, const SeqGroup& g, int kp8) {
   switch (gqa_heads_per_wave(a.Hq / a.Hkv)) {
     case 8:
-      return launch_gqa_g<8>(a, g, kp8);
+      return launch_gqa_g<T, 8>(a, g, kp8);
     case 4:
-      return launch_gqa_g<4>(a, g, kp8);
+      return launch_gqa_g<T, 4>(a, g, kp8);
     case 2:
-      return launch_gqa_g<2>(a, g, kp8);
+      return launch_gqa_g<T, 2>(a, g, kp8);
     default:
       return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_attn_gqa(const DecodeLaunch& a, const SeqGroup& g, int kp8) {
+  if (a.dtype == SWAN_F16_E4M3) return launch_gqa_t<E4M3V>(a, g, kp8);
+  return launch_gqa_t<_Float16>(a, g, kp8);
 }
 
 }  // namespace swan

@@ -1,4 +1,5 @@
-// Compress-append of many tokens at once (prefill), fp16 storage.
+// Compress-append of many tokens at once (prefill), fp16 storage (sparse
+// values fp16 or E4M3).
 //
 // Same result as token-by-token Algorithm 1 (and as insert_kernel): each new
 // key/value is rotated exactly (float64 products and sums) and rounded once
@@ -18,6 +19,8 @@
 //              an LDS copy of the page
 //   output     each lane stores its own 16-byte slot chunks of the page (a
 //              wave store is 1 KiB contiguous), or its dense row to the ring
+#include <type_traits>
+
 #include "swan_device.h"
 #include "swan_internal.h"
 
@@ -90,11 +93,18 @@ __device__ __forceinline__ void kth_magnitude(const uint32_t* v, int k, uint32_t
 
 // One token per lane: its kept (value, index) pairs in ascending index
 // order, then the padding (value +0 at the lowest unselected dims), written
-// into the LDS page copy: values [kp/8][64][16 B] at sv, indices
-// [kp/8][64][8 B] at si.
-template <bool kVals, bool kIdx>
+// into the LDS page copy at the lane's offsets: values [kp/8][64][CB] at sv
+// (fp16 bits, or their E4M3 codes), indices [kp/8][64][8 B] at si.
+template <typename F, bool kVals, bool kIdx>
 __device__ __forceinline__ void emit_slots(const uint32_t* v, uint32_t tau, int need_eq, int k,
-                                           int npad, uint16_t* sv, uint8_t* si) {
+                                           int npad, char* sv, uint8_t* si) {
+  constexpr bool kE4M3 = std::is_same<F, E4M3V>::value;
+  auto put = [&](int e, uint32_t hb) {
+    if constexpr (kE4M3)
+      ((uint8_t*)sv)[(e >> 3) * 512 + (e & 7)] = (uint8_t)f16_bits_to_e4m3(hb);
+    else
+      ((uint16_t*)sv)[(e >> 3) * 512 + (e & 7)] = (uint16_t)hb;
+  };
   int e = 0, eq = 0, pad = 0;
 #pragma unroll
   for (int j = 0; j < kD; ++j) {
@@ -104,19 +114,22 @@ __device__ __forceinline__ void emit_slots(const uint32_t* v, uint32_t tau, int 
     const bool sel = m > tau || (tie && eq < need_eq);
     eq += tie ? 1 : 0;
     if (sel) {
-      if (kVals) sv[(e >> 3) * 512 + (e & 7)] = (uint16_t)hb;
+      if (kVals) put(e, hb);
       if (kIdx) si[(e >> 3) * 512 + (e & 7)] = (uint8_t)j;
       ++e;
     } else if (pad < npad) {
       const int ep = k + pad;
-      if (kVals) sv[(ep >> 3) * 512 + (ep & 7)] = 0;
+      if (kVals) put(ep, 0u);
       if (kIdx) si[(ep >> 3) * 512 + (ep & 7)] = (uint8_t)j;
       ++pad;
     }
   }
 }
 
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void prefill_kernel(CompressLaunch a) {
+template <typename F>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void prefill_kernel(CompressLaunch a) {
+  constexpr int VB = Fmt<F>::kValBytes, CB = Fmt<F>::kChunkBytes;
   __shared__ __attribute__((aligned(16))) char lds[kStageBytes];
   _Float16* rows = (_Float16*)lds;  // [64 tokens][kRowHalves], then reused as the page copy
   const int lane = threadIdx.x;
@@ -146,7 +159,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 
   const int k = a.tab.kact[b];
   const int kp = kpad_of(k);
-  const int64_t pbytes = page_bytes_of(2, k);
+  const int64_t pbytes = page_bytes_of(VB, k);
   char* pages = (char*)(role ? a.v_pages : a.k_pages) + a.tab.page_off[b] +
                 (int64_t)h * a.n_pages_cap * pbytes;
   uint16_t* ring = (uint16_t*)(role ? a.v_ring : a.k_ring) + ((int64_t)b * a.Hkv + h) * a.bb * kD;
@@ -235,7 +248,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
       for (int c = 0; c < 16; ++c) dst[c] = u32x4{v[4 * c], v[4 * c + 1], v[4 * c + 2], v[4 * c + 3]};
     }
     const bool sparse = mine && !dense;
-    const bool two_rounds = 64 * kp * 3 > kStageBytes;  // uniform
+    // uniform; never for one-byte values (64 * 128 * 2 bytes fit)
+    const bool two_rounds = VB > 1 && 64 * kp * (VB + 1) > kStageBytes;
+    const int vregion = 64 * kp * VB;                            // value bytes of a page
     uint32_t tau_keep = 0;
     int need_keep = 0, npad = 0;
     if (sparse) {
@@ -245,10 +260,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
       kth_magnitude(v, k, tau, need_eq);
       npad = kp - k;
       if (!two_rounds)
-        emit_slots<true, true>(v, tau, need_eq, k, npad, (uint16_t*)lds + lane * 8,
-                               (uint8_t*)lds + 64 * kp * 2 + lane * 8);
+        emit_slots<F, true, true>(v, tau, need_eq, k, npad, lds + lane * CB,
+                                  (uint8_t*)lds + vregion + lane * 8);
       else
-        emit_slots<true, false>(v, tau, need_eq, k, npad, (uint16_t*)lds + lane * 8, nullptr);
+        emit_slots<F, true, false>(v, tau, need_eq, k, npad, lds + lane * CB, nullptr);
       tau_keep = tau;
       need_keep = need_eq;
     }
@@ -257,24 +272,28 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     char* page = pages + (int64_t)blk * pbytes;
     const int nch = kp >> 3;
     if (sparse) {  // this lane's slot chunks of the page
-      for (int c = 0; c < nch; ++c)
-        *(u32x4*)(page + c * 1024 + lane * 16) = *(const u32x4*)(lds + c * 1024 + lane * 16);
+      for (int c = 0; c < nch; ++c) {
+        if constexpr (CB == 16)
+          *(u32x4*)(page + c * 1024 + lane * 16) = *(const u32x4*)(lds + c * 1024 + lane * 16);
+        else
+          *(u32x2*)(page + c * 512 + lane * 8) = *(const u32x2*)(lds + c * 512 + lane * 8);
+      }
       if (!two_rounds)
         for (int c = 0; c < nch; ++c)
-          *(u32x2*)(page + 64 * kp * 2 + c * 512 + lane * 8) =
-              *(const u32x2*)(lds + 64 * kp * 2 + c * 512 + lane * 8);
+          *(u32x2*)(page + vregion + c * 512 + lane * 8) =
+              *(const u32x2*)(lds + vregion + c * 512 + lane * 8);
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
     if (two_rounds) {  // indices: the same selection again, then their chunks
       if (sparse)
-        emit_slots<false, true>(v, tau_keep, need_keep, k, npad, nullptr,
-                                (uint8_t*)lds + lane * 8);
+        emit_slots<F, false, true>(v, tau_keep, need_keep, k, npad, nullptr,
+                                   (uint8_t*)lds + lane * 8);
       __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
       __builtin_amdgcn_wave_barrier();
       if (sparse)
         for (int c = 0; c < nch; ++c)
-          *(u32x2*)(page + 64 * kp * 2 + c * 512 + lane * 8) =
+          *(u32x2*)(page + vregion + c * 512 + lane * 8) =
               *(const u32x2*)(lds + c * 512 + lane * 8);
       __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
       __builtin_amdgcn_wave_barrier();
@@ -290,8 +309,11 @@ int prefill_groups(int max_new_tokens, int min_len_old) {
 
 hipError_t launch_prefill(const CompressLaunch& a) {
   const int units = a.B * a.Hkv * 2;
-  hipLaunchKernelGGL(prefill_kernel, dim3((int64_t)units * a.prefill_groups), dim3(64), 0,
-                     a.stream, a);
+  const dim3 grid((int64_t)units * a.prefill_groups);
+  if (a.dtype == SWAN_F16_E4M3)
+    hipLaunchKernelGGL(prefill_kernel<E4M3V>, grid, dim3(64), 0, a.stream, a);
+  else
+    hipLaunchKernelGGL(prefill_kernel<_Float16>, grid, dim3(64), 0, a.stream, a);
   return hipGetLastError();
 }
 

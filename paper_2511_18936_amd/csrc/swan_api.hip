@@ -33,7 +33,13 @@ swan_status ok() {
   return SWAN_OK;
 }
 
-int elem_bytes(int32_t dtype) { return dtype == SWAN_F16 ? 2 : 4; }
+// bytes of one element of queries, outputs, new keys / values and the ring
+int elem_bytes(int32_t dtype) { return dtype == SWAN_F32 ? 4 : 2; }
+// bytes of one sparse value
+int value_bytes(int32_t dtype) { return dtype == SWAN_F32 ? 4 : dtype == SWAN_F16 ? 2 : 1; }
+bool dtype_ok(int32_t dtype) {
+  return dtype == SWAN_F32 || dtype == SWAN_F16 || dtype == SWAN_F16_E4M3;
+}
 
 swan_status check_cache_shape(const swan_cache* c) {
   if (!c) return fail(SWAN_ERR_INVALID_ARG, "cache descriptor is NULL");
@@ -55,8 +61,7 @@ swan_status check_cache_shape(const swan_cache* c) {
                 swan::kMaxRing);
   if (c->sparse_capacity < 0)
     return fail(SWAN_ERR_INVALID_ARG, "sparse_capacity %d < 0", c->sparse_capacity);
-  if (c->dtype != SWAN_F16 && c->dtype != SWAN_F32)
-    return fail(SWAN_ERR_UNSUPPORTED, "dtype %d not supported", c->dtype);
+  if (!dtype_ok(c->dtype)) return fail(SWAN_ERR_UNSUPPORTED, "dtype %d not supported", c->dtype);
   if (c->reserved != 0) return fail(SWAN_ERR_INVALID_ARG, "reserved field must be 0");
   return SWAN_OK;
 }
@@ -97,7 +102,7 @@ int64_t fill_layout(const swan_cache* c, const int32_t* k_active_host, swan::Seq
   for (int b = 0; b < c->batch; ++b) {
     tab.kact[b] = k_active_host[b];
     tab.page_off[b] = off;
-    off += (int64_t)c->n_kv_heads * npc * swan::page_bytes_of(elem_bytes(c->dtype), k_active_host[b]);
+    off += (int64_t)c->n_kv_heads * npc * swan::page_bytes_of(value_bytes(c->dtype), k_active_host[b]);
   }
   return off;
 }
@@ -158,15 +163,14 @@ extern "C" {
 
 const char* swan_last_error(void) { return g_last_error.c_str(); }
 
-int32_t swan_version(void) { return 101; }
+int32_t swan_version(void) { return 102; }
 
 swan_status swan_page_bytes(int32_t dtype, int32_t k_active, size_t* bytes) {
   if (!bytes) return fail(SWAN_ERR_INVALID_ARG, "bytes is NULL");
-  if (dtype != SWAN_F16 && dtype != SWAN_F32)
-    return fail(SWAN_ERR_UNSUPPORTED, "dtype %d not supported", dtype);
+  if (!dtype_ok(dtype)) return fail(SWAN_ERR_UNSUPPORTED, "dtype %d not supported", dtype);
   if (k_active < 1 || k_active > SWAN_HEAD_DIM)
     return fail(SWAN_ERR_INVALID_ARG, "k_active %d outside 1..%d", k_active, SWAN_HEAD_DIM);
-  *bytes = (size_t)swan::page_bytes_of(elem_bytes(dtype), k_active);
+  *bytes = (size_t)swan::page_bytes_of(value_bytes(dtype), k_active);
   return ok();
 }
 

@@ -93,6 +93,51 @@ struct Store<float> {
   __device__ static uint32_t mag(Bits b) { return b & 0x7FFFFFFFu; }
 };
 
+// fp16 bits -> OCP FP8 E4M3 (bias 7, no infinities, 0x7f = NaN): nearest
+// value, ties to the even code, magnitudes above 448 (and infinities) to 448,
+// NaN to NaN, sign kept.  Integer arithmetic only: the fp16 value is
+// sig * 2^e2 with an 11-bit significand; the E4M3 quantum at its magnitude is
+// 2^eq with eq = max(E, -6) - 3 (E = its binary exponent), so the code is
+// (eq + 9) * 8 + round(sig / 2^(eq - e2)) for subnormal and normal results
+// alike (a rounding carry moves into the exponent field by itself).
+__device__ __forceinline__ uint32_t f16_bits_to_e4m3(uint32_t h) {
+  const uint32_t sign = (h >> 8) & 0x80u;
+  const uint32_t a = h & 0x7FFFu;
+  if (a >= 0x7C00u) return sign | (a > 0x7C00u ? 0x7Fu : 0x7Eu);
+  if (a == 0u) return sign;
+  const int e16 = (int)(a >> 10);
+  const uint32_t sig = e16 ? (a & 0x3FFu) | 0x400u : a;
+  const int e2 = (e16 ? e16 : 1) - 25;                  // value = sig * 2^e2
+  const int E = (31 - __builtin_clz(sig)) + e2;         // binary exponent
+  const int eq = (E > -6 ? E : -6) - 3;                 // log2 of the E4M3 quantum
+  const int sh = eq - e2;                               // >= 1 for every fp16 input
+  const uint32_t half = 1u << (sh - 1);
+  const uint32_t r = (sig + half - 1u + ((sig >> sh) & 1u)) >> sh;  // round half to even
+  uint32_t code = (uint32_t)((eq + 9) * 8) + r;
+  if (code > 0x7Eu) code = 0x7Eu;                       // saturate at 448
+  return sign | code;
+}
+
+// Storage formats.  The template argument of the decode and compress kernels
+// names the element type of queries, outputs, new keys / values and the dense
+// buffer (Elem) and the layout of sparse values: T values in 16-byte chunks of
+// 16 / sizeof(T) entries, or, for E4M3V, one-byte E4M3 values in 8-byte chunks
+// of 8 entries (with fp16 everywhere else).
+struct E4M3V {};
+
+template <typename T>
+struct Fmt {
+  using Elem = T;
+  static constexpr int kValBytes = (int)sizeof(T);
+  static constexpr int kChunkBytes = 16;
+};
+template <>
+struct Fmt<E4M3V> {
+  using Elem = _Float16;
+  static constexpr int kValBytes = 1;
+  static constexpr int kChunkBytes = 8;
+};
+
 // ---------------------------------------------------------------------------
 // wave64 helpers
 // ---------------------------------------------------------------------------

@@ -69,7 +69,7 @@ struct SeqGroup {
 int gqa_heads_per_wave(int G);
 inline int decode_heads_per_wave(int dtype, int n_q, int n_kv) {
   const int G = n_q / n_kv;
-  return (dtype == SWAN_F16 && G > 1) ? gqa_heads_per_wave(G) : 1;
+  return ((dtype == SWAN_F16 || dtype == SWAN_F16_E4M3) && G > 1) ? gqa_heads_per_wave(G) : 1;
 }
 hipError_t launch_attn_gqa(const DecodeLaunch& a, const SeqGroup& g, int kp8);
 

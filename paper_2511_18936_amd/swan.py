@@ -24,6 +24,7 @@ SWAN_ERR_HIP = 5
 SWAN_ERR_NO_CONVERGENCE = 6
 SWAN_F32 = 0
 SWAN_F16 = 1
+SWAN_F16_E4M3 = 2  # fp16 everywhere, sparse values as OCP FP8 E4M3
 MAX_BATCH = 64
 HEAD_DIM = 128
 PAGE_TOKENS = 64
@@ -124,9 +125,15 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream
 
 
-def dtype_code(torch_dtype) -> int:
+def dtype_code(torch_dtype, sparse_values: str = "same") -> int:
     import torch
 
+    if sparse_values not in ("same", "e4m3"):
+        raise SwanError(SWAN_ERR_INVALID_ARG, f"sparse_values {sparse_values!r}")
+    if sparse_values == "e4m3":
+        if torch_dtype != torch.float16:
+            raise SwanError(SWAN_ERR_UNSUPPORTED, "E4M3 sparse values need float16 storage")
+        return SWAN_F16_E4M3
     if torch_dtype == torch.float16:
         return SWAN_F16
     if torch_dtype == torch.float32:
@@ -202,22 +209,25 @@ class SwanCache:
     """Owns the device arrays of one layer's hybrid cache and the host-side lengths.
 
     The arrays are plain torch tensors (uint8 pages, storage-typed ring); the
-    library only ever receives their device pointers.
+    library only ever receives their device pointers.  sparse_values="e4m3"
+    (float16 only) stores the pruned values as one-byte E4M3 codes.
     """
 
     def __init__(self, batch: int, n_q_heads: int, n_kv_heads: int, buffer_tokens: int,
                  sparse_capacity: int, k_active: Sequence[int], dtype, device,
-                 head_dim: int = HEAD_DIM):
+                 head_dim: int = HEAD_DIM, sparse_values: str = "same"):
         import torch
 
         self.dtype = dtype
+        self.sparse_values = sparse_values
         self.device = torch.device(device)
         self.k_active = [int(k) for k in k_active]
         if len(self.k_active) != batch:
             raise ValueError("k_active needs one entry per sequence")
         self.seq_len = [0] * batch
         self.desc = CacheDesc(batch, n_q_heads, n_kv_heads, head_dim, buffer_tokens,
-                              sparse_capacity, dtype_code(dtype), 0, None, None, None, None)
+                              sparse_capacity, dtype_code(dtype, sparse_values), 0, None, None,
+                              None, None)
         pb, rb = cache_bytes(self.desc, self.k_active)
         # torch's caching allocator returns 256-byte aligned blocks
         self.k_pages = torch.zeros(max(pb, 16), dtype=torch.uint8, device=self.device)

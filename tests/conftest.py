@@ -20,3 +20,17 @@ def gpu_device():
     if not torch.cuda.is_available():
         pytest.skip("no GPU visible")
     return torch.device("cuda:0")
+
+
+@pytest.fixture(scope="session")
+def torch_mod(gpu_device):
+    import torch
+
+    return torch
+
+
+@pytest.fixture(scope="session")
+def swan_mod(gpu_device):
+    from paper_2511_18936_amd import swan
+
+    return swan

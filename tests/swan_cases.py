@@ -68,23 +68,26 @@ def ring_rows(cache, b, h, role, L):
     return ring[pos % bb] if bb else ring[:0]
 
 
-def compare_unit(cache, oc, b, h, L, dtype_np):
-    """Bit-exact comparison of one unit's GPU cache with the oracle's cache dict."""
+def compare_unit(cache, oc, b, h, L, dtype_np, values: str = "same"):
+    """Bit-exact comparison of one unit's GPU cache with the oracle's cache dict
+    (values="e4m3": the sparse values as E4M3 codes, the ring in dtype_np)."""
     S = oc["n_sparse"]
     assert S == max(L - cache.desc.buffer_tokens, 0)
     k = cache.k_active[b]
-    for role, (ik, iv) in enumerate((("k_idx", "k_val"), ("v_idx", "v_val"))):
-        idx, val, pidx, pval = unit_pages(cache, b, h, role, S, dtype_np)
-        bad = np.nonzero(np.any(idx != oc[ik], axis=1))[0]
+    e4m3 = values == "e4m3"
+    for role, r in enumerate(("k", "v")):
+        idx, val, pidx, pval = unit_pages(cache, b, h, role, S, np.uint8 if e4m3 else dtype_np)
+        bad = np.nonzero(np.any(idx != oc[f"{r}_idx"], axis=1))[0]
         assert bad.size == 0, f"role {role}: {bad.size} of {S} tokens select other indices"
-        assert np.array_equal(val.view(np.uint8), np.asarray(oc[iv], dtype_np).view(np.uint8)), \
+        want_val = oc[f"{r}_code"] if e4m3 else np.asarray(oc[f"{r}_val"], dtype_np)
+        assert np.array_equal(val.view(np.uint8), np.asarray(want_val).view(np.uint8)), \
             f"role {role}: values differ"
         if pidx.size:  # padding: value +0 at the lowest dims not kept
-            assert np.all(pval.astype(np.float64) == 0)
+            assert np.all(pval.view(np.uint8) == 0)
             for t in range(S):
-                free = np.setdiff1d(np.arange(128), oc[ik][t])[: pidx.shape[1]]
+                free = np.setdiff1d(np.arange(128), oc[f"{r}_idx"][t])[: pidx.shape[1]]
                 assert np.array_equal(pidx[t], free), f"role {role}: padding of token {t}"
         buf = ring_rows(cache, b, h, role, L)
-        want = oc["k_buf" if role == 0 else "v_buf"]
+        want = oc[f"{r}_buf"]
         assert np.array_equal(np.asarray(buf).view(np.uint8),
                               np.asarray(want, dtype_np).view(np.uint8)), f"role {role}: ring"

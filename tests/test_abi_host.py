@@ -54,6 +54,14 @@ def test_page_and_cache_sizes():
     npc = (1000 + 63) // 64
     assert pb == 2 * npc * 64 * 3 * (48 + 64)
     assert rb == 2 * 2 * 16 * 128 * 2
+    # E4M3 sparse values: one byte per value plus one per index; the ring stays fp16
+    assert swan.page_bytes(swan.SWAN_F16_E4M3, 48) == 64 * 48 * 2
+    assert swan.page_bytes(swan.SWAN_F16_E4M3, 41) == 64 * 48 * 2
+    pb8, rb8 = swan.cache_bytes(_desc(dtype=swan.SWAN_F16_E4M3), [48, 64])
+    assert pb8 == 2 * npc * 64 * 2 * (48 + 64)
+    assert rb8 == rb
+    with pytest.raises(swan.SwanError):
+        swan.page_bytes(3, 48)
 
 
 @pytest.mark.parametrize("kw,status", [

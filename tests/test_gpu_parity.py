@@ -25,20 +25,6 @@ def _log(msg):
     sys.stdout.flush()
 
 
-@pytest.fixture(scope="module")
-def torch_mod(gpu_device):
-    import torch
-
-    return torch
-
-
-@pytest.fixture(scope="module")
-def swan_mod(gpu_device):
-    from paper_2511_18936_amd import swan
-
-    return swan
-
-
 # --------------------------------------------------------------------------- #
 # calibration (Sec. 4.1.2)
 # --------------------------------------------------------------------------- #
@@ -75,7 +61,7 @@ def test_calibrate_constructed_basis(gpu_device):
 # compress-append: indices and values bit-exact
 # --------------------------------------------------------------------------- #
 def _build(swan_mod, torch_mod, device, *, B, Hq, Hkv, L, b, k_active, dtype, chunks=None,
-           seed=0, capacity=None, wid=99):
+           seed=0, capacity=None, wid=99, values="same"):
     """GPU cache + oracle caches for synthetic rows of the recipe."""
     torch = torch_mod
     np_dt = si.np_dtype(dtype)
@@ -93,7 +79,8 @@ def _build(swan_mod, torch_mod, device, *, B, Hq, Hkv, L, b, k_active, dtype, ch
             K[bi, h] = si.lowrank_rows(si.rng_for(wid, seed, bi, h, 0), Lmax, R).astype(np_dt)
             V[bi, h] = si.lowrank_rows(si.rng_for(wid, seed, bi, h, 1), Lmax, R).astype(np_dt)
     cap = capacity if capacity is not None else max(Lmax - b, 1)
-    cache = swan_mod.SwanCache(B, Hq, Hkv, b, cap, k_active, C.torch_dtype(dtype), device)
+    cache = swan_mod.SwanCache(B, Hq, Hkv, b, cap, k_active, C.torch_dtype(dtype), device,
+                               sparse_values=values)
     tP_qk = torch.tensor(Pqk, device=device)
     tP_vo = torch.tensor(Pvo, device=device)
     # sequences of different lengths: each chunk appends min(n, what is left)
@@ -112,8 +99,10 @@ def _build(swan_mod, torch_mod, device, *, B, Hq, Hkv, L, b, k_active, dtype, ch
         t0 += n
     assert cache.seq_len == Ls
     torch.cuda.synchronize()
+    ovals = "e4m3" if values == "e4m3" else "t"
     oc = [[O.compress_block(K[bi, h, :Ls[bi]], V[bi, h, :Ls[bi]], Pqk[h], Pvo[h], b,
-                            k_active[bi], np_dt) for h in range(Hkv)] for bi in range(B)]
+                            k_active[bi], np_dt, values=ovals) for h in range(Hkv)]
+          for bi in range(B)]
     return cache, oc, Pqk, Pvo, tP_qk, tP_vo, K, V
 
 
