@@ -75,15 +75,21 @@ def read_traffic(wl: str, digest: str):
         return None
 
 
+def value_bytes(w, esize):
+    """Bytes of one stored sparse value (one for 8-bit E4M3 values)."""
+    return 1 if w.sparse_values == "e4m3" else esize
+
+
 def attention_bytes(w, seq_len, k_active, esize):
     """Algorithmic bytes of one attention launch: every sparse (value, index) pair of
     keys and values once, plus the dense buffer of keys and values once."""
     total = 0
+    vb = value_bytes(w, esize)
     for b in range(w.batch):
         L = seq_len[b]
         S = max(L - w.buffer, 0)
         nb = min(L, w.buffer)
-        per_head = S * 2 * k_active[b] * (esize + 1) + 2 * nb * w.head_dim * esize
+        per_head = S * 2 * k_active[b] * (vb + 1) + 2 * nb * w.head_dim * esize
         total += w.n_kv_heads * per_head
     return total
 
@@ -119,6 +125,7 @@ def cpu_baseline(w, n_units: int):
 
     ks = si.k_active_for(w)
     np_dt = si.np_dtype(w.dtype)
+    vals = "e4m3" if w.sparse_values == "e4m3" else "t"
     L = w.context
     units = []
     for u in range(n_units):
@@ -128,17 +135,17 @@ def cpu_baseline(w, n_units: int):
         K = si.kv_rows_host(w.wid, b, h, si.ROLE_K, L, w.dtype)
         V = si.kv_rows_host(w.wid, b, h, si.ROLE_V, L, w.dtype)
         # cache state after the step's append (the attention input) ...
-        c = O.compress_block(K, V, Pqk, Pvo, w.buffer, int(ks[b]), np_dt)
+        c = O.compress_block(K, V, Pqk, Pvo, w.buffer, int(ks[b]), np_dt, values=vals)
         # ... and the buffer just before it (the append input)
         c_prev = O.compress_block(K[L - 1 - w.buffer:L - 1], V[L - 1 - w.buffer:L - 1], Pqk, Pvo,
-                                  w.buffer, int(ks[b]), np_dt)
+                                  w.buffer, int(ks[b]), np_dt, values=vals)
         q = si.queries_host(w.wid, 1, 1, w.dtype)[0, 0].astype(np.float64)
         units.append((Pqk, Pvo, c, c_prev, K[L - 1], V[L - 1], q, int(ks[b])))
     t_append, t_attend = [], []
     with threadpool_limits(limits=1):
         for rep in range(2):
             for Pqk, Pvo, c, c_prev, kl, vl, q, k in units:
-                uc = O.UnitCache(Pqk, Pvo, w.buffer, k, np_dt)
+                uc = O.UnitCache(Pqk, Pvo, w.buffer, k, np_dt, values=vals)
                 uc.k_buf.extend(list(c_prev["k_buf"]))
                 uc.v_buf.extend(list(c_prev["v_buf"]))
                 t0 = time.perf_counter()
@@ -208,7 +215,8 @@ def main():
     qs = [si.queries_device(w.wid, w.batch, w.n_q_heads, w.dtype, dev, step=i)
           for i in range(n_extra)]
     capacity = max(w.context + n_extra - w.buffer, 1)
-    cache = swan.SwanCache(w.batch, w.n_q_heads, w.n_kv_heads, w.buffer, capacity, ks, tdt, dev)
+    cache = swan.SwanCache(w.batch, w.n_q_heads, w.n_kv_heads, w.buffer, capacity, ks, tdt, dev,
+                           sparse_values=w.sparse_values)
     torch.cuda.synchronize()
     log(f"[bench] inputs ready in {time.perf_counter() - t:.1f}s "
         f"(raw K/V {2 * Kp.numel() * esize / 1e9:.2f} GB, pages {cache.k_pages.numel() * 2 / 1e9:.2f} GB)")
@@ -221,7 +229,7 @@ def main():
     torch.cuda.synchronize()
     t_prefill = e0.elapsed_time(e1) * 1e-3
     prefill_bytes = 2 * Kp.numel() * esize + sum(
-        2 * w.n_kv_heads * max(L0 - w.buffer, 0) * k * (esize + 1) for k in ks)
+        2 * w.n_kv_heads * max(L0 - w.buffer, 0) * k * (value_bytes(w, esize) + 1) for k in ks)
     log(f"[bench] prefill compress of {L0} tokens: {t_prefill * 1e3:.2f} ms "
         f"({prefill_bytes / t_prefill / 1e9:.0f} GB/s algorithmic)")
     del Kp, Vp
@@ -320,6 +328,7 @@ def main():
             "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "context": w.context,
             "buffer": w.buffer, "k_active": ks if not w.k_active else w.k_active,
             "storage": w.dtype, "index": "u8",
+            "sparse_values": "e4m3" if w.sparse_values == "e4m3" else w.dtype,
         },
         "roofline": {
             "bound": "hbm",

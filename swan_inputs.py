@@ -51,6 +51,7 @@ class Workload:
     prefill: int = 0
     k_choices: Tuple[int, ...] = ()
     description: str = ""
+    sparse_values: str = "same"  # "same" (values stored in dtype) or "e4m3" (8-bit)
 
     @property
     def group(self) -> int:
@@ -72,6 +73,10 @@ WORKLOADS = {
                  prefill=16384, k_choices=(32, 48, 64, 96),
                  description="Llama-2-7B layer, B=8, prefill 16384 then decode, k per sequence "
                              "from {32,48,64,96}, b=128, fp16"),
+        Workload(5, "llama2_7b_L32k_b16_e4m3", 16, 32, 32, 128, 32768, 128, 48, "f16",
+                 sparse_values="e4m3",
+                 description="the 32k x 16 Llama-2-7B layer with 8-bit (E4M3) sparse values, "
+                             "fp16 buffer, k=48"),
     )
 }
 WORKLOAD_BY_ID = {w.wid: w for w in WORKLOADS.values()}

@@ -48,7 +48,8 @@ def _run(device, name: str, n_units: int):
     V1 = si.kv_rows_device(w.wid, w.batch, w.n_kv_heads, si.ROLE_V, 1, w.dtype, device, block=1)
     q = si.queries_device(w.wid, w.batch, w.n_q_heads, w.dtype, device)
     cache = swan.SwanCache(w.batch, w.n_q_heads, w.n_kv_heads, w.buffer, L - w.buffer, ks,
-                           C.torch_dtype(w.dtype), device)
+                           C.torch_dtype(w.dtype), device, sparse_values=w.sparse_values)
+    vals = "e4m3" if w.sparse_values == "e4m3" else "t"
     cache.append(K, V, Pqk, Pvo)
     cache.append(K1, V1, Pqk, Pvo)
     out = cache.decode(q, Pqk, Pvo)
@@ -66,8 +67,8 @@ def _run(device, name: str, n_units: int):
     for b, h in units:
         Kh = np.concatenate([K[b, h].cpu().numpy(), K1[b, h].cpu().numpy()])
         Vh = np.concatenate([V[b, h].cpu().numpy(), V1[b, h].cpu().numpy()])
-        oc = O.compress_block(Kh, Vh, P_qk[h], P_vo[h], w.buffer, ks[b], np_dt)
-        C.compare_unit(cache, oc, b, h, L, np_dt)
+        oc = O.compress_block(Kh, Vh, P_qk[h], P_vo[h], w.buffer, ks[b], np_dt, values=vals)
+        C.compare_unit(cache, oc, b, h, L, np_dt, values=w.sparse_values)
         for hq in range(h * G, (h + 1) * G):
             ref = O.attend_arrays(q_np[b, hq], P_qk[h], P_vo[h], oc)
             err = C.max_rel_err(out_np[b, hq][None], ref[None])
@@ -87,3 +88,7 @@ def test_llama3_8b_gqa_128k_batch4(gpu_device):
 
 def test_prefill16k_batch8_per_sequence_k(gpu_device):
     _run(gpu_device, "llama2_7b_prefill16k_b8", 8)
+
+
+def test_llama2_7b_32k_batch16_e4m3_values(gpu_device):
+    _run(gpu_device, "llama2_7b_L32k_b16_e4m3", 4)
