@@ -1,23 +1,28 @@
 // Decode attention on the hybrid SWAN cache (Algorithm 1, attention part).
 //
-// Three launches on the caller's stream:
+// Launches, in order on the caller's stream:
 //   qrot_kernel    q_hat = q . P_QK[g], pre-multiplied by scale * log2(e)
 //   attn_kernel    one wave per (sequence, query head, token split) over the
 //                  sparse pages, plus one wave per (sequence, query head) over
 //                  the dense buffer; each writes a partial (m, l, acc[128]) in
-//                  the rotated space
+//                  the rotated space.  One launch per distinct k_pad of the
+//                  batch; several run side by side on library-owned streams,
+//                  joined back before the merge.  For fp16 GQA the launch is
+//                  attn_gqa_kernel (decode_gqa.hip) instead, one workgroup per
+//                  KV stream for several query heads.
 //   merge_kernel   log-sum-exp merge of the partials, then o = o_hat . P_VO^T
 //                  (the inverse rotation that Sec. 4.2 absorbs into W_O)
 //
-// Sparse wave: one token per lane.  The rotated query is replicated 32 times
-// in LDS (q_rep[dim][32]) so that the per-lane gathers q_hat[idx] of a half
-// wave never share a bank; the value accumulator is acc[dim][32] in LDS,
-// shared by lanes l and l+32 and updated with LDS float atomics.  Pages of
-// keys and values are streamed with 16-byte coalesced loads, the next page in
-// flight while the current one is consumed.  The softmax reference m is the
-// first page's maximum and is only raised (with a rescale of acc) when a page
-// maximum exceeds it by more than kTau in log2 units, so exponentials stay
-// bounded by 2^kTau while rescales are rare.
+// Sparse wave: one token per lane.  The rotated query is replicated 8 times in
+// LDS (q_rep[dim][8]) so that the gathers q_hat[idx] of 8 consecutive lanes
+// fall on distinct banks; the value accumulator is lane-private, acc[dim][64]
+// in LDS: a token's indices are distinct, so each page's update is a plain
+// read-modify-write with all reads issued before the writes.  Pages of keys
+// and values are streamed with coalesced nontemporal loads, the page after
+// next in flight while the current one is consumed.  The softmax reference m
+// is the first page's maximum and is only raised (with a rescale of acc) when
+// a score exceeds it by more than kTau in log2 units (one ballot per page), so
+// exponentials stay bounded by 2^kTau while rescales are rare.
 #include <mutex>
 
 #include "decode_common.h"
@@ -48,11 +53,9 @@ __global__ __launch_bounds__(128) void qrot_kernel(const T* __restrict__ q,
 // LDS layouts of one wave (a workgroup is one wave):
 //   qrep[dim][8]   the rotated query, 8 copies so that lanes l, l+8, ... of a
 //                  half wave spread over the banks
-//   acc[dim][C]    accumulators: lane t owns column t % C (C = kAccCols), so
-//                  within one pass no two lanes update the same word
+//   acc[dim][64]   accumulators: lane t owns column t, so no two lanes ever
+//                  update the same word
 constexpr int kQRep = 8;
-// accumulator columns: 64 = one per lane; 32 = lanes l and l+32 share column
-// l, updated in two half-wave passes (half the LDS, twice the waves per CU)
 constexpr int kAccCols = 64;
 
 template <typename T, int KP8>
@@ -69,9 +72,9 @@ __device__ __forceinline__ float page_score(const PageRegs<T, KP8>& r, const flo
   return s0 + s1;
 }
 
-// acc[idx][lane] += p * v for the k entries of this lane's token.  A token's
-// indices are distinct, so the reads of a chunk can all be issued before its
-// writes; chunks of 16 entries bound the live registers.
+// acc[idx][lane] += p * v for entries of groups G0 .. G0 + NG - 1 of this
+// lane's token.  A token's indices are distinct, so all reads of the chunk can
+// be issued before its writes.
 template <typename T, int KP8, int G0, int NG>
 __device__ __forceinline__ void accumulate_groups(const PageRegs<T, KP8>& r, float* acc_l,
                                                   float p) {
@@ -91,34 +94,17 @@ __device__ __forceinline__ void accumulate_groups(const PageRegs<T, KP8>& r, flo
     for (int u = 0; u < 8; ++u) acc_l[entry_idx(r, G0 + g, u) * kAccCols] = a[g * 8 + u];
 }
 
-// acc[idx][lane] += p * v for the k entries of this lane's token.  A token's
-// indices are distinct, so every read of a chunk is issued before its writes
-// (one LDS round trip per chunk); up to 64 entries form one chunk.
+// acc[idx][lane] += p * v for the k entries of this lane's token, in chunks
+// of up to 64 entries (one LDS round trip per chunk).
 template <typename T, int KP8>
-__device__ __forceinline__ void page_accumulate_lanes(const PageRegs<T, KP8>& r, float* acc_l,
-                                                      float p) {
+__device__ __forceinline__ void page_accumulate(const PageRegs<T, KP8>& r, float* acc_l, float p,
+                                                bool valid) {
+  if (!valid) return;
   if constexpr (KP8 <= 8) {
     accumulate_groups<T, KP8, 0, KP8>(r, acc_l, p);
   } else {
     accumulate_groups<T, KP8, 0, 8>(r, acc_l, p);
     accumulate_groups<T, KP8, 8, KP8 - 8>(r, acc_l, p);
-  }
-}
-
-template <typename T, int KP8>
-__device__ __forceinline__ void page_accumulate(const PageRegs<T, KP8>& r, float* acc_l, float p,
-                                                bool valid, int lane) {
-  if constexpr (kAccCols == 64) {
-    if (valid) page_accumulate_lanes<T, KP8>(r, acc_l, p);
-  } else {
-    // two half-wave passes: within a pass every lane owns its column; the
-    // fence keeps the passes in program order (LDS executes a wave's
-    // accesses in that order)
-#pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      if (valid && (lane >> 5) == half) page_accumulate_lanes<T, KP8>(r, acc_l, p);
-      wave_lds_fence();
-    }
   }
 }
 
@@ -153,7 +139,7 @@ __device__ __forceinline__ void process_page(const PageRegs<T, KP8>& kr, const P
   }
   const float p = valid ? exp2f(s - st.m) : 0.f;
   st.l += p;
-  page_accumulate<T, KP8>(vr, acc_l, p, valid, lane);
+  page_accumulate<T, KP8>(vr, acc_l, p, valid);
 }
 
 // One wave: pages [pbeg, pend) of one (sequence, kv head), for one query head.

@@ -1,6 +1,6 @@
 // Decode attention for grouped-query attention (GQA, G query heads per KV
-// head), fp16 storage: one workgroup of two waves streams a KV head's pages
-// once for GH of its query heads.
+// head), fp16 storage with fp16 or E4M3 sparse values: one workgroup of two
+// waves streams a KV head's pages once for GH of its query heads.
 //
 // Per 64-token page (one token per lane in each wave):
 //   score wave  holds the key pages: s_h = q_hat_h . k for the GH heads, one
