@@ -30,6 +30,7 @@ typedef double d4 __attribute__((ext_vector_type(4)));
 
 constexpr int kRowHalves = 136;                // LDS row of one token's 128 fp16 values (+ pad)
 constexpr int kPrefillBlocksPerWave = 4;       // 64-position blocks per wave
+constexpr int kXcds = 8;                       // MI355X: 8 XCDs, each with its own L2
 constexpr int kStageBytes = 64 * kRowHalves * 2;  // the rows, then the page copy
 // a page (64 * k_pad * 3 bytes) fits the copy up to k_pad 88; above, values and
 // indices are emitted and stored in two rounds
@@ -135,14 +136,19 @@ void prefill_kernel(CompressLaunch a) {
   const int lane = threadIdx.x;
   const int q = lane >> 4, r16 = lane & 15;
   // grid: (b, h, role, block group)
-  int w = blockIdx.x;
+  // Workgroups go to the 8 XCDs round-robin by id, so XCD id % 8 gets the
+  // (head, role) pairs u = xcd, xcd + 8, ...: its L2 then holds 1/8 of the P
+  // matrices instead of all of them.  Pairs are padded to a multiple of 8.
+  const int xcd = blockIdx.x % kXcds;
+  int w = blockIdx.x / kXcds;
   const int ngrp = a.prefill_groups;
   const int grp = w % ngrp;
   w /= ngrp;
-  const int role = w & 1;
-  w >>= 1;
-  const int h = w % a.Hkv;
-  const int b = w / a.Hkv;
+  const int b = w % a.B;
+  const int u = xcd + kXcds * (w / a.B);  // (head, role) pair
+  if (u >= 2 * a.Hkv) return;
+  const int h = u >> 1;
+  const int role = u & 1;
   const int len_old = a.tab.len[b];
   const int nnew = a.tab.nnew[b];
   if (nnew <= 0) return;
@@ -166,7 +172,7 @@ void prefill_kernel(CompressLaunch a) {
 
   for (int blk = bbeg; blk < bend; ++blk) {
     const int pos0 = blk * kPage;
-    // ---- rotation: two halves of the output dims x 4 passes of 16 tokens,
+    // ---- rotation: 4 quarters of the output dims x 4 passes of 16 tokens,
     //      results rounded to fp16 into LDS rows ----
 #pragma unroll 1
     for (int nh = 0; nh < 4; ++nh) {
@@ -205,12 +211,12 @@ void prefill_kernel(CompressLaunch a) {
           for (int nt = 0; nt < 2; ++nt)
           {
             float pv = pb[nt][ks];
-            asm volatile("" : "+v"(pv));  // convert per pass: 128 doubles would not fit
+            asm volatile("" : "+v"(pv));  // convert per use: as doubles pb would not fit
             acc[nt] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, (double)pv, acc[nt], 0, 0, 0);
           }
         }
         // f64 MFMA result layout: register v of lane l holds D[l / 16 + 4 v][l % 16],
-        // i.e. token row q + 4 v of the pass, output dim 64 nh + 16 nt + r16
+        // i.e. token row q + 4 v of the pass, output dim 32 nh + 16 nt + r16
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
@@ -308,8 +314,8 @@ int prefill_groups(int max_new_tokens, int min_len_old) {
 }
 
 hipError_t launch_prefill(const CompressLaunch& a) {
-  const int units = a.B * a.Hkv * 2;
-  const dim3 grid((int64_t)units * a.prefill_groups);
+  const int pairs = (2 * a.Hkv + kXcds - 1) / kXcds * kXcds;  // (head, role), padded
+  const dim3 grid((int64_t)pairs * a.B * a.prefill_groups);
   if (a.dtype == SWAN_F16_E4M3)
     hipLaunchKernelGGL(prefill_kernel<E4M3V>, grid, dim3(64), 0, a.stream, a);
   else
