@@ -3,7 +3,7 @@
 //
 //   gram_kernel     G = S^T S in float64 (products of float32 are exact in
 //                   float64), 16x16 output tile per workgroup
-//   jacobi_kernel   one workgroup: parallel cyclic Jacobi on G in float64 with
+//   jacobi_kernel   one workgroup, G held in LDS: parallel cyclic Jacobi in float64 with
 //                   round-robin pairing (64 disjoint rotations per round, 127
 //                   rounds per sweep) until the off-diagonal mass is negligible;
 //                   then columns sorted by eigenvalue (descending, stable),
@@ -46,25 +46,38 @@ __device__ __forceinline__ void rr_pair(int r, int i, int& p, int& q) {
   q = a < b ? b : a;
 }
 
-__global__ __launch_bounds__(1024) void jacobi_kernel(double* __restrict__ A,
+constexpr int kLdA = kD + 1;  // LDS row stride of A, in doubles
+
+__global__ __launch_bounds__(1024) void jacobi_kernel(double* __restrict__ Ag,
                                                       double* __restrict__ V,
                                                       float* __restrict__ P_out,
                                                       float* __restrict__ sigma_out,
                                                       int32_t* __restrict__ status) {
+  // A lives in LDS for the whole solve, rows padded to kLdA doubles so that a
+  // column walk (one row per lane) spreads over the banks.  The eigenvectors
+  // are kept transposed in the workspace, W = V^T: the column updates V J are
+  // row updates of W, contiguous across lanes.
+  extern __shared__ __attribute__((aligned(16))) double A[];  // [kD][kLdA]
+  double* __restrict__ W = V;
   __shared__ double cs_c[kD / 2], cs_s[kD / 2];
   __shared__ int pp[kD / 2], qq[kD / 2];
   __shared__ double red[1024 / 64];
+  __shared__ double red2[1024 / 64];
   __shared__ int done;
   const int tid = threadIdx.x;
-  for (int e = tid; e < kD * kD; e += 1024) V[e] = (e / kD == e % kD) ? 1.0 : 0.0;
+  for (int e = tid; e < kD * kD; e += 1024) {
+    A[(e / kD) * kLdA + e % kD] = Ag[e];
+    W[e] = (e / kD == e % kD) ? 1.0 : 0.0;
+  }
   if (tid == 0) done = 0;
   __syncthreads();
+  constexpr int kPerThread = (kD / 2) * kD / 1024;  // (pair, row) updates per thread
   int sweep = 0;
   for (; sweep < kJacobiMaxSweeps; ++sweep) {
     // convergence test: off-diagonal Frobenius mass vs the diagonal's
     double off = 0.0, dia = 0.0;
     for (int e = tid; e < kD * kD; e += 1024) {
-      const double v = A[e];
+      const double v = A[(e / kD) * kLdA + e % kD];
       if (e / kD == e % kD) dia += v * v; else off += v * v;
     }
 #pragma unroll
@@ -72,7 +85,6 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(double* __restrict__ A,
       off += __shfl_xor(off, o, 64);
       dia += __shfl_xor(dia, o, 64);
     }
-    __shared__ double red2[1024 / 64];
     if ((tid & 63) == 0) {
       red[tid / 64] = off;
       red2[tid / 64] = dia;
@@ -94,8 +106,8 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(double* __restrict__ A,
         rr_pair(r, tid, p, q);
         pp[tid] = p;
         qq[tid] = q;
-        const double apq = A[p * kD + q];
-        const double app = A[p * kD + p], aqq = A[q * kD + q];
+        const double apq = A[p * kLdA + q];
+        const double app = A[p * kLdA + p], aqq = A[q * kLdA + q];
         double c = 1.0, s = 0.0;
         if (fabs(apq) > 1e-300 && fabs(apq) > 1e-18 * sqrt(fabs(app) * fabs(aqq))) {
           const double tau = (aqq - app) / (2.0 * apq);
@@ -107,18 +119,32 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(double* __restrict__ A,
         cs_s[tid] = s;
       }
       __syncthreads();
-      // A <- A J and V <- V J (column pairs)
+      // V <- V J, i.e. rows p, q of W: all of this thread's loads first
+      {
+        double wp[kPerThread], wq[kPerThread];
+#pragma unroll
+        for (int u = 0; u < kPerThread; ++u) {
+          const int e = tid + 1024 * u, i = e / kD, col = e % kD;
+          wp[u] = W[pp[i] * kD + col];
+          wq[u] = W[qq[i] * kD + col];
+        }
+#pragma unroll
+        for (int u = 0; u < kPerThread; ++u) {
+          const int e = tid + 1024 * u, i = e / kD, col = e % kD;
+          const double c = cs_c[i], s = cs_s[i];
+          W[pp[i] * kD + col] = c * wp[u] - s * wq[u];
+          W[qq[i] * kD + col] = s * wp[u] + c * wq[u];
+        }
+      }
+      // A <- A J (column pairs)
       for (int e = tid; e < (kD / 2) * kD; e += 1024) {
         const int i = e / kD, row = e % kD;
         const double c = cs_c[i], s = cs_s[i];
         if (s == 0.0) continue;
         const int p = pp[i], q = qq[i];
-        const double ap = A[row * kD + p], aq = A[row * kD + q];
-        A[row * kD + p] = c * ap - s * aq;
-        A[row * kD + q] = s * ap + c * aq;
-        const double vp = V[row * kD + p], vq = V[row * kD + q];
-        V[row * kD + p] = c * vp - s * vq;
-        V[row * kD + q] = s * vp + c * vq;
+        const double ap = A[row * kLdA + p], aq = A[row * kLdA + q];
+        A[row * kLdA + p] = c * ap - s * aq;
+        A[row * kLdA + q] = s * ap + c * aq;
       }
       __syncthreads();
       // A <- J^T A (row pairs)
@@ -127,9 +153,9 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(double* __restrict__ A,
         const double c = cs_c[i], s = cs_s[i];
         if (s == 0.0) continue;
         const int p = pp[i], q = qq[i];
-        const double ap = A[p * kD + col], aq = A[q * kD + col];
-        A[p * kD + col] = c * ap - s * aq;
-        A[q * kD + col] = s * ap + c * aq;
+        const double ap = A[p * kLdA + col], aq = A[q * kLdA + col];
+        A[p * kLdA + col] = c * ap - s * aq;
+        A[q * kLdA + col] = s * ap + c * aq;
       }
       __syncthreads();
     }
@@ -138,23 +164,23 @@ __global__ __launch_bounds__(1024) void jacobi_kernel(double* __restrict__ A,
   // canonical sign, write float32 P and sigma
   if (tid < kD) {
     const int j = tid;
-    const double lj = A[j * kD + j];
+    const double lj = A[j * kLdA + j];
     int rank = 0;
     for (int i = 0; i < kD; ++i) {
-      const double li = A[i * kD + i];
+      const double li = A[i * kLdA + i];
       rank += (li > lj || (li == lj && i < j)) ? 1 : 0;
     }
     int arg = 0;
     double best = -1.0;
     for (int i = 0; i < kD; ++i) {
-      const double v = fabs(V[i * kD + j]);
+      const double v = fabs(W[j * kD + i]);
       if (v > best) {
         best = v;
         arg = i;
       }
     }
-    const double sgn = V[arg * kD + j] < 0.0 ? -1.0 : 1.0;
-    for (int i = 0; i < kD; ++i) P_out[i * kD + rank] = (float)(sgn * V[i * kD + j]);
+    const double sgn = W[j * kD + arg] < 0.0 ? -1.0 : 1.0;
+    for (int i = 0; i < kD; ++i) P_out[i * kD + rank] = (float)(sgn * W[j * kD + i]);
     if (sigma_out) sigma_out[rank] = (float)sqrt(lj > 0.0 ? lj : 0.0);
   }
   if (tid == 0) {
@@ -168,7 +194,11 @@ hipError_t launch_calibrate(const CalibLaunch& a) {
                      a.n_rows, a.gram);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(jacobi_kernel, dim3(1), dim3(1024), 0, a.stream, a.gram, a.vecs, a.P_out,
+  constexpr size_t kLds = sizeof(double) * kD * kLdA;  // A in LDS
+  e = hipFuncSetAttribute((const void*)jacobi_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                          (int)kLds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(jacobi_kernel, dim3(1), dim3(1024), kLds, a.stream, a.gram, a.vecs, a.P_out,
                      a.sigma_out, a.status);
   return hipGetLastError();
 }
