@@ -237,8 +237,8 @@ __global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup g) {
   const int nsb = a.tab.nsplit[b];
   const int ns = np < nsb ? np : nsb;
   if (split >= ns) return;
-  const int pbeg = (int)((int64_t)split * np / ns);
-  const int pend = (int)((int64_t)(split + 1) * np / ns);
+  const int pbeg = split_begin(split, ns, np);
+  const int pend = split_begin(split + 1, ns, np);
   const int k = a.tab.kact[b];
   const int64_t pbytes = page_bytes_of(Fmt<T>::kValBytes, k);
   const int64_t unit_off = a.tab.page_off[b] + (int64_t)h * a.n_pages_cap * pbytes;

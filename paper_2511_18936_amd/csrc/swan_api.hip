@@ -109,9 +109,10 @@ int64_t fill_layout(const swan_cache* c, const int32_t* k_active_host, swan::Seq
 
 // Token splits per (sequence, query head): about two waves per CU slot in total
 // (measured best for long contexts; SWAN_DECODE_WAVES overrides the target),
-// each sequence cut into equal page ranges carrying about the same bytes (a
-// page weighs k_pad), never more splits than pages.  Fills nsplit[b] (may be
-// NULL); returns the largest.
+// the split count of each sequence following its bytes (a page weighs k_pad);
+// the splits themselves shrink in size (split_begin), and their count is
+// capped so that every split keeps a page.  Fills nsplit[b] (may be NULL);
+// returns the largest.
 int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t* k_active_host,
                 int32_t* nsplit) {
   // waves per sequence and split: one per query head, or one per GH query
@@ -136,7 +137,7 @@ int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t*
     const int np = swan::pages_for(S);
     const int64_t work = (int64_t)np * swan::kpad_of(k_active_host[b]);
     int ns = (int)((work + per_wave - 1) / per_wave);
-    if (ns > np) ns = np;
+    while (ns > 1 && (int64_t)ns * (ns + 1) / 2 > np) --ns;  // every split keeps a page
     if (ns > swan::kMaxSplits) ns = swan::kMaxSplits;
     if (ns < 1) ns = 1;
     if (nsplit) nsplit[b] = ns;

@@ -25,6 +25,17 @@ struct SeqTab {
 
 __host__ __device__ inline int kpad_of(int k) { return (k + 7) & ~7; }
 
+// First page of split s when a sequence's np pages are cut into ns splits of
+// shrinking size (weights ns, ns - 1, ..., 1): the grids are split-major, so
+// the longest splits are dispatched first and the last ones are short, which
+// shortens the tail.  Every split has at least one page when
+// ns (ns + 1) / 2 <= np (the planner keeps to that).
+__host__ __device__ inline int split_begin(int s, int ns, int np) {
+  const int64_t before = (int64_t)s * ns - (int64_t)s * (s - 1) / 2;  // sum_{i<s} (ns - i)
+  const int64_t total = (int64_t)ns * (ns + 1) / 2;
+  return (int)(before * np / total);
+}
+
 __host__ __device__ inline int64_t page_bytes_of(int elem_bytes, int k) {
   return int64_t(kPage) * kpad_of(k) * (elem_bytes + 1);
 }
