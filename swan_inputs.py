@@ -77,6 +77,10 @@ WORKLOADS = {
                  sparse_values="e4m3",
                  description="the 32k x 16 Llama-2-7B layer with 8-bit (E4M3) sparse values, "
                              "fp16 buffer, k=48"),
+        Workload(6, "llama3_8b_gqa_L128k_b4_e4m3", 4, 32, 8, 128, 131072, 256, 64, "f16",
+                 sparse_values="e4m3",
+                 description="the 128k x 4 Llama-3-8B GQA layer with 8-bit (E4M3) sparse "
+                             "values, fp16 buffer, k=64"),
     )
 }
 WORKLOAD_BY_ID = {w.wid: w for w in WORKLOADS.values()}
