@@ -28,6 +28,8 @@ paper states the method (SWAN: Sparse Winnowed Attention, arXiv 2511.18936):
                            with Appendix A.2.
 * ``to_e4m3_codes``        8-bit sparse values (reading 9), by brute force over
                            the format's 127 finite magnitudes.
+* ``k_value``              keys and values pruned to different k (reading 10,
+                           the key/value ablation of Appendix A.5, Table 2).
 
 Readings of the paper used here (where it is silent or ambiguous):
   1. top-k ranks the stored (T-rounded) buffer value, because Algorithm 1 pops
@@ -42,7 +44,12 @@ Readings of the paper used here (where it is silent or ambiguous):
   9. 8-bit sparse values (Sec. 4.3, Sec. 5.1 name 8-bit values without a
      format) are OCP FP8 E4M3 without a scale: the kept T values, rounded to the
      nearest E4M3 value (ties to the even code, saturating at +-448); the
-     selection still ranks the T values (reading 1) and the buffer stays T.
+     selection still ranks the T values (reading 1) and the buffer stays T;
+ 10. Algorithm 1 prunes keys and values to the same k_active; the ablation of
+     Appendix A.5 (Table 2) retains different fractions of the key and the value
+     dimensions.  Here a key keeps its k_active largest components and a value
+     its k_value largest, by the same rule (readings 1-3); k_value defaults to
+     k_active.  A retention ratio r maps to round(r * d_h) components.
 
 Parity status: every function above is pinned by tests/test_oracle_pins.py;
 nothing here is "parity unpinned" except the end-task accuracy of Tables 1-3,
@@ -178,16 +185,18 @@ class UnitCache:
     """Sparse cache + dense FIFO buffer of one (sequence, KV head), as in Algorithm 1.
 
     The buffer holds rotated vectors already rounded to T.  The sparse cache
-    holds, per pruned token, k ascending indices and the T values at them,
-    separately for keys and values.
+    holds, per pruned token, ascending indices and the T values at them,
+    separately for keys (k_active of them) and values (k_value, reading 10).
     """
 
     def __init__(self, P_qk: np.ndarray, P_vo: np.ndarray, buffer_tokens: int,
-                 k_active: int, dtype=np.float16, values: str = "t"):
+                 k_active: int, dtype=np.float16, values: str = "t",
+                 k_value: Optional[int] = None):
         self.P_qk = np.asarray(P_qk, dtype=F64)
         self.P_vo = np.asarray(P_vo, dtype=F64)
         self.b = int(buffer_tokens)
         self.k = int(k_active)
+        self.kv = int(k_active if k_value is None else k_value)
         self.dtype = dtype
         self.values = values  # "t": sparse values in T; "e4m3": 8-bit (reading 9)
         self.k_buf: collections.deque = collections.deque()
@@ -212,7 +221,7 @@ class UnitCache:
             i_k = topk_indices(k_old, self.k)
             self.k_idx.append(i_k)
             self.k_val.append(self._sparse_value(k_old[i_k]))
-            i_v = topk_indices(v_old, self.k)
+            i_v = topk_indices(v_old, self.kv)
             self.v_idx.append(i_v)
             self.v_val.append(self._sparse_value(v_old[i_v]))
 
@@ -230,8 +239,8 @@ class UnitCache:
         return {
             "k_idx": stack(self.k_idx, np.int64, self.k),
             "k_val": stack(self.k_val, vdt, self.k),
-            "v_idx": stack(self.v_idx, np.int64, self.k),
-            "v_val": stack(self.v_val, vdt, self.k),
+            "v_idx": stack(self.v_idx, np.int64, self.kv),
+            "v_val": stack(self.v_val, vdt, self.kv),
             "k_buf": np.stack(list(self.k_buf)) if self.k_buf else np.zeros((0, d), self.dtype),
             "v_buf": np.stack(list(self.v_buf)) if self.v_buf else np.zeros((0, d), self.dtype),
             "n_sparse": n,
@@ -243,13 +252,15 @@ class UnitCache:
 
 def compress_block(K_rows: np.ndarray, V_rows: np.ndarray, P_qk: np.ndarray,
                    P_vo: np.ndarray, buffer_tokens: int, k_active: int,
-                   dtype=np.float16, values: str = "t") -> Dict[str, np.ndarray]:
+                   dtype=np.float16, values: str = "t",
+                   k_value: Optional[int] = None) -> Dict[str, np.ndarray]:
     """Algorithm 1 applied to n tokens of an empty unit, all at once.
 
     Equal, bit for bit, to n successive ``UnitCache.append`` calls (tested):
     the first max(n - b, 0) tokens end up pruned, the last min(n, b) stay dense.
     With values="e4m3" the kept values are stored as 8-bit codes (reading 9):
     "k_code"/"v_code" hold the codes and "k_val"/"v_val" their values.
+    Values keep k_value components (reading 10; default k_active).
     """
     n = K_rows.shape[0]
     b = int(buffer_tokens)
@@ -257,7 +268,7 @@ def compress_block(K_rows: np.ndarray, V_rows: np.ndarray, P_qk: np.ndarray,
     v_hat = to_storage(rotate(V_rows, P_vo), dtype)
     n_sparse = max(n - b, 0)
     k_idx = topk_indices_rows(k_hat[:n_sparse], k_active)
-    v_idx = topk_indices_rows(v_hat[:n_sparse], k_active)
+    v_idx = topk_indices_rows(v_hat[:n_sparse], k_active if k_value is None else k_value)
     out = {
         "k_idx": k_idx,
         "k_val": np.take_along_axis(k_hat[:n_sparse], k_idx, axis=1),

@@ -161,12 +161,14 @@ def test_topk_special_cases():
 # --------------------------------------------------------------------------- #
 # Algorithm 1 end to end: brute force over a dense masked formulation
 # --------------------------------------------------------------------------- #
-def _brute_swan(q, K, V, Pqk, Pvo, b, k, dtype):
+def _brute_swan(q, K, V, Pqk, Pvo, b, k, dtype, kv=None):
     """Independent restatement with Python loops.
 
-    Token t (0-based) of L is dense if t >= L - b, else pruned to its k
-    largest-magnitude rotated components (ties: lower index), the rest zeroed.
+    Token t (0-based) of L is dense if t >= L - b, else its key is pruned to the
+    k largest-magnitude rotated components (ties: lower index) and its value to
+    the kv largest (kv = k unless given), the rest zeroed.
     """
+    kv = k if kv is None else kv
     d = len(q)
     L = len(K)
     def rot(x, P):
@@ -179,8 +181,8 @@ def _brute_swan(q, K, V, Pqk, Pvo, b, k, dtype):
         kh = rnd(rot(K[t], Pqk))
         vh = rnd(rot(V[t], Pvo))
         if t < L - b:
-            for vec in (kh, vh):
-                keep = sorted(range(d), key=lambda j: (-abs(vec[j]), j))[:k]
+            for vec, kk in ((kh, k), (vh, kv)):
+                keep = sorted(range(d), key=lambda j: (-abs(vec[j]), j))[:kk]
                 for j in range(d):
                     if j not in keep:
                         vec[j] = 0.0
@@ -208,6 +210,30 @@ def test_attention_brute_force_tiny(d, dtype):
                 got = uc.attend(q[0])
                 want = _brute_swan(q[0], K[0], V[0], Pqk, Pvo, b, k, dtype)
                 assert np.allclose(got, want, rtol=1e-12, atol=1e-12), (L, k, b)
+
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float16])
+@pytest.mark.parametrize("d", [4, 8])
+def test_attention_brute_force_tiny_asymmetric_k(d, dtype):
+    """Appendix A.5 (Table 2): keys and values pruned to different k (reading 10)."""
+    pairs = [(kk, kv) for kk in range(1, d + 1) for kv in range(1, d + 1) if kk != kv]
+    if d == 8:
+        pairs = [(1, 8), (8, 1), (2, 7), (5, 3), (3, 6), (7, 4)]
+    for L in (1, 5, 12):
+        q, K, V = si.tiny_case(L * 13 + d, d, L)
+        Pqk = si.random_orthogonal(L + 3, d)
+        Pvo = si.random_orthogonal(L + 4, d)
+        for kk, kv in pairs:
+            for b in (0, 2, L):
+                uc = O.UnitCache(Pqk, Pvo, b, kk, dtype, k_value=kv)
+                for t in range(L):
+                    uc.append(K[0, t], V[0, t])
+                got = uc.attend(q[0])
+                want = _brute_swan(q[0], K[0], V[0], Pqk, Pvo, b, kk, dtype, kv)
+                assert np.allclose(got, want, rtol=1e-12, atol=1e-12), (L, kk, kv, b)
+                arr = uc.sparse_arrays()
+                assert arr["k_idx"].shape == (max(L - b, 0), kk)
+                assert arr["v_idx"].shape == (max(L - b, 0), kv)
 
 
 # --------------------------------------------------------------------------- #
@@ -271,6 +297,38 @@ def test_prefill_equals_token_by_token_appends(b, k):
         assert np.array_equal(a[key], c[key]), key
     assert a["n_sparse"] == c["n_sparse"] == max(L - b, 0)
     assert np.array_equal(uc.attend(q[0]), O.attend_arrays(q[0], Pqk, Pvo, c))
+
+
+@pytest.mark.parametrize("b,kk,kv", [(0, 77, 51), (8, 13, 115), (4, 128, 1), (16, 51, 77)])
+def test_asymmetric_prefill_equals_appends_and_splits_by_role(b, kk, kv):
+    """Reading 10: the key side of a (k_key, k_value) cache is the k_key cache's,
+    the value side the k_value cache's, and a block equals token-by-token appends."""
+    d, L = 128, 70
+    q, K, V = si.tiny_case(40 + kk + kv, d, L)
+    K16, V16 = K.astype(np.float16), V.astype(np.float16)
+    Pqk = si.random_orthogonal(41, d)
+    Pvo = si.random_orthogonal(42, d)
+    uc = O.UnitCache(Pqk, Pvo, b, kk, np.float16, k_value=kv)
+    for t in range(L):
+        uc.append(K16[0, t], V16[0, t])
+    a = uc.sparse_arrays()
+    c = O.compress_block(K16[0], V16[0], Pqk, Pvo, b, kk, np.float16, k_value=kv)
+    ck = O.compress_block(K16[0], V16[0], Pqk, Pvo, b, kk, np.float16)
+    cv = O.compress_block(K16[0], V16[0], Pqk, Pvo, b, kv, np.float16)
+    for key in ("k_idx", "k_val", "v_idx", "v_val", "k_buf", "v_buf"):
+        assert np.array_equal(a[key], c[key]), key
+    for key in ("k_idx", "k_val"):
+        assert np.array_equal(c[key], ck[key]), key
+    for key in ("v_idx", "v_val"):
+        assert np.array_equal(c[key], cv[key]), key
+    assert np.array_equal(uc.attend(q[0]), O.attend_arrays(q[0], Pqk, Pvo, c))
+
+
+def test_table2_ratios_map_to_components():
+    """Appendix A.5, Table 2: the retention pairs sum to 1, so k_key + k_value = d_h."""
+    for rk in range(1, 10):
+        kk, kv = round(rk / 10 * 128), round((10 - rk) / 10 * 128)
+        assert kk + kv == 128 and 1 <= kk <= 127
 
 
 def test_column_sign_flip_changes_nothing_but_signs():
