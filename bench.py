@@ -25,8 +25,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic_{wl}.txt")
 # sources of the decode attention kernels: counter summaries are valid only for these bytes
-ATTN_SOURCES = ("decode.hip", "decode_gqa.hip", "decode_common.h", "swan_device.h",
-                "swan_internal.h")
+ATTN_SOURCES = ("decode.hip", "decode_gqa.hip", "decode_score_pass.hip", "decode_value_pass.hip",
+                "decode_common.h", "decode_gqa_common.h", "swan_device.h", "swan_internal.h")
 
 
 def log(*a):
@@ -80,28 +80,45 @@ def value_bytes(w, esize):
     return 1 if w.sparse_values == "e4m3" else esize
 
 
-def attention_bytes(w, seq_len, k_active, esize):
-    """Algorithmic bytes of one attention launch: every sparse (value, index) pair of
-    keys and values once, plus the dense buffer of keys and values once."""
+def attention_bytes(w, seq_len, k_key, k_val, esize):
+    """Algorithmic bytes of one step's attention: every sparse (value, index) pair of
+    the keys (k_key per token) and of the values (k_val) once, plus the dense buffer
+    of keys and values once."""
     total = 0
     vb = value_bytes(w, esize)
     for b in range(w.batch):
         L = seq_len[b]
         S = max(L - w.buffer, 0)
         nb = min(L, w.buffer)
-        per_head = S * 2 * k_active[b] * (vb + 1) + 2 * nb * w.head_dim * esize
+        per_head = S * (k_key[b] + k_val[b]) * (vb + 1) + 2 * nb * w.head_dim * esize
         total += w.n_kv_heads * per_head
     return total
 
 
-def attn_kernel_name(w) -> str:
-    """The decode attention kernel the library launches for this shape (one launch per
-    distinct padded k in the batch)."""
+def kpad(k: int) -> int:
+    return (k + 7) // 8 * 8
+
+
+def attn_kernel_name(w, k_key, k_val) -> str:
+    """The decode attention kernels the library launches for this shape: one launch per
+    distinct padded k in the batch, or a score and a value launch for sequences whose
+    keys and values have different padded k."""
     g = w.n_q_heads // w.n_kv_heads
+    hpw = 1
     if w.dtype == "f16" and g > 1 and g % 2 == 0:
         hpw = 8 if g % 8 == 0 else 4 if g % 4 == 0 else 2
+    if any(kpad(a) != kpad(b) for a, b in zip(k_key, k_val)):
+        value = "gqa_value_kernel" if hpw > 1 else "value_kernel"
+        return (f"score_kernel + {value} (two-pass: keys and values with different k_pad; "
+                f"{hpw} query head(s) per wave, sparse split-K; dense buffer in the value pass)")
+    if hpw > 1:
         return f"attn_gqa_kernel ({hpw} query heads per wave, sparse split-K + dense buffer)"
     return "attn_kernel (one query head per wave, sparse split-K + dense buffer)"
+
+
+def launches_per_step(k_key, k_val) -> int:
+    pairs = {(kpad(a), kpad(b)) for a, b in zip(k_key, k_val)}
+    return sum(1 if a == b else 2 for a, b in pairs)
 
 
 def cpu_model() -> str:
@@ -124,6 +141,8 @@ def cpu_baseline(w, n_units: int):
     from oracle import swan_oracle as O
 
     ks = si.k_active_for(w)
+    kvs = si.k_value_for(w)
+    kvs = ks if kvs is None else kvs
     np_dt = si.np_dtype(w.dtype)
     vals = "e4m3" if w.sparse_values == "e4m3" else "t"
     L = w.context
@@ -135,17 +154,18 @@ def cpu_baseline(w, n_units: int):
         K = si.kv_rows_host(w.wid, b, h, si.ROLE_K, L, w.dtype)
         V = si.kv_rows_host(w.wid, b, h, si.ROLE_V, L, w.dtype)
         # cache state after the step's append (the attention input) ...
-        c = O.compress_block(K, V, Pqk, Pvo, w.buffer, int(ks[b]), np_dt, values=vals)
+        c = O.compress_block(K, V, Pqk, Pvo, w.buffer, int(ks[b]), np_dt, values=vals,
+                             k_value=int(kvs[b]))
         # ... and the buffer just before it (the append input)
         c_prev = O.compress_block(K[L - 1 - w.buffer:L - 1], V[L - 1 - w.buffer:L - 1], Pqk, Pvo,
-                                  w.buffer, int(ks[b]), np_dt, values=vals)
+                                  w.buffer, int(ks[b]), np_dt, values=vals, k_value=int(kvs[b]))
         q = si.queries_host(w.wid, 1, 1, w.dtype)[0, 0].astype(np.float64)
-        units.append((Pqk, Pvo, c, c_prev, K[L - 1], V[L - 1], q, int(ks[b])))
+        units.append((Pqk, Pvo, c, c_prev, K[L - 1], V[L - 1], q, int(ks[b]), int(kvs[b])))
     t_append, t_attend = [], []
     with threadpool_limits(limits=1):
         for rep in range(2):
-            for Pqk, Pvo, c, c_prev, kl, vl, q, k in units:
-                uc = O.UnitCache(Pqk, Pvo, w.buffer, k, np_dt, values=vals)
+            for Pqk, Pvo, c, c_prev, kl, vl, q, k, kv in units:
+                uc = O.UnitCache(Pqk, Pvo, w.buffer, k, np_dt, values=vals, k_value=kv)
                 uc.k_buf.extend(list(c_prev["k_buf"]))
                 uc.v_buf.extend(list(c_prev["v_buf"]))
                 t0 = time.perf_counter()
@@ -189,6 +209,9 @@ def main():
     tdt = {"f16": torch.float16, "f32": torch.float32}[w.dtype]
     esize = 2 if w.dtype == "f16" else 4
     ks = [int(k) for k in si.k_active_for(w)]
+    kvs = si.k_value_for(w)  # None: values keep the keys' k
+    kvs = None if kvs is None else [int(k) for k in kvs]
+    kv_list = ks if kvs is None else kvs
     n_extra = args.warmup + args.steps
     L0 = w.context - 1  # tokens cached before the first measured step
 
@@ -216,10 +239,11 @@ def main():
           for i in range(n_extra)]
     capacity = max(w.context + n_extra - w.buffer, 1)
     cache = swan.SwanCache(w.batch, w.n_q_heads, w.n_kv_heads, w.buffer, capacity, ks, tdt, dev,
-                           sparse_values=w.sparse_values)
+                           sparse_values=w.sparse_values, k_value=kvs)
     torch.cuda.synchronize()
     log(f"[bench] inputs ready in {time.perf_counter() - t:.1f}s "
-        f"(raw K/V {2 * Kp.numel() * esize / 1e9:.2f} GB, pages {cache.k_pages.numel() * 2 / 1e9:.2f} GB)")
+        f"(raw K/V {2 * Kp.numel() * esize / 1e9:.2f} GB, "
+        f"pages {(cache.k_pages.numel() + cache.v_pages.numel()) / 1e9:.2f} GB)")
 
     # ---- prefill compress (Algorithm 1 over L0 tokens at once), timed ----
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -229,7 +253,8 @@ def main():
     torch.cuda.synchronize()
     t_prefill = e0.elapsed_time(e1) * 1e-3
     prefill_bytes = 2 * Kp.numel() * esize + sum(
-        2 * w.n_kv_heads * max(L0 - w.buffer, 0) * k * (value_bytes(w, esize) + 1) for k in ks)
+        w.n_kv_heads * max(L0 - w.buffer, 0) * (k + kv) * (value_bytes(w, esize) + 1)
+        for k, kv in zip(ks, kv_list))
     log(f"[bench] prefill compress of {L0} tokens: {t_prefill * 1e3:.2f} ms "
         f"({prefill_bytes / t_prefill / 1e9:.0f} GB/s algorithmic)")
     del Kp, Vp
@@ -237,9 +262,9 @@ def main():
 
     # workspace sized for the longest step, allocated before timing
     final_len = [L + n_extra for L in cache.seq_len]
-    ws = torch.empty(swan.decode_workspace_bytes(cache.desc, final_len, ks), dtype=torch.uint8,
-                     device=dev)
-    ws_need = max(swan.decode_workspace_bytes(cache.desc, [L + i for L in cache.seq_len], ks)
+    ws = torch.empty(swan.decode_workspace_bytes(cache.desc, final_len, ks, kvs),
+                     dtype=torch.uint8, device=dev)
+    ws_need = max(swan.decode_workspace_bytes(cache.desc, [L + i for L in cache.seq_len], ks, kvs)
                   for i in range(1, n_extra + 1))
     assert ws.numel() >= ws_need
     out = torch.empty((w.batch, w.n_q_heads, 128), dtype=tdt, device=dev)
@@ -251,7 +276,8 @@ def main():
         if evs is not None:
             evs[1].record()
             swan.set_profile_events(evs[2], evs[3])
-        swan.decode_attention(cache.desc, cache.seq_len, ks, qs[i], Pqk, Pvo, out, ws)
+        swan.decode_attention(cache.desc, cache.seq_len, ks, qs[i], Pqk, Pvo, out, ws,
+                              k_value=kvs)
         if evs is not None:
             swan.set_profile_events(None, None)
             evs[4].record()
@@ -277,7 +303,7 @@ def main():
     t_comp = [e[0].elapsed_time(e[1]) * 1e-3 for e in evs]
     t_attn = [e[2].elapsed_time(e[3]) * 1e-3 for e in evs]
     t_dec = [e[1].elapsed_time(e[4]) * 1e-3 for e in evs]
-    bytes_attn = [attention_bytes(w, L, ks, esize) for L in lens]
+    bytes_attn = [attention_bytes(w, L, ks, kv_list, esize) for L in lens]
     attn_avg = float(np.mean(t_attn))
     bytes_avg = float(np.mean(bytes_attn))
     achieved = bytes_avg / attn_avg / 1e9
@@ -327,6 +353,7 @@ def main():
             "workload": w.name, "batch": w.batch, "n_q_heads": w.n_q_heads,
             "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "context": w.context,
             "buffer": w.buffer, "k_active": ks if not w.k_active else w.k_active,
+            "k_value": None if kvs is None else (kvs if not w.k_value else w.k_value),
             "storage": w.dtype, "index": "u8",
             "sparse_values": "e4m3" if w.sparse_values == "e4m3" else w.dtype,
         },
@@ -337,10 +364,10 @@ def main():
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
             "traffic": traffic,
-            "kernel": attn_kernel_name(w),
-            # one launch per distinct padded k in the batch; bytes and time cover all of
-            # a step's attention launches together
-            "launches_per_step": len({(k + 7) // 8 for k in ks}),
+            "kernel": attn_kernel_name(w, ks, kv_list),
+            # one launch per distinct padded k in the batch (two for a two-pass group);
+            # bytes and time cover all of a step's attention launches together
+            "launches_per_step": launches_per_step(ks, kv_list),
             "algorithmic_bytes_per_launch": bytes_avg,
             "avg_launch_ms": attn_avg * 1e3,
             "source_digest": digest,

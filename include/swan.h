@@ -11,6 +11,11 @@
  * buffer; softmax and the weighted sum of values stay in the rotated space and
  * one inverse rotation per head maps the output back (Sec. 4.2, Lemma 2).
  *
+ * Keys and values may keep different numbers of components per sequence
+ * (k_active for the keys, k_value for the values), as in the key/value
+ * retention ablation of Appendix A.5 (Table 2).  Algorithm 1 itself uses one
+ * k_active for both; passing k_value_host = NULL selects that.
+ *
  * Conventions for every entry point:
  *  - Pointers are DEVICE pointers unless the name ends in _host.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
@@ -89,10 +94,12 @@ typedef enum swan_dtype {
  * (e % 8).  A page is 64 * k_pad * (VB + 1) bytes.  Entries 0..k-1 are the kept components in ascending index order;
  * entries k..k_pad-1 are padding with value +0 at the lowest dims that were not
  * kept, so the k_pad indices of a token are distinct (the decode kernel relies
- * on it).  Sequence s owns n_kv_heads * ceil(sparse_capacity / 64)
- * pages of its own k, stored after those of sequences 0..s-1; within it, head h
- * owns the consecutive pages [h * ceil(sparse_capacity / 64), ...).  The keys'
- * pages live in k_pages, the values' in v_pages, with identical layouts.
+ * on it).  The keys' pages live in k_pages and use the sequence's k_active; the
+ * values' pages live in v_pages and use its k_value (k_active when
+ * k_value_host is NULL).  In each array, sequence s owns
+ * n_kv_heads * ceil(sparse_capacity / 64) pages of that role's k, stored after
+ * those of sequences 0..s-1; within it, head h owns the consecutive pages
+ * [h * ceil(sparse_capacity / 64), ...).
  */
 typedef struct swan_cache {
   int32_t batch;            /* sequences, 1..SWAN_MAX_BATCH */
@@ -123,13 +130,16 @@ int32_t swan_version(void);
 swan_status swan_page_bytes(int32_t dtype, int32_t k_active, size_t* bytes);
 
 /*
- * Sizes of the cache arrays: *page_bytes for each of k_pages / v_pages and
- * *ring_bytes for each of k_ring / v_ring.  k_active_host[batch] is each
- * sequence's k (1..head_dim); it fixes the page layout, so every later call on
- * this cache must pass the same values.  The array pointers in `c` are ignored.
+ * Sizes of the cache arrays: *k_page_bytes for k_pages, *v_page_bytes for
+ * v_pages and *ring_bytes for each of k_ring / v_ring.  k_active_host[batch] is
+ * each sequence's k for its keys (1..head_dim); k_value_host[batch], if not
+ * NULL, its k for its values (1..head_dim; NULL: the same as the keys).  They
+ * fix the page layout, so every later call on this cache must pass the same
+ * values.  The array pointers in `c` are ignored.
  */
 swan_status swan_cache_bytes(const swan_cache* c, const int32_t* k_active_host,
-                             size_t* page_bytes, size_t* ring_bytes);
+                             const int32_t* k_value_host, size_t* k_page_bytes,
+                             size_t* v_page_bytes, size_t* ring_bytes);
 
 /* Device workspace needed by swan_calibrate_rotation for head dimension d. */
 swan_status swan_calibrate_workspace_bytes(int32_t d, size_t* bytes);
@@ -153,7 +163,8 @@ swan_status swan_calibrate_rotation(const float* rows, int64_t n_rows, int32_t d
 /*
  * Algorithm 1, compress part, for up to n_new tokens per sequence.
  *  seq_len_host[batch]  tokens already cached per sequence (before this call);
- *  k_active_host[batch] k of each sequence (1..head_dim), as in swan_cache_bytes;
+ *  k_active_host[batch] k of each sequence's keys (1..head_dim), and
+ *  k_value_host[batch]  of its values (NULL: as the keys), as in swan_cache_bytes;
  *  k_new, v_new         [batch][n_kv_heads][n_new][head_dim] storage type, the
  *                       un-rotated (post-RoPE) keys and values;
  *  n_new_host[batch]    tokens to append per sequence, 0..n_new (the first ones
@@ -163,24 +174,32 @@ swan_status swan_calibrate_rotation(const float* rows, int64_t n_rows, int32_t d
  * float64 and rounded once to the storage type) and appended to the buffer;
  * every token that leaves the buffer (position < L_new - b) is pruned to the
  * top-k magnitudes of its stored values (ties: lower index), separately for
- * keys and values, and packed into its page slot.  With b == 0 every token is
+ * keys (k_active) and values (k_value), and packed into its page slot.  With b == 0 every token is
  * pruned on arrival.  Appending n tokens at once gives the same bytes as n
  * single appends.  The caller then adds each sequence's count to its seq_len.
  * Errors: SWAN_ERR_CAPACITY if L_new - b > sparse_capacity for a sequence.
  */
 swan_status swan_compress_append(const swan_cache* c, const int32_t* seq_len_host,
-                                 const int32_t* k_active_host, const void* k_new,
-                                 const void* v_new, int32_t n_new, const int32_t* n_new_host,
-                                 const float* P_qk, const float* P_vo, void* stream);
+                                 const int32_t* k_active_host, const int32_t* k_value_host,
+                                 const void* k_new, const void* v_new, int32_t n_new,
+                                 const int32_t* n_new_host, const float* P_qk,
+                                 const float* P_vo, void* stream);
 
-/* Device workspace needed by swan_decode_attention for these lengths and k. */
+/*
+ * Device workspace needed by swan_decode_attention for these lengths and k.
+ * Sequences whose keys and values have different k_pad are attended in two
+ * passes (scores, then values); their per-token scores take
+ * batch * n_q_heads * (their longest sparse part, rounded up to 64) floats.
+ */
 swan_status swan_decode_workspace_bytes(const swan_cache* c, const int32_t* seq_len_host,
-                                        const int32_t* k_active_host, size_t* bytes);
+                                        const int32_t* k_active_host,
+                                        const int32_t* k_value_host, size_t* bytes);
 
 /*
  * Algorithm 1, attention part, one decode query per (sequence, query head):
  *  seq_len_host[batch]  L >= 1, tokens in the cache with the current one
  *                       already appended by swan_compress_append;
+ *  k_active_host, k_value_host  as in swan_compress_append;
  *  q                    [batch][n_q_heads][head_dim] storage type (post-RoPE);
  *  scale                softmax scale; <= 0 means 1 / sqrt(head_dim);
  *  out                  [batch][n_q_heads][head_dim] storage type.
@@ -190,16 +209,17 @@ swan_status swan_decode_workspace_bytes(const swan_cache* c, const int32_t* seq_
  * the storage type.  Scores, probabilities and accumulators are float32.
  */
 swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_host,
-                                  const int32_t* k_active_host, const void* q,
-                                  const float* P_qk, const float* P_vo, float scale,
-                                  void* out, void* workspace, size_t workspace_bytes,
-                                  void* stream);
+                                  const int32_t* k_active_host, const int32_t* k_value_host,
+                                  const void* q, const float* P_qk, const float* P_vo,
+                                  float scale, void* out, void* workspace,
+                                  size_t workspace_bytes, void* stream);
 
 /*
  * Profiling hook.  While both are non-NULL, swan_decode_attention on this
  * thread records start_event (a hipEvent_t) on its stream right before its
- * sparse/buffer attention launches and stop_event right after them, so that
- * hipEventElapsedTime gives the duration of that kernel alone.  NULL, NULL
+ * sparse/buffer attention launches and stop_event right after them (both
+ * passes, for two-pass sequences), so that hipEventElapsedTime gives the
+ * duration of those kernels alone.  NULL, NULL
  * (the default) disables it.  The events stay owned by the caller.
  */
 swan_status swan_set_profile_events(void* start_event, void* stop_event);

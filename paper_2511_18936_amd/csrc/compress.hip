@@ -123,9 +123,9 @@ __global__ __launch_bounds__(64) void evict_kernel(CompressLaunch a) {
       (((int64_t)b * a.Hkv + h) * a.bb + (p % a.bb)) * kD;
   const typename St::Bits x0 = ring[2 * lane];
   const typename St::Bits x1 = ring[2 * lane + 1];
-  const int k = a.tab.kact[b];
+  const int k = a.tab.kact[role][b];
   const int64_t pbytes = page_bytes_of(Fmt<F>::kValBytes, k);
-  char* page = (char*)(role ? a.v_pages : a.k_pages) + a.tab.page_off[b] +
+  char* page = (char*)(role ? a.v_pages : a.k_pages) + a.tab.page_off[role][b] +
                ((int64_t)h * a.n_pages_cap + p / kPage) * pbytes;
   select_and_pack<F>(x0, x1, k, page, p % kPage, lane);
 }
@@ -178,9 +178,9 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
   }
   const int len_old = a.tab.len[b];
   const int len_new = len_old + nnew;
-  const int k = a.tab.kact[b];
+  const int k = a.tab.kact[role][b];
   const int64_t pbytes = page_bytes_of(Fmt<F>::kValBytes, k);
-  char* pages = (char*)(role ? a.v_pages : a.k_pages) + a.tab.page_off[b] +
+  char* pages = (char*)(role ? a.v_pages : a.k_pages) + a.tab.page_off[role][b] +
                 (int64_t)h * a.n_pages_cap * pbytes;
   typename St::Bits* ring = (typename St::Bits*)(role ? a.v_ring : a.k_ring) +
                             ((int64_t)b * a.Hkv + h) * a.bb * kD;

@@ -9,7 +9,10 @@
 //                  batch; several run side by side on library-owned streams,
 //                  joined back before the merge.  For fp16 GQA the launch is
 //                  attn_gqa_kernel (decode_gqa.hip) instead, one workgroup per
-//                  KV stream for several query heads.
+//                  KV stream for several query heads.  Sequences whose keys and
+//                  values have different k_pad take two launches instead, a
+//                  score pass and a value pass (decode_score_pass.hip,
+//                  decode_value_pass.hip).
 //   merge_kernel   log-sum-exp merge of the partials, then o = o_hat . P_VO^T
 //                  (the inverse rotation that Sec. 4.2 absorbs into W_O)
 //
@@ -48,64 +51,6 @@ __global__ __launch_bounds__(128) void qrot_kernel(const T* __restrict__ q,
 #pragma unroll 32
   for (int i = 0; i < kD; ++i) acc = fmaf(qs[i], P[i * kD + j], acc);
   qhat[(int64_t)bh * kD + j] = acc * mult;
-}
-
-// LDS layouts of one wave (a workgroup is one wave):
-//   qrep[dim][8]   the rotated query, 8 copies so that lanes l, l+8, ... of a
-//                  half wave spread over the banks
-//   acc[dim][64]   accumulators: lane t owns column t, so no two lanes ever
-//                  update the same word
-constexpr int kQRep = 8;
-constexpr int kAccCols = 64;
-
-template <typename T, int KP8>
-__device__ __forceinline__ float page_score(const PageRegs<T, KP8>& r, const float* qrep_l) {
-  float s0 = 0.f, s1 = 0.f;
-#pragma unroll
-  for (int g = 0; g < KP8; ++g) {
-#pragma unroll
-    for (int u = 0; u < 8; u += 2) {
-      s0 = fmaf(qrep_l[entry_idx(r, g, u) * kQRep], EntryVal<T, KP8>::get(r, g, u), s0);
-      s1 = fmaf(qrep_l[entry_idx(r, g, u + 1) * kQRep], EntryVal<T, KP8>::get(r, g, u + 1), s1);
-    }
-  }
-  return s0 + s1;
-}
-
-// acc[idx][lane] += p * v for entries of groups G0 .. G0 + NG - 1 of this
-// lane's token.  A token's indices are distinct, so all reads of the chunk can
-// be issued before its writes.
-template <typename T, int KP8, int G0, int NG>
-__device__ __forceinline__ void accumulate_groups(const PageRegs<T, KP8>& r, float* acc_l,
-                                                  float p) {
-  float a[NG * 8];
-#pragma unroll
-  for (int g = 0; g < NG; ++g)
-#pragma unroll
-    for (int u = 0; u < 8; ++u) a[g * 8 + u] = acc_l[entry_idx(r, G0 + g, u) * kAccCols];
-#pragma unroll
-  for (int g = 0; g < NG; ++g)
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      a[g * 8 + u] = fmaf(p, EntryVal<T, KP8>::get(r, G0 + g, u), a[g * 8 + u]);
-#pragma unroll
-  for (int g = 0; g < NG; ++g)
-#pragma unroll
-    for (int u = 0; u < 8; ++u) acc_l[entry_idx(r, G0 + g, u) * kAccCols] = a[g * 8 + u];
-}
-
-// acc[idx][lane] += p * v for the k entries of this lane's token, in chunks
-// of up to 64 entries (one LDS round trip per chunk).
-template <typename T, int KP8>
-__device__ __forceinline__ void page_accumulate(const PageRegs<T, KP8>& r, float* acc_l, float p,
-                                                bool valid) {
-  if (!valid) return;
-  if constexpr (KP8 <= 8) {
-    accumulate_groups<T, KP8, 0, KP8>(r, acc_l, p);
-  } else {
-    accumulate_groups<T, KP8, 0, 8>(r, acc_l, p);
-    accumulate_groups<T, KP8, 8, KP8 - 8>(r, acc_l, p);
-  }
 }
 
 __device__ __forceinline__ void rescale_acc(float* acc, int lane, float f) {
@@ -180,21 +125,7 @@ __device__ void sparse_split(const char* kbase, const char* vbase, int64_t pbyte
   }
   const float ltot = wave_sum(st.l);
   wave_lds_fence();
-  // reduce acc[dim][cols] over its columns: lane owns dims lane and lane + 64;
-  // the starting chunk is staggered per lane to spread the banks
-  constexpr int kRowChunks = kAccCols / 4;
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int r = lane + 64 * h;
-    const float4* row = (const float4*)(acc + r * kAccCols);
-    float sum = 0.f;
-#pragma unroll
-    for (int c = 0; c < kRowChunks; ++c) {
-      const float4 v = row[(c + lane) & (kRowChunks - 1)];
-      sum += (v.x + v.y) + (v.z + v.w);
-    }
-    part[4 + r] = sum;
-  }
+  reduce_acc(acc, lane, part);
   if (lane == 0) {
     part[0] = st.m;
     part[1] = ltot;
@@ -239,11 +170,11 @@ __global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup g) {
   if (split >= ns) return;
   const int pbeg = split_begin(split, ns, np);
   const int pend = split_begin(split + 1, ns, np);
-  const int k = a.tab.kact[b];
-  const int64_t pbytes = page_bytes_of(Fmt<T>::kValBytes, k);
-  const int64_t unit_off = a.tab.page_off[b] + (int64_t)h * a.n_pages_cap * pbytes;
-  const char* kbase = (const char*)a.k_pages + unit_off;
-  const char* vbase = (const char*)a.v_pages + unit_off;
+  // keys and values share k_pad here (so the page size), not the offsets
+  const int64_t pbytes = page_bytes_of(Fmt<T>::kValBytes, a.tab.kact[0][b]);
+  const int64_t head_off = (int64_t)h * a.n_pages_cap * pbytes;
+  const char* kbase = (const char*)a.k_pages + a.tab.page_off[0][b] + head_off;
+  const char* vbase = (const char*)a.v_pages + a.tab.page_off[1][b] + head_off;
   float* part = a.part + ((int64_t)bhq * pstride + split) * kPartFloats;
 
   // replicate q_hat: q_rep[dim][8]; lane writes dims lane and lane + 64
@@ -387,26 +318,38 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
     e = hipEventRecord(a.prof_start, a.stream);
     if (e != hipSuccess) return e;
   }
-  // sequences grouped by k_pad: one launch per group, each specialised on its
-  // exact k_pad
-  SeqGroup groups[kD / 8];
-  int kp8s[kD / 8];
+  // sequences grouped by (k_pad of the keys, k_pad of the values), largest
+  // first: one launch per group specialised on its k_pad, or a score and a
+  // value launch when the two differ
+  SeqGroup groups[SWAN_MAX_BATCH];
+  int kp8k[SWAN_MAX_BATCH], kp8v[SWAN_MAX_BATCH];
+  uint32_t present[kD / 8 + 1] = {};  // bit v of present[k]: some sequence has (k, v)
+  for (int b = 0; b < a.B; ++b)
+    present[kpad_of(a.tab.kact[0][b]) / 8] |= 1u << (kpad_of(a.tab.kact[1][b]) / 8);
   int ng = 0;
-  for (int kp8 = kD / 8; kp8 >= 1; --kp8) {
-    SeqGroup& g = groups[ng];
-    g.n = 0;
-    g.n_splits = 0;
-    for (int b = 0; b < a.B; ++b)
-      if (kpad_of(a.tab.kact[b]) / 8 == kp8) {
-        g.seq[g.n++] = b;
-        g.n_splits = a.tab.nsplit[b] > g.n_splits ? a.tab.nsplit[b] : g.n_splits;
-      }
-    if (g.n > 0) kp8s[ng++] = kp8;
-  }
+  for (int pk = kD / 8; pk >= 1; --pk)
+    for (int pv = kD / 8; pv >= 1; --pv) {
+      if (!((present[pk] >> pv) & 1u)) continue;
+      SeqGroup& g = groups[ng];
+      g.n = 0;
+      g.n_splits = 0;
+      for (int b = 0; b < a.B; ++b)
+        if (kpad_of(a.tab.kact[0][b]) / 8 == pk && kpad_of(a.tab.kact[1][b]) / 8 == pv) {
+          g.seq[g.n++] = b;
+          g.n_splits = a.tab.nsplit[b] > g.n_splits ? a.tab.nsplit[b] : g.n_splits;
+        }
+      kp8k[ng] = pk;
+      kp8v[ng] = pv;
+      ++ng;
+    }
+  auto launch_one = [&](const DecodeLaunch& ai, int i) {
+    return kp8k[i] == kp8v[i] ? launch_group<T>(ai, groups[i], kp8k[i])
+                              : launch_two_pass(ai, groups[i], kp8k[i], kp8v[i]);
+  };
   SideStreams* ss = ng > 1 ? side_streams(a.stream) : nullptr;
   if (!ss) {  // one launch, or no side streams: back to back on the caller's stream
     for (int i = 0; i < ng; ++i)
-      if ((e = launch_group<T>(a, groups[i], kp8s[i])) != hipSuccess) return e;
+      if ((e = launch_one(a, i)) != hipSuccess) return e;
   } else {
     std::lock_guard<std::mutex> lk(ss->mu);
     const int nside = ng - 1 < kSideStreams ? ng - 1 : kSideStreams;
@@ -417,7 +360,7 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
       DecodeLaunch ai = a;
       const int lane = i % (nside + 1);  // 0: the caller's stream
       if (lane > 0) ai.stream = ss->s[lane - 1];
-      if ((e = launch_group<T>(ai, groups[i], kp8s[i])) != hipSuccess) return e;
+      if ((e = launch_one(ai, i)) != hipSuccess) return e;
     }
     for (int j = 0; j < nside; ++j) {
       if ((e = hipEventRecord(ss->join[j], ss->s[j])) != hipSuccess) return e;

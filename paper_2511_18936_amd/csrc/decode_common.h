@@ -85,6 +85,85 @@ __device__ __forceinline__ int entry_idx(const PageRegs<T, KP8>& r, int g, int u
   return (int)((w >> (8 * (u & 3))) & 0xFFu);
 }
 
+// ---------------------------------------------------------------------------
+// lane-per-token sparse wave: q replicas, scores and the LDS accumulator
+// ---------------------------------------------------------------------------
+// LDS layouts of one wave (a workgroup is one wave):
+//   qrep[dim][8]   the rotated query, 8 copies so that lanes l, l+8, ... of a
+//                  half wave spread over the banks
+//   acc[dim][64]   accumulators: lane t owns column t, so no two lanes ever
+//                  update the same word
+constexpr int kQRep = 8;
+constexpr int kAccCols = 64;
+
+template <typename T, int KP8>
+__device__ __forceinline__ float page_score(const PageRegs<T, KP8>& r, const float* qrep_l) {
+  float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+  for (int g = 0; g < KP8; ++g) {
+#pragma unroll
+    for (int u = 0; u < 8; u += 2) {
+      s0 = fmaf(qrep_l[entry_idx(r, g, u) * kQRep], EntryVal<T, KP8>::get(r, g, u), s0);
+      s1 = fmaf(qrep_l[entry_idx(r, g, u + 1) * kQRep], EntryVal<T, KP8>::get(r, g, u + 1), s1);
+    }
+  }
+  return s0 + s1;
+}
+
+// acc[idx][lane] += p * v for entries of groups G0 .. G0 + NG - 1 of this
+// lane's token.  A token's indices are distinct, so all reads of the chunk can
+// be issued before its writes.
+template <typename T, int KP8, int G0, int NG>
+__device__ __forceinline__ void accumulate_groups(const PageRegs<T, KP8>& r, float* acc_l,
+                                                  float p) {
+  float a[NG * 8];
+#pragma unroll
+  for (int g = 0; g < NG; ++g)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) a[g * 8 + u] = acc_l[entry_idx(r, G0 + g, u) * kAccCols];
+#pragma unroll
+  for (int g = 0; g < NG; ++g)
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      a[g * 8 + u] = fmaf(p, EntryVal<T, KP8>::get(r, G0 + g, u), a[g * 8 + u]);
+#pragma unroll
+  for (int g = 0; g < NG; ++g)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc_l[entry_idx(r, G0 + g, u) * kAccCols] = a[g * 8 + u];
+}
+
+// acc[idx][lane] += p * v for the k entries of this lane's token, in chunks
+// of up to 64 entries (one LDS round trip per chunk).
+template <typename T, int KP8>
+__device__ __forceinline__ void page_accumulate(const PageRegs<T, KP8>& r, float* acc_l, float p,
+                                                bool valid) {
+  if (!valid) return;
+  if constexpr (KP8 <= 8) {
+    accumulate_groups<T, KP8, 0, KP8>(r, acc_l, p);
+  } else {
+    accumulate_groups<T, KP8, 0, 8>(r, acc_l, p);
+    accumulate_groups<T, KP8, 8, KP8 - 8>(r, acc_l, p);
+  }
+}
+
+// part[4 + r] = the sum over the columns of acc row r; lane owns rows lane and
+// lane + 64, its starting chunk staggered per lane to spread the banks
+__device__ __forceinline__ void reduce_acc(const float* acc, int lane, float* __restrict__ part) {
+  constexpr int kRowChunks = kAccCols / 4;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int r = lane + 64 * h;
+    const float4* row = (const float4*)(acc + r * kAccCols);
+    float sum = 0.f;
+#pragma unroll
+    for (int c = 0; c < kRowChunks; ++c) {
+      const float4 v = row[(c + lane) & (kRowChunks - 1)];
+      sum += (v.x + v.y) + (v.z + v.w);
+    }
+    part[4 + r] = sum;
+  }
+}
+
 struct SoftmaxState {
   float m;     // reference maximum (log2 units), wave-uniform
   float l;     // per-lane sum of exp2(s - m)

@@ -19,37 +19,9 @@
 // in the value wave's registers; rows >= GH of the MFMA's A operand are zero.
 // This is the dense contraction of the value update, done once for all heads
 // of the group, instead of GH scatters into LDS accumulators.
-#include "decode_common.h"
+#include "decode_gqa_common.h"
 
 namespace swan {
-
-typedef _Float16 h4 __attribute__((ext_vector_type(4)));
-typedef float f4 __attribute__((ext_vector_type(4)));
-
-constexpr int kVtStride = 68;    // halves per row of the value tile (64 + pad)
-constexpr int kPtStride = 68;    // halves per row of the probability tile (64 + pad)
-
-// replicas of the GH-head query rows (lane % R): 8 keep the gathers of 8
-// consecutive lanes on distinct banks; 4 for GH = 8 to bound the LDS
-template <int GH>
-constexpr int qrep_replicas() {
-  return GH >= 8 ? 4 : 8;
-}
-
-template <int GH>
-struct QVec;
-template <>
-struct QVec<2> {
-  typedef float type __attribute__((ext_vector_type(2)));
-};
-template <>
-struct QVec<4> {
-  typedef float type __attribute__((ext_vector_type(4)));
-};
-template <>
-struct QVec<8> {
-  typedef float type __attribute__((ext_vector_type(8)));
-};
 
 template <int GH>
 struct GqaLds {
@@ -64,23 +36,10 @@ template <typename T, int KP8, int GH>
 __device__ __forceinline__ void gqa_scores(const PageRegs<T, KP8>& kr, bool valid,
                                            GqaLds<GH>& sh, int par, int lane, float* m, float* l,
                                            bool& first) {
-  using QV = typename QVec<GH>::type;
   constexpr int R = qrep_replicas<GH>();
   float s[GH];
-#pragma unroll
-  for (int h = 0; h < GH; ++h) s[h] = 0.f;
   if (valid) {
-    const float* ql = sh.qrep + (lane & (R - 1)) * GH;
-#pragma unroll
-    for (int g = 0; g < KP8; ++g) {
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const float v = EntryVal<T, KP8>::get(kr, g, u);
-        const QV q = *(const QV*)(ql + entry_idx(kr, g, u) * (R * GH));
-#pragma unroll
-        for (int h = 0; h < GH; ++h) s[h] = fmaf(q[h], v, s[h]);
-      }
-    }
+    gather_scores<T, KP8, GH>(kr, sh.qrep + (lane & (R - 1)) * GH, s);
   } else {
 #pragma unroll
     for (int h = 0; h < GH; ++h) s[h] = -INFINITY;
@@ -108,67 +67,6 @@ __device__ __forceinline__ void gqa_scores(const PageRegs<T, KP8>& kr, bool vali
     sh.pt[par][1][h][lane] = (_Float16)(p - (float)hi);
   }
   if (lane < GH) sh.fr[par][lane] = frl;
-}
-
-// value wave, one page: zero the value tile, scatter the kept components
-template <typename T, int KP8, int GH>
-__device__ __forceinline__ void gqa_scatter(const PageRegs<T, KP8>& vr, bool valid,
-                                            GqaLds<GH>& sh, int lane) {
-  wave_lds_fence();  // the previous page's tile reads come first
-  {
-    u32x4* z = (u32x4*)sh.vt;
-    constexpr int kChunks = kD * kVtStride * 2 / 16;
-#pragma unroll
-    for (int c = lane; c < kChunks; c += 64) z[c] = u32x4{0u, 0u, 0u, 0u};
-  }
-  wave_lds_fence();
-  if (valid) {
-    uint16_t* vt16 = (uint16_t*)sh.vt + lane;
-#pragma unroll
-    for (int g = 0; g < KP8; ++g) {
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        vt16[entry_idx(vr, g, u) * kVtStride] = (uint16_t)entry_f16_bits<T, KP8>(vr, g, u);
-    }
-  }
-}
-
-// value wave, after the page barrier: rescale, then O += P . V on MFMA
-// (k-steps of 16 tokens, n-tiles of 16 dims)
-template <int GH>
-__device__ __forceinline__ void gqa_mfma(const GqaLds<GH>& sh, int par, int lane, f4* acc) {
-  const int row = lane & 15;
-  const int kq = 4 * (lane >> 4);
-  // accumulator rows 4 (lane / 16) + r hold head 4 (lane / 16) + r
-  float fr[4];
-  bool any = false;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int h = 4 * (lane >> 4) + r;
-    fr[r] = h < GH ? sh.fr[par][h < GH ? h : 0] : 1.f;
-  }
-#pragma unroll
-  for (int h = 0; h < GH; ++h) any |= sh.fr[par][h] != 1.f;
-  if (any) {
-#pragma unroll
-    for (int nt = 0; nt < 8; ++nt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[nt][r] *= fr[r];
-  }
-  const bool arow = row < GH;
-  const int rr = arow ? row : 0;
-  const h4 zero = {(_Float16)0.f, (_Float16)0.f, (_Float16)0.f, (_Float16)0.f};
-#pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    const h4 ahi = arow ? *(const h4*)&sh.pt[par][0][rr][16 * ks + kq] : zero;
-    const h4 alo = arow ? *(const h4*)&sh.pt[par][1][rr][16 * ks + kq] : zero;
-#pragma unroll
-    for (int nt = 0; nt < 8; ++nt) {
-      const h4 b = *(const h4*)(sh.vt + (16 * nt + row) * kVtStride + 16 * ks + kq);
-      acc[nt] = __builtin_amdgcn_mfma_f32_16x16x16f16(ahi, b, acc[nt], 0, 0, 0);
-      acc[nt] = __builtin_amdgcn_mfma_f32_16x16x16f16(alo, b, acc[nt], 0, 0, 0);
-    }
-  }
 }
 
 // Grid: n * Hq dense-buffer blocks (wave 0 serves one query head), then
@@ -215,9 +113,9 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
   if (split >= ns) return;  // uniform over the block
   const int pbeg = split_begin(split, ns, np);
   const int pend = split_begin(split + 1, ns, np);
-  const int k = a.tab.kact[b];
-  const int64_t pbytes = page_bytes_of(Fmt<T>::kValBytes, k);
-  const int64_t unit_off = a.tab.page_off[b] + (int64_t)h * a.n_pages_cap * pbytes;
+  // keys and values share k_pad here (so the page size), not the offsets
+  const int64_t pbytes = page_bytes_of(Fmt<T>::kValBytes, a.tab.kact[0][b]);
+  const int64_t head_off = (int64_t)h * a.n_pages_cap * pbytes;
 
   // q_rep[dim][r][head]: thread t writes dim t, all replicas
   {
@@ -236,7 +134,7 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
   const int plast = pend - 1;
   if (wave == 0) {
     // ---- score wave ----
-    const char* kbase = (const char*)a.k_pages + unit_off;
+    const char* kbase = (const char*)a.k_pages + a.tab.page_off[0][b] + head_off;
     float m[GH], l[GH];
     bool first = true;
 #pragma unroll
@@ -270,7 +168,7 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
     }
   } else {
     // ---- value wave ----
-    const char* vbase = (const char*)a.v_pages + unit_off;
+    const char* vbase = (const char*)a.v_pages + a.tab.page_off[1][b] + head_off;
     f4 acc[8];
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt) acc[nt] = f4{0.f, 0.f, 0.f, 0.f};
@@ -279,13 +177,13 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
     for (int p = pbeg; p < pend; p += 2) {
       const int p1 = p + 1 < plast ? p + 1 : plast;
       load_page<T, KP8>(vb, vbase + p1 * pbytes, lane);
-      gqa_scatter<T, KP8, GH>(va, p * kPage + lane < S, sh, lane);
+      gqa_scatter<T, KP8>(va, p * kPage + lane < S, sh, lane);
       __syncthreads();
       gqa_mfma<GH>(sh, (p - pbeg) & 1, lane, acc);
       const int p2 = p + 2 < plast ? p + 2 : plast;
       load_page<T, KP8>(va, vbase + p2 * pbytes, lane);
       if (p + 1 < pend) {
-        gqa_scatter<T, KP8, GH>(vb, (p + 1) * kPage + lane < S, sh, lane);
+        gqa_scatter<T, KP8>(vb, (p + 1) * kPage + lane < S, sh, lane);
         __syncthreads();
         gqa_mfma<GH>(sh, (p + 1 - pbeg) & 1, lane, acc);
       }

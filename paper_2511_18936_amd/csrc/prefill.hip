@@ -163,10 +163,10 @@ void prefill_kernel(CompressLaunch a) {
                       ((int64_t)b * a.Hkv + h) * a.n_new * kD;
   const float* P = (role ? a.P_vo : a.P_qk) + (int64_t)h * kD * kD;
 
-  const int k = a.tab.kact[b];
+  const int k = a.tab.kact[role][b];
   const int kp = kpad_of(k);
   const int64_t pbytes = page_bytes_of(VB, k);
-  char* pages = (char*)(role ? a.v_pages : a.k_pages) + a.tab.page_off[b] +
+  char* pages = (char*)(role ? a.v_pages : a.k_pages) + a.tab.page_off[role][b] +
                 (int64_t)h * a.n_pages_cap * pbytes;
   uint16_t* ring = (uint16_t*)(role ? a.v_ring : a.k_ring) + ((int64_t)b * a.Hkv + h) * a.bb * kD;
 

@@ -66,14 +66,25 @@ swan_status check_cache_shape(const swan_cache* c) {
   return SWAN_OK;
 }
 
-swan_status check_k(const swan_cache* c, const int32_t* k_active_host) {
+// k of the keys (k_active_host) and, if not NULL, of the values (k_value_host)
+swan_status check_k(const swan_cache* c, const int32_t* k_active_host,
+                    const int32_t* k_value_host) {
   if (!k_active_host) return fail(SWAN_ERR_INVALID_ARG, "k_active_host is NULL");
   for (int b = 0; b < c->batch; ++b) {
     const int k = k_active_host[b];
     if (k < 1 || k > c->head_dim)
       return fail(SWAN_ERR_INVALID_ARG, "k_active[%d] = %d outside 1..%d", b, k, c->head_dim);
+    if (!k_value_host) continue;
+    const int kv = k_value_host[b];
+    if (kv < 1 || kv > c->head_dim)
+      return fail(SWAN_ERR_INVALID_ARG, "k_value[%d] = %d outside 1..%d", b, kv, c->head_dim);
   }
   return SWAN_OK;
+}
+
+// k of role r (0 keys, 1 values) of sequence b
+inline int k_of(const int32_t* k_active_host, const int32_t* k_value_host, int r, int b) {
+  return (r == 1 && k_value_host) ? k_value_host[b] : k_active_host[b];
 }
 
 swan_status check_cache_ptrs(const swan_cache* c) {
@@ -88,33 +99,43 @@ swan_status check_cache_ptrs(const swan_cache* c) {
   return SWAN_OK;
 }
 
-// fills tab.kact and tab.page_off; returns total page bytes per role
-int64_t fill_layout(const swan_cache* c, const int32_t* k_active_host, swan::SeqTab& tab) {
+// fills tab.kact and tab.page_off of both roles; bytes[r] = total page bytes of role r
+void fill_layout(const swan_cache* c, const int32_t* k_active_host, const int32_t* k_value_host,
+                 swan::SeqTab& tab, int64_t bytes[2]) {
   const int npc = swan::pages_for(c->sparse_capacity);
-  int64_t off = 0;
   for (int b = 0; b < SWAN_MAX_BATCH; ++b) {
-    tab.kact[b] = 0;
-    tab.page_off[b] = 0;
+    for (int r = 0; r < 2; ++r) {
+      tab.kact[r][b] = 0;
+      tab.page_off[r][b] = 0;
+    }
     tab.len[b] = 0;
     tab.nnew[b] = 0;
     tab.nsplit[b] = 1;
   }
-  for (int b = 0; b < c->batch; ++b) {
-    tab.kact[b] = k_active_host[b];
-    tab.page_off[b] = off;
-    off += (int64_t)c->n_kv_heads * npc * swan::page_bytes_of(value_bytes(c->dtype), k_active_host[b]);
+  for (int r = 0; r < 2; ++r) {
+    int64_t off = 0;
+    for (int b = 0; b < c->batch; ++b) {
+      const int k = k_of(k_active_host, k_value_host, r, b);
+      tab.kact[r][b] = k;
+      tab.page_off[r][b] = off;
+      off += (int64_t)c->n_kv_heads * npc * swan::page_bytes_of(value_bytes(c->dtype), k);
+    }
+    bytes[r] = off;
   }
-  return off;
 }
 
 // Token splits per (sequence, query head): about two waves per CU slot in total
 // (measured best for long contexts; SWAN_DECODE_WAVES overrides the target),
-// the split count of each sequence following its bytes (a page weighs k_pad);
-// the splits themselves shrink in size (split_begin), and their count is
-// capped so that every split keeps a page.  Fills nsplit[b] (may be NULL);
-// returns the largest.
+// the split count of each sequence following its bytes (a page weighs the
+// k_pad of its keys plus that of its values); the splits themselves shrink in
+// size (split_begin), and their count is capped so that every split keeps a
+// page.  Fills nsplit[b] (may be NULL); returns the largest.
 int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t* k_active_host,
-                int32_t* nsplit) {
+                const int32_t* k_value_host, int32_t* nsplit) {
+  auto weight = [&](int b) {
+    return swan::kpad_of(k_of(k_active_host, k_value_host, 0, b)) +
+           swan::kpad_of(k_of(k_active_host, k_value_host, 1, b));
+  };
   // waves per sequence and split: one per query head, or one per GH query
   // heads of a KV head on the GQA path
   const int hpw = swan::decode_heads_per_wave(c->dtype, c->n_q_heads, c->n_kv_heads);
@@ -122,7 +143,7 @@ int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t*
   int64_t total = 0;
   for (int b = 0; b < c->batch; ++b) {
     const int S = seq_len_host[b] > c->buffer_tokens ? seq_len_host[b] - c->buffer_tokens : 0;
-    total += (int64_t)swan::pages_for(S) * swan::kpad_of(k_active_host[b]) * waves_per_seq;
+    total += (int64_t)swan::pages_for(S) * weight(b) * waves_per_seq;
   }
   static const int64_t target_waves = [] {
     const char* s = getenv("SWAN_DECODE_WAVES");  // tuning override
@@ -135,7 +156,7 @@ int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t*
   for (int b = 0; b < c->batch; ++b) {
     const int S = seq_len_host[b] > c->buffer_tokens ? seq_len_host[b] - c->buffer_tokens : 0;
     const int np = swan::pages_for(S);
-    const int64_t work = (int64_t)np * swan::kpad_of(k_active_host[b]);
+    const int64_t work = (int64_t)np * weight(b);
     int ns = (int)((work + per_wave - 1) / per_wave);
     while (ns > 1 && (int64_t)ns * (ns + 1) / 2 > np) --ns;  // every split keeps a page
     if (ns > swan::kMaxSplits) ns = swan::kMaxSplits;
@@ -146,11 +167,32 @@ int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t*
   return ns_max;
 }
 
-size_t decode_ws_bytes(const swan_cache* c, int ns) {
+// Tokens per (sequence, query head) row of the two-pass decode's scores: the
+// longest sparse part, in whole pages, of a sequence whose keys and values
+// have different k_pad (0 when there is none).
+int64_t score_stride(const swan_cache* c, const int32_t* seq_len_host,
+                     const int32_t* k_active_host, const int32_t* k_value_host) {
+  int64_t st = 0;
+  for (int b = 0; b < c->batch; ++b) {
+    if (swan::kpad_of(k_of(k_active_host, k_value_host, 0, b)) ==
+        swan::kpad_of(k_of(k_active_host, k_value_host, 1, b)))
+      continue;
+    const int S = seq_len_host[b] > c->buffer_tokens ? seq_len_host[b] - c->buffer_tokens : 0;
+    const int64_t t = (int64_t)swan::pages_for(S) * swan::kPage;
+    if (t > st) st = t;
+  }
+  return st;
+}
+
+size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// workspace: q_hat, the partials, then the two-pass scores
+size_t decode_ws_bytes(const swan_cache* c, int ns, int64_t sstride) {
   const size_t units = (size_t)c->batch * c->n_q_heads;
   const size_t qhat = units * swan::kD * sizeof(float);
   const size_t part = units * (size_t)(ns + 1) * swan::kPartFloats * sizeof(float);
-  return ((qhat + 255) & ~(size_t)255) + part;
+  const size_t scores = units * (size_t)sstride * sizeof(float);
+  return round256(qhat) + round256(part) + scores;
 }
 
 swan_status hip_status(hipError_t e, const char* what) {
@@ -164,7 +206,7 @@ extern "C" {
 
 const char* swan_last_error(void) { return g_last_error.c_str(); }
 
-int32_t swan_version(void) { return 102; }
+int32_t swan_version(void) { return 200; }
 
 swan_status swan_page_bytes(int32_t dtype, int32_t k_active, size_t* bytes) {
   if (!bytes) return fail(SWAN_ERR_INVALID_ARG, "bytes is NULL");
@@ -175,14 +217,19 @@ swan_status swan_page_bytes(int32_t dtype, int32_t k_active, size_t* bytes) {
   return ok();
 }
 
-swan_status swan_cache_bytes(const swan_cache* c, const int32_t* k_active_host, size_t* page_bytes,
-                             size_t* ring_bytes) {
+swan_status swan_cache_bytes(const swan_cache* c, const int32_t* k_active_host,
+                             const int32_t* k_value_host, size_t* k_page_bytes,
+                             size_t* v_page_bytes, size_t* ring_bytes) {
   swan_status st = check_cache_shape(c);
   if (st != SWAN_OK) return st;
-  if ((st = check_k(c, k_active_host)) != SWAN_OK) return st;
-  if (!page_bytes || !ring_bytes) return fail(SWAN_ERR_INVALID_ARG, "output pointer is NULL");
+  if ((st = check_k(c, k_active_host, k_value_host)) != SWAN_OK) return st;
+  if (!k_page_bytes || !v_page_bytes || !ring_bytes)
+    return fail(SWAN_ERR_INVALID_ARG, "output pointer is NULL");
   swan::SeqTab tab;
-  *page_bytes = (size_t)fill_layout(c, k_active_host, tab);
+  int64_t bytes[2];
+  fill_layout(c, k_active_host, k_value_host, tab, bytes);
+  *k_page_bytes = (size_t)bytes[0];
+  *v_page_bytes = (size_t)bytes[1];
   *ring_bytes = (size_t)c->batch * c->n_kv_heads * c->buffer_tokens * c->head_dim *
                 elem_bytes(c->dtype);
   return ok();
@@ -232,12 +279,13 @@ swan_status swan_calibrate_rotation(const float* rows, int64_t n_rows, int32_t d
 }
 
 swan_status swan_compress_append(const swan_cache* c, const int32_t* seq_len_host,
-                                 const int32_t* k_active_host, const void* k_new, const void* v_new,
-                                 int32_t n_new, const int32_t* n_new_host, const float* P_qk,
-                                 const float* P_vo, void* stream) {
+                                 const int32_t* k_active_host, const int32_t* k_value_host,
+                                 const void* k_new, const void* v_new, int32_t n_new,
+                                 const int32_t* n_new_host, const float* P_qk, const float* P_vo,
+                                 void* stream) {
   swan_status st = check_cache_shape(c);
   if (st != SWAN_OK) return st;
-  if ((st = check_k(c, k_active_host)) != SWAN_OK) return st;
+  if ((st = check_k(c, k_active_host, k_value_host)) != SWAN_OK) return st;
   if ((st = check_cache_ptrs(c)) != SWAN_OK) return st;
   if (!seq_len_host) return fail(SWAN_ERR_INVALID_ARG, "seq_len_host is NULL");
   if (n_new < 0) return fail(SWAN_ERR_INVALID_ARG, "n_new %d < 0", n_new);
@@ -266,7 +314,8 @@ swan_status swan_compress_append(const swan_cache* c, const int32_t* seq_len_hos
     if (p1 - p0 > max_evict) max_evict = (int)(p1 - p0);
   }
   swan::CompressLaunch a;
-  fill_layout(c, k_active_host, a.tab);
+  int64_t role_bytes[2];
+  fill_layout(c, k_active_host, k_value_host, a.tab, role_bytes);
   for (int b = 0; b < c->batch; ++b) {
     a.tab.len[b] = seq_len_host[b];
     a.tab.nnew[b] = n_new_host ? n_new_host[b] : n_new;
@@ -293,22 +342,25 @@ swan_status swan_compress_append(const swan_cache* c, const int32_t* seq_len_hos
 }
 
 swan_status swan_decode_workspace_bytes(const swan_cache* c, const int32_t* seq_len_host,
-                                        const int32_t* k_active_host, size_t* bytes) {
+                                        const int32_t* k_active_host,
+                                        const int32_t* k_value_host, size_t* bytes) {
   swan_status st = check_cache_shape(c);
   if (st != SWAN_OK) return st;
-  if ((st = check_k(c, k_active_host)) != SWAN_OK) return st;
+  if ((st = check_k(c, k_active_host, k_value_host)) != SWAN_OK) return st;
   if (!seq_len_host || !bytes) return fail(SWAN_ERR_INVALID_ARG, "NULL argument");
-  *bytes = decode_ws_bytes(c, plan_splits(c, seq_len_host, k_active_host, nullptr));
+  *bytes = decode_ws_bytes(c, plan_splits(c, seq_len_host, k_active_host, k_value_host, nullptr),
+                           score_stride(c, seq_len_host, k_active_host, k_value_host));
   return ok();
 }
 
 swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_host,
-                                  const int32_t* k_active_host, const void* q, const float* P_qk,
-                                  const float* P_vo, float scale, void* out, void* workspace,
-                                  size_t workspace_bytes, void* stream) {
+                                  const int32_t* k_active_host, const int32_t* k_value_host,
+                                  const void* q, const float* P_qk, const float* P_vo, float scale,
+                                  void* out, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
   swan_status st = check_cache_shape(c);
   if (st != SWAN_OK) return st;
-  if ((st = check_k(c, k_active_host)) != SWAN_OK) return st;
+  if ((st = check_k(c, k_active_host, k_value_host)) != SWAN_OK) return st;
   if ((st = check_cache_ptrs(c)) != SWAN_OK) return st;
   if (!seq_len_host) return fail(SWAN_ERR_INVALID_ARG, "seq_len_host is NULL");
   if (!q || !out || !P_qk || !P_vo) return fail(SWAN_ERR_INVALID_ARG, "q / out / P is NULL");
@@ -323,9 +375,11 @@ swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_ho
   }
   if (!(scale == scale) || isinf(scale)) return fail(SWAN_ERR_INVALID_ARG, "scale is not finite");
   swan::DecodeLaunch a;
-  fill_layout(c, k_active_host, a.tab);
-  const int ns = plan_splits(c, seq_len_host, k_active_host, a.tab.nsplit);
-  const size_t need = decode_ws_bytes(c, ns);
+  int64_t role_bytes[2];
+  fill_layout(c, k_active_host, k_value_host, a.tab, role_bytes);
+  const int ns = plan_splits(c, seq_len_host, k_active_host, k_value_host, a.tab.nsplit);
+  const int64_t sstride = score_stride(c, seq_len_host, k_active_host, k_value_host);
+  const size_t need = decode_ws_bytes(c, ns, sstride);
   if (!workspace || workspace_bytes < need)
     return fail(SWAN_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, need);
   if (((uintptr_t)workspace & 255) != 0)
@@ -341,8 +395,12 @@ swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_ho
   a.k_ring = c->k_ring;
   a.v_ring = c->v_ring;
   const size_t units = (size_t)c->batch * c->n_q_heads;
+  const size_t qhat_bytes = round256(units * swan::kD * sizeof(float));
+  const size_t part_bytes = round256(units * (size_t)(ns + 1) * swan::kPartFloats * sizeof(float));
   a.qhat = (float*)workspace;
-  a.part = (float*)((char*)workspace + ((units * swan::kD * sizeof(float) + 255) & ~(size_t)255));
+  a.part = (float*)((char*)workspace + qhat_bytes);
+  a.scores = sstride > 0 ? (float*)((char*)workspace + qhat_bytes + part_bytes) : nullptr;
+  a.score_stride = sstride;
   a.B = c->batch;
   a.Hq = c->n_q_heads;
   a.Hkv = c->n_kv_heads;

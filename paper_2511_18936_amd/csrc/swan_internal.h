@@ -15,12 +15,13 @@ constexpr int kMaxRing = 4096; // largest dense buffer the decode kernel stages 
 constexpr int kPartFloats = 132;  // m, l, 2 pad, acc[128]
 
 // Per-sequence parameters passed by value to every kernel (batch <= 64).
+// Role 0 is the keys, role 1 the values: each has its own k and page layout.
 struct SeqTab {
-  int32_t len[SWAN_MAX_BATCH];       // tokens cached (compress: before the call; decode: L)
-  int32_t kact[SWAN_MAX_BATCH];      // k_active
-  int64_t page_off[SWAN_MAX_BATCH];  // byte offset of the sequence's first page
-  int32_t nnew[SWAN_MAX_BATCH];      // compress: tokens appended to the sequence
-  int32_t nsplit[SWAN_MAX_BATCH];    // decode: token splits of the sequence's launch
+  int32_t len[SWAN_MAX_BATCH];          // tokens cached (compress: before the call; decode: L)
+  int32_t kact[2][SWAN_MAX_BATCH];      // k of the keys / of the values
+  int64_t page_off[2][SWAN_MAX_BATCH];  // byte offset of the sequence's first key / value page
+  int32_t nnew[SWAN_MAX_BATCH];         // compress: tokens appended to the sequence
+  int32_t nsplit[SWAN_MAX_BATCH];       // decode: token splits of the sequence's launch
 };
 
 __host__ __device__ inline int kpad_of(int k) { return (k + 7) & ~7; }
@@ -55,6 +56,8 @@ struct DecodeLaunch {
   const void* v_ring;
   float* qhat;   // [B][Hq][128] workspace
   float* part;   // [B][Hq][NS + 1][kPartFloats] workspace
+  float* scores;         // two-pass decode: [B][Hq][score_stride] workspace (or NULL)
+  int64_t score_stride;  // tokens per (sequence, query head) row of `scores`
   int B, Hq, Hkv, bb, n_pages_cap;
   int n_splits;  // NS: largest split count of any launch (slot NS holds the buffer partial)
   float qmult;   // scale * log2(e)
@@ -83,6 +86,9 @@ inline int decode_heads_per_wave(int dtype, int n_q, int n_kv) {
   return ((dtype == SWAN_F16 || dtype == SWAN_F16_E4M3) && G > 1) ? gqa_heads_per_wave(G) : 1;
 }
 hipError_t launch_attn_gqa(const DecodeLaunch& a, const SeqGroup& g, int kp8);
+// sequences whose keys and values have different k_pad: a score pass over the
+// key pages (exact per-split maxima, scores to a.scores), then a value pass
+hipError_t launch_two_pass(const DecodeLaunch& a, const SeqGroup& g, int kp8_key, int kp8_val);
 
 
 struct CompressLaunch {

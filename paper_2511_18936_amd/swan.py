@@ -77,12 +77,13 @@ def _load() -> ctypes.CDLL:
     lib.swan_version.argtypes = []
     sigs = {
         "swan_page_bytes": [i32, i32, psz],
-        "swan_cache_bytes": [pdesc, pi32, psz, psz],
+        "swan_cache_bytes": [pdesc, pi32, pi32, psz, psz, psz],
         "swan_calibrate_workspace_bytes": [i32, psz],
         "swan_calibrate_rotation": [vp, i64, i32, vp, vp, vp, sz, vp],
-        "swan_compress_append": [pdesc, pi32, pi32, vp, vp, i32, pi32, vp, vp, vp],
-        "swan_decode_workspace_bytes": [pdesc, pi32, pi32, psz],
-        "swan_decode_attention": [pdesc, pi32, pi32, vp, vp, vp, ctypes.c_float, vp, vp, sz, vp],
+        "swan_compress_append": [pdesc, pi32, pi32, pi32, vp, vp, i32, pi32, vp, vp, vp],
+        "swan_decode_workspace_bytes": [pdesc, pi32, pi32, pi32, psz],
+        "swan_decode_attention": [pdesc, pi32, pi32, pi32, vp, vp, vp, ctypes.c_float, vp, vp, sz,
+                                  vp],
         "swan_set_profile_events": [vp, vp],
     }
     for name, args in sigs.items():
@@ -111,6 +112,10 @@ def _check(status: int) -> None:
 def _i32_array(values: Sequence[int]):
     arr = (ctypes.c_int32 * len(values))(*[int(v) for v in values])
     return arr
+
+
+def _opt_i32_array(values: Optional[Sequence[int]]):
+    return None if values is None else _i32_array(values)
 
 
 def _ptr(t) -> Optional[int]:
@@ -147,11 +152,14 @@ def page_bytes(dtype: int, k_active: int) -> int:
     return out.value
 
 
-def cache_bytes(desc: CacheDesc, k_active: Sequence[int]):
-    pb, rb = ctypes.c_size_t(), ctypes.c_size_t()
-    _check(_lib.swan_cache_bytes(ctypes.byref(desc), _i32_array(k_active), ctypes.byref(pb),
+def cache_bytes(desc: CacheDesc, k_active: Sequence[int],
+                k_value: Optional[Sequence[int]] = None):
+    """(key page bytes, value page bytes, ring bytes); k_value None: as k_active."""
+    kb, vb, rb = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+    _check(_lib.swan_cache_bytes(ctypes.byref(desc), _i32_array(k_active),
+                                 _opt_i32_array(k_value), ctypes.byref(kb), ctypes.byref(vb),
                                  ctypes.byref(rb)))
-    return pb.value, rb.value
+    return kb.value, vb.value, rb.value
 
 
 def calibrate_workspace_bytes(d: int = HEAD_DIM) -> int:
@@ -174,28 +182,31 @@ def calibrate_rotation(rows, P_out, sigma_out=None, workspace=None, stream=None)
 
 def compress_append(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence[int], k_new,
                     v_new, P_qk, P_vo, n_new_per_seq: Optional[Sequence[int]] = None,
-                    stream=None) -> None:
+                    stream=None, k_value: Optional[Sequence[int]] = None) -> None:
     n_new = 0 if k_new is None else int(k_new.shape[2])
     per = None if n_new_per_seq is None else _i32_array(n_new_per_seq)
     _check(_lib.swan_compress_append(ctypes.byref(desc), _i32_array(seq_len),
-                                     _i32_array(k_active), _ptr(k_new), _ptr(v_new), n_new, per,
-                                     _ptr(P_qk), _ptr(P_vo), _stream(stream)))
+                                     _i32_array(k_active), _opt_i32_array(k_value), _ptr(k_new),
+                                     _ptr(v_new), n_new, per, _ptr(P_qk), _ptr(P_vo),
+                                     _stream(stream)))
 
 
-def decode_workspace_bytes(desc: CacheDesc, seq_len: Sequence[int],
-                           k_active: Sequence[int]) -> int:
+def decode_workspace_bytes(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence[int],
+                           k_value: Optional[Sequence[int]] = None) -> int:
     out = ctypes.c_size_t()
     _check(_lib.swan_decode_workspace_bytes(ctypes.byref(desc), _i32_array(seq_len),
-                                            _i32_array(k_active), ctypes.byref(out)))
+                                            _i32_array(k_active), _opt_i32_array(k_value),
+                                            ctypes.byref(out)))
     return out.value
 
 
 def decode_attention(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence[int], q,
-                     P_qk, P_vo, out, workspace, scale: float = 0.0, stream=None) -> None:
+                     P_qk, P_vo, out, workspace, scale: float = 0.0, stream=None,
+                     k_value: Optional[Sequence[int]] = None) -> None:
     _check(_lib.swan_decode_attention(ctypes.byref(desc), _i32_array(seq_len),
-                                      _i32_array(k_active), _ptr(q), _ptr(P_qk), _ptr(P_vo),
-                                      float(scale), _ptr(out), _ptr(workspace),
-                                      workspace.numel(), _stream(stream)))
+                                      _i32_array(k_active), _opt_i32_array(k_value), _ptr(q),
+                                      _ptr(P_qk), _ptr(P_vo), float(scale), _ptr(out),
+                                      _ptr(workspace), workspace.numel(), _stream(stream)))
 
 
 def set_profile_events(start=None, stop=None) -> None:
@@ -210,12 +221,15 @@ class SwanCache:
 
     The arrays are plain torch tensors (uint8 pages, storage-typed ring); the
     library only ever receives their device pointers.  sparse_values="e4m3"
-    (float16 only) stores the pruned values as one-byte E4M3 codes.
+    (float16 only) stores the pruned values as one-byte E4M3 codes.  k_value
+    (one per sequence) prunes the values to other k than the keys (k_active);
+    None keeps both at k_active.
     """
 
     def __init__(self, batch: int, n_q_heads: int, n_kv_heads: int, buffer_tokens: int,
                  sparse_capacity: int, k_active: Sequence[int], dtype, device,
-                 head_dim: int = HEAD_DIM, sparse_values: str = "same"):
+                 head_dim: int = HEAD_DIM, sparse_values: str = "same",
+                 k_value: Optional[Sequence[int]] = None):
         import torch
 
         self.dtype = dtype
@@ -224,14 +238,17 @@ class SwanCache:
         self.k_active = [int(k) for k in k_active]
         if len(self.k_active) != batch:
             raise ValueError("k_active needs one entry per sequence")
+        self.k_value = None if k_value is None else [int(k) for k in k_value]
+        if self.k_value is not None and len(self.k_value) != batch:
+            raise ValueError("k_value needs one entry per sequence")
         self.seq_len = [0] * batch
         self.desc = CacheDesc(batch, n_q_heads, n_kv_heads, head_dim, buffer_tokens,
                               sparse_capacity, dtype_code(dtype, sparse_values), 0, None, None,
                               None, None)
-        pb, rb = cache_bytes(self.desc, self.k_active)
+        kb, vb, rb = cache_bytes(self.desc, self.k_active, self.k_value)
         # torch's caching allocator returns 256-byte aligned blocks
-        self.k_pages = torch.zeros(max(pb, 16), dtype=torch.uint8, device=self.device)
-        self.v_pages = torch.zeros(max(pb, 16), dtype=torch.uint8, device=self.device)
+        self.k_pages = torch.zeros(max(kb, 16), dtype=torch.uint8, device=self.device)
+        self.v_pages = torch.zeros(max(vb, 16), dtype=torch.uint8, device=self.device)
         shape = (batch, n_kv_heads, buffer_tokens, head_dim)
         self.k_ring = torch.zeros(shape, dtype=dtype, device=self.device)
         self.v_ring = torch.zeros(shape, dtype=dtype, device=self.device)
@@ -251,7 +268,7 @@ class SwanCache:
         n_new_per_seq optionally appends only the first n_b rows of sequence b.
         """
         compress_append(self.desc, self.seq_len, self.k_active, k_new, v_new, P_qk, P_vo,
-                        n_new_per_seq, stream)
+                        n_new_per_seq, stream, self.k_value)
         n = int(k_new.shape[2])
         per = [n] * self.batch if n_new_per_seq is None else [int(x) for x in n_new_per_seq]
         self.seq_len = [L + m for L, m in zip(self.seq_len, per)]
@@ -259,7 +276,7 @@ class SwanCache:
     def workspace(self):
         import torch
 
-        need = decode_workspace_bytes(self.desc, self.seq_len, self.k_active)
+        need = decode_workspace_bytes(self.desc, self.seq_len, self.k_active, self.k_value)
         if self._ws is None or self._ws.numel() < need:
             self._ws = torch.empty(need, dtype=torch.uint8, device=self.device)
         return self._ws
@@ -270,5 +287,5 @@ class SwanCache:
         if out is None:
             out = torch.empty_like(q)
         decode_attention(self.desc, self.seq_len, self.k_active, q, P_qk, P_vo, out,
-                         self.workspace(), scale, stream)
+                         self.workspace(), scale, stream, self.k_value)
         return out

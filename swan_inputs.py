@@ -52,6 +52,7 @@ class Workload:
     k_choices: Tuple[int, ...] = ()
     description: str = ""
     sparse_values: str = "same"  # "same" (values stored in dtype) or "e4m3" (8-bit)
+    k_value: int = 0       # k of the values; 0 means the same k as the keys
 
     @property
     def group(self) -> int:
@@ -81,6 +82,16 @@ WORKLOADS = {
                  sparse_values="e4m3",
                  description="the 128k x 4 Llama-3-8B GQA layer with 8-bit (E4M3) sparse "
                              "values, fp16 buffer, k=64"),
+        # key/value retention 0.6 / 0.4 of d_h (the asymmetric rows of the
+        # Appendix A.5 ablation): k = 77 for keys, 51 for values
+        Workload(7, "llama2_7b_L32k_b16_k77_v51", 16, 32, 32, 128, 32768, 128, 77, "f16",
+                 k_value=51,
+                 description="the 32k x 16 Llama-2-7B layer, keys keep 77 and values 51 "
+                             "components, b=128, fp16"),
+        Workload(8, "llama3_8b_gqa_L128k_b4_k77_v51", 4, 32, 8, 128, 131072, 256, 77, "f16",
+                 k_value=51,
+                 description="the 128k x 4 Llama-3-8B GQA layer, keys keep 77 and values 51 "
+                             "components, b=256, fp16"),
     )
 }
 WORKLOAD_BY_ID = {w.wid: w for w in WORKLOADS.values()}
@@ -153,6 +164,13 @@ def k_active_for(w: Workload) -> np.ndarray:
         return np.full(w.batch, w.k_active, dtype=np.int32)
     r = rng_for(w.wid, 5000)
     return r.choice(np.array(w.k_choices, dtype=np.int32), size=w.batch)
+
+
+def k_value_for(w: Workload) -> Optional[np.ndarray]:
+    """Per-sequence k of the values, or None when the values keep the keys' k."""
+    if not w.k_value:
+        return None
+    return np.full(w.batch, w.k_value, dtype=np.int32)
 
 
 def kv_rows_device(wid: int, batch: int, n_kv_heads: int, role: int, n: int, dtype: str,

@@ -52,11 +52,18 @@ def max_rel_err(got: np.ndarray, ref: np.ndarray) -> float:
 def unit_pages(cache, b, h, role, n_tokens, dtype_np):
     """(idx, val, pad_idx, pad_val) of one unit's sparse tokens read back from the GPU."""
     esize = np.dtype(dtype_np).itemsize
-    s, e = lay.unit_slice(cache.k_active, cache.desc.n_kv_heads, cache.desc.sparse_capacity,
-                          esize, b, h)
+    ks = role_k(cache, role)
+    s, e = lay.unit_slice(ks, cache.desc.n_kv_heads, cache.desc.sparse_capacity, esize, b, h)
     pages = cache.k_pages if role == 0 else cache.v_pages
     raw = pages[s:e].cpu().numpy()
-    return lay.unpack(raw, dtype_np, cache.k_active[b], n_tokens)
+    return lay.unpack(raw, dtype_np, ks[b], n_tokens)
+
+
+def role_k(cache, role):
+    """Per-sequence k of the keys (role 0) or of the values (role 1)."""
+    if role == 1 and getattr(cache, "k_value", None) is not None:
+        return cache.k_value
+    return cache.k_active
 
 
 def ring_rows(cache, b, h, role, L):
@@ -73,7 +80,6 @@ def compare_unit(cache, oc, b, h, L, dtype_np, values: str = "same"):
     (values="e4m3": the sparse values as E4M3 codes, the ring in dtype_np)."""
     S = oc["n_sparse"]
     assert S == max(L - cache.desc.buffer_tokens, 0)
-    k = cache.k_active[b]
     e4m3 = values == "e4m3"
     for role, r in enumerate(("k", "v")):
         idx, val, pidx, pval = unit_pages(cache, b, h, role, S, np.uint8 if e4m3 else dtype_np)

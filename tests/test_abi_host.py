@@ -50,15 +50,20 @@ def test_page_and_cache_sizes():
     assert swan.page_bytes(swan.SWAN_F16, 48) == 64 * 48 * 3
     assert swan.page_bytes(swan.SWAN_F16, 45) == 64 * 48 * 3  # k padded to 8
     assert swan.page_bytes(swan.SWAN_F32, 64) == 64 * 64 * 5
-    pb, rb = swan.cache_bytes(_desc(), [48, 64])
+    kb, vb, rb = swan.cache_bytes(_desc(), [48, 64])
     npc = (1000 + 63) // 64
-    assert pb == 2 * npc * 64 * 3 * (48 + 64)
+    assert kb == vb == 2 * npc * 64 * 3 * (48 + 64)
     assert rb == 2 * 2 * 16 * 128 * 2
+    # keys and values with their own k (k_pad 80 / 56 and 8 / 128)
+    kb, vb, rb2 = swan.cache_bytes(_desc(), [77, 1], [51, 128])
+    assert kb == 2 * npc * 64 * 3 * (80 + 8)
+    assert vb == 2 * npc * 64 * 3 * (56 + 128)
+    assert rb2 == rb
     # E4M3 sparse values: one byte per value plus one per index; the ring stays fp16
     assert swan.page_bytes(swan.SWAN_F16_E4M3, 48) == 64 * 48 * 2
     assert swan.page_bytes(swan.SWAN_F16_E4M3, 41) == 64 * 48 * 2
-    pb8, rb8 = swan.cache_bytes(_desc(dtype=swan.SWAN_F16_E4M3), [48, 64])
-    assert pb8 == 2 * npc * 64 * 2 * (48 + 64)
+    kb8, vb8, rb8 = swan.cache_bytes(_desc(dtype=swan.SWAN_F16_E4M3), [48, 64])
+    assert kb8 == vb8 == 2 * npc * 64 * 2 * (48 + 64)
     assert rb8 == rb
     with pytest.raises(swan.SwanError):
         swan.page_bytes(3, 48)
@@ -82,7 +87,8 @@ def test_compress_rejects_bad_descriptors(kw, status):
     n = max(1, min(d.batch, 64))
     seq = swan._i32_array([0] * n)
     kk = swan._i32_array([48] * n)
-    st = lib.swan_compress_append(ctypes.byref(d), seq, kk, FAKE, FAKE, 1, None, FAKE, FAKE, None)
+    st = lib.swan_compress_append(ctypes.byref(d), seq, kk, None, FAKE, FAKE, 1, None, FAKE,
+                                  FAKE, None)
     assert st == status, swan.last_error()
     assert swan.last_error()
 
@@ -93,26 +99,26 @@ def test_compress_rejects_bad_arguments():
     ok_seq = swan._i32_array([10, 20])
     ok_k = swan._i32_array([48, 64])
     E = swan.SWAN_ERR_INVALID_ARG
-    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, swan._i32_array([0, 48]), FAKE,
+    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, swan._i32_array([0, 48]), None, FAKE,
                                     FAKE, 1, None, FAKE, FAKE, None) == E
-    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, swan._i32_array([48, 129]), FAKE,
+    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, swan._i32_array([48, 129]), None, FAKE,
                                     FAKE, 1, None, FAKE, FAKE, None) == E
-    assert lib.swan_compress_append(ctypes.byref(d), None, ok_k, FAKE, FAKE, 1, None, FAKE,
+    assert lib.swan_compress_append(ctypes.byref(d), None, ok_k, None, FAKE, FAKE, 1, None, FAKE,
                                     FAKE, None) == E
-    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, FAKE, FAKE, 2,
+    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, None, FAKE, FAKE, 2,
                                     swan._i32_array([1, 3]), FAKE, FAKE, None) == E
-    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, FAKE, FAKE, -1, None, FAKE,
+    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, None, FAKE, FAKE, -1, None, FAKE,
                                     FAKE, None) == E
-    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, None, FAKE, 1, None, FAKE,
+    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, None, None, FAKE, 1, None, FAKE,
                                     FAKE, None) == E
-    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, FAKE, FAKE, 1, None, None,
+    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, None, FAKE, FAKE, 1, None, None,
                                     FAKE, None) == E
-    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, FAKE, FAKE, 1, None, FAKE + 8,
+    assert lib.swan_compress_append(ctypes.byref(d), ok_seq, ok_k, None, FAKE, FAKE, 1, None, FAKE + 8,
                                     FAKE, None) == E
-    assert lib.swan_compress_append(ctypes.byref(d), swan._i32_array([-1, 0]), ok_k, FAKE, FAKE,
+    assert lib.swan_compress_append(ctypes.byref(d), swan._i32_array([-1, 0]), ok_k, None, FAKE, FAKE,
                                     1, None, FAKE, FAKE, None) == E
     # capacity: 1000 + 16 tokens fit, one more does not
-    st = lib.swan_compress_append(ctypes.byref(d), swan._i32_array([1016, 0]), ok_k, FAKE, FAKE,
+    st = lib.swan_compress_append(ctypes.byref(d), swan._i32_array([1016, 0]), ok_k, None, FAKE, FAKE,
                                   1, None, FAKE, FAKE, None)
     assert st == swan.SWAN_ERR_CAPACITY
 
@@ -125,8 +131,8 @@ def test_decode_rejects_bad_arguments():
     need = swan.decode_workspace_bytes(d, [100, 200], [48, 64])
     assert need > 0
     E = swan.SWAN_ERR_INVALID_ARG
-    args = lambda seq_, ws, wsb, scale=0.0: (ctypes.byref(d), seq_, ok_k, FAKE, FAKE, FAKE,
-                                            scale, FAKE, ws, wsb, None)
+    args = lambda seq_, ws, wsb, scale=0.0: (ctypes.byref(d), seq_, ok_k, None, FAKE, FAKE,
+                                            FAKE, scale, FAKE, ws, wsb, None)
     assert lib.swan_decode_attention(*args(swan._i32_array([0, 5]), FAKE, need)) == E
     assert lib.swan_decode_attention(*args(seq, None, need)) == swan.SWAN_ERR_WORKSPACE
     assert lib.swan_decode_attention(*args(seq, FAKE, need - 1)) == swan.SWAN_ERR_WORKSPACE
@@ -134,8 +140,12 @@ def test_decode_rejects_bad_arguments():
     assert lib.swan_decode_attention(*args(seq, FAKE, need, float("nan"))) == E
     assert lib.swan_decode_attention(*args(swan._i32_array([1017, 5]), FAKE, 1 << 30)) == \
         swan.SWAN_ERR_CAPACITY
-    assert lib.swan_decode_attention(ctypes.byref(d), seq, ok_k, None, FAKE, FAKE, 0.0, FAKE,
-                                     FAKE, need, None) == E
+    assert lib.swan_decode_attention(ctypes.byref(d), seq, ok_k, None, None, FAKE, FAKE, 0.0,
+                                     FAKE, FAKE, need, None) == E
+    # k_value outside 1..128
+    for bad in ([48, 0], [129, 48]):
+        assert lib.swan_decode_attention(ctypes.byref(d), seq, ok_k, swan._i32_array(bad), FAKE,
+                                         FAKE, FAKE, 0.0, FAKE, FAKE, 1 << 30, None) == E
 
 
 def test_calibrate_rejects_bad_arguments():
@@ -163,3 +173,17 @@ def test_workspace_grows_with_splits():
     small = swan.decode_workspace_bytes(d, [100], [48])
     large = swan.decode_workspace_bytes(d, [1 << 19], [48])
     assert large > small > 0
+
+
+def test_two_pass_workspace_holds_the_scores():
+    """Keys and values with different k_pad: one float per sparse token (rounded up
+    to a page) and query head for the scores; same k_pad: no scores."""
+    d = _desc(batch=2, n_q_heads=8, n_kv_heads=2, buffer_tokens=16, sparse_capacity=1 << 16)
+    L = [5000, 3000]
+    base = swan.decode_workspace_bytes(d, L, [48, 48])
+    assert swan.decode_workspace_bytes(d, L, [48, 48], [48, 48]) == base
+    assert swan.decode_workspace_bytes(d, L, [48, 48], [41, 47]) == base  # same k_pad
+    two = swan.decode_workspace_bytes(d, L, [48, 48], [32, 48])
+    stride = -(-(5000 - 16) // 64) * 64
+    assert two - base >= 2 * 8 * stride * 4
+    assert two - base < 2 * 8 * stride * 4 + 2048  # the rest is split-count rounding

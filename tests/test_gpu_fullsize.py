@@ -32,6 +32,8 @@ def _run(device, name: str, n_units: int):
     w = si.WORKLOADS[name]
     np_dt = si.np_dtype(w.dtype)
     ks = [int(k) for k in si.k_active_for(w)]
+    kvs = si.k_value_for(w)
+    kvs = None if kvs is None else [int(k) for k in kvs]
     L = w.context
     _log(f"[{name}] calibrating {2 * w.n_kv_heads} rotations")
     Pqk = torch.empty((w.n_kv_heads, 128, 128), dtype=torch.float32, device=device)
@@ -48,7 +50,8 @@ def _run(device, name: str, n_units: int):
     V1 = si.kv_rows_device(w.wid, w.batch, w.n_kv_heads, si.ROLE_V, 1, w.dtype, device, block=1)
     q = si.queries_device(w.wid, w.batch, w.n_q_heads, w.dtype, device)
     cache = swan.SwanCache(w.batch, w.n_q_heads, w.n_kv_heads, w.buffer, L - w.buffer, ks,
-                           C.torch_dtype(w.dtype), device, sparse_values=w.sparse_values)
+                           C.torch_dtype(w.dtype), device, sparse_values=w.sparse_values,
+                           k_value=kvs)
     vals = "e4m3" if w.sparse_values == "e4m3" else "t"
     cache.append(K, V, Pqk, Pvo)
     cache.append(K1, V1, Pqk, Pvo)
@@ -67,13 +70,15 @@ def _run(device, name: str, n_units: int):
     for b, h in units:
         Kh = np.concatenate([K[b, h].cpu().numpy(), K1[b, h].cpu().numpy()])
         Vh = np.concatenate([V[b, h].cpu().numpy(), V1[b, h].cpu().numpy()])
-        oc = O.compress_block(Kh, Vh, P_qk[h], P_vo[h], w.buffer, ks[b], np_dt, values=vals)
+        oc = O.compress_block(Kh, Vh, P_qk[h], P_vo[h], w.buffer, ks[b], np_dt, values=vals,
+                              k_value=None if kvs is None else kvs[b])
         C.compare_unit(cache, oc, b, h, L, np_dt, values=w.sparse_values)
         for hq in range(h * G, (h + 1) * G):
             ref = O.attend_arrays(q_np[b, hq], P_qk[h], P_vo[h], oc)
             err = C.max_rel_err(out_np[b, hq][None], ref[None])
             worst = max(worst, err)
-        _log(f"[{name}] unit (b={b}, h={h}, k={ks[b]}): pages and ring bit-exact, "
+        kv_txt = "" if kvs is None else f"/{kvs[b]}"
+        _log(f"[{name}] unit (b={b}, h={h}, k={ks[b]}{kv_txt}): pages and ring bit-exact, "
              f"worst output err so far {worst:.2e}")
     assert worst <= TOL
 
@@ -92,3 +97,11 @@ def test_prefill16k_batch8_per_sequence_k(gpu_device):
 
 def test_llama2_7b_32k_batch16_e4m3_values(gpu_device):
     _run(gpu_device, "llama2_7b_L32k_b16_e4m3", 4)
+
+
+def test_llama2_7b_32k_batch16_keys77_values51(gpu_device):
+    _run(gpu_device, "llama2_7b_L32k_b16_k77_v51", 4)
+
+
+def test_llama3_8b_gqa_128k_batch4_keys77_values51(gpu_device):
+    _run(gpu_device, "llama3_8b_gqa_L128k_b4_k77_v51", 2)

@@ -61,7 +61,7 @@ def test_calibrate_constructed_basis(gpu_device):
 # compress-append: indices and values bit-exact
 # --------------------------------------------------------------------------- #
 def _build(swan_mod, torch_mod, device, *, B, Hq, Hkv, L, b, k_active, dtype, chunks=None,
-           seed=0, capacity=None, wid=99, values="same"):
+           seed=0, capacity=None, wid=99, values="same", k_value=None):
     """GPU cache + oracle caches for synthetic rows of the recipe."""
     torch = torch_mod
     np_dt = si.np_dtype(dtype)
@@ -80,7 +80,7 @@ def _build(swan_mod, torch_mod, device, *, B, Hq, Hkv, L, b, k_active, dtype, ch
             V[bi, h] = si.lowrank_rows(si.rng_for(wid, seed, bi, h, 1), Lmax, R).astype(np_dt)
     cap = capacity if capacity is not None else max(Lmax - b, 1)
     cache = swan_mod.SwanCache(B, Hq, Hkv, b, cap, k_active, C.torch_dtype(dtype), device,
-                               sparse_values=values)
+                               sparse_values=values, k_value=k_value)
     tP_qk = torch.tensor(Pqk, device=device)
     tP_vo = torch.tensor(Pvo, device=device)
     # sequences of different lengths: each chunk appends min(n, what is left)
@@ -101,7 +101,9 @@ def _build(swan_mod, torch_mod, device, *, B, Hq, Hkv, L, b, k_active, dtype, ch
     torch.cuda.synchronize()
     ovals = "e4m3" if values == "e4m3" else "t"
     oc = [[O.compress_block(K[bi, h, :Ls[bi]], V[bi, h, :Ls[bi]], Pqk[h], Pvo[h], b,
-                            k_active[bi], np_dt, values=ovals) for h in range(Hkv)]
+                            k_active[bi], np_dt, values=ovals,
+                            k_value=None if k_value is None else k_value[bi])
+           for h in range(Hkv)]
           for bi in range(B)]
     return cache, oc, Pqk, Pvo, tP_qk, tP_vo, K, V
 
