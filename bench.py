@@ -25,8 +25,9 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic_{wl}.txt")
 # sources of the decode attention kernels: counter summaries are valid only for these bytes
-ATTN_SOURCES = ("decode.hip", "decode_gqa.hip", "decode_score_pass.hip", "decode_value_pass.hip",
-                "decode_common.h", "decode_gqa_common.h", "swan_device.h", "swan_internal.h")
+ATTN_SOURCES = ("decode.hip", "decode_gqa.hip", "decode_asym.hip", "decode_gqa_asym.hip",
+                "decode_mha.h", "decode_gqa.h", "decode_common.h", "decode_gqa_common.h",
+                "swan_device.h", "swan_internal.h")
 
 
 def log(*a):
@@ -100,25 +101,21 @@ def kpad(k: int) -> int:
 
 
 def attn_kernel_name(w, k_key, k_val) -> str:
-    """The decode attention kernels the library launches for this shape: one launch per
-    distinct padded k in the batch, or a score and a value launch for sequences whose
-    keys and values have different padded k."""
+    """The decode attention kernel the library launches for this shape (one launch per
+    distinct (key, value) padded k in the batch)."""
     g = w.n_q_heads // w.n_kv_heads
-    hpw = 1
+    asym = any(kpad(a) != kpad(b) for a, b in zip(k_key, k_val))
+    note = ("; keys and values with different k_pad: specialised on the larger, each role "
+            "at its own page size" if asym else "")
     if w.dtype == "f16" and g > 1 and g % 2 == 0:
         hpw = 8 if g % 8 == 0 else 4 if g % 4 == 0 else 2
-    if any(kpad(a) != kpad(b) for a, b in zip(k_key, k_val)):
-        value = "gqa_value_kernel" if hpw > 1 else "value_kernel"
-        return (f"score_kernel + {value} (two-pass: keys and values with different k_pad; "
-                f"{hpw} query head(s) per wave, sparse split-K; dense buffer in the value pass)")
-    if hpw > 1:
-        return f"attn_gqa_kernel ({hpw} query heads per wave, sparse split-K + dense buffer)"
-    return "attn_kernel (one query head per wave, sparse split-K + dense buffer)"
+        return (f"attn_gqa_kernel ({hpw} query heads per wave, sparse split-K + dense buffer"
+                f"{note})")
+    return f"attn_kernel (one query head per wave, sparse split-K + dense buffer{note})"
 
 
 def launches_per_step(k_key, k_val) -> int:
-    pairs = {(kpad(a), kpad(b)) for a, b in zip(k_key, k_val)}
-    return sum(1 if a == b else 2 for a, b in pairs)
+    return len({(kpad(a), kpad(b)) for a, b in zip(k_key, k_val)})
 
 
 def cpu_model() -> str:
@@ -365,8 +362,8 @@ def main():
             "frac": achieved / HBM_PEAK_GBPS,
             "traffic": traffic,
             "kernel": attn_kernel_name(w, ks, kv_list),
-            # one launch per distinct padded k in the batch (two for a two-pass group);
-            # bytes and time cover all of a step's attention launches together
+            # one launch per distinct (key, value) padded k in the batch; bytes and
+            # time cover all of a step's attention launches together
             "launches_per_step": launches_per_step(ks, kv_list),
             "algorithmic_bytes_per_launch": bytes_avg,
             "avg_launch_ms": attn_avg * 1e3,

@@ -185,12 +185,7 @@ swan_status swan_compress_append(const swan_cache* c, const int32_t* seq_len_hos
                                  const int32_t* n_new_host, const float* P_qk,
                                  const float* P_vo, void* stream);
 
-/*
- * Device workspace needed by swan_decode_attention for these lengths and k.
- * Sequences whose keys and values have different k_pad are attended in two
- * passes (scores, then values); their per-token scores take
- * batch * n_q_heads * (their longest sparse part, rounded up to 64) floats.
- */
+/* Device workspace needed by swan_decode_attention for these lengths and k. */
 swan_status swan_decode_workspace_bytes(const swan_cache* c, const int32_t* seq_len_host,
                                         const int32_t* k_active_host,
                                         const int32_t* k_value_host, size_t* bytes);
@@ -217,9 +212,8 @@ swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_ho
 /*
  * Profiling hook.  While both are non-NULL, swan_decode_attention on this
  * thread records start_event (a hipEvent_t) on its stream right before its
- * sparse/buffer attention launches and stop_event right after them (both
- * passes, for two-pass sequences), so that hipEventElapsedTime gives the
- * duration of those kernels alone.  NULL, NULL
+ * sparse/buffer attention launches and stop_event right after them, so that
+ * hipEventElapsedTime gives the duration of those kernels alone.  NULL, NULL
  * (the default) disables it.  The events stay owned by the caller.
  */
 swan_status swan_set_profile_events(void* start_event, void* stop_event);

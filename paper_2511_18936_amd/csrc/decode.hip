@@ -8,27 +8,16 @@
 //                  the rotated space.  One launch per distinct k_pad of the
 //                  batch; several run side by side on library-owned streams,
 //                  joined back before the merge.  For fp16 GQA the launch is
-//                  attn_gqa_kernel (decode_gqa.hip) instead, one workgroup per
+//                  attn_gqa_kernel (decode_gqa.h) instead, one workgroup per
 //                  KV stream for several query heads.  Sequences whose keys and
-//                  values have different k_pad take two launches instead, a
-//                  score pass and a value pass (decode_score_pass.hip,
-//                  decode_value_pass.hip).
+//                  values have different k_pad run the same kernels specialised
+//                  on the larger k_pad (decode_asym.hip, decode_gqa_asym.hip).
 //   merge_kernel   log-sum-exp merge of the partials, then o = o_hat . P_VO^T
 //                  (the inverse rotation that Sec. 4.2 absorbs into W_O)
-//
-// Sparse wave: one token per lane.  The rotated query is replicated 8 times in
-// LDS (q_rep[dim][8]) so that the gathers q_hat[idx] of 8 consecutive lanes
-// fall on distinct banks; the value accumulator is lane-private, acc[dim][64]
-// in LDS: a token's indices are distinct, so each page's update is a plain
-// read-modify-write with all reads issued before the writes.  Pages of keys
-// and values are streamed with coalesced nontemporal loads, the page after
-// next in flight while the current one is consumed.  The softmax reference m
-// is the first page's maximum and is only raised (with a rescale of acc) when
-// a score exceeds it by more than kTau in log2 units (one ballot per page), so
-// exponentials stay bounded by 2^kTau while rescales are rare.
+// The sparse attention wave itself is described in decode_mha.h.
 #include <mutex>
 
-#include "decode_common.h"
+#include "decode_mha.h"
 
 namespace swan {
 
@@ -51,147 +40,6 @@ __global__ __launch_bounds__(128) void qrot_kernel(const T* __restrict__ q,
 #pragma unroll 32
   for (int i = 0; i < kD; ++i) acc = fmaf(qs[i], P[i * kD + j], acc);
   qhat[(int64_t)bh * kD + j] = acc * mult;
-}
-
-__device__ __forceinline__ void rescale_acc(float* acc, int lane, float f) {
-  wave_lds_fence();
-#pragma unroll 8
-  for (int c = 0; c < kAccCols / 2; ++c) {
-    float4* p = (float4*)acc + c * 64 + lane;
-    float4 v = *p;
-    v.x *= f; v.y *= f; v.z *= f; v.w *= f;
-    *p = v;
-  }
-  wave_lds_fence();
-}
-
-template <typename T, int KP8>
-__device__ __forceinline__ void process_page(const PageRegs<T, KP8>& kr, const PageRegs<T, KP8>& vr,
-                                             bool valid, const float* qrep_l, float* acc_l,
-                                             float* acc, int lane, SoftmaxState& st) {
-  const float s = valid ? page_score<T, KP8>(kr, qrep_l) : -INFINITY;
-  // the reference m only moves when a score passes m + kTau: one ballot per
-  // page, a wave max only on the first page and on the rare raise
-  if (st.first) {
-    st.m = wave_max(s);
-    st.first = false;
-  } else if (__ballot(s > st.m + kTau) != 0) {
-    const float pm = wave_max(s);
-    const float f = exp2f(st.m - pm);
-    rescale_acc(acc, lane, f);
-    st.l *= f;
-    st.m = pm;
-  }
-  const float p = valid ? exp2f(s - st.m) : 0.f;
-  st.l += p;
-  page_accumulate<T, KP8>(vr, acc_l, p, valid);
-}
-
-// One wave: pages [pbeg, pend) of one (sequence, kv head), for one query head.
-// The next page is always loaded (clamped to the last page) so that no load
-// sits under a branch and the compiler can keep one page in flight.
-template <typename T, int KP8>
-__device__ void sparse_split(const char* kbase, const char* vbase, int64_t pbytes, int pbeg,
-                             int pend, int S, float* qrep, float* acc, int lane,
-                             float* __restrict__ part) {
-  const float* qrep_l = qrep + (lane & (kQRep - 1));
-  float* acc_l = acc + (lane & (kAccCols - 1));
-  SoftmaxState st{0.f, 0.f, true};
-  // pipeline depth by the register footprint of a page (16-byte chunks per lane)
-  constexpr int kChunks = KP8 * PageRegs<T, KP8>::VCH;
-  if constexpr (kChunks <= 12) {  // two register sets: one page in flight
-    PageRegs<T, KP8> ka, va, kb, vb;
-    const int plast = pend - 1;
-    load_page<T, KP8>(ka, kbase + pbeg * pbytes, lane);
-    load_page<T, KP8>(va, vbase + pbeg * pbytes, lane);
-    for (int p = pbeg; p < pend; p += 2) {
-      const int p1 = p + 1 < plast ? p + 1 : plast;
-      load_page<T, KP8>(kb, kbase + p1 * pbytes, lane);
-      load_page<T, KP8>(vb, vbase + p1 * pbytes, lane);
-      process_page<T, KP8>(ka, va, p * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
-      const int p2 = p + 2 < plast ? p + 2 : plast;
-      load_page<T, KP8>(ka, kbase + p2 * pbytes, lane);
-      load_page<T, KP8>(va, vbase + p2 * pbytes, lane);
-      if (p + 1 < pend)
-        process_page<T, KP8>(kb, vb, (p + 1) * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
-    }
-  } else {  // large pages: one page at a time
-    PageRegs<T, KP8> ka, va;
-    for (int p = pbeg; p < pend; ++p) {
-      load_page<T, KP8>(ka, kbase + p * pbytes, lane);
-      load_page<T, KP8>(va, vbase + p * pbytes, lane);
-      process_page<T, KP8>(ka, va, p * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
-    }
-  }
-  const float ltot = wave_sum(st.l);
-  wave_lds_fence();
-  reduce_acc(acc, lane, part);
-  if (lane == 0) {
-    part[0] = st.m;
-    part[1] = ltot;
-  }
-}
-
-// One launch per distinct k_pad of the batch (KP8 = k_pad / 8), over the
-// sequences g.seq[0..g.n) that use it.  Grid: n * Hq dense-buffer waves first,
-// then n * Hq * g.n_splits sparse waves.
-template <typename T, int KP8>
-__global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup g) {
-  __shared__ __attribute__((aligned(16))) float qrep[kD * kQRep];
-  __shared__ __attribute__((aligned(16))) float acc[kD * kAccCols];
-  const int lane = threadIdx.x;
-  const int GH = g.n * a.Hq;
-  const int G = a.Hq / a.Hkv;
-  const int pstride = a.n_splits + 1;  // partial slots per (sequence, q-head)
-  int w = blockIdx.x;
-  if (w < GH) {  // dense-buffer wave
-    const int b = g.seq[w / a.Hq], hq = w % a.Hq, h = hq / G;
-    const int bhq = b * a.Hq + hq;
-    const int L = a.tab.len[b];
-    const int nb = L < a.bb ? L : a.bb;
-    if (nb == 0) return;
-    const int64_t ring_off = ((int64_t)b * a.Hkv + h) * a.bb * kD;
-    float* part = a.part + ((int64_t)bhq * pstride + a.n_splits) * kPartFloats;
-    using E = typename Fmt<T>::Elem;
-    buffer_part<E>((const E*)a.k_ring + ring_off, (const E*)a.v_ring + ring_off, nb,
-                   a.qhat + (int64_t)bhq * kD, qrep, acc, lane, part);
-    return;
-  }
-  w -= GH;
-  const int split = w / GH;
-  const int gi = w % GH;
-  const int b = g.seq[gi / a.Hq], hq = gi % a.Hq, h = hq / G;
-  const int bhq = b * a.Hq + hq;
-  const int L = a.tab.len[b];
-  const int S = L > a.bb ? L - a.bb : 0;
-  const int np = pages_for(S);
-  const int nsb = a.tab.nsplit[b];
-  const int ns = np < nsb ? np : nsb;
-  if (split >= ns) return;
-  const int pbeg = split_begin(split, ns, np);
-  const int pend = split_begin(split + 1, ns, np);
-  // keys and values share k_pad here (so the page size), not the offsets
-  const int64_t pbytes = page_bytes_of(Fmt<T>::kValBytes, a.tab.kact[0][b]);
-  const int64_t head_off = (int64_t)h * a.n_pages_cap * pbytes;
-  const char* kbase = (const char*)a.k_pages + a.tab.page_off[0][b] + head_off;
-  const char* vbase = (const char*)a.v_pages + a.tab.page_off[1][b] + head_off;
-  float* part = a.part + ((int64_t)bhq * pstride + split) * kPartFloats;
-
-  // replicate q_hat: q_rep[dim][8]; lane writes dims lane and lane + 64
-  const float* qh = a.qhat + (int64_t)bhq * kD;
-#pragma unroll
-  for (int hh = 0; hh < 2; ++hh) {
-    const int r = lane + 64 * hh;
-    const float v = qh[r];
-    float4* row = (float4*)(qrep + r * kQRep);
-    row[0] = make_float4(v, v, v, v);
-    row[1] = make_float4(v, v, v, v);
-  }
-#pragma unroll 8
-  for (int c = 0; c < kAccCols / 2; ++c)
-    ((float4*)acc)[c * 64 + lane] = make_float4(0.f, 0.f, 0.f, 0.f);
-  wave_lds_fence();
-  sparse_split<T, KP8>(kbase, vbase, pbytes, pbeg, pend, S, qrep, acc, lane, part);
 }
 
 // ---------------------------------------------------------------------------
@@ -252,7 +100,7 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeLaunch a) {
 template <typename T, int KP8>
 static hipError_t launch_attn(const DecodeLaunch& a, const SeqGroup& g) {
   const dim3 grid(g.n * a.Hq * (g.n_splits + 1));
-  hipLaunchKernelGGL((attn_kernel<T, KP8>), grid, dim3(64), 0, a.stream, a, g);
+  hipLaunchKernelGGL((attn_kernel<T, KP8, false>), grid, dim3(64), 0, a.stream, a, g);
   return hipGetLastError();
 }
 
@@ -319,8 +167,8 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
     if (e != hipSuccess) return e;
   }
   // sequences grouped by (k_pad of the keys, k_pad of the values), largest
-  // first: one launch per group specialised on its k_pad, or a score and a
-  // value launch when the two differ
+  // first: one launch per group, specialised on its k_pad, or on the larger of
+  // the two when they differ
   SeqGroup groups[SWAN_MAX_BATCH];
   int kp8k[SWAN_MAX_BATCH], kp8v[SWAN_MAX_BATCH];
   uint32_t present[kD / 8 + 1] = {};  // bit v of present[k]: some sequence has (k, v)
@@ -343,8 +191,11 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
       ++ng;
     }
   auto launch_one = [&](const DecodeLaunch& ai, int i) {
-    return kp8k[i] == kp8v[i] ? launch_group<T>(ai, groups[i], kp8k[i])
-                              : launch_two_pass(ai, groups[i], kp8k[i], kp8v[i]);
+    if (kp8k[i] == kp8v[i]) return launch_group<T>(ai, groups[i], kp8k[i]);
+    const int kp8 = kp8k[i] > kp8v[i] ? kp8k[i] : kp8v[i];
+    return decode_heads_per_wave(ai.dtype, ai.Hq, ai.Hkv) > 1
+               ? launch_attn_gqa_asym(ai, groups[i], kp8)
+               : launch_attn_asym(ai, groups[i], kp8);
   };
   SideStreams* ss = ng > 1 ? side_streams(a.stream) : nullptr;
   if (!ss) {  // one launch, or no side streams: back to back on the caller's stream

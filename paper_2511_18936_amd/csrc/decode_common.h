@@ -23,19 +23,52 @@ struct PageRegs {
   u32x2 idx[KP8];
 };
 
+// Spare groups.  The registers hold KP8 groups of 8 entries; a page of a
+// smaller k_pad = 8 n8 (n8 < KP8, wave-uniform) fills the first n8 of them.
+// Groups n8..KP8-1 are loaded from the two read-only arrays below instead:
+// value 0 and index kSpareRow, a row past the head dimension that the
+// kernels using spare groups add to their LDS query replicas (zeroed), their
+// accumulators and their value tiles.  So the compute runs over all KP8
+// groups with no branch (a branch per group keeps the compiler from batching
+// a page's LDS accesses), and the spare entries change nothing: 0 * q = 0 in
+// the score, and the accumulator updates land in the spare row.  With
+// n8 = KP8 (a compile-time constant) the selection folds away.
+constexpr int kSpareRow = kD;
+#define SWAN_X8(v) v, v, v, v, v, v, v, v
+#define SWAN_X64(v) SWAN_X8(v), SWAN_X8(v), SWAN_X8(v), SWAN_X8(v), \
+                    SWAN_X8(v), SWAN_X8(v), SWAN_X8(v), SWAN_X8(v)
+static __device__ const u32x4 kZeroChunks[64] = {};  // a value chunk of 64 lanes
+static __device__ const uint32_t kSpareIdx[128] = {SWAN_X64(0x80808080u),
+                                                   SWAN_X64(0x80808080u)};  // kSpareRow bytes
+#undef SWAN_X64
+#undef SWAN_X8
+static_assert(kSpareRow == 0x80, "the spare index bytes are 0x80");
+
 // Loads one page into registers (nontemporal: the pages are streamed once).
+// The addresses are global-memory pointers so that the choice between page
+// and spare arrays stays a global load (a generic pointer would make it a
+// flat load, which also holds up the waits for LDS accesses).
+#define SWAN_GLOBAL __attribute__((address_space(1)))
 template <typename T, int KP8>
-__device__ __forceinline__ void load_page(PageRegs<T, KP8>& r, const char* page, int lane) {
+__device__ __forceinline__ void load_page(PageRegs<T, KP8>& r, const char* page, int lane,
+                                          int n8 = KP8) {
   using PR = PageRegs<T, KP8>;
-  const char* vp = page + lane * PR::CB;
+  using Chunk = typename PR::VChunk;
+  const SWAN_GLOBAL char* pg = (const SWAN_GLOBAL char*)page;
+  const SWAN_GLOBAL char* vp = pg + lane * PR::CB;
+  const SWAN_GLOBAL char* zp = (const SWAN_GLOBAL char*)kZeroChunks + lane * PR::CB;
 #pragma unroll
-  for (int c = 0; c < KP8 * PR::VCH; ++c)
-    r.val[c] = __builtin_nontemporal_load((const typename PR::VChunk*)(vp + c * 64 * PR::CB));
-  const char* ip = page + KP8 * PR::VCH * 64 * PR::CB + lane * 8;  // 64 * k_pad value bytes
+  for (int c = 0; c < KP8 * PR::VCH; ++c) {
+    const SWAN_GLOBAL char* src = c < n8 * PR::VCH ? vp + c * 64 * PR::CB : zp;
+    r.val[c] = __builtin_nontemporal_load((const SWAN_GLOBAL Chunk*)src);
+  }
+  const SWAN_GLOBAL char* ip = pg + n8 * PR::VCH * 64 * PR::CB + lane * 8;  // past the values
+  const SWAN_GLOBAL char* sp = (const SWAN_GLOBAL char*)kSpareIdx + lane * 8;
 #pragma unroll
   for (int g = 0; g < KP8; ++g)
-    r.idx[g] = __builtin_nontemporal_load((const u32x2*)(ip + g * 512));
+    r.idx[g] = __builtin_nontemporal_load((const SWAN_GLOBAL u32x2*)(g < n8 ? ip + g * 512 : sp));
 }
+#undef SWAN_GLOBAL
 
 // E4M3 byte `sel` (compile-time after unrolling) of w, as float (exact)
 __device__ __forceinline__ float e4m3_byte_to_f32(uint32_t w, int sel) {
@@ -83,6 +116,14 @@ template <typename T, int KP8>
 __device__ __forceinline__ int entry_idx(const PageRegs<T, KP8>& r, int g, int u) {
   const uint32_t w = (u < 4) ? r.idx[g].x : r.idx[g].y;
   return (int)((w >> (8 * (u & 3))) & 0xFFu);
+}
+
+// LDS accesses of one wave execute in program order; this keeps the compiler
+// from moving them across the point (no workgroup barrier: waves of one
+// workgroup may take different branches).
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
 }
 
 // ---------------------------------------------------------------------------
@@ -146,6 +187,19 @@ __device__ __forceinline__ void page_accumulate(const PageRegs<T, KP8>& r, float
   }
 }
 
+// acc *= f (the whole accumulator of this wave)
+__device__ __forceinline__ void rescale_acc(float* acc, int lane, float f) {
+  wave_lds_fence();
+#pragma unroll 8
+  for (int c = 0; c < kAccCols / 2; ++c) {
+    float4* p = (float4*)acc + c * 64 + lane;
+    float4 v = *p;
+    v.x *= f; v.y *= f; v.z *= f; v.w *= f;
+    *p = v;
+  }
+  wave_lds_fence();
+}
+
 // part[4 + r] = the sum over the columns of acc row r; lane owns rows lane and
 // lane + 64, its starting chunk staggered per lane to spread the banks
 __device__ __forceinline__ void reduce_acc(const float* acc, int lane, float* __restrict__ part) {
@@ -169,14 +223,6 @@ struct SoftmaxState {
   float l;     // per-lane sum of exp2(s - m)
   bool first;
 };
-
-// LDS accesses of one wave execute in program order; this keeps the compiler
-// from moving them across the point (no workgroup barrier: waves of one
-// workgroup may take different branches).
-__device__ __forceinline__ void wave_lds_fence() {
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-}
 
 // One wave: the dense buffer of one (sequence, kv head), for one query head.
 // Lane t scores buffer token t (a dense 128-dim dot product), then lane l

@@ -167,32 +167,14 @@ int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t*
   return ns_max;
 }
 
-// Tokens per (sequence, query head) row of the two-pass decode's scores: the
-// longest sparse part, in whole pages, of a sequence whose keys and values
-// have different k_pad (0 when there is none).
-int64_t score_stride(const swan_cache* c, const int32_t* seq_len_host,
-                     const int32_t* k_active_host, const int32_t* k_value_host) {
-  int64_t st = 0;
-  for (int b = 0; b < c->batch; ++b) {
-    if (swan::kpad_of(k_of(k_active_host, k_value_host, 0, b)) ==
-        swan::kpad_of(k_of(k_active_host, k_value_host, 1, b)))
-      continue;
-    const int S = seq_len_host[b] > c->buffer_tokens ? seq_len_host[b] - c->buffer_tokens : 0;
-    const int64_t t = (int64_t)swan::pages_for(S) * swan::kPage;
-    if (t > st) st = t;
-  }
-  return st;
-}
-
 size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// workspace: q_hat, the partials, then the two-pass scores
-size_t decode_ws_bytes(const swan_cache* c, int ns, int64_t sstride) {
+// workspace: q_hat, then the partials
+size_t decode_ws_bytes(const swan_cache* c, int ns) {
   const size_t units = (size_t)c->batch * c->n_q_heads;
   const size_t qhat = units * swan::kD * sizeof(float);
   const size_t part = units * (size_t)(ns + 1) * swan::kPartFloats * sizeof(float);
-  const size_t scores = units * (size_t)sstride * sizeof(float);
-  return round256(qhat) + round256(part) + scores;
+  return round256(qhat) + part;
 }
 
 swan_status hip_status(hipError_t e, const char* what) {
@@ -348,8 +330,7 @@ swan_status swan_decode_workspace_bytes(const swan_cache* c, const int32_t* seq_
   if (st != SWAN_OK) return st;
   if ((st = check_k(c, k_active_host, k_value_host)) != SWAN_OK) return st;
   if (!seq_len_host || !bytes) return fail(SWAN_ERR_INVALID_ARG, "NULL argument");
-  *bytes = decode_ws_bytes(c, plan_splits(c, seq_len_host, k_active_host, k_value_host, nullptr),
-                           score_stride(c, seq_len_host, k_active_host, k_value_host));
+  *bytes = decode_ws_bytes(c, plan_splits(c, seq_len_host, k_active_host, k_value_host, nullptr));
   return ok();
 }
 
@@ -378,8 +359,7 @@ swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_ho
   int64_t role_bytes[2];
   fill_layout(c, k_active_host, k_value_host, a.tab, role_bytes);
   const int ns = plan_splits(c, seq_len_host, k_active_host, k_value_host, a.tab.nsplit);
-  const int64_t sstride = score_stride(c, seq_len_host, k_active_host, k_value_host);
-  const size_t need = decode_ws_bytes(c, ns, sstride);
+  const size_t need = decode_ws_bytes(c, ns);
   if (!workspace || workspace_bytes < need)
     return fail(SWAN_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, need);
   if (((uintptr_t)workspace & 255) != 0)
@@ -395,12 +375,8 @@ swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_ho
   a.k_ring = c->k_ring;
   a.v_ring = c->v_ring;
   const size_t units = (size_t)c->batch * c->n_q_heads;
-  const size_t qhat_bytes = round256(units * swan::kD * sizeof(float));
-  const size_t part_bytes = round256(units * (size_t)(ns + 1) * swan::kPartFloats * sizeof(float));
   a.qhat = (float*)workspace;
-  a.part = (float*)((char*)workspace + qhat_bytes);
-  a.scores = sstride > 0 ? (float*)((char*)workspace + qhat_bytes + part_bytes) : nullptr;
-  a.score_stride = sstride;
+  a.part = (float*)((char*)workspace + round256(units * swan::kD * sizeof(float)));
   a.B = c->batch;
   a.Hq = c->n_q_heads;
   a.Hkv = c->n_kv_heads;

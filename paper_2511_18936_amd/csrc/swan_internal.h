@@ -56,8 +56,6 @@ struct DecodeLaunch {
   const void* v_ring;
   float* qhat;   // [B][Hq][128] workspace
   float* part;   // [B][Hq][NS + 1][kPartFloats] workspace
-  float* scores;         // two-pass decode: [B][Hq][score_stride] workspace (or NULL)
-  int64_t score_stride;  // tokens per (sequence, query head) row of `scores`
   int B, Hq, Hkv, bb, n_pages_cap;
   int n_splits;  // NS: largest split count of any launch (slot NS holds the buffer partial)
   float qmult;   // scale * log2(e)
@@ -86,9 +84,9 @@ inline int decode_heads_per_wave(int dtype, int n_q, int n_kv) {
   return ((dtype == SWAN_F16 || dtype == SWAN_F16_E4M3) && G > 1) ? gqa_heads_per_wave(G) : 1;
 }
 hipError_t launch_attn_gqa(const DecodeLaunch& a, const SeqGroup& g, int kp8);
-// sequences whose keys and values have different k_pad: a score pass over the
-// key pages (exact per-split maxima, scores to a.scores), then a value pass
-hipError_t launch_two_pass(const DecodeLaunch& a, const SeqGroup& g, int kp8_key, int kp8_val);
+// sequences whose keys and values have different k_pad; kp8 = the larger / 8
+hipError_t launch_attn_asym(const DecodeLaunch& a, const SeqGroup& g, int kp8);
+hipError_t launch_attn_gqa_asym(const DecodeLaunch& a, const SeqGroup& g, int kp8);
 
 
 struct CompressLaunch {

@@ -3,9 +3,10 @@ Table 2), on the GPU through the C ABI, against the oracle.
 
 Compress: indices and stored values bit-exact for each role with its own k.
 Decode: outputs within 2e-3 (max |o - o_ref| / max |o_ref| per query head).  A
-sequence whose keys and values have different k_pad takes the two-pass decode
-(score pass, value pass); one whose k differ within the same k_pad, the one-pass
-kernels; a batch can mix all of them.
+sequence whose keys and values have different k_pad takes the decode kernels
+specialised on the larger k_pad, with each role's own page size and group count;
+one whose k differ within the same k_pad, the equal-k_pad kernels; a batch can
+mix all of them.
 """
 import sys
 
@@ -58,7 +59,7 @@ def test_asym_chunked_appends(gpu_device, swan_mod, torch_mod, fmt, chunks):
 
 @pytest.mark.parametrize("fmt,L,b,kk,kv,Hq,Hkv", [
     ("f16", 700, 128, 77, 51, 4, 4), ("f16", 1000, 0, 77, 51, 4, 4), ("f16", 1, 0, 77, 51, 2, 2),
-    ("f16", 40, 64, 77, 51, 4, 4),  # buffer only: no sparse page in the two-pass group
+    ("f16", 40, 64, 77, 51, 4, 4),  # buffer only: no sparse page in the group
     ("f16", 2049, 128, 13, 115, 8, 2),  # GQA, 4 heads per wave
     ("f16", 1500, 64, 51, 77, 16, 2),  # GQA, 8 heads per wave
     ("f16", 900, 32, 24, 40, 4, 2),  # GQA, 2 heads per wave
@@ -81,8 +82,8 @@ def test_asym_decode_matches_oracle(gpu_device, swan_mod, torch_mod, fmt, L, b, 
 @pytest.mark.parametrize("fmt,Hq,Hkv", [("f16", 4, 4), ("f16", 8, 2), ("e4m3", 8, 2),
                                         ("f32", 2, 1)])
 def test_asym_mixed_batch(gpu_device, swan_mod, torch_mod, fmt, Hq, Hkv):
-    """One batch: symmetric k, equal k_pad with different k (one-pass), and several
-    different-k_pad pairs (two-pass), at ragged lengths, launched side by side."""
+    """One batch: symmetric k, equal k_pad with different k, and several different-k_pad
+    pairs, at ragged lengths, launched side by side."""
     _log(f"asym mixed batch fmt={fmt} Hq={Hq} Hkv={Hkv}")
     dtype, vals = _dt(fmt)
     kk = [48, 77, 48, 13, 77, 128, 64]
