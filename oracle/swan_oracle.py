@@ -30,6 +30,9 @@ paper states the method (SWAN: Sparse Winnowed Attention, arXiv 2511.18936):
                            the format's 127 finite magnitudes.
 * ``k_value``              keys and values pruned to different k (reading 10,
                            the key/value ablation of Appendix A.5, Table 2).
+* ``change_k_rows`` / ``UnitCache.change_k``  k changed for a running sequence
+                           (reading 11: k_active is a run-time input of
+                           Algorithm 1, Sec. 1 / Sec. 3).
 
 Readings of the paper used here (where it is silent or ambiguous):
   1. top-k ranks the stored (T-rounded) buffer value, because Algorithm 1 pops
@@ -49,7 +52,16 @@ Readings of the paper used here (where it is silent or ambiguous):
      Appendix A.5 (Table 2) retains different fractions of the key and the value
      dimensions.  Here a key keeps its k_active largest components and a value
      its k_value largest, by the same rule (readings 1-3); k_value defaults to
-     k_active.  A retention ratio r maps to round(r * d_h) components.
+     k_active.  A retention ratio r maps to round(r * d_h) components;
+ 11. k changed for a running sequence (Algorithm 1 takes k_active as an input
+     at every step).  Lowering it to k' re-prunes the tokens already in the
+     sparse cache: each keeps the k' largest of its stored values (ties to the
+     lower index), which for values stored in T is exactly its top-k' (the
+     top-k' of a top-k set, under one tie rule) and for 8-bit values ranks the
+     stored codes.  Raising it keeps their pairs (they were pruned with the k of
+     their step, as Algorithm 1 does) and fills the new slots with value 0 at
+     the lowest dims not kept, after the kept pairs.  Tokens that leave the
+     buffer afterwards are pruned with the new k.
 
 Parity status: every function above is pinned by tests/test_oracle_pins.py;
 nothing here is "parity unpinned" except the end-task accuracy of Tables 1-3,
@@ -134,6 +146,50 @@ def topk_indices_rows(Y: np.ndarray, k: int) -> np.ndarray:
     mag = np.abs(np.asarray(Y, dtype=F64))
     order = np.argsort(-mag, axis=1, kind="stable")[:, :k]
     return np.sort(order, axis=1)
+
+
+def change_k_rows(idx: np.ndarray, val: np.ndarray, k_new: int, d: int,
+                  code: Optional[np.ndarray] = None):
+    """Stored pairs [n][k_old] of n tokens, laid out again for k_new (reading 11).
+
+    k_new <= k_old: each token keeps its k_new largest stored magnitudes, lower
+    index first on ties, in ascending index order.  k_new > k_old: each token
+    keeps its pairs and gains k_new - k_old entries of value 0 at its lowest
+    dims not kept, placed after them in ascending order.  ``code`` (8-bit
+    values) follows ``val``.  Returns (idx, val, code).
+    """
+    idx = np.asarray(idx, dtype=np.int64)
+    val = np.asarray(val)
+    n, k_old = idx.shape
+    if k_new <= k_old:
+        mag = np.abs(val.astype(F64))
+        keep = np.zeros((n, k_new), dtype=np.int64)
+        for t in range(n):  # rank by (-|value|, index), keep the first k_new
+            order = np.lexsort((idx[t], -mag[t]))[:k_new]
+            keep[t] = order[np.argsort(idx[t][order])]
+        pick = lambda a: None if a is None else np.take_along_axis(np.asarray(a), keep, 1)
+        return pick(idx), pick(val), pick(code)
+    extra = k_new - k_old
+    fill = np.zeros((n, extra), dtype=np.int64)
+    for t in range(n):
+        fill[t] = np.setdiff1d(np.arange(d), idx[t])[:extra]
+    zeros = np.zeros((n, extra), dtype=val.dtype)
+    out_code = None if code is None else np.concatenate(
+        [np.asarray(code), np.zeros((n, extra), dtype=np.asarray(code).dtype)], 1)
+    return np.concatenate([idx, fill], 1), np.concatenate([val, zeros], 1), out_code
+
+
+def change_k_cache(cache: Dict[str, np.ndarray], k_new: int, k_value_new: Optional[int] = None,
+                   d: int = 128) -> Dict[str, np.ndarray]:
+    """``change_k_rows`` applied to both roles of a cache dict (``compress_block``'s)."""
+    out = dict(cache)
+    for r, k in (("k", k_new), ("v", k_new if k_value_new is None else k_value_new)):
+        i, v, c = change_k_rows(cache[f"{r}_idx"], cache[f"{r}_val"], k, d,
+                                cache.get(f"{r}_code"))
+        out[f"{r}_idx"], out[f"{r}_val"] = i, v
+        if c is not None:
+            out[f"{r}_code"] = c
+    return out
 
 
 # --------------------------------------------------------------------------- #
@@ -224,6 +280,18 @@ class UnitCache:
             i_v = topk_indices(v_old, self.kv)
             self.v_idx.append(i_v)
             self.v_val.append(self._sparse_value(v_old[i_v]))
+
+    def change_k(self, k_new: int, k_value_new: Optional[int] = None) -> None:
+        """Reading 11: the stored tokens laid out again for the new k, which the
+        tokens leaving the buffer from now on are pruned with."""
+        d = self.P_qk.shape[0]
+        kv_new = k_new if k_value_new is None else k_value_new
+        for idx_l, val_l, k in ((self.k_idx, self.k_val, k_new), (self.v_idx, self.v_val, kv_new)):
+            if idx_l:
+                i, v, _ = change_k_rows(np.stack(idx_l), np.stack(val_l), k, d)
+                idx_l[:] = list(i)
+                val_l[:] = list(v)
+        self.k, self.kv = int(k_new), int(kv_new)
 
     def _sparse_value(self, kept: np.ndarray) -> np.ndarray:
         if self.values == "e4m3":

@@ -331,6 +331,120 @@ def test_table2_ratios_map_to_components():
         assert kk + kv == 128 and 1 <= kk <= 127
 
 
+# --------------------------------------------------------------------------- #
+# Reading 11: k changed for a running sequence
+# --------------------------------------------------------------------------- #
+def _brute_swan_k_schedule(q, K, V, Pqk, Pvo, b, changes, dtype):
+    """Python loops: token t leaves the buffer at step t + b (when token t + b is
+    appended) and is pruned with the k then in force; each later change to a smaller
+    k re-prunes it, which the nested top-k makes equal to pruning its rotated vector
+    at the smallest k in force from its eviction on.  changes: {step: (k, k_value)},
+    in force from that step's append on (step 0 gives the initial k)."""
+    d, L = len(q), len(K)
+    def rot(x, P):
+        return [sum(float(x[i]) * float(P[i][j]) for i in range(d)) for j in range(d)]
+    def rnd(v):
+        return [float(np.asarray(x).astype(dtype)) for x in v]
+    def k_at(step):
+        return changes[max(s for s in changes if s <= step)]
+    eff = {}
+    for t in range(L - b):
+        ev = t + b  # the step whose append evicts token t
+        ks = [k_at(ev)] + [changes[s] for s in changes if ev < s <= L - 1]
+        eff[t] = (min(k for k, _ in ks), min(kv for _, kv in ks))
+    qh = rot(q, Pqk)
+    scores, vrows = [], []
+    for t in range(L):
+        kh, vh = rnd(rot(K[t], Pqk)), rnd(rot(V[t], Pvo))
+        if t in eff:
+            for vec, kk in ((kh, eff[t][0]), (vh, eff[t][1])):
+                keep = sorted(range(d), key=lambda j: (-abs(vec[j]), j))[:kk]
+                for j in range(d):
+                    if j not in keep:
+                        vec[j] = 0.0
+        scores.append(sum(qh[j] * kh[j] for j in range(d)) / math.sqrt(d))
+        vrows.append(vh)
+    m = max(scores)
+    w = [math.exp(s - m) for s in scores]
+    z = sum(w)
+    oh = [sum(w[t] / z * vrows[t][j] for t in range(L)) for j in range(d)]
+    return [sum(oh[j] * float(Pvo[i][j]) for j in range(d)) for i in range(d)]
+
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float16])
+def test_change_k_mid_sequence_brute_force(dtype):
+    d, L = 8, 12
+    q, K, V = si.tiny_case(61, d, L)
+    Pqk = si.random_orthogonal(62, d)
+    Pvo = si.random_orthogonal(63, d)
+    schedules = [{0: (5, 5), 4: (2, 3)}, {0: (2, 3), 6: (7, 8)}, {0: (6, 2), 3: (3, 6), 8: (8, 1)},
+                 {0: (4, 4), 11: (1, 1)}, {0: (8, 8), 1: (1, 8), 5: (8, 1)}]
+    for changes in schedules:
+        for b in (0, 2, 5):
+            uc = O.UnitCache(Pqk, Pvo, b, changes[0][0], dtype, k_value=changes[0][1])
+            for t in range(L):
+                if t in changes and t > 0:
+                    uc.change_k(*changes[t])
+                uc.append(K[0, t], V[0, t])
+            got = uc.attend(q[0])
+            want = _brute_swan_k_schedule(q[0], K[0], V[0], Pqk, Pvo, b, changes, dtype)
+            assert np.allclose(got, want, rtol=1e-12, atol=1e-12), (changes, b)
+            arr = uc.sparse_arrays()
+            assert arr["k_idx"].shape[1] == uc.k and arr["v_idx"].shape[1] == uc.kv
+
+
+@pytest.mark.parametrize("k,kv,k2,kv2", [(48, 48, 32, 32), (77, 51, 40, 51), (128, 64, 1, 13)])
+def test_lowering_k_equals_pruning_at_the_lower_k(k, kv, k2, kv2):
+    """Nested top-k: re-pruning the stored top-k to k' is the top-k' of the vector."""
+    d, L, b = 128, 90, 8
+    _, K, V = si.tiny_case(70 + k2, d, L)
+    Pqk = si.random_orthogonal(71, d)
+    Pvo = si.random_orthogonal(72, d)
+    K16, V16 = K[0].astype(np.float16), V[0].astype(np.float16)
+    c = O.compress_block(K16, V16, Pqk, Pvo, b, k, np.float16, k_value=kv)
+    got = O.change_k_cache(c, k2, kv2)
+    want = O.compress_block(K16, V16, Pqk, Pvo, b, k2, np.float16, k_value=kv2)
+    for key in ("k_idx", "k_val", "v_idx", "v_val", "k_buf", "v_buf"):
+        assert np.array_equal(got[key], want[key]), key
+
+
+def test_raising_k_keeps_pairs_and_attention():
+    d, L, b = 128, 70, 4
+    q, K, V = si.tiny_case(80, d, L)
+    Pqk = si.random_orthogonal(81, d)
+    Pvo = si.random_orthogonal(82, d)
+    c = O.compress_block(K[0], V[0], Pqk, Pvo, b, 24, np.float16, k_value=40)
+    up = O.change_k_cache(c, 40, 48)
+    for r, k0, k1 in (("k", 24, 40), ("v", 40, 48)):
+        assert np.array_equal(up[f"{r}_idx"][:, :k0], c[f"{r}_idx"])
+        assert np.array_equal(up[f"{r}_val"][:, :k0], c[f"{r}_val"])
+        assert np.all(up[f"{r}_val"][:, k0:] == 0)
+        for t in range(up[f"{r}_idx"].shape[0]):  # the fillers: lowest dims not kept
+            free = np.setdiff1d(np.arange(d), c[f"{r}_idx"][t])[: k1 - k0]
+            assert np.array_equal(up[f"{r}_idx"][t, k0:], free)
+    a0 = O.attend_arrays(q[0], Pqk, Pvo, c)
+    a1 = O.attend_arrays(q[0], Pqk, Pvo, up)
+    assert np.allclose(a0, a1, rtol=0, atol=1e-15 * np.abs(a0).max())
+
+
+def test_lowering_k_of_e4m3_values_on_exact_values():
+    """8-bit values rank the stored codes; where every value is exact in E4M3 this is
+    the same selection as pruning the fp16 values at the lower k."""
+    rng = np.random.default_rng(90)
+    mags = O.e4m3_magnitudes()
+    mags = mags[(mags > 0) & (mags <= 448)]
+    X = (rng.choice(mags, size=(60, 128)) * rng.choice([-1.0, 1.0], size=(60, 128)))
+    X = X.astype(np.float16)
+    eye = np.eye(128)
+    c = O.compress_block(X, X[::-1].copy(), eye, eye, 0, 64, np.float16, values="e4m3",
+                         k_value=48)
+    got = O.change_k_cache(c, 20, 33)
+    want = O.compress_block(X, X[::-1].copy(), eye, eye, 0, 20, np.float16, values="e4m3",
+                            k_value=33)
+    for key in ("k_idx", "k_code", "v_idx", "v_code"):
+        assert np.array_equal(got[key], want[key]), key
+
+
 def test_column_sign_flip_changes_nothing_but_signs():
     d, L, b, k = 128, 90, 8, 40
     q, K, V = si.tiny_case(15, d, L)
