@@ -43,6 +43,8 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-units", type=int, default=3,
                     help="(sequence, head) units in the oracle's timed sample")
+    ap.add_argument("--change-k", type=int, default=0,
+                    help="also time swan_change_k of the cache from the workload's k to this k")
     ap.add_argument("--probe-copy", type=int, default=0,
                     help="also run a device copy of this many bytes (HBM counter calibration)")
     return ap.parse_args()
@@ -116,6 +118,36 @@ def attn_kernel_name(w, k_key, k_val) -> str:
 
 def launches_per_step(k_key, k_val) -> int:
     return len({(kpad(a), kpad(b)) for a, b in zip(k_key, k_val)})
+
+
+def time_change_k(swan, torch, w, cache, ks, kvs, k_new, esize, reps=5):
+    """swan_change_k of the whole cache from the workload's k to k_new (both roles),
+    timed with HIP events on the stream it runs on; bytes = the pages read (old k_pad)
+    plus the pages written (new k_pad)."""
+    kd = [k_new] * w.batch
+    dst = swan.CacheDesc(*[getattr(cache.desc, f) for f, _ in swan.CacheDesc._fields_])
+    kb, vb, _ = swan.cache_bytes(dst, kd, None)
+    kp = torch.empty(kb, dtype=torch.uint8, device=cache.device)
+    vp = torch.empty(vb, dtype=torch.uint8, device=cache.device)
+    dst.k_pages, dst.v_pages = kp.data_ptr(), vp.data_ptr()
+    swan.change_k(cache.desc, ks, kvs, dst, kd, None, cache.seq_len)  # warm-up
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        swan.change_k(cache.desc, ks, kvs, dst, kd, None, cache.seq_len)
+    e1.record()
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) * 1e-3 / reps
+    vbytes = value_bytes(w, esize) + 1
+    kvl = ks if kvs is None else kvs
+    nbytes = 0
+    for b in range(w.batch):
+        S = max(cache.seq_len[b] - w.buffer, 0)
+        n = w.n_kv_heads * S * vbytes
+        nbytes += n * (kpad(ks[b]) + kpad(kvl[b]) + 2 * kpad(k_new))
+    return {"from": [ks[0], kvl[0]], "to": k_new, "ms": t * 1e3, "bytes": nbytes,
+            "gbps": nbytes / t / 1e9, "frac": nbytes / t / 1e9 / HBM_PEAK_GBPS,
+            "kernel": "change_k_kernel (one launch per role)"}
 
 
 def cpu_model() -> str:
@@ -327,6 +359,12 @@ def main():
         log(f"[bench] probe copy of {args.probe_copy} bytes: {tc * 1e3:.3f} ms, "
             f"{2 * args.probe_copy / tc / 1e9:.0f} GB/s read+write")
 
+    change_k = None
+    if args.change_k:
+        change_k = time_change_k(swan, torch, w, cache, ks, kvs, args.change_k, esize)
+        log(f"[bench] change_k {change_k['from']} -> {change_k['to']}: {change_k['ms']:.3f} ms, "
+            f"{change_k['gbps']:.0f} GB/s read+write ({change_k['frac'] * 100:.1f}% of 8 TB/s)")
+
     cpu = None
     if not args.no_cpu_baseline:
         t = time.perf_counter()
@@ -378,6 +416,7 @@ def main():
             "prefill_compress_ms": t_prefill * 1e3,
             "prefill_compress_gbps": prefill_bytes / t_prefill / 1e9,
             "kv_tokens_per_s": float(np.mean([sum(L) for L in lens])) / dec_avg,
+            "change_k": change_k,
         },
     }
     print(json.dumps(result), flush=True)

@@ -210,6 +210,37 @@ swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_ho
                                   size_t workspace_bytes, void* stream);
 
 /*
+ * Run-time change of k for running sequences (Algorithm 1 takes k_active as an
+ * input at every step; Sec. 1 and Sec. 3 present k as tunable at inference
+ * time).  Lays the sparse caches of `src` (laid out with k_active_src /
+ * k_value_src) out again in `dst` (laid out with k_active_dst / k_value_dst),
+ * per sequence and role:
+ *  - k' < k: each stored token keeps the k' largest of its k stored values,
+ *    ties to the lower index.  For SWAN_F16 / SWAN_F32 values this is exactly
+ *    the token's top-k' (the top-k' of a top-k set, under one tie rule), so the
+ *    result equals pruning at k' from the start; for SWAN_F16_E4M3 it ranks the
+ *    stored 8-bit values.
+ *  - k' > k: each stored token keeps its k pairs (it was pruned with the k of
+ *    its step) and slots k..k'-1 take value +0 at its lowest dims not kept.
+ *  - k' == k: the pairs are copied.
+ * Slots past k' are padding as always.  Tokens still in the dense buffer are not
+ * touched: they are pruned with the new k when they leave it, so later calls on
+ * the sequence pass k_active_dst / k_value_dst.
+ *  seq_len_host[batch]  tokens cached per sequence (0 allowed);
+ *  src, dst             descriptors with the same batch, heads, buffer_tokens and
+ *                       dtype; dst's sparse_capacity may differ but must hold every
+ *                       sequence's sparse tokens; dst must use src's ring arrays
+ *                       (k_ring, v_ring) and page arrays that do not overlap src's,
+ *                       sized with swan_cache_bytes for the new k.
+ * Errors: SWAN_ERR_INVALID_ARG (mismatched descriptors, overlap, other rings,
+ * k outside 1..head_dim), SWAN_ERR_CAPACITY.
+ */
+swan_status swan_change_k(const swan_cache* src, const int32_t* k_active_src,
+                          const int32_t* k_value_src, const swan_cache* dst,
+                          const int32_t* k_active_dst, const int32_t* k_value_dst,
+                          const int32_t* seq_len_host, void* stream);
+
+/*
  * Profiling hook.  While both are non-NULL, swan_decode_attention on this
  * thread records start_event (a hipEvent_t) on its stream right before its
  * sparse/buffer attention launches and stop_event right after them, so that

@@ -391,6 +391,73 @@ swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_ho
   return hip_status(swan::launch_decode(a), "decode launch");
 }
 
+swan_status swan_change_k(const swan_cache* src, const int32_t* k_active_src,
+                          const int32_t* k_value_src, const swan_cache* dst,
+                          const int32_t* k_active_dst, const int32_t* k_value_dst,
+                          const int32_t* seq_len_host, void* stream) {
+  swan_status st = check_cache_shape(src);
+  if (st != SWAN_OK) return st;
+  if ((st = check_cache_shape(dst)) != SWAN_OK) return st;
+  if (src->batch != dst->batch || src->n_q_heads != dst->n_q_heads ||
+      src->n_kv_heads != dst->n_kv_heads || src->buffer_tokens != dst->buffer_tokens ||
+      src->dtype != dst->dtype)
+    return fail(SWAN_ERR_INVALID_ARG,
+                "src and dst differ in batch, heads, buffer_tokens or dtype");
+  if ((st = check_k(src, k_active_src, k_value_src)) != SWAN_OK) return st;
+  if ((st = check_k(dst, k_active_dst, k_value_dst)) != SWAN_OK) return st;
+  if ((st = check_cache_ptrs(src)) != SWAN_OK) return st;
+  if ((st = check_cache_ptrs(dst)) != SWAN_OK) return st;
+  if (src->k_ring != dst->k_ring || src->v_ring != dst->v_ring)
+    return fail(SWAN_ERR_INVALID_ARG, "dst must share src's ring arrays (the buffer is unchanged)");
+  if (!seq_len_host) return fail(SWAN_ERR_INVALID_ARG, "seq_len_host is NULL");
+  int max_pages = 0;
+  for (int b = 0; b < src->batch; ++b) {
+    const int64_t L = seq_len_host[b];
+    if (L < 0) return fail(SWAN_ERR_INVALID_ARG, "seq_len[%d] = %lld < 0", b, (long long)L);
+    const int64_t S = L > src->buffer_tokens ? L - src->buffer_tokens : 0;
+    if (S > src->sparse_capacity || S > dst->sparse_capacity)
+      return fail(SWAN_ERR_CAPACITY, "sequence %d has %lld sparse tokens, capacities %d / %d", b,
+                  (long long)S, src->sparse_capacity, dst->sparse_capacity);
+    const int np = swan::pages_for((int)S);
+    if (np > max_pages) max_pages = np;
+  }
+  swan::SeqTab ts, td;
+  int64_t bytes_src[2], bytes_dst[2];
+  fill_layout(src, k_active_src, k_value_src, ts, bytes_src);
+  fill_layout(dst, k_active_dst, k_value_dst, td, bytes_dst);
+  // no destination page array may overlap a source one
+  const char* sa[2] = {(const char*)src->k_pages, (const char*)src->v_pages};
+  const char* da[2] = {(const char*)dst->k_pages, (const char*)dst->v_pages};
+  for (int i = 0; i < 2; ++i)
+    for (int j = 0; j < 2; ++j)
+      if (bytes_src[i] > 0 && bytes_dst[j] > 0 && da[j] < sa[i] + bytes_src[i] &&
+          sa[i] < da[j] + bytes_dst[j])
+        return fail(SWAN_ERR_INVALID_ARG, "dst page arrays overlap src page arrays");
+  for (int r = 0; r < 2; ++r) {
+    swan::ChangeKLaunch a;
+    a.src = sa[r];
+    a.dst = (char*)da[r];
+    a.B = src->batch;
+    a.Hkv = src->n_kv_heads;
+    a.bb = src->buffer_tokens;
+    a.npc_src = swan::pages_for(src->sparse_capacity);
+    a.npc_dst = swan::pages_for(dst->sparse_capacity);
+    a.max_pages = max_pages;
+    a.dtype = src->dtype;
+    for (int b = 0; b < SWAN_MAX_BATCH; ++b) {
+      a.len[b] = b < src->batch ? seq_len_host[b] : 0;
+      a.k_src[b] = ts.kact[r][b];
+      a.k_dst[b] = td.kact[r][b];
+      a.off_src[b] = ts.page_off[r][b];
+      a.off_dst[b] = td.page_off[r][b];
+    }
+    a.stream = (hipStream_t)stream;
+    const hipError_t e = swan::launch_change_k(a);
+    if (e != hipSuccess) return hip_status(e, "change_k launch");
+  }
+  return ok();
+}
+
 swan_status swan_set_profile_events(void* start_event, void* stop_event) {
   if ((start_event == nullptr) != (stop_event == nullptr))
     return fail(SWAN_ERR_INVALID_ARG, "pass both events or neither");

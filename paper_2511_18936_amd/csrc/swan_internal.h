@@ -111,6 +111,21 @@ constexpr int kPrefillMinTokens = 64;
 int prefill_groups(int max_new_tokens, int min_len_old);
 hipError_t launch_prefill(const CompressLaunch& a);
 
+// run-time change of k: one launch per role, over the role's page arrays
+// (change_k.hip)
+struct ChangeKLaunch {
+  const char* src;  // the role's pages in the source cache
+  char* dst;        // the role's pages in the destination cache
+  int B, Hkv, bb, npc_src, npc_dst, max_pages, dtype;
+  int32_t len[SWAN_MAX_BATCH];      // tokens cached
+  int32_t k_src[SWAN_MAX_BATCH];    // the role's k in the source layout
+  int32_t k_dst[SWAN_MAX_BATCH];    // the role's k in the destination layout
+  int64_t off_src[SWAN_MAX_BATCH];  // byte offset of the sequence's first source page
+  int64_t off_dst[SWAN_MAX_BATCH];  // byte offset of the sequence's first destination page
+  hipStream_t stream;
+};
+hipError_t launch_change_k(const ChangeKLaunch& a);
+
 struct CalibLaunch {
   const float* rows;
   int64_t n_rows;

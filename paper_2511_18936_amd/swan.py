@@ -32,7 +32,8 @@ PAGE_TOKENS = 64
 EXPORTED = (
     "swan_last_error", "swan_version", "swan_page_bytes", "swan_cache_bytes",
     "swan_calibrate_workspace_bytes", "swan_calibrate_rotation", "swan_compress_append",
-    "swan_decode_workspace_bytes", "swan_decode_attention", "swan_set_profile_events",
+    "swan_decode_workspace_bytes", "swan_decode_attention", "swan_change_k",
+    "swan_set_profile_events",
 )
 
 
@@ -84,6 +85,7 @@ def _load() -> ctypes.CDLL:
         "swan_decode_workspace_bytes": [pdesc, pi32, pi32, pi32, psz],
         "swan_decode_attention": [pdesc, pi32, pi32, pi32, vp, vp, vp, ctypes.c_float, vp, vp, sz,
                                   vp],
+        "swan_change_k": [pdesc, pi32, pi32, pdesc, pi32, pi32, pi32, vp],
         "swan_set_profile_events": [vp, vp],
     }
     for name, args in sigs.items():
@@ -209,6 +211,16 @@ def decode_attention(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence
                                       _ptr(workspace), workspace.numel(), _stream(stream)))
 
 
+def change_k(src: CacheDesc, k_active_src: Sequence[int], k_value_src: Optional[Sequence[int]],
+             dst: CacheDesc, k_active_dst: Sequence[int], k_value_dst: Optional[Sequence[int]],
+             seq_len: Sequence[int], stream=None) -> None:
+    """Lay src's sparse caches out again in dst for the new k (see swan_change_k)."""
+    _check(_lib.swan_change_k(ctypes.byref(src), _i32_array(k_active_src),
+                              _opt_i32_array(k_value_src), ctypes.byref(dst),
+                              _i32_array(k_active_dst), _opt_i32_array(k_value_dst),
+                              _i32_array(seq_len), _stream(stream)))
+
+
 def set_profile_events(start=None, stop=None) -> None:
     """Record torch.cuda.Event start/stop around the attention kernels of the next
     decode calls on this thread (None, None disables)."""
@@ -272,6 +284,29 @@ class SwanCache:
         n = int(k_new.shape[2])
         per = [n] * self.batch if n_new_per_seq is None else [int(x) for x in n_new_per_seq]
         self.seq_len = [L + m for L, m in zip(self.seq_len, per)]
+
+    def change_k(self, k_active: Sequence[int], k_value: Optional[Sequence[int]] = None,
+                 stream=None) -> None:
+        """Change k of the running sequences (swan_change_k): new page arrays for the new
+        k, the stored tokens converted into them, the dense buffer kept.  Tokens that
+        leave the buffer from now on are pruned with the new k."""
+        import torch
+
+        k_active = [int(k) for k in k_active]
+        k_value = None if k_value is None else [int(k) for k in k_value]
+        dst = CacheDesc(*[getattr(self.desc, f) for f, _ in CacheDesc._fields_])
+        kb, vb, _ = cache_bytes(dst, k_active, k_value)
+        k_pages = torch.zeros(max(kb, 16), dtype=torch.uint8, device=self.device)
+        v_pages = torch.zeros(max(vb, 16), dtype=torch.uint8, device=self.device)
+        dst.k_pages = k_pages.data_ptr()
+        dst.v_pages = v_pages.data_ptr()
+        change_k(self.desc, self.k_active, self.k_value, dst, k_active, k_value, self.seq_len,
+                 stream)
+        # the old pages stay alive until the conversion on the stream has read them
+        (stream or torch.cuda.current_stream()).synchronize()
+        self.desc, self.k_pages, self.v_pages = dst, k_pages, v_pages
+        self.k_active, self.k_value = k_active, k_value
+        self._ws = None
 
     def workspace(self):
         import torch

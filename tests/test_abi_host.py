@@ -22,7 +22,7 @@ def _declared_functions():
 
 def test_header_and_binding_agree_on_exports():
     declared = _declared_functions()
-    assert len(declared) == 10
+    assert len(declared) == 11
     assert sorted(swan.EXPORTED) == declared
     lib = swan.lib()
     for name in declared:
@@ -185,3 +185,28 @@ def test_asymmetric_k_workspace():
     assert swan.decode_workspace_bytes(d, L, [48, 48], [41, 47]) == base  # same k_pad
     assert swan.decode_workspace_bytes(d, L, [48, 48], [32, 48]) == \
         swan.decode_workspace_bytes(d, L, [40, 48])
+
+
+def test_change_k_rejects_bad_arguments():
+    lib = swan.lib()
+    d = _desc()
+    seq = swan._i32_array([100, 200])
+    ks = swan._i32_array([48, 64])
+    E = swan.SWAN_ERR_INVALID_ARG
+    B2 = 0x20000000  # another page region, far from FAKE
+    dst = _desc(k_pages=B2, v_pages=B2 + (1 << 24))
+    call = lambda src_, dst_, kd=ks, seq_=seq: lib.swan_change_k(
+        ctypes.byref(src_), ks, None, ctypes.byref(dst_), kd, None, seq_, None)
+    assert call(d, _desc(batch=1, k_pages=B2, v_pages=B2 + (1 << 24))) == E  # other batch
+    assert call(d, _desc(buffer_tokens=8, k_pages=B2, v_pages=B2 + (1 << 24))) == E
+    assert call(d, _desc(dtype=swan.SWAN_F32, k_pages=B2, v_pages=B2 + (1 << 24))) == E
+    assert call(d, _desc(k_ring=FAKE + 256, k_pages=B2, v_pages=B2 + (1 << 24))) == E  # ring
+    assert call(d, d) == E  # dst pages overlap src pages
+    assert call(d, dst, kd=swan._i32_array([0, 48])) == E
+    assert call(d, dst, kd=swan._i32_array([48, 129])) == E
+    assert call(d, dst, seq_=swan._i32_array([-1, 5])) == E
+    assert lib.swan_change_k(ctypes.byref(d), ks, None, ctypes.byref(dst), ks, None, None,
+                             None) == E
+    # the sparse tokens must fit the destination's capacity
+    assert call(d, _desc(sparse_capacity=50, k_pages=B2, v_pages=B2 + (1 << 24))) == \
+        swan.SWAN_ERR_CAPACITY
