@@ -33,6 +33,10 @@ paper states the method (SWAN: Sparse Winnowed Attention, arXiv 2511.18936):
 * ``change_k_rows`` / ``UnitCache.change_k``  k changed for a running sequence
                            (reading 11: k_active is a run-time input of
                            Algorithm 1, Sec. 1 / Sec. 3).
+* ``rope`` / ``absorbed_weights`` / ``layer_decode``  a Llama-shaped attention
+                           layer around the cache: RoPE before the rotation
+                           (Sec. 4.2), W_V and W_O absorbing P_VO (Sec. 4.2,
+                           Lemma 2), readings 12-13.
 
 Readings of the paper used here (where it is silent or ambiguous):
   1. top-k ranks the stored (T-rounded) buffer value, because Algorithm 1 pops
@@ -61,7 +65,16 @@ Readings of the paper used here (where it is silent or ambiguous):
      stored codes.  Raising it keeps their pairs (they were pruned with the k of
      their step, as Algorithm 1 does) and fills the new slots with value 0 at
      the lowest dims not kept, after the kept pairs.  Tokens that leave the
-     buffer afterwards are pruned with the new k.
+     buffer afterwards are pruned with the new k;
+ 12. RoPE (the rotary embedding of the Llama models the paper evaluates): dims
+     j and j + d/2 of a head rotate by pos * base^(-2j/d), computed in float64
+     and rounded once to T; the SWAN rotation takes the rounded post-RoPE rows,
+     as it would take a model's post-RoPE tensors;
+ 13. the absorbed layer: q, k and v_hat = x . W_V_hat are the model's tensors,
+     each rounded once to T from a float64 product; W_V_hat = W_V . P_VO and
+     W_O_hat = P_VO^T . W_O per head are formed in float64; the values enter
+     the cache without a further rotation and the attention output leaves it
+     rotated, straight into W_O_hat.
 
 Parity status: every function above is pinned by tests/test_oracle_pins.py;
 nothing here is "parity unpinned" except the end-task accuracy of Tables 1-3,
@@ -401,6 +414,79 @@ def decode_batch(q: np.ndarray, P_qk: np.ndarray, P_vo: np.ndarray,
             g = hq // G
             out[b, hq] = attend_arrays(q[b, hq], P_qk[g], P_vo[g], caches[b][g], scale)
     return out
+
+
+# --------------------------------------------------------------------------- #
+# A Llama-shaped attention layer around the cache (readings 12-13)
+# --------------------------------------------------------------------------- #
+def rope(x: np.ndarray, pos: np.ndarray, base: float, dtype=None) -> np.ndarray:
+    """Rotary embedding of rows x [..., n, d] at positions pos [n] (reading 12).
+
+    Dims j and j + d/2 rotate by the angle pos * base^(-2j/d); float64, then
+    rounded once to ``dtype`` if given.
+    """
+    x = np.asarray(x, dtype=F64)
+    d = x.shape[-1]
+    h = d // 2
+    inv = base ** (-(2.0 * np.arange(h)) / d)
+    ang = np.asarray(pos, dtype=F64)[:, None] * inv[None, :]
+    c, s = np.cos(ang), np.sin(ang)
+    a, b = x[..., :h], x[..., h:]
+    y = np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+    return y if dtype is None else y.astype(dtype)
+
+
+def absorbed_weights(W_v: np.ndarray, W_o: np.ndarray, P_vo: np.ndarray, n_heads: int,
+                     n_kv_heads: int):
+    """W_V_hat = W_V . P_VO per KV head and W_O_hat = P_VO^T . W_O per query head
+    (Sec. 4.2), float64.  W_v [hidden][n_kv * d], W_o [n_q * d][hidden], P_vo [n_kv][d][d]."""
+    d = P_vo.shape[-1]
+    G = n_heads // n_kv_heads
+    Wv = np.asarray(W_v, dtype=F64).copy()
+    Wo = np.asarray(W_o, dtype=F64).copy()
+    for h in range(n_kv_heads):
+        Wv[:, h * d:(h + 1) * d] = Wv[:, h * d:(h + 1) * d] @ P_vo[h]
+    for hq in range(n_heads):
+        Wo[hq * d:(hq + 1) * d, :] = np.asarray(P_vo[hq // G], dtype=F64).T @ Wo[hq * d:(hq + 1) * d, :]
+    return Wv, Wo
+
+
+def layer_tensors(x: np.ndarray, W_q, W_k, W_v_hat, n_heads: int, n_kv_heads: int,
+                  pos: np.ndarray, base: float, dtype):
+    """The layer's post-RoPE q, k and absorbed v_hat for rows x [n][hidden] at
+    positions pos: each product rounded once to T, RoPE rounded once (13)."""
+    d = 128
+    n = x.shape[0]
+    x = np.asarray(x, dtype=F64)
+    q = to_storage(x @ np.asarray(W_q, dtype=F64), dtype).reshape(n, n_heads, d)
+    k = to_storage(x @ np.asarray(W_k, dtype=F64), dtype).reshape(n, n_kv_heads, d)
+    v = to_storage(x @ np.asarray(W_v_hat, dtype=F64), dtype).reshape(n, n_kv_heads, d)
+    q = rope(q.transpose(1, 0, 2), pos, base, dtype).transpose(1, 0, 2)
+    k = rope(k.transpose(1, 0, 2), pos, base, dtype).transpose(1, 0, 2)
+    return q, k, v
+
+
+def layer_decode(x_seq: np.ndarray, W_q, W_k, W_v, W_o, P_qk, P_vo, n_heads: int,
+                 n_kv_heads: int, base: float, buffer_tokens: int, k_active: int,
+                 dtype=np.float16, k_value: Optional[int] = None) -> np.ndarray:
+    """Output of the attention layer for the last of the rows x_seq [L][hidden]
+    (positions 0..L-1), every row having been appended to the SWAN cache first
+    (Algorithm 1 inside the layer, readings 12-13).  Returns y [hidden] float64."""
+    L = x_seq.shape[0]
+    d = 128
+    G = n_heads // n_kv_heads
+    W_v_hat, W_o_hat = absorbed_weights(W_v, W_o, P_vo, n_heads, n_kv_heads)
+    q, k, v = layer_tensors(x_seq, W_q, W_k, W_v_hat, n_heads, n_kv_heads, np.arange(L), base,
+                            dtype)
+    eye = np.eye(d)
+    o = np.zeros(n_heads * d, dtype=F64)
+    for h in range(n_kv_heads):
+        # values arrive rotated: the cache's value rotation is the identity
+        c = compress_block(k[:, h], v[:, h], P_qk[h], eye, buffer_tokens, k_active, dtype,
+                           k_value=k_value)
+        for hq in range(h * G, (h + 1) * G):
+            o[hq * d:(hq + 1) * d] = attend_arrays(q[L - 1, hq], P_qk[h], eye, c)
+    return o @ W_o_hat
 
 
 # --------------------------------------------------------------------------- #

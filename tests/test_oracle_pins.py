@@ -445,6 +445,100 @@ def test_lowering_k_of_e4m3_values_on_exact_values():
         assert np.array_equal(got[key], want[key]), key
 
 
+# --------------------------------------------------------------------------- #
+# Readings 12-13: RoPE and the absorbed layer
+# --------------------------------------------------------------------------- #
+def test_rope_against_complex_rotation_and_closed_forms():
+    rng = np.random.default_rng(101)
+    x = rng.standard_normal((4, 9, 128))
+    pos = np.array([0, 1, 2, 7, 100, 4095, 32767, 131071, 5])
+    for base in (10000.0, 500000.0):
+        y = O.rope(x, pos, base)
+        # an independent form: dims (j, j + 64) as the complex number x_j + i x_{j+64},
+        # multiplied by exp(i pos theta_j), theta_j = 1 / base^(j / 64)
+        theta = 1.0 / np.power(base, np.arange(64) / 64.0)
+        z = (x[..., :64] + 1j * x[..., 64:]) * np.exp(1j * pos[:, None] * theta[None, :])
+        # theta rounds differently in the two forms; at position 131071 that moves the
+        # angle by ~1e-11, so the bound is 1e-9 (far below an fp16 ulp)
+        assert np.allclose(y[..., :64], z.real, rtol=0, atol=1e-9)
+        assert np.allclose(y[..., 64:], z.imag, rtol=0, atol=1e-9)
+        assert np.allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(x, axis=-1))
+        assert np.array_equal(y[:, 0], x[:, 0])  # position 0
+    # relative positions: <rope(q, m), rope(k, n)> depends on m - n only
+    q, k = rng.standard_normal(128), rng.standard_normal(128)
+    for m, n in ((5, 2), (1000, 997), (70000, 69997)):
+        a = O.rope(q[None], np.array([m]), 10000.0)[0] @ O.rope(k[None], np.array([n]), 10000.0)[0]
+        b = O.rope(q[None], np.array([3]), 10000.0)[0] @ O.rope(k[None], np.array([0]), 10000.0)[0]
+        assert abs(a - b) < 1e-9 * max(1.0, abs(b))
+    # e_0 at position 1 with theta_0 = 1: (cos 1, sin 1) on dims 0 and 64
+    e0 = np.zeros((1, 128))
+    e0[0, 0] = 1.0
+    y = O.rope(e0, np.array([1]), 10000.0)[0]
+    assert y[0] == math.cos(1.0) and y[64] == math.sin(1.0) and np.count_nonzero(y) == 2
+
+
+def _textbook_layer(x_seq, W_q, W_k, W_v, W_o, n_heads, n_kv, base):
+    """Standard attention of a Llama layer for the last row (no SWAN, float64)."""
+    L, d, G = x_seq.shape[0], 128, n_heads // n_kv
+    q = (x_seq @ W_q).reshape(L, n_heads, d)
+    k = (x_seq @ W_k).reshape(L, n_kv, d)
+    v = (x_seq @ W_v).reshape(L, n_kv, d)
+    pos = np.arange(L)
+    q = O.rope(q.transpose(1, 0, 2), pos, base).transpose(1, 0, 2)
+    k = O.rope(k.transpose(1, 0, 2), pos, base).transpose(1, 0, 2)
+    o = np.zeros(n_heads * d)
+    for hq in range(n_heads):
+        o[hq * d:(hq + 1) * d] = _textbook_attention(q[L - 1, hq], k[:, hq // G], v[:, hq // G])
+    return o @ W_o
+
+
+def _layer_weights(seed, hidden, n_heads, n_kv):
+    r = np.random.default_rng(seed)
+    d = 128
+    W_q = r.standard_normal((hidden, n_heads * d)) / math.sqrt(hidden)
+    W_k = r.standard_normal((hidden, n_kv * d)) / math.sqrt(hidden)
+    W_v = r.standard_normal((hidden, n_kv * d)) / math.sqrt(hidden)
+    W_o = r.standard_normal((n_heads * d, hidden)) / math.sqrt(n_heads * d)
+    P_qk = np.stack([si.random_orthogonal(seed * 10 + h, d) for h in range(n_kv)])
+    P_vo = np.stack([si.random_orthogonal(seed * 10 + 5 + h, d) for h in range(n_kv)])
+    return W_q, W_k, W_v, W_o, P_qk, P_vo
+
+
+@pytest.mark.parametrize("n_heads,n_kv", [(4, 2), (2, 2)])
+def test_layer_with_full_retention_is_the_textbook_layer(n_heads, n_kv):
+    """k = d or b >= L, float64 storage: SWAN with W_V / W_O absorbed (Lemma 2) equals
+    the plain attention layer, RoPE and the GQA head mapping included."""
+    hidden, L = 96, 40
+    W_q, W_k, W_v, W_o, P_qk, P_vo = _layer_weights(3 + n_heads, hidden, n_heads, n_kv)
+    x = np.random.default_rng(4).standard_normal((L, hidden))
+    want = _textbook_layer(x, W_q, W_k, W_v, W_o, n_heads, n_kv, 10000.0)
+    for b, k in ((0, 128), (4, 128), (L, 7)):
+        got = O.layer_decode(x, W_q, W_k, W_v, W_o, P_qk, P_vo, n_heads, n_kv, 10000.0, b, k,
+                             np.float64)
+        assert np.allclose(got, want, rtol=0, atol=1e-11 * np.abs(want).max()), (b, k)
+
+
+def test_absorbed_layer_equals_explicit_rotation_with_pruning():
+    """Lemma 2 with pruning active: rotating v inside the cache and rotating the output
+    back (the library's explicit form) equals absorbing P_VO into W_V and W_O."""
+    hidden, L, n_heads, n_kv, b, k = 96, 60, 4, 2, 8, 40
+    W_q, W_k, W_v, W_o, P_qk, P_vo = _layer_weights(11, hidden, n_heads, n_kv)
+    x = np.random.default_rng(12).standard_normal((L, hidden))
+    got = O.layer_decode(x, W_q, W_k, W_v, W_o, P_qk, P_vo, n_heads, n_kv, 10000.0, b, k,
+                         np.float64)
+    # explicit: v = x W_v, the cache rotates it with P_VO and attend rotates back
+    q, kk, _ = O.layer_tensors(x, W_q, W_k, W_v, n_heads, n_kv, np.arange(L), 10000.0,
+                               np.float64)
+    v = (x @ W_v).reshape(L, n_kv, 128)
+    o = np.zeros(n_heads * 128)
+    for h in range(n_kv):
+        c = O.compress_block(kk[:, h], v[:, h], P_qk[h], P_vo[h], b, k, np.float64)
+        for hq in range(h * 2, (h + 1) * 2):
+            o[hq * 128:(hq + 1) * 128] = O.attend_arrays(q[L - 1, hq], P_qk[h], P_vo[h], c)
+    want = o @ W_o
+    assert np.allclose(got, want, rtol=0, atol=1e-11 * np.abs(want).max())
+
+
 def test_column_sign_flip_changes_nothing_but_signs():
     d, L, b, k = 128, 90, 8, 40
     q, K, V = si.tiny_case(15, d, L)
