@@ -170,6 +170,9 @@ swan_status swan_calibrate_rotation(const float* rows, int64_t n_rows, int32_t d
  *  n_new_host[batch]    tokens to append per sequence, 0..n_new (the first ones
  *                       of its rows); NULL means n_new for every sequence;
  *  P_qk, P_vo           [n_kv_heads][head_dim][head_dim] float32 rotations.
+ *                       P_vo may be NULL: the values are then already in the
+ *                       rotated basis (a model with P_VO absorbed into W_V,
+ *                       Sec. 4.2) and are stored as given.
  * Each new token is rotated (k_hat = k . P_qk, v_hat = v . P_vo, accumulated in
  * float64 and rounded once to the storage type) and appended to the buffer;
  * every token that leaves the buffer (position < L_new - b) is pruned to the
@@ -201,13 +204,30 @@ swan_status swan_decode_workspace_bytes(const swan_cache* c, const int32_t* seq_
  * Computes q_hat = q . P_qk[g] (g = h_q / G), scores q_hat . k over the sparse
  * pairs and the dense buffer, softmax, o_hat = sum_t p_t v_hat_t, and returns
  * out = o_hat . P_vo[g]^T (the inverse rotation of Sec. 4.2), rounded once to
- * the storage type.  Scores, probabilities and accumulators are float32.
+ * the storage type.  With P_vo NULL it returns o_hat itself, for a model that
+ * absorbs P_VO^T into W_O (Sec. 4.2).  Scores, probabilities and accumulators
+ * are float32.
  */
 swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_host,
                                   const int32_t* k_active_host, const int32_t* k_value_host,
                                   const void* q, const float* P_qk, const float* P_vo,
                                   float scale, void* out, void* workspace,
                                   size_t workspace_bytes, void* stream);
+
+/*
+ * Rotary position embedding, for the query and key rows of a layer before the
+ * cache rotates them (the paper rotates post-RoPE queries and keys, Sec. 4.2).
+ *  x, y          [batch][n_heads][n][head_dim] rows of the storage type of
+ *                `dtype` (binary16 for SWAN_F16 and SWAN_F16_E4M3), device; y may
+ *                be x (in place);
+ *  pos0_host[b]  position of sequence b's first row (row i sits at pos0 + i);
+ *  base          the RoPE base (10000 for Llama-2, 500000 for Llama-3), > 1.
+ * Dims j and j + head_dim/2 rotate by the angle pos * base^(-2j/head_dim), in
+ * float64, rounded once to the storage type.  Needs head_dim == 128.
+ */
+swan_status swan_rope(const void* x, void* y, int32_t dtype, int32_t batch, int32_t n_heads,
+                      int32_t n, int32_t head_dim, const int32_t* pos0_host, double base,
+                      void* stream);
 
 /*
  * Run-time change of k for running sequences (Algorithm 1 takes k_active as an

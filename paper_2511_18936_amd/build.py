@@ -14,7 +14,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libswan.so")
 SOURCES = ["swan_api.hip", "decode.hip", "decode_gqa.hip", "decode_asym.hip",
-           "decode_gqa_asym.hip", "compress.hip", "prefill.hip", "change_k.hip", "calibrate.hip"]
+           "decode_gqa_asym.hip", "compress.hip", "prefill.hip", "change_k.hip", "rope.hip",
+           "calibrate.hip"]
 ARCH = "gfx950"
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "-shared", f"--offload-arch={ARCH}",

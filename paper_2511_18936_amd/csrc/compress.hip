@@ -160,20 +160,29 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
     xs[2 * lane + 1][t] = v1;
   }
   __syncthreads();
-  const float2* P = (const float2*)((role ? a.P_vo : a.P_qk) + (int64_t)h * kD * kD) + lane;
   double acc0[TPW], acc1[TPW];
-#pragma unroll
-  for (int t = 0; t < TPW; ++t) acc0[t] = acc1[t] = 0.0;
-  // 32 rows of P in flight per batch: the loads are the latency of this kernel
-#pragma unroll 32
-  for (int i = 0; i < kD; ++i) {
-    const float2 pr = P[i * (kD / 2)];
-    const double p0 = (double)pr.x, p1 = (double)pr.y;
+  const float* Prole = role ? a.P_vo : a.P_qk;
+  if (!Prole) {  // values already in the rotated basis (P_VO absorbed into W_V)
 #pragma unroll
     for (int t = 0; t < TPW; ++t) {
-      const double xv = xs[i][t];
-      acc0[t] = fma(xv, p0, acc0[t]);
-      acc1[t] = fma(xv, p1, acc1[t]);
+      acc0[t] = xs[2 * lane][t];
+      acc1[t] = xs[2 * lane + 1][t];
+    }
+  } else {
+    const float2* P = (const float2*)(Prole + (int64_t)h * kD * kD) + lane;
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) acc0[t] = acc1[t] = 0.0;
+    // 32 rows of P in flight per batch: the loads are the latency of this kernel
+#pragma unroll 32
+    for (int i = 0; i < kD; ++i) {
+      const float2 pr = P[i * (kD / 2)];
+      const double p0 = (double)pr.x, p1 = (double)pr.y;
+#pragma unroll
+      for (int t = 0; t < TPW; ++t) {
+        const double xv = xs[i][t];
+        acc0[t] = fma(xv, p0, acc0[t]);
+        acc1[t] = fma(xv, p1, acc1[t]);
+      }
     }
   }
   const int len_old = a.tab.len[b];

@@ -83,6 +83,10 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeLaunch a) {
   float o = 0.f;
   for (int i = 0; i < np_all; ++i) o = fmaf(wts[i], part[slot(i) * kPartFloats + 4 + t], o);
   oh[t] = o * inv;
+  if (!a.P_vo) {  // the output stays in the rotated basis (P_VO absorbed into W_O)
+    ((T*)a.out)[(int64_t)bhq * kD + t] = (T)oh[t];
+    return;
+  }
   __syncthreads();
   const float4* P = (const float4*)(a.P_vo + ((int64_t)h * kD + t) * kD);
   float r = 0.f;

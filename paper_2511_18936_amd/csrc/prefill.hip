@@ -161,7 +161,9 @@ void prefill_kernel(CompressLaunch a) {
 
   const _Float16* x = (const _Float16*)(role ? a.v_new : a.k_new) +
                       ((int64_t)b * a.Hkv + h) * a.n_new * kD;
-  const float* P = (role ? a.P_vo : a.P_qk) + (int64_t)h * kD * kD;
+  // NULL P_vo: values already in the rotated basis; the rotation is then by I
+  const float* Prole = role ? a.P_vo : a.P_qk;
+  const float* P = Prole ? Prole + (int64_t)h * kD * kD : nullptr;
 
   const int k = a.tab.kact[role][b];
   const int kp = kpad_of(k);
@@ -182,7 +184,8 @@ void prefill_kernel(CompressLaunch a) {
       for (int ks = 0; ks < 32; ++ks)
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt)
-          pb[nt][ks] = P[(32 * q + ks) * kD + 32 * nh + 16 * nt + r16];
+          pb[nt][ks] = P ? P[(32 * q + ks) * kD + 32 * nh + 16 * nt + r16]
+                         : (32 * q + ks == 32 * nh + 16 * nt + r16 ? 1.f : 0.f);
 #pragma unroll 1
       for (int mt = 0; mt < 4; ++mt) {
         const int tp0 = pos0 + 16 * mt - len_old;  // token index of the pass's first row

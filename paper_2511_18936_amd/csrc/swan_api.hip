@@ -272,7 +272,7 @@ swan_status swan_compress_append(const swan_cache* c, const int32_t* seq_len_hos
   if (!seq_len_host) return fail(SWAN_ERR_INVALID_ARG, "seq_len_host is NULL");
   if (n_new < 0) return fail(SWAN_ERR_INVALID_ARG, "n_new %d < 0", n_new);
   if (n_new > 0 && (!k_new || !v_new)) return fail(SWAN_ERR_INVALID_ARG, "k_new / v_new is NULL");
-  if (!P_qk || !P_vo) return fail(SWAN_ERR_INVALID_ARG, "P_qk / P_vo is NULL");
+  if (!P_qk) return fail(SWAN_ERR_INVALID_ARG, "P_qk is NULL");
   if ((((uintptr_t)P_qk | (uintptr_t)P_vo) & 15) != 0)
     return fail(SWAN_ERR_INVALID_ARG, "P_qk / P_vo must be 16-byte aligned");
   if ((((uintptr_t)k_new | (uintptr_t)v_new) & 15) != 0)
@@ -344,7 +344,7 @@ swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_ho
   if ((st = check_k(c, k_active_host, k_value_host)) != SWAN_OK) return st;
   if ((st = check_cache_ptrs(c)) != SWAN_OK) return st;
   if (!seq_len_host) return fail(SWAN_ERR_INVALID_ARG, "seq_len_host is NULL");
-  if (!q || !out || !P_qk || !P_vo) return fail(SWAN_ERR_INVALID_ARG, "q / out / P is NULL");
+  if (!q || !out || !P_qk) return fail(SWAN_ERR_INVALID_ARG, "q / out / P_qk is NULL");
   if ((((uintptr_t)P_qk | (uintptr_t)P_vo) & 15) != 0)
     return fail(SWAN_ERR_INVALID_ARG, "P_qk / P_vo must be 16-byte aligned");
   for (int b = 0; b < c->batch; ++b) {
@@ -456,6 +456,38 @@ swan_status swan_change_k(const swan_cache* src, const int32_t* k_active_src,
     if (e != hipSuccess) return hip_status(e, "change_k launch");
   }
   return ok();
+}
+
+swan_status swan_rope(const void* x, void* y, int32_t dtype, int32_t batch, int32_t n_heads,
+                      int32_t n, int32_t head_dim, const int32_t* pos0_host, double base,
+                      void* stream) {
+  if (!dtype_ok(dtype)) return fail(SWAN_ERR_UNSUPPORTED, "dtype %d not supported", dtype);
+  if (head_dim != SWAN_HEAD_DIM)
+    return fail(SWAN_ERR_UNSUPPORTED, "head_dim %d: the GPU path supports %d only", head_dim,
+                SWAN_HEAD_DIM);
+  if (batch < 1 || batch > SWAN_MAX_BATCH || n_heads < 1 || n < 0)
+    return fail(SWAN_ERR_INVALID_ARG, "batch %d, n_heads %d, n %d", batch, n_heads, n);
+  if (!(base > 1.0) || isinf(base)) return fail(SWAN_ERR_INVALID_ARG, "base must be > 1");
+  if (!pos0_host) return fail(SWAN_ERR_INVALID_ARG, "pos0_host is NULL");
+  if (n == 0) return ok();
+  if (!x || !y) return fail(SWAN_ERR_INVALID_ARG, "x / y is NULL");
+  if ((((uintptr_t)x | (uintptr_t)y) & 15) != 0)
+    return fail(SWAN_ERR_INVALID_ARG, "x / y must be 16-byte aligned");
+  swan::RopeLaunch a;
+  a.x = x;
+  a.y = y;
+  a.B = batch;
+  a.H = n_heads;
+  a.n = n;
+  a.dtype = dtype;
+  for (int b = 0; b < SWAN_MAX_BATCH; ++b) {
+    if (b < batch && (pos0_host[b] < 0 || (int64_t)pos0_host[b] + n > INT32_MAX))
+      return fail(SWAN_ERR_INVALID_ARG, "pos0[%d] = %d out of range", b, pos0_host[b]);
+    a.pos0[b] = b < batch ? pos0_host[b] : 0;
+  }
+  a.base = base;
+  a.stream = (hipStream_t)stream;
+  return hip_status(swan::launch_rope(a), "rope launch");
 }
 
 swan_status swan_set_profile_events(void* start_event, void* stop_event) {

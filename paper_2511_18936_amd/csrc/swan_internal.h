@@ -126,6 +126,17 @@ struct ChangeKLaunch {
 };
 hipError_t launch_change_k(const ChangeKLaunch& a);
 
+// RoPE of query / key rows before the rotation (rope.hip)
+struct RopeLaunch {
+  const void* x;
+  void* y;
+  int B, H, n, dtype;
+  int32_t pos0[SWAN_MAX_BATCH];  // position of each sequence's first row
+  double base;
+  hipStream_t stream;
+};
+hipError_t launch_rope(const RopeLaunch& a);
+
 struct CalibLaunch {
   const float* rows;
   int64_t n_rows;

@@ -1,0 +1,83 @@
+"""A Llama-shaped attention layer on the SWAN cache, in the paper's model-side form.
+
+Sec. 4.2: queries and keys take RoPE first and are then rotated by P_QK at run
+time (RoPE keeps P_QK out of W_Q and W_K), while P_VO is absorbed into the
+weights, W_V_hat = W_V . P_VO per KV head and W_O_hat = P_VO^T . W_O per query
+head, so the values enter the cache already rotated and the attention output
+leaves it rotated, straight into W_O_hat (Lemma 2).
+
+One call with n new tokens per sequence, on the current stream:
+  q, k, v_hat = x . W_Q, x . W_K, x . W_V_hat    dense GEMMs (torch: the GEMM library)
+  swan_rope on q and k at each sequence's next positions
+  swan_compress_append(k, v_hat, P_QK, P_VO = NULL)
+  for a decode step (n = 1): swan_decode_attention(q, P_QK, P_VO = NULL) -> o_hat,
+  and y = o_hat . W_O_hat                         dense GEMM
+The SWAN steps run in libswan's kernels; attention over a prompt is the dense,
+standard kind and is not part of this layer (a prompt call only fills the cache).
+Weights are [in][out] row-major, x . W.
+"""
+from __future__ import annotations
+
+from typing import Optional, Sequence
+
+from . import swan
+
+HEAD_DIM = swan.HEAD_DIM
+
+
+class SwanAttentionLayer:
+    def __init__(self, W_q, W_k, W_v, W_o, P_qk, P_vo, n_heads: int, n_kv_heads: int,
+                 rope_base: float, batch: int, buffer_tokens: int, capacity: int,
+                 k_active: Sequence[int], k_value: Optional[Sequence[int]] = None,
+                 sparse_values: str = "same"):
+        """W_q [hidden][n_heads*128], W_k and W_v [hidden][n_kv*128], W_o
+        [n_heads*128][hidden] (float16 or float32, cuda); P_qk, P_vo [n_kv][128][128]
+        float32 (swan_calibrate_rotation of post-RoPE keys and of values)."""
+        import torch
+
+        d = HEAD_DIM
+        self.n_heads, self.n_kv_heads = n_heads, n_kv_heads
+        self.rope_base = float(rope_base)
+        self.dtype = W_q.dtype
+        self.P_qk = P_qk.contiguous()
+        G = n_heads // n_kv_heads
+        # absorbed weights, formed once in float64 and rounded to the weights' type
+        Wv = W_v.double().clone()
+        Wo = W_o.double().clone()
+        P = P_vo.double()
+        for h in range(n_kv_heads):
+            Wv[:, h * d:(h + 1) * d] = Wv[:, h * d:(h + 1) * d] @ P[h]
+        for hq in range(n_heads):
+            Wo[hq * d:(hq + 1) * d, :] = P[hq // G].T @ Wo[hq * d:(hq + 1) * d, :]
+        self.W_q = W_q.contiguous()
+        self.W_k = W_k.contiguous()
+        self.W_v_hat = Wv.to(self.dtype).contiguous()
+        self.W_o_hat = Wo.to(self.dtype).contiguous()
+        self.cache = swan.SwanCache(batch, n_heads, n_kv_heads, buffer_tokens, capacity,
+                                    k_active, self.dtype, W_q.device,
+                                    sparse_values=sparse_values, k_value=k_value)
+        self._torch = torch
+
+    def project(self, x):
+        """Post-RoPE q [B][H_q][n][128], k and v_hat [B][H_kv][n][128] of new rows x
+        [B][n][hidden] at each sequence's next positions."""
+        B, n, _ = x.shape
+        d = HEAD_DIM
+        pos0 = list(self.cache.seq_len)
+        q = (x @ self.W_q).view(B, n, self.n_heads, d).transpose(1, 2).contiguous()
+        k = (x @ self.W_k).view(B, n, self.n_kv_heads, d).transpose(1, 2).contiguous()
+        v = (x @ self.W_v_hat).view(B, n, self.n_kv_heads, d).transpose(1, 2).contiguous()
+        swan.rope(q, pos0, self.rope_base, out=q)
+        swan.rope(k, pos0, self.rope_base, out=k)
+        return q, k, v
+
+    def __call__(self, x):
+        """x [B][n][hidden]: append the n rows of every sequence to the cache; for a
+        decode step (n = 1) return y [B][hidden], the layer's attention output."""
+        q, k, v = self.project(x)
+        self.cache.append(k, v, self.P_qk, None)
+        if x.shape[1] != 1:
+            return None
+        B = x.shape[0]
+        o_hat = self.cache.decode(q[:, :, 0].contiguous(), self.P_qk, None)
+        return o_hat.view(B, self.n_heads * HEAD_DIM) @ self.W_o_hat

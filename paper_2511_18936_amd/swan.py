@@ -32,7 +32,7 @@ PAGE_TOKENS = 64
 EXPORTED = (
     "swan_last_error", "swan_version", "swan_page_bytes", "swan_cache_bytes",
     "swan_calibrate_workspace_bytes", "swan_calibrate_rotation", "swan_compress_append",
-    "swan_decode_workspace_bytes", "swan_decode_attention", "swan_change_k",
+    "swan_decode_workspace_bytes", "swan_decode_attention", "swan_change_k", "swan_rope",
     "swan_set_profile_events",
 )
 
@@ -86,6 +86,7 @@ def _load() -> ctypes.CDLL:
         "swan_decode_attention": [pdesc, pi32, pi32, pi32, vp, vp, vp, ctypes.c_float, vp, vp, sz,
                                   vp],
         "swan_change_k": [pdesc, pi32, pi32, pdesc, pi32, pi32, pi32, vp],
+        "swan_rope": [vp, vp, i32, i32, i32, i32, i32, pi32, ctypes.c_double, vp],
         "swan_set_profile_events": [vp, vp],
     }
     for name, args in sigs.items():
@@ -219,6 +220,20 @@ def change_k(src: CacheDesc, k_active_src: Sequence[int], k_value_src: Optional[
                               _opt_i32_array(k_value_src), ctypes.byref(dst),
                               _i32_array(k_active_dst), _opt_i32_array(k_value_dst),
                               _i32_array(seq_len), _stream(stream)))
+
+
+def rope(x, pos0: Sequence[int], base: float, out=None, stream=None):
+    """RoPE of rows x [B][H][n][128] (float16 or float32, cuda) at positions pos0[b] + i;
+    out=None writes a new tensor, out=x works in place."""
+    import torch
+
+    if out is None:
+        out = torch.empty_like(x)
+    B, H, n, d = x.shape
+    code = SWAN_F16 if x.dtype == torch.float16 else SWAN_F32
+    _check(_lib.swan_rope(_ptr(x), _ptr(out), code, B, H, n, d, _i32_array(pos0), float(base),
+                          _stream(stream)))
+    return out
 
 
 def set_profile_events(start=None, stop=None) -> None:

@@ -22,7 +22,7 @@ def _declared_functions():
 
 def test_header_and_binding_agree_on_exports():
     declared = _declared_functions()
-    assert len(declared) == 11
+    assert len(declared) == 12
     assert sorted(swan.EXPORTED) == declared
     lib = swan.lib()
     for name in declared:
@@ -210,3 +210,20 @@ def test_change_k_rejects_bad_arguments():
     # the sparse tokens must fit the destination's capacity
     assert call(d, _desc(sparse_capacity=50, k_pages=B2, v_pages=B2 + (1 << 24))) == \
         swan.SWAN_ERR_CAPACITY
+
+
+def test_rope_rejects_bad_arguments():
+    lib = swan.lib()
+    pos = swan._i32_array([0, 5])
+    E = swan.SWAN_ERR_INVALID_ARG
+    assert lib.swan_rope(FAKE, FAKE, swan.SWAN_F16, 2, 4, 3, 64, pos, 1e4, None) == \
+        swan.SWAN_ERR_UNSUPPORTED
+    assert lib.swan_rope(FAKE, FAKE, 9, 2, 4, 3, 128, pos, 1e4, None) == swan.SWAN_ERR_UNSUPPORTED
+    assert lib.swan_rope(FAKE, FAKE, swan.SWAN_F16, 0, 4, 3, 128, pos, 1e4, None) == E
+    assert lib.swan_rope(FAKE, FAKE, swan.SWAN_F16, 2, 4, 3, 128, pos, 1.0, None) == E
+    assert lib.swan_rope(FAKE, FAKE, swan.SWAN_F16, 2, 4, 3, 128, None, 1e4, None) == E
+    assert lib.swan_rope(None, FAKE, swan.SWAN_F16, 2, 4, 3, 128, pos, 1e4, None) == E
+    assert lib.swan_rope(FAKE + 8, FAKE, swan.SWAN_F16, 2, 4, 3, 128, pos, 1e4, None) == E
+    assert lib.swan_rope(FAKE, FAKE, swan.SWAN_F16, 2, 4, 3, 128, swan._i32_array([0, -1]), 1e4,
+                         None) == E
+    assert lib.swan_rope(None, None, swan.SWAN_F16, 2, 4, 0, 128, pos, 1e4, None) == swan.SWAN_OK

@@ -1,0 +1,166 @@
+"""The attention layer around the cache (RoPE, W_V / W_O absorbing P_VO) on the GPU.
+
+* RoPE: bit-exact against the oracle's float64 rotation rounded once to fp16
+  (float32 rows: within one ulp, see the test).
+* Values already rotated (P_vo = NULL): stored as given, bit for bit, and decode
+  returns the rotated output, within 2e-3 of the oracle.
+* Layer decode steps: given the GPU's own post-RoPE q, k and v_hat, the cache is
+  bit-exact and the output within 2e-3 (max |y - y_ref| / max |y_ref| per
+  sequence); end to end against the oracle's float64 layer from the same float16
+  weights, within 5e-2 (see E2E_TOL).
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import swan_inputs as si
+from oracle import swan_oracle as O
+from tests import swan_cases as C
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-3
+# End to end, q, k and v_hat come from float16 GEMMs on one side and float64 products
+# on the other; a one-ulp difference can swap the k-th and (k+1)-th largest rotated
+# components of a key, which moves that token's score by a whole component.  So the
+# bound checks the wiring (absorbed weights, RoPE positions, head mapping, W_O
+# layout), whose mistakes give errors of order 1; the kernels' parity is the 2e-3
+# check on the GPU's own q, k and v_hat.
+E2E_TOL = 5e-2
+
+
+def _log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.mark.parametrize("dtype", ["f16", "f32"])
+@pytest.mark.parametrize("base", [10000.0, 500000.0])
+def test_rope_matches_oracle_bit_exact(gpu_device, swan_mod, torch_mod, dtype, base):
+    torch = torch_mod
+    _log(f"rope dtype={dtype} base={base}")
+    np_dt = si.np_dtype(dtype)
+    x = si.rng_for(505, int(base)).standard_normal((3, 4, 50, 128)).astype(np_dt)
+    pos0 = [0, 1000, 131000]
+    tx = torch.tensor(x, device=gpu_device)
+    y = swan_mod.rope(tx, pos0, base).cpu().numpy()
+    swan_mod.rope(tx, pos0, base, out=tx)  # in place
+    torch.cuda.synchronize()
+    for b in range(3):
+        want = O.rope(x[b], np.arange(pos0[b], pos0[b] + 50), base, np_dt)
+        if dtype == "f16":
+            assert np.array_equal(y[b].view(np.uint8), want.view(np.uint8)), b
+        else:
+            # the device's float64 pow / sincos and the host's may differ in the last
+            # place; at positions ~1e5 that can move a float32 result by one ulp
+            assert np.all(np.abs(y[b] - want) <= np.spacing(np.abs(want))), b
+        assert np.array_equal(tx[b].cpu().numpy().view(np.uint8), y[b].view(np.uint8)), b
+
+
+@pytest.mark.parametrize("Hq,Hkv,L,b,k", [(4, 4, 700, 16, 48), (8, 2, 900, 64, 32),
+                                          (4, 2, 130, 0, 96)])
+def test_values_already_rotated(gpu_device, swan_mod, torch_mod, Hq, Hkv, L, b, k):
+    """P_vo = NULL: the values are stored as given and decode returns o_hat."""
+    torch = torch_mod
+    _log(f"P_vo NULL Hq={Hq} Hkv={Hkv} L={L} b={b} k={k}")
+    B = 2
+    r = si.rng_for(606, L, k)
+    K = r.standard_normal((B, Hkv, L, 128)).astype(np.float16)
+    V = r.standard_normal((B, Hkv, L, 128)).astype(np.float16)
+    Pqk = np.stack([si.random_orthogonal(60 + h, 128) for h in range(Hkv)]).astype(np.float32)
+    tqk = torch.tensor(Pqk, device=gpu_device)
+    cache = swan_mod.SwanCache(B, Hq, Hkv, b, max(L - b, 1), [k, k], torch.float16, gpu_device)
+    cache.append(torch.tensor(K, device=gpu_device), torch.tensor(V, device=gpu_device), tqk,
+                 None)
+    q = r.standard_normal((B, Hq, 128)).astype(np.float16)
+    out = cache.decode(torch.tensor(q, device=gpu_device), tqk, None).cpu().numpy()
+    eye = np.eye(128)
+    G = Hq // Hkv
+    for bi in range(B):
+        for h in range(Hkv):
+            oc = O.compress_block(K[bi, h], V[bi, h], Pqk[h], eye, b, k, np.float16)
+            C.compare_unit(cache, oc, bi, h, L, np.float16)
+            for hq in range(h * G, (h + 1) * G):
+                ref = O.attend_arrays(q[bi, hq].astype(np.float64), Pqk[h], eye, oc)
+                assert C.max_rel_err(out[bi, hq][None], ref[None]) <= TOL
+
+
+def _weights(seed, hidden, Hq, Hkv):
+    r = si.rng_for(707, seed)
+    W_q = r.standard_normal((hidden, Hq * 128)) / math.sqrt(hidden)
+    W_k = r.standard_normal((hidden, Hkv * 128)) / math.sqrt(hidden)
+    W_v = r.standard_normal((hidden, Hkv * 128)) / math.sqrt(hidden)
+    W_o = r.standard_normal((Hq * 128, hidden)) / math.sqrt(Hq * 128)
+    # the rotations as the GPU holds them (float32), for both sides
+    P_qk = np.stack([si.random_orthogonal(seed * 10 + h, 128) for h in range(Hkv)])
+    P_vo = np.stack([si.random_orthogonal(seed * 10 + 5 + h, 128) for h in range(Hkv)])
+    return (W_q, W_k, W_v, W_o, P_qk.astype(np.float32).astype(np.float64),
+            P_vo.astype(np.float32).astype(np.float64))
+
+
+@pytest.mark.parametrize("Hq,Hkv,base,k", [(8, 8, 10000.0, 48), (8, 2, 500000.0, 64)])
+def test_layer_decode_steps(gpu_device, swan_mod, torch_mod, Hq, Hkv, base, k):
+    torch = torch_mod
+    from paper_2511_18936_amd.layer import SwanAttentionLayer
+
+    _log(f"layer Hq={Hq} Hkv={Hkv} base={base} k={k}")
+    B, hidden, L0, steps, b = 2, 512, 300, 3, 32
+    W_q, W_k, W_v, W_o, P_qk, P_vo = _weights(Hq + Hkv, hidden, Hq, Hkv)
+    W16 = [w.astype(np.float16).astype(np.float64) for w in (W_q, W_k, W_v, W_o)]
+    t16 = lambda a: torch.tensor(a, dtype=torch.float16, device=gpu_device)
+    layer = SwanAttentionLayer(t16(W_q), t16(W_k), t16(W_v), t16(W_o),
+                               torch.tensor(P_qk, dtype=torch.float32, device=gpu_device),
+                               torch.tensor(P_vo, dtype=torch.float32, device=gpu_device),
+                               Hq, Hkv, base, B, b, L0 + steps, [k] * B)
+    X = (si.rng_for(708, Hq).standard_normal((B, L0 + steps, hidden))).astype(np.float16)
+    G = Hq // Hkv
+    eye = np.eye(128)
+    W_o_hat = layer.W_o_hat.double().cpu().numpy()
+    # the prompt through the layer (fills the cache), then decode steps driven step by
+    # step so that the GPU's own q, k and v_hat can be checked against the oracle
+    ks, vs = [], []
+    q, kk, vv = layer.project(t16(X[:, :L0]))
+    layer.cache.append(kk, vv, layer.P_qk, None)
+    ks.append(kk.cpu().numpy())
+    vs.append(vv.cpu().numpy())
+    for s in range(steps):
+        L = L0 + s + 1
+        x = t16(X[:, L - 1:L])
+        q, kk, vv = layer.project(x)
+        layer.cache.append(kk, vv, layer.P_qk, None)
+        o_hat = layer.cache.decode(q[:, :, 0].contiguous(), layer.P_qk, None)
+        y = (o_hat.view(B, Hq * 128) @ layer.W_o_hat).double().cpu().numpy()
+        ks.append(kk.cpu().numpy())
+        vs.append(vv.cpu().numpy())
+        Kall = np.concatenate(ks, axis=2)
+        Vall = np.concatenate(vs, axis=2)
+        qn = q[:, :, 0].double().cpu().numpy()
+        for bi in range(B):
+            o_ref = np.zeros(Hq * 128)
+            for h in range(Hkv):
+                oc = O.compress_block(Kall[bi, h], Vall[bi, h], P_qk[h], eye, b, k, np.float16)
+                if s == steps - 1:
+                    C.compare_unit(layer.cache, oc, bi, h, L, np.float16)
+                for hq in range(h * G, (h + 1) * G):
+                    o_ref[hq * 128:(hq + 1) * 128] = O.attend_arrays(qn[bi, hq], P_qk[h], eye,
+                                                                     oc)
+            y_ref = o_ref @ W_o_hat
+            err = np.abs(y[bi] - y_ref).max() / np.abs(y_ref).max()
+            # end to end: the float64 layer from the same (float16) weights
+            y_e2e = O.layer_decode(X[bi, :L].astype(np.float64), *W16, P_qk, P_vo, Hq, Hkv, base,
+                                   b, k)
+            err2 = np.abs(y[bi] - y_e2e).max() / np.abs(y_e2e).max()
+            _log(f"  step {s} seq {bi}: err {err:.2e} (same q/k/v), {err2:.2e} (end to end)")
+            assert err <= TOL
+            assert err2 <= E2E_TOL
+    # the layer's own call gives the same output as the steps above
+    layer2 = SwanAttentionLayer(t16(W_q), t16(W_k), t16(W_v), t16(W_o),
+                                torch.tensor(P_qk, dtype=torch.float32, device=gpu_device),
+                                torch.tensor(P_vo, dtype=torch.float32, device=gpu_device),
+                                Hq, Hkv, base, B, b, L0 + steps, [k] * B)
+    assert layer2(t16(X[:, :L0])) is None
+    for s in range(steps):
+        y2 = layer2(t16(X[:, L0 + s:L0 + s + 1]))
+    torch.cuda.synchronize()
+    assert np.allclose(y2.double().cpu().numpy(), y, rtol=0, atol=0)
