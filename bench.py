@@ -45,6 +45,8 @@ def parse_args():
                     help="(sequence, head) units in the oracle's timed sample")
     ap.add_argument("--change-k", type=int, default=0,
                     help="also time swan_change_k of the cache from the workload's k to this k")
+    ap.add_argument("--layer", action="store_true",
+                    help="also time decode steps of the whole attention layer (synthetic weights)")
     ap.add_argument("--probe-copy", type=int, default=0,
                     help="also run a device copy of this many bytes (HBM counter calibration)")
     return ap.parse_args()
@@ -148,6 +150,52 @@ def time_change_k(swan, torch, w, cache, ks, kvs, k_new, esize, reps=5):
     return {"from": [ks[0], kvl[0]], "to": k_new, "ms": t * 1e3, "bytes": nbytes,
             "gbps": nbytes / t / 1e9, "frac": nbytes / t / 1e9 / HBM_PEAK_GBPS,
             "kernel": "change_k_kernel (one launch per role)"}
+
+
+def time_layer(swan, torch, si, w, Pqk, Pvo, ks, kvs, dev, warmup, steps):
+    """Decode steps of the attention layer around the cache (RoPE, W_V / W_O absorbing
+    P_VO, paper_2511_18936_amd.layer) at the workload's shape: synthetic float16
+    weights, hidden = n_heads * 128, the cache filled to the workload's context; each
+    step = q/k/v GEMMs, RoPE, append, decode, output GEMM, timed with HIP events."""
+    import math
+
+    from paper_2511_18936_amd.layer import SwanAttentionLayer
+
+    hidden = w.n_q_heads * w.head_dim
+    base = 500000.0 if "llama3" in w.name else 10000.0
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(si.torch_seed_for(w.wid, 9000))
+    def weight(n_in, n_out):
+        m = torch.randn(n_in, n_out, generator=gen, device=dev, dtype=torch.float32)
+        return (m / math.sqrt(n_in)).to(torch.float16 if w.dtype == "f16" else torch.float32)
+    d = w.head_dim
+    L0 = w.context - 1
+    cap = max(w.context + warmup + steps - w.buffer, 1)
+    layer = SwanAttentionLayer(weight(hidden, w.n_q_heads * d), weight(hidden, w.n_kv_heads * d),
+                               weight(hidden, w.n_kv_heads * d), weight(w.n_q_heads * d, hidden),
+                               Pqk, Pvo, w.n_q_heads, w.n_kv_heads, base, w.batch, w.buffer, cap,
+                               ks, kvs, w.sparse_values)
+    K = si.kv_rows_device(w.wid, w.batch, w.n_kv_heads, si.ROLE_K, L0, w.dtype, dev)
+    V = si.kv_rows_device(w.wid, w.batch, w.n_kv_heads, si.ROLE_V, L0, w.dtype, dev)
+    layer.cache.append(K, V, layer.P_qk, None)  # the context, its values taken as rotated
+    del K, V
+    torch.cuda.empty_cache()
+    xs = [torch.randn(w.batch, 1, hidden, generator=gen, device=dev).to(layer.dtype)
+          for _ in range(warmup + steps)]
+    for i in range(warmup):
+        layer(xs[i])
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(steps):
+        y = layer(xs[warmup + i])
+    e1.record()
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(y).all())
+    t = e0.elapsed_time(e1) * 1e-3 / steps
+    return {"hidden": hidden, "rope_base": base, "step_ms": t * 1e3,
+            "tokens_per_s": w.batch / t,
+            "weights_bytes": 2 * hidden * d * (2 * w.n_q_heads + 2 * w.n_kv_heads)}
 
 
 def cpu_model() -> str:
@@ -365,6 +413,14 @@ def main():
         log(f"[bench] change_k {change_k['from']} -> {change_k['to']}: {change_k['ms']:.3f} ms, "
             f"{change_k['gbps']:.0f} GB/s read+write ({change_k['frac'] * 100:.1f}% of 8 TB/s)")
 
+    layer = None
+    if args.layer:
+        del cache
+        torch.cuda.empty_cache()
+        layer = time_layer(swan, torch, si, w, Pqk, Pvo, ks, kvs, dev, args.warmup, args.steps)
+        log(f"[bench] layer decode step (hidden {layer['hidden']}): {layer['step_ms']:.3f} ms, "
+            f"{layer['tokens_per_s']:.0f} tokens/s (attention alone {dec_avg * 1e3:.3f} ms)")
+
     cpu = None
     if not args.no_cpu_baseline:
         t = time.perf_counter()
@@ -417,6 +473,7 @@ def main():
             "prefill_compress_gbps": prefill_bytes / t_prefill / 1e9,
             "kv_tokens_per_s": float(np.mean([sum(L) for L in lens])) / dec_avg,
             "change_k": change_k,
+            "layer": layer,
         },
     }
     print(json.dumps(result), flush=True)
