@@ -58,19 +58,22 @@ def test_rope_matches_oracle_bit_exact(gpu_device, swan_mod, torch_mod, dtype, b
         assert np.array_equal(tx[b].cpu().numpy().view(np.uint8), y[b].view(np.uint8)), b
 
 
-@pytest.mark.parametrize("Hq,Hkv,L,b,k", [(4, 4, 700, 16, 48), (8, 2, 900, 64, 32),
-                                          (4, 2, 130, 0, 96)])
-def test_values_already_rotated(gpu_device, swan_mod, torch_mod, Hq, Hkv, L, b, k):
+@pytest.mark.parametrize("Hq,Hkv,L,b,k,vals", [(4, 4, 700, 16, 48, "same"),
+                                               (8, 2, 900, 64, 32, "same"),
+                                               (4, 2, 130, 0, 96, "same"),
+                                               (8, 2, 600, 16, 64, "e4m3")])
+def test_values_already_rotated(gpu_device, swan_mod, torch_mod, Hq, Hkv, L, b, k, vals):
     """P_vo = NULL: the values are stored as given and decode returns o_hat."""
     torch = torch_mod
-    _log(f"P_vo NULL Hq={Hq} Hkv={Hkv} L={L} b={b} k={k}")
+    _log(f"P_vo NULL Hq={Hq} Hkv={Hkv} L={L} b={b} k={k} values={vals}")
     B = 2
     r = si.rng_for(606, L, k)
     K = r.standard_normal((B, Hkv, L, 128)).astype(np.float16)
     V = r.standard_normal((B, Hkv, L, 128)).astype(np.float16)
     Pqk = np.stack([si.random_orthogonal(60 + h, 128) for h in range(Hkv)]).astype(np.float32)
     tqk = torch.tensor(Pqk, device=gpu_device)
-    cache = swan_mod.SwanCache(B, Hq, Hkv, b, max(L - b, 1), [k, k], torch.float16, gpu_device)
+    cache = swan_mod.SwanCache(B, Hq, Hkv, b, max(L - b, 1), [k, k], torch.float16, gpu_device,
+                               sparse_values=vals)
     cache.append(torch.tensor(K, device=gpu_device), torch.tensor(V, device=gpu_device), tqk,
                  None)
     q = r.standard_normal((B, Hq, 128)).astype(np.float16)
@@ -79,8 +82,9 @@ def test_values_already_rotated(gpu_device, swan_mod, torch_mod, Hq, Hkv, L, b, 
     G = Hq // Hkv
     for bi in range(B):
         for h in range(Hkv):
-            oc = O.compress_block(K[bi, h], V[bi, h], Pqk[h], eye, b, k, np.float16)
-            C.compare_unit(cache, oc, bi, h, L, np.float16)
+            oc = O.compress_block(K[bi, h], V[bi, h], Pqk[h], eye, b, k, np.float16,
+                                  values="e4m3" if vals == "e4m3" else "t")
+            C.compare_unit(cache, oc, bi, h, L, np.float16, values=vals)
             for hq in range(h * G, (h + 1) * G):
                 ref = O.attend_arrays(q[bi, hq].astype(np.float64), Pqk[h], eye, oc)
                 assert C.max_rel_err(out[bi, hq][None], ref[None]) <= TOL
