@@ -188,7 +188,7 @@ extern "C" {
 
 const char* swan_last_error(void) { return g_last_error.c_str(); }
 
-int32_t swan_version(void) { return 200; }
+int32_t swan_version(void) { return 202; }
 
 swan_status swan_page_bytes(int32_t dtype, int32_t k_active, size_t* bytes) {
   if (!bytes) return fail(SWAN_ERR_INVALID_ARG, "bytes is NULL");

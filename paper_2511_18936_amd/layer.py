@@ -56,7 +56,6 @@ class SwanAttentionLayer:
         self.cache = swan.SwanCache(batch, n_heads, n_kv_heads, buffer_tokens, capacity,
                                     k_active, self.dtype, W_q.device,
                                     sparse_values=sparse_values, k_value=k_value)
-        self._torch = torch
 
     def project(self, x):
         """Post-RoPE q [B][H_q][n][128], k and v_hat [B][H_kv][n][128] of new rows x

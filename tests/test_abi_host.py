@@ -29,6 +29,11 @@ def test_header_and_binding_agree_on_exports():
         assert hasattr(lib, name), name
 
 
+def test_version_is_the_current_abi():
+    """2.02: keys and values with their own k (2.00), swan_change_k, swan_rope."""
+    assert swan.lib().swan_version() == 202
+
+
 def test_nm_shows_exported_symbols():
     import subprocess
 
