@@ -33,8 +33,6 @@ class SwanAttentionLayer:
         """W_q [hidden][n_heads*128], W_k and W_v [hidden][n_kv*128], W_o
         [n_heads*128][hidden] (float16 or float32, cuda); P_qk, P_vo [n_kv][128][128]
         float32 (swan_calibrate_rotation of post-RoPE keys and of values)."""
-        import torch
-
         d = HEAD_DIM
         self.n_heads, self.n_kv_heads = n_heads, n_kv_heads
         self.rope_base = float(rope_base)
