@@ -11,34 +11,63 @@
 // Slots past k' up to k'_pad are the usual padding: value 0 at the next lowest
 // dims not kept.
 //
-// One wave per (sequence, KV head, page) and one launch per role; lane t owns
-// token t of the page.  The source page is staged in LDS with 16-byte loads,
-// the destination page is assembled in LDS and written with 16-byte stores.
-// Lowering finds the k'-th largest magnitude key of the lane's k entries by a
-// bitwise search (one pass over the entries per key bit), then walks the
-// entries in index order keeping those above it and the first ties.
+// One wave per (sequence, KV head, page) and one launch per role and source
+// k_pad; lane t owns token t of the page.  The kernel is specialised on the
+// source k_pad, so a lane holds its token's k_pad values and indices in
+// registers, loaded with one coalesced 16-byte (8-byte for E4M3) load per
+// chunk.  Lowering finds the k'-th largest magnitude key by a bitwise search,
+// counting the keys at or above a candidate several at a time with packed
+// integer arithmetic on the stored words; the entries are then walked in index
+// order.  The destination page is assembled in LDS and written with 16-byte
+// stores.
+#include <utility>
+
 #include "swan_device.h"
 #include "swan_internal.h"
 
 namespace swan {
 
-// magnitude key of a stored value (larger key = larger magnitude) and its bits
+// Per format: magnitude keys (larger key = larger magnitude) of the values
+// packed in a 32-bit word, and the number of them >= a candidate.
 template <typename F>
 struct MagKey;
+
+// binary16: two keys of 15 bits per word.  (key | 0x8000) - cand keeps bit 15
+// set exactly when key >= cand, and never borrows out of its half; the count
+// is the population of bits 15 and 31.
 template <>
 struct MagKey<_Float16> {
   static constexpr int kBits = 15;
-  __device__ static uint32_t get(uint32_t v) { return v & 0x7FFFu; }
+  static constexpr uint32_t kMax = 0x7FFFu;
+  __device__ static uint32_t prep(uint32_t w) { return (w & 0x7FFF7FFFu) | 0x80008000u; }
+  __device__ static uint32_t count_ge(uint32_t p, uint32_t cand) {
+    return (uint32_t)__builtin_popcount((p - cand * 0x10001u) & 0x80008000u);
+  }
+  __device__ static uint32_t total(uint32_t acc) { return acc; }
+  __device__ static uint32_t key(uint32_t v) { return v & 0x7FFFu; }
 };
-template <>
-struct MagKey<float> {
-  static constexpr int kBits = 31;
-  __device__ static uint32_t get(uint32_t v) { return v & 0x7FFFFFFFu; }
-};
+// E4M3 codes: four keys of 7 bits per word, the same trick per byte (the
+// codes saturate at 448, so no key is the NaN code)
 template <>
 struct MagKey<E4M3V> {
   static constexpr int kBits = 7;
-  __device__ static uint32_t get(uint32_t v) { return v & 0x7Fu; }
+  static constexpr uint32_t kMax = 0x7Fu;
+  __device__ static uint32_t prep(uint32_t w) { return (w & 0x7F7F7F7Fu) | 0x80808080u; }
+  __device__ static uint32_t count_ge(uint32_t p, uint32_t cand) {
+    return (uint32_t)__builtin_popcount((p - cand * 0x01010101u) & 0x80808080u);
+  }
+  __device__ static uint32_t total(uint32_t acc) { return acc; }
+  __device__ static uint32_t key(uint32_t v) { return v & 0x7Fu; }
+};
+// float32: one key of 31 bits per word
+template <>
+struct MagKey<float> {
+  static constexpr int kBits = 31;
+  static constexpr uint32_t kMax = 0x7FFFFFFFu;
+  __device__ static uint32_t prep(uint32_t w) { return w & 0x7FFFFFFFu; }
+  __device__ static uint32_t count_ge(uint32_t p, uint32_t cand) { return p >= cand ? 1u : 0u; }
+  __device__ static uint32_t total(uint32_t acc) { return acc; }
+  __device__ static uint32_t key(uint32_t v) { return v & 0x7FFFFFFFu; }
 };
 
 // byte offsets of entry e of slot t in a page of k_pad kp (include/swan.h)
@@ -47,18 +76,10 @@ __device__ __forceinline__ int val_off(int e, int t) {
   constexpr int VB = Fmt<F>::kValBytes, CB = Fmt<F>::kChunkBytes, GV = CB / VB;
   return (e / GV) * 64 * CB + t * CB + (e % GV) * VB;
 }
-template <typename F>
-__device__ __forceinline__ int idx_off(int e, int t, int kp) {
-  return 64 * kp * Fmt<F>::kValBytes + (e / 8) * 512 + t * 8 + (e % 8);
+__device__ __forceinline__ int idx_off(int e, int t, int kp, int vb) {
+  return 64 * kp * vb + (e / 8) * 512 + t * 8 + (e % 8);
 }
 
-template <typename F>
-__device__ __forceinline__ uint32_t read_val(const char* page, int off) {
-  constexpr int VB = Fmt<F>::kValBytes;
-  if constexpr (VB == 1) return *(const uint8_t*)(page + off);
-  else if constexpr (VB == 2) return *(const uint16_t*)(page + off);
-  else return *(const uint32_t*)(page + off);
-}
 template <typename F>
 __device__ __forceinline__ void write_val(char* page, int off, uint32_t v) {
   constexpr int VB = Fmt<F>::kValBytes;
@@ -67,115 +88,179 @@ __device__ __forceinline__ void write_val(char* page, int off, uint32_t v) {
   else *(uint32_t*)(page + off) = v;
 }
 
-// Grid: B * Hkv * max_pages waves.  Dynamic LDS: the largest source page
-// (rounded to 16 bytes) plus the largest destination page of the launch.
-template <typename F>
+// Grid: nsel * Hkv * max_pages waves over the selected sequences, whose source
+// k_pad is KPS8 * 8.  Dynamic LDS: the largest destination page of the launch.
+template <typename F, int KPS8>
 __global__ __launch_bounds__(64) void change_k_kernel(ChangeKLaunch a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   using MK = MagKey<F>;
+  constexpr int VB = Fmt<F>::kValBytes, CB = Fmt<F>::kChunkBytes;
+  constexpr int KPS = KPS8 * 8;
+  constexpr int NW = KPS * VB / 4;   // value words per token
+  constexpr int NVC = KPS * VB / CB; // value chunks per token
+  constexpr int WPC = CB / 4;        // words per chunk
+  constexpr int EPW = 4 / VB;        // entries per word
+  constexpr uint32_t VMASK = VB == 4 ? 0xFFFFFFFFu : VB == 2 ? 0xFFFFu : 0xFFu;
   const int lane = threadIdx.x;
   const int p = blockIdx.x % a.max_pages;
-  const int bh = blockIdx.x / a.max_pages;
-  const int b = bh / a.Hkv, h = bh % a.Hkv;
+  const int sh = blockIdx.x / a.max_pages;
+  const int b = a.sel[sh / a.Hkv], h = sh % a.Hkv;
   const int L = a.len[b];
   const int S = L > a.bb ? L - a.bb : 0;
   if (p >= pages_for(S)) return;
   const int ks = a.k_src[b], kd = a.k_dst[b];
-  const int kps = kpad_of(ks), kpd = kpad_of(kd);
-  const int64_t pbs = page_bytes_of(Fmt<F>::kValBytes, ks);
-  const int64_t pbd = page_bytes_of(Fmt<F>::kValBytes, kd);
+  const int kpd = kpad_of(kd);
+  constexpr int64_t pbs = (int64_t)64 * KPS * (VB + 1);
+  const int64_t pbd = page_bytes_of(VB, kd);
   const char* sp = a.src + a.off_src[b] + ((int64_t)h * a.npc_src + p) * pbs;
   char* dp = a.dst + a.off_dst[b] + ((int64_t)h * a.npc_dst + p) * pbd;
-  char* ls = lds;                                  // source page
-  char* ld = lds + ((pbs + 15) & ~(int64_t)15);    // destination page
 
-  for (int64_t off = lane * 16; off < pbs; off += 64 * 16)
-    *(u32x4*)(ls + off) = __builtin_nontemporal_load((const u32x4*)(sp + off));
-  for (int64_t off = lane * 16; off < pbd; off += 64 * 16)
-    *(u32x4*)(ld + off) = u32x4{0u, 0u, 0u, 0u};
-  __syncthreads();
-
-  if (p * kPage + lane < S) {
-    // k'-th largest key (lowering only): the largest tau with at least kd keys >= tau
-    uint32_t tau = 0;
-    int need_eq = 0;
-    if (kd < ks) {
-      for (int bit = MK::kBits - 1; bit >= 0; --bit) {
-        const uint32_t cand = tau | (1u << bit);
-        int cnt = 0;
-        for (int e = 0; e < ks; ++e)
-          cnt += MK::get(read_val<F>(ls, val_off<F>(e, lane))) >= cand ? 1 : 0;
-        if (cnt >= kd) tau = cand;
-      }
-      int greater = 0;
-      for (int e = 0; e < ks; ++e)
-        greater += MK::get(read_val<F>(ls, val_off<F>(e, lane))) > tau ? 1 : 0;
-      need_eq = kd - greater;
+  // the lane's values and indices
+  uint32_t w[NW], ix[KPS / 4];
+#pragma unroll
+  for (int c = 0; c < NVC; ++c) {
+    if constexpr (CB == 16) {
+      const u32x4 v = __builtin_nontemporal_load((const u32x4*)(sp + c * 64 * CB + lane * CB));
+      w[c * WPC + 0] = v.x;
+      w[c * WPC + 1] = v.y;
+      w[c * WPC + 2] = v.z;
+      w[c * WPC + 3] = v.w;
+    } else {
+      const u32x2 v = __builtin_nontemporal_load((const u32x2*)(sp + c * 64 * CB + lane * CB));
+      w[c * WPC + 0] = v.x;
+      w[c * WPC + 1] = v.y;
     }
-    // kept entries in index order, then zero-valued slots at the lowest free dims;
-    // u0..u3: the dims used so far, as a 128-bit mask
-    uint32_t u0 = 0u, u1 = 0u, u2 = 0u, u3 = 0u;
-    int j = 0;
-    for (int e = 0; e < ks; ++e) {
-      const uint32_t v = read_val<F>(ls, val_off<F>(e, lane));
-      bool keep = true;
-      if (kd < ks) {
-        const uint32_t key = MK::get(v);
-        keep = key > tau || (key == tau && need_eq > 0);
-        if (keep && key == tau) --need_eq;
+  }
+#pragma unroll
+  for (int g = 0; g < KPS8; ++g) {
+    const u32x2 v =
+        __builtin_nontemporal_load((const u32x2*)(sp + 64 * KPS * VB + g * 512 + lane * 8));
+    ix[2 * g] = v.x;
+    ix[2 * g + 1] = v.y;
+  }
+  const bool valid = p * kPage + lane < S;
+
+  // the k'-th largest key (lowering): the largest tau with at least kd keys >= tau.
+  // The padding entries hold +0 (key 0) and every candidate is >= 1, so they
+  // never count.  Raising or copying keeps every entry: tau = 0 and all ties.
+  uint32_t tau = 0;
+  int need_eq = KPS;
+  if (kd < ks) {
+    uint32_t pk[NW];
+#pragma unroll
+    for (int i = 0; i < NW; ++i) pk[i] = MK::prep(w[i]);
+#pragma unroll 1
+    for (int bit = MK::kBits - 1; bit >= 0; --bit) {
+      const uint32_t cand = tau | (1u << bit);
+      uint32_t acc = 0;
+#pragma unroll
+      for (int i = 0; i < NW; ++i) acc += MK::count_ge(pk[i], cand);
+      if ((int)MK::total(acc) >= kd) tau = cand;
+    }
+    uint32_t greater = 0;
+    if (tau < MK::kMax) {
+      uint32_t acc = 0;
+#pragma unroll
+      for (int i = 0; i < NW; ++i) acc += MK::count_ge(pk[i], tau + 1u);
+      greater = MK::total(acc);
+    }
+    need_eq = kd - (int)greater;
+  }
+
+  // kept entries in index order; u0..u3 mark the dims they use (for the padding)
+  const bool pad = kpd > (kd < ks ? kd : ks);
+  const int kv = valid ? ks : 0;
+  uint32_t u0 = 0u, u1 = 0u, u2 = 0u, u3 = 0u;
+  int j = 0;
+#pragma unroll
+  for (int e = 0; e < KPS; ++e) {
+    const uint32_t v = (w[e / EPW] >> ((e % EPW) * VB * 8)) & VMASK;
+    const uint32_t key = MK::key(v);
+    const bool tie = key == tau;
+    const bool keep = e < kv && (key > tau || (tie && need_eq > 0));
+    if (keep) {
+      need_eq -= tie ? 1 : 0;
+      const uint32_t d = (ix[e / 4] >> ((e % 4) * 8)) & 0xFFu;
+      write_val<F>(lds, val_off<F>(j, lane), v);
+      lds[idx_off(j, lane, kpd, VB)] = (char)d;
+      if (pad) {  // uniform
+        const uint32_t bit = 1u << (d & 31);
+        const uint32_t wd = d >> 5;  // indices are < 128 in a valid cache
+        u0 |= wd == 0u ? bit : 0u;
+        u1 |= wd == 1u ? bit : 0u;
+        u2 |= wd == 2u ? bit : 0u;
+        u3 |= wd == 3u ? bit : 0u;
       }
-      if (!keep) continue;
-      const uint32_t d = (uint8_t)ls[idx_off<F>(e, lane, kps)];
-      write_val<F>(ld, val_off<F>(j, lane), v);
-      ld[idx_off<F>(j, lane, kpd)] = (char)d;
-      const uint32_t bit = 1u << (d & 31);
-      const uint32_t w = (d >> 5) & 3u;  // indices are < 128 in a valid cache
-      u0 |= w == 0u ? bit : 0u;
-      u1 |= w == 1u ? bit : 0u;
-      u2 |= w == 2u ? bit : 0u;
-      u3 |= w == 3u ? bit : 0u;
       ++j;
     }
-    // at most 128 - j dims are used, so the free ones never run out before kpd
-    int word = 0;
-    uint32_t fr = ~u0;
-    for (; j < kpd; ++j) {  // values are already 0
-      while (fr == 0u && word < 3) {
-        ++word;
-        fr = word == 1 ? ~u1 : word == 2 ? ~u2 : ~u3;
-      }
-      const int d = word * 32 + __builtin_ctz(fr);
-      fr &= fr - 1u;
-      ld[idx_off<F>(j, lane, kpd)] = (char)d;
+  }
+  // value 0 at the lowest free dims (at most 128 - j dims are used, so they never
+  // run out before kpd); slots of tokens past the end get value 0 and index 0
+  int word = 0;
+  uint32_t fr = ~u0;
+  for (; j < kpd; ++j) {
+    while (fr == 0u && word < 3) {
+      ++word;
+      fr = word == 1 ? ~u1 : word == 2 ? ~u2 : ~u3;
     }
+    const int d = valid ? word * 32 + __builtin_ctz(fr) : 0;
+    fr &= fr - 1u;
+    write_val<F>(lds, val_off<F>(j, lane), 0u);
+    lds[idx_off(j, lane, kpd, VB)] = (char)d;
   }
   __syncthreads();
   for (int64_t off = lane * 16; off < pbd; off += 64 * 16)
-    *(u32x4*)(dp + off) = *(const u32x4*)(ld + off);
+    *(u32x4*)(dp + off) = *(const u32x4*)(lds + off);
 }
 
-template <typename F>
-static hipError_t launch_change_k_t(const ChangeKLaunch& a, size_t lds_bytes) {
-  hipError_t e = hipFuncSetAttribute((const void*)change_k_kernel<F>,
+template <typename F, int KPS8>
+static hipError_t launch_sel(const ChangeKLaunch& a, size_t lds_bytes) {
+  hipError_t e = hipFuncSetAttribute((const void*)change_k_kernel<F, KPS8>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
   if (e != hipSuccess) return e;
-  const dim3 grid(a.B * a.Hkv * a.max_pages);
-  hipLaunchKernelGGL(change_k_kernel<F>, grid, dim3(64), lds_bytes, a.stream, a);
+  const dim3 grid(a.nsel * a.Hkv * a.max_pages);
+  hipLaunchKernelGGL((change_k_kernel<F, KPS8>), grid, dim3(64), lds_bytes, a.stream, a);
   return hipGetLastError();
 }
 
-hipError_t launch_change_k(const ChangeKLaunch& a) {
-  if (a.max_pages <= 0) return hipSuccess;
-  size_t lds = 0;
-  const int vb = a.dtype == SWAN_F32 ? 4 : a.dtype == SWAN_F16 ? 2 : 1;
-  for (int b = 0; b < a.B; ++b) {
-    const size_t n = (size_t)((page_bytes_of(vb, a.k_src[b]) + 15) & ~(int64_t)15) +
-                     (size_t)page_bytes_of(vb, a.k_dst[b]);
-    if (n > lds) lds = n;
+template <typename F, int... Is>
+static hipError_t dispatch_kps8(int kps8, const ChangeKLaunch& a, size_t lds,
+                                std::integer_sequence<int, Is...>) {
+  hipError_t e = hipErrorInvalidValue;
+  ((kps8 == Is + 1 ? (e = launch_sel<F, Is + 1>(a, lds), 0) : 0), ...);
+  return e;
+}
+
+// One launch per distinct source k_pad among the sequences.
+hipError_t launch_change_k(const ChangeKLaunch& in) {
+  const int vb = in.dtype == SWAN_F32 ? 4 : in.dtype == SWAN_F16 ? 2 : 1;
+  uint32_t present = 0;
+  for (int b = 0; b < in.B; ++b) present |= 1u << (kpad_of(in.k_src[b]) / 8 - 1);
+  for (int kps8 = 1; kps8 <= 16; ++kps8) {
+    if (!(present & (1u << (kps8 - 1)))) continue;
+    ChangeKLaunch a = in;
+    a.nsel = 0;
+    a.max_pages = 0;
+    size_t lds = 16;
+    for (int b = 0; b < in.B; ++b) {
+      if (kpad_of(in.k_src[b]) / 8 != kps8) continue;
+      a.sel[a.nsel++] = b;
+      const int S = in.len[b] > in.bb ? in.len[b] - in.bb : 0;
+      if (pages_for(S) > a.max_pages) a.max_pages = pages_for(S);
+      const size_t n = (size_t)page_bytes_of(vb, in.k_dst[b]);
+      if (n > lds) lds = n;
+    }
+    if (a.max_pages == 0) continue;
+    hipError_t e;
+    if (in.dtype == SWAN_F16)
+      e = dispatch_kps8<_Float16>(kps8, a, lds, std::make_integer_sequence<int, 16>{});
+    else if (in.dtype == SWAN_F16_E4M3)
+      e = dispatch_kps8<E4M3V>(kps8, a, lds, std::make_integer_sequence<int, 16>{});
+    else
+      e = dispatch_kps8<float>(kps8, a, lds, std::make_integer_sequence<int, 16>{});
+    if (e != hipSuccess) return e;
   }
-  if (a.dtype == SWAN_F16) return launch_change_k_t<_Float16>(a, lds);
-  if (a.dtype == SWAN_F16_E4M3) return launch_change_k_t<E4M3V>(a, lds);
-  return launch_change_k_t<float>(a, lds);
+  return hipSuccess;
 }
 
 }  // namespace swan

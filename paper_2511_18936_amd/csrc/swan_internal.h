@@ -122,6 +122,8 @@ struct ChangeKLaunch {
   int32_t k_dst[SWAN_MAX_BATCH];    // the role's k in the destination layout
   int64_t off_src[SWAN_MAX_BATCH];  // byte offset of the sequence's first source page
   int64_t off_dst[SWAN_MAX_BATCH];  // byte offset of the sequence's first destination page
+  int nsel;                         // set by launch_change_k: the sequences of one launch
+  int32_t sel[SWAN_MAX_BATCH];
   hipStream_t stream;
 };
 hipError_t launch_change_k(const ChangeKLaunch& a);
