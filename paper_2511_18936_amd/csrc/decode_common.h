@@ -70,14 +70,23 @@ __device__ __forceinline__ void load_page(PageRegs<T, KP8>& r, const char* page,
 }
 #undef SWAN_GLOBAL
 
-// E4M3 byte `sel` (compile-time after unrolling) of w, as float (exact)
+// E4M3 byte `sel` (compile-time after unrolling) of w, as float (exact).  The
+// packed conversion decodes bytes 0-1 or 2-3 at once; the two entries of a
+// pair call it with the same operands, so it is computed once for both.
 __device__ __forceinline__ float e4m3_byte_to_f32(uint32_t w, int sel) {
-  switch (sel & 3) {
-    case 0: return __builtin_amdgcn_cvt_f32_fp8((int)w, 0);
-    case 1: return __builtin_amdgcn_cvt_f32_fp8((int)w, 1);
-    case 2: return __builtin_amdgcn_cvt_f32_fp8((int)w, 2);
-    default: return __builtin_amdgcn_cvt_f32_fp8((int)w, 3);
-  }
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  const f2 v = (sel & 2) ? __builtin_amdgcn_cvt_pk_f32_fp8((int)w, true)
+                         : __builtin_amdgcn_cvt_pk_f32_fp8((int)w, false);
+  return (sel & 1) ? v.y : v.x;
+}
+
+// E4M3 byte `sel` of w as binary16 bits (exact: binary16 holds every E4M3
+// value), two bytes per conversion (scale 1)
+__device__ __forceinline__ uint32_t e4m3_byte_to_f16_bits(uint32_t w, int sel) {
+  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+  const h2 v = (sel & 2) ? __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 1.0f, true)
+                         : __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 1.0f, false);
+  return (uint32_t)__builtin_bit_cast(uint16_t, (sel & 1) ? v.y : v.x);
 }
 
 // value of entry u (0..7) of group g, as float
@@ -104,8 +113,8 @@ struct EntryVal {
 template <typename T, int KP8>
 __device__ __forceinline__ uint32_t entry_f16_bits(const PageRegs<T, KP8>& r, int g, int u) {
   if constexpr (std::is_same<T, E4M3V>::value) {
-    const _Float16 h = (_Float16)EntryVal<T, KP8>::get(r, g, u);
-    return (uint32_t)__builtin_bit_cast(uint16_t, h);
+    const u32x2 c = r.val[g];
+    return e4m3_byte_to_f16_bits(u < 4 ? c.x : c.y, u);
   } else {
     const uint32_t w = r.val[g][u >> 1];
     return (u & 1) ? (w >> 16) : (w & 0xFFFFu);
