@@ -104,13 +104,31 @@ def kpad(k: int) -> int:
     return (k + 7) // 8 * 8
 
 
+def attention_launches(k_key, k_val):
+    """The library's attention launches for these per-sequence k: [(kp8, same_k_pad)].
+    Sequences are grouped by (key, value) k_pad; from the largest k_pad down, a group
+    joins the launch before it when its k_pad is at least SWAN_MERGE_PCT (default 66) %
+    of that launch's, and a launch whose sequences do not all have its k_pad for both
+    roles runs the instances for different k_pad."""
+    pct = int(os.environ.get("SWAN_MERGE_PCT", "66"))
+    groups = sorted({(kpad(a) // 8, kpad(b) // 8) for a, b in zip(k_key, k_val)},
+                    key=lambda g: (-max(g), -g[0], -g[1]))
+    launches = []
+    for pk, pv in groups:
+        kp = max(pk, pv)
+        if launches and pct > 0 and kp * 100 >= launches[-1][0] * pct:
+            launches[-1] = (launches[-1][0], False)
+        else:
+            launches.append((kp, pk == pv))
+    return launches
+
+
 def attn_kernel_name(w, k_key, k_val) -> str:
-    """The decode attention kernel the library launches for this shape (one launch per
-    distinct (key, value) padded k in the batch)."""
+    """The decode attention kernel the library launches for this shape."""
     g = w.n_q_heads // w.n_kv_heads
-    asym = any(kpad(a) != kpad(b) for a, b in zip(k_key, k_val))
-    note = ("; keys and values with different k_pad: specialised on the larger, each role "
-            "at its own page size" if asym else "")
+    asym = not all(same for _, same in attention_launches(k_key, k_val))
+    note = ("; launches mixing k_pad (keys and values, or merged sequences): specialised on "
+            "the largest, each role and sequence at its own page size" if asym else "")
     if w.dtype == "f16" and g > 1 and g % 2 == 0:
         hpw = 8 if g % 8 == 0 else 4 if g % 4 == 0 else 2
         return (f"attn_gqa_kernel ({hpw} query heads per wave, sparse split-K + dense buffer"
@@ -119,7 +137,7 @@ def attn_kernel_name(w, k_key, k_val) -> str:
 
 
 def launches_per_step(k_key, k_val) -> int:
-    return len({(kpad(a), kpad(b)) for a, b in zip(k_key, k_val)})
+    return len(attention_launches(k_key, k_val))
 
 
 def time_change_k(swan, torch, w, cache, ks, kvs, k_new, esize, reps=5):

@@ -15,6 +15,7 @@
 //   merge_kernel   log-sum-exp merge of the partials, then o = o_hat . P_VO^T
 //                  (the inverse rotation that Sec. 4.2 absorbs into W_O)
 // The sparse attention wave itself is described in decode_mha.h.
+#include <cstdlib>
 #include <mutex>
 
 #include "decode_mha.h"
@@ -170,9 +171,14 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
     e = hipEventRecord(a.prof_start, a.stream);
     if (e != hipSuccess) return e;
   }
-  // sequences grouped by (k_pad of the keys, k_pad of the values), largest
-  // first: one launch per group, specialised on its k_pad, or on the larger of
-  // the two when they differ
+  // sequences grouped by (k_pad of the keys, k_pad of the values); then, from
+  // the largest k_pad down, a group joins the launch before it when its k_pad
+  // is at least kMergePct % of that launch's (two thirds: the spare groups then
+  // add at most half again the compute of its pages, which the HBM time still
+  // covers, and fewer launches share the GPU more evenly).  A launch whose
+  // sequences all have its k_pad for both roles runs the kernels specialised
+  // on it; any other runs the instances for different k_pad (spare groups) at
+  // the launch's largest.
   SeqGroup groups[SWAN_MAX_BATCH];
   int kp8k[SWAN_MAX_BATCH], kp8v[SWAN_MAX_BATCH];
   uint32_t present[kD / 8 + 1] = {};  // bit v of present[k]: some sequence has (k, v)
@@ -194,24 +200,58 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
       kp8v[ng] = pv;
       ++ng;
     }
-  auto launch_one = [&](const DecodeLaunch& ai, int i) {
-    if (kp8k[i] == kp8v[i]) return launch_group<T>(ai, groups[i], kp8k[i]);
-    const int kp8 = kp8k[i] > kp8v[i] ? kp8k[i] : kp8v[i];
-    return decode_heads_per_wave(ai.dtype, ai.Hq, ai.Hkv) > 1
-               ? launch_attn_gqa_asym(ai, groups[i], kp8)
-               : launch_attn_asym(ai, groups[i], kp8);
+  static const int kMergePct = [] {
+    const char* s = getenv("SWAN_MERGE_PCT");  // tuning override; 0 merges nothing
+    return s ? atoi(s) : 66;
+  }();
+  struct Launch {
+    SeqGroup g;
+    int kp8;
+    bool sym;  // every sequence has k_pad 8 kp8 for keys and values
   };
-  SideStreams* ss = ng > 1 ? side_streams(a.stream) : nullptr;
+  Launch ls[SWAN_MAX_BATCH];
+  bool used[SWAN_MAX_BATCH] = {};
+  int nl = 0;
+  for (int done = 0; done < ng; ++done) {
+    int best = -1, bkp = 0;  // the largest k_pad left (ties: first in group order)
+    for (int i = 0; i < ng; ++i) {
+      const int kp = kp8k[i] > kp8v[i] ? kp8k[i] : kp8v[i];
+      if (!used[i] && kp > bkp) {
+        best = i;
+        bkp = kp;
+      }
+    }
+    used[best] = true;
+    const bool sym = kp8k[best] == kp8v[best];
+    if (nl > 0 && kMergePct > 0 && bkp * 100 >= ls[nl - 1].kp8 * kMergePct) {
+      Launch& l = ls[nl - 1];
+      for (int j = 0; j < groups[best].n; ++j) l.g.seq[l.g.n++] = groups[best].seq[j];
+      if (groups[best].n_splits > l.g.n_splits) l.g.n_splits = groups[best].n_splits;
+      l.sym = false;
+    } else {
+      ls[nl].g = groups[best];
+      ls[nl].kp8 = bkp;
+      ls[nl].sym = sym;
+      ++nl;
+    }
+  }
+  auto launch_one = [&](const DecodeLaunch& ai, int i) {
+    if (ls[i].sym) return launch_group<T>(ai, ls[i].g, ls[i].kp8);
+    return decode_heads_per_wave(ai.dtype, ai.Hq, ai.Hkv) > 1
+               ? launch_attn_gqa_asym(ai, ls[i].g, ls[i].kp8)
+               : launch_attn_asym(ai, ls[i].g, ls[i].kp8);
+  };
+  SideStreams* ss = nl > 1 ? side_streams(a.stream) : nullptr;
   if (!ss) {  // one launch, or no side streams: back to back on the caller's stream
-    for (int i = 0; i < ng; ++i)
+    for (int i = 0; i < nl; ++i)
       if ((e = launch_one(a, i)) != hipSuccess) return e;
   } else {
     std::lock_guard<std::mutex> lk(ss->mu);
-    const int nside = ng - 1 < kSideStreams ? ng - 1 : kSideStreams;
+    const int nside = nl - 1 < kSideStreams ? nl - 1 : kSideStreams;
     if ((e = hipEventRecord(ss->fork, a.stream)) != hipSuccess) return e;
     for (int j = 0; j < nside; ++j)
       if ((e = hipStreamWaitEvent(ss->s[j], ss->fork, 0)) != hipSuccess) return e;
-    for (int i = 0; i < ng; ++i) {
+    for (int i = 0; i < nl; ++i) {
       DecodeLaunch ai = a;
       const int lane = i % (nside + 1);  // 0: the caller's stream
       if (lane > 0) ai.stream = ss->s[lane - 1];
