@@ -15,11 +15,12 @@
 // k_pad; lane t owns token t of the page.  The kernel is specialised on the
 // source k_pad, so a lane holds its token's k_pad values and indices in
 // registers, loaded with one coalesced 16-byte (8-byte for E4M3) load per
-// chunk.  Lowering finds the k'-th largest magnitude key by a bitwise search,
-// counting the keys at or above a candidate several at a time with packed
-// integer arithmetic on the stored words; the entries are then walked in index
-// order.  The destination page is assembled in LDS and written with 16-byte
-// stores.
+// chunk.  Raising and copying store those chunks back in place, then the new
+// padding, straight from registers.  Lowering finds the k'-th largest
+// magnitude key by a bitwise search, counting the keys at or above a candidate
+// several at a time with packed integer arithmetic on the stored words; the
+// entries are then walked in index order, the destination page is assembled
+// in LDS and written with 16-byte stores.
 #include <utility>
 
 #include "swan_device.h"
@@ -89,8 +90,9 @@ __device__ __forceinline__ void write_val(char* page, int off, uint32_t v) {
 }
 
 // Grid: nsel * Hkv * max_pages waves over the selected sequences, whose source
-// k_pad is KPS8 * 8.  Dynamic LDS: the largest destination page of the launch.
-template <typename F, int KPS8>
+// k_pad is KPS8 * 8 and whose k is raised or kept (kRaise) or lowered.  Dynamic
+// LDS (lowering): the largest destination page of the launch.
+template <typename F, int KPS8, bool kRaise>
 __global__ __launch_bounds__(64) void change_k_kernel(ChangeKLaunch a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   using MK = MagKey<F>;
@@ -140,12 +142,72 @@ __global__ __launch_bounds__(64) void change_k_kernel(ChangeKLaunch a) {
   }
   const bool valid = p * kPage + lane < S;
 
-  // the k'-th largest key (lowering): the largest tau with at least kd keys >= tau.
-  // The padding entries hold +0 (key 0) and every candidate is >= 1, so they
-  // never count.  Raising or copying keeps every entry: tau = 0 and all ties.
+  if constexpr (kRaise) {
+    // Raising or copying keeps every pair in place.  The source's padding already
+    // holds the lowest dims not kept, in ascending order, and so do the
+    // destination's first padding slots, so the destination starts with the
+    // source page's entries; slots from the source k_pad on take value 0 at the
+    // next lowest dims not among the source's indices.  Each lane writes its own
+    // chunks, so no page is staged.
+    const int nvc_dst = kpd * VB / CB;
+#pragma unroll
+    for (int c = 0; c < NVC; ++c) {
+      char* o = dp + c * 64 * CB + lane * CB;
+      if constexpr (CB == 16) {
+        const u32x4 v = valid ? u32x4{w[c * WPC], w[c * WPC + 1], w[c * WPC + 2], w[c * WPC + 3]}
+                              : u32x4{0u, 0u, 0u, 0u};
+        *(u32x4*)o = v;
+      } else {
+        *(u32x2*)o = valid ? u32x2{w[c * WPC], w[c * WPC + 1]} : u32x2{0u, 0u};
+      }
+    }
+    for (int c = NVC; c < nvc_dst; ++c) {
+      char* o = dp + c * 64 * CB + lane * CB;
+      if constexpr (CB == 16) *(u32x4*)o = u32x4{0u, 0u, 0u, 0u};
+      else *(u32x2*)o = u32x2{0u, 0u};
+    }
+    char* di = dp + 64 * kpd * VB;
+#pragma unroll
+    for (int g = 0; g < KPS8; ++g)
+      *(u32x2*)(di + g * 512 + lane * 8) = valid ? u32x2{ix[2 * g], ix[2 * g + 1]} : u32x2{0u, 0u};
+    if (kpd > KPS) {  // uniform
+      // the source's dims (indices are < 128 and distinct in a valid cache, so at
+      // least kpd - KPS dims are free)
+      uint64_t m0 = 0, m1 = 0;
+#pragma unroll
+      for (int e = 0; e < KPS; ++e) {
+        const uint32_t d = (ix[e / 4] >> ((e % 4) * 8)) & 0x7Fu;
+        const uint64_t bit = 1ull << (d & 63);
+        m0 |= d < 64 ? bit : 0ull;
+        m1 |= d < 64 ? 0ull : bit;
+      }
+      uint64_t f0 = ~m0, f1 = ~m1;
+      for (int g = KPS8; g < kpd / 8; ++g) {
+        uint32_t lo = 0u, hi = 0u;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          uint32_t d;
+          if (f0 != 0ull) {
+            d = (uint32_t)__builtin_ctzll(f0);
+            f0 &= f0 - 1ull;
+          } else {
+            d = 64u + (uint32_t)__builtin_ctzll(f1);
+            f1 &= f1 - 1ull;
+          }
+          if (u < 4) lo |= d << (8 * u);
+          else hi |= d << (8 * (u - 4));
+        }
+        *(u32x2*)(di + g * 512 + lane * 8) = valid ? u32x2{lo, hi} : u32x2{0u, 0u};
+      }
+    }
+    return;
+  } else {
+  // the k'-th largest key: the largest tau with at least kd keys >= tau.  The
+  // padding entries hold +0 (key 0) and every candidate is >= 1, so they never
+  // count.
   uint32_t tau = 0;
-  int need_eq = KPS;
-  if (kd < ks) {
+  int need_eq;
+  {
     uint32_t pk[NW];
 #pragma unroll
     for (int i = 0; i < NW; ++i) pk[i] = MK::prep(w[i]);
@@ -168,7 +230,7 @@ __global__ __launch_bounds__(64) void change_k_kernel(ChangeKLaunch a) {
   }
 
   // kept entries in index order; u0..u3 mark the dims they use (for the padding)
-  const bool pad = kpd > (kd < ks ? kd : ks);
+  const bool pad = kpd > kd;
   const int kv = valid ? ks : 0;
   uint32_t u0 = 0u, u1 = 0u, u2 = 0u, u3 = 0u;
   int j = 0;
@@ -211,54 +273,63 @@ __global__ __launch_bounds__(64) void change_k_kernel(ChangeKLaunch a) {
   __syncthreads();
   for (int64_t off = lane * 16; off < pbd; off += 64 * 16)
     *(u32x4*)(dp + off) = *(const u32x4*)(lds + off);
+  }
 }
 
-template <typename F, int KPS8>
+template <typename F, int KPS8, bool kRaise>
 static hipError_t launch_sel(const ChangeKLaunch& a, size_t lds_bytes) {
-  hipError_t e = hipFuncSetAttribute((const void*)change_k_kernel<F, KPS8>,
+  hipError_t e = hipFuncSetAttribute((const void*)change_k_kernel<F, KPS8, kRaise>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
   if (e != hipSuccess) return e;
   const dim3 grid(a.nsel * a.Hkv * a.max_pages);
-  hipLaunchKernelGGL((change_k_kernel<F, KPS8>), grid, dim3(64), lds_bytes, a.stream, a);
+  hipLaunchKernelGGL((change_k_kernel<F, KPS8, kRaise>), grid, dim3(64), lds_bytes, a.stream, a);
   return hipGetLastError();
 }
 
 template <typename F, int... Is>
-static hipError_t dispatch_kps8(int kps8, const ChangeKLaunch& a, size_t lds,
+static hipError_t dispatch_kps8(int kps8, bool raise, const ChangeKLaunch& a, size_t lds,
                                 std::integer_sequence<int, Is...>) {
   hipError_t e = hipErrorInvalidValue;
-  ((kps8 == Is + 1 ? (e = launch_sel<F, Is + 1>(a, lds), 0) : 0), ...);
+  ((kps8 == Is + 1 ? (e = raise ? launch_sel<F, Is + 1, true>(a, lds)
+                                : launch_sel<F, Is + 1, false>(a, lds),
+                      0)
+                   : 0),
+   ...);
   return e;
 }
 
-// One launch per distinct source k_pad among the sequences.
+// One launch per source k_pad and direction (raised or kept, lowered) among the
+// sequences.
 hipError_t launch_change_k(const ChangeKLaunch& in) {
   const int vb = in.dtype == SWAN_F32 ? 4 : in.dtype == SWAN_F16 ? 2 : 1;
   uint32_t present = 0;
   for (int b = 0; b < in.B; ++b) present |= 1u << (kpad_of(in.k_src[b]) / 8 - 1);
   for (int kps8 = 1; kps8 <= 16; ++kps8) {
     if (!(present & (1u << (kps8 - 1)))) continue;
-    ChangeKLaunch a = in;
-    a.nsel = 0;
-    a.max_pages = 0;
-    size_t lds = 16;
-    for (int b = 0; b < in.B; ++b) {
-      if (kpad_of(in.k_src[b]) / 8 != kps8) continue;
-      a.sel[a.nsel++] = b;
-      const int S = in.len[b] > in.bb ? in.len[b] - in.bb : 0;
-      if (pages_for(S) > a.max_pages) a.max_pages = pages_for(S);
-      const size_t n = (size_t)page_bytes_of(vb, in.k_dst[b]);
-      if (n > lds) lds = n;
+    for (int raise = 0; raise < 2; ++raise) {
+      ChangeKLaunch a = in;
+      a.nsel = 0;
+      a.max_pages = 0;
+      size_t lds = 16;
+      for (int b = 0; b < in.B; ++b) {
+        if (kpad_of(in.k_src[b]) / 8 != kps8 || (in.k_dst[b] >= in.k_src[b]) != (raise != 0))
+          continue;
+        a.sel[a.nsel++] = b;
+        const int S = in.len[b] > in.bb ? in.len[b] - in.bb : 0;
+        if (pages_for(S) > a.max_pages) a.max_pages = pages_for(S);
+        const size_t n = raise ? 0 : (size_t)page_bytes_of(vb, in.k_dst[b]);
+        if (n > lds) lds = n;
+      }
+      if (a.max_pages == 0) continue;
+      hipError_t e;
+      if (in.dtype == SWAN_F16)
+        e = dispatch_kps8<_Float16>(kps8, raise, a, lds, std::make_integer_sequence<int, 16>{});
+      else if (in.dtype == SWAN_F16_E4M3)
+        e = dispatch_kps8<E4M3V>(kps8, raise, a, lds, std::make_integer_sequence<int, 16>{});
+      else
+        e = dispatch_kps8<float>(kps8, raise, a, lds, std::make_integer_sequence<int, 16>{});
+      if (e != hipSuccess) return e;
     }
-    if (a.max_pages == 0) continue;
-    hipError_t e;
-    if (in.dtype == SWAN_F16)
-      e = dispatch_kps8<_Float16>(kps8, a, lds, std::make_integer_sequence<int, 16>{});
-    else if (in.dtype == SWAN_F16_E4M3)
-      e = dispatch_kps8<E4M3V>(kps8, a, lds, std::make_integer_sequence<int, 16>{});
-    else
-      e = dispatch_kps8<float>(kps8, a, lds, std::make_integer_sequence<int, 16>{});
-    if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
