@@ -7,7 +7,7 @@ head, so the values enter the cache already rotated and the attention output
 leaves it rotated, straight into W_O_hat (Lemma 2).
 
 One call with n new tokens per sequence, on the current stream:
-  q, k, v_hat = x . W_Q, x . W_K, x . W_V_hat    dense GEMMs (torch: the GEMM library)
+  [q | k | v_hat] = x . [W_Q | W_K | W_V_hat]    one dense GEMM (torch: the GEMM library)
   swan_rope on q and k at each sequence's next positions
   swan_compress_append(k, v_hat, P_QK, P_VO = NULL)
   for a decode step (n = 1): swan_decode_attention(q, P_QK, P_VO = NULL) -> o_hat,
@@ -33,6 +33,8 @@ class SwanAttentionLayer:
         """W_q [hidden][n_heads*128], W_k and W_v [hidden][n_kv*128], W_o
         [n_heads*128][hidden] (float16 or float32, cuda); P_qk, P_vo [n_kv][128][128]
         float32 (swan_calibrate_rotation of post-RoPE keys and of values)."""
+        import torch
+
         d = HEAD_DIM
         self.n_heads, self.n_kv_heads = n_heads, n_kv_heads
         self.rope_base = float(rope_base)
@@ -47,9 +49,8 @@ class SwanAttentionLayer:
             Wv[:, h * d:(h + 1) * d] = Wv[:, h * d:(h + 1) * d] @ P[h]
         for hq in range(n_heads):
             Wo[hq * d:(hq + 1) * d, :] = P[hq // G].T @ Wo[hq * d:(hq + 1) * d, :]
-        self.W_q = W_q.contiguous()
-        self.W_k = W_k.contiguous()
-        self.W_v_hat = Wv.to(self.dtype).contiguous()
+        # the three projections as one GEMM: [W_Q | W_K | W_V_hat], [hidden][(n_q + 2 n_kv) 128]
+        self.W_qkv = torch.cat([W_q, W_k, Wv.to(self.dtype)], dim=1).contiguous()
         self.W_o_hat = Wo.to(self.dtype).contiguous()
         self.cache = swan.SwanCache(batch, n_heads, n_kv_heads, buffer_tokens, capacity,
                                     k_active, self.dtype, W_q.device,
@@ -61,9 +62,11 @@ class SwanAttentionLayer:
         B, n, _ = x.shape
         d = HEAD_DIM
         pos0 = list(self.cache.seq_len)
-        q = (x @ self.W_q).view(B, n, self.n_heads, d).transpose(1, 2).contiguous()
-        k = (x @ self.W_k).view(B, n, self.n_kv_heads, d).transpose(1, 2).contiguous()
-        v = (x @ self.W_v_hat).view(B, n, self.n_kv_heads, d).transpose(1, 2).contiguous()
+        qkv = x @ self.W_qkv
+        nq, nkv = self.n_heads * d, self.n_kv_heads * d
+        q = qkv[..., :nq].reshape(B, n, self.n_heads, d).transpose(1, 2).contiguous()
+        k = qkv[..., nq:nq + nkv].reshape(B, n, self.n_kv_heads, d).transpose(1, 2).contiguous()
+        v = qkv[..., nq + nkv:].reshape(B, n, self.n_kv_heads, d).transpose(1, 2).contiguous()
         swan.rope(q, pos0, self.rope_base, out=q)
         swan.rope(k, pos0, self.rope_base, out=k)
         return q, k, v
