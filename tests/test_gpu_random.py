@@ -1,6 +1,8 @@
 """Randomised parity sweep: many small caches with seeded random shapes (batch, heads,
-GQA group, lengths, buffer, per-sequence k, storage, E4M3 values, append chunking),
-each compared with the oracle: pages and ring bit-exact, outputs within 2e-3."""
+GQA group, lengths, buffer, per-sequence k, values with their own k, storage, E4M3
+values, append chunking, a change of k after the appends), each compared with the
+oracle: pages and ring bit-exact, outputs within 2e-3."""
+import os
 import sys
 
 import numpy as np
@@ -12,7 +14,7 @@ from tests import swan_cases as C
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-3
-N_CASES = 24
+N_CASES = int(os.environ.get("SWAN_RANDOM_CASES", "64"))  # a wider sweep on request
 
 
 def _log(msg):
@@ -31,8 +33,15 @@ def _case(i):
     Ls = [int(x) for x in r.integers(1, 700, B)]
     ks = [int(x) for x in r.integers(1, 129, B)]
     chunking = str(r.choice(["one", "two", "steps"]))
+    # drawn from a stream of their own, so the draws above stay those of earlier versions
+    r2 = si.rng_for(31339, i)
+    kvs = [int(x) for x in r2.integers(1, 129, B)] if r2.random() < 0.4 else None
+    change = None
+    if r2.random() < 0.4:
+        change = ([int(x) for x in r2.integers(1, 129, B)],
+                  [int(x) for x in r2.integers(1, 129, B)] if r2.random() < 0.5 else None)
     return dict(Hkv=Hkv, Hq=Hkv * G, dtype=dtype, values=values, B=B, b=b, Ls=Ls, ks=ks,
-                chunking=chunking)
+                kvs=kvs, change=change, chunking=chunking)
 
 
 @pytest.mark.parametrize("i", range(N_CASES))
@@ -55,8 +64,9 @@ def test_random_cache_matches_oracle(gpu_device, swan_mod, torch_mod, i):
             R = si.haar_orthogonal(si.rng_for(9000, i, h), 128)
             K[bi, h] = si.lowrank_rows(si.rng_for(9001, i, bi, h), Lmax, R).astype(np_dt)
             V[bi, h] = si.lowrank_rows(si.rng_for(9002, i, bi, h), Lmax, R).astype(np_dt)
+    kvs = c["kvs"]
     cache = swan_mod.SwanCache(B, Hq, Hkv, b, max(Lmax - b, 1), ks, C.torch_dtype(c["dtype"]),
-                               gpu_device, sparse_values=c["values"])
+                               gpu_device, sparse_values=c["values"], k_value=kvs)
     tqk = torch.tensor(Pqk, device=gpu_device)
     tvo = torch.tensor(Pvo, device=gpu_device)
     if c["chunking"] == "one":
@@ -75,7 +85,13 @@ def test_random_cache_matches_oracle(gpu_device, swan_mod, torch_mod, i):
     assert cache.seq_len == Ls
     ov = "e4m3" if c["values"] == "e4m3" else "t"
     oc = [[O.compress_block(K[bi, h, :Ls[bi]], V[bi, h, :Ls[bi]], Pqk[h], Pvo[h], b, ks[bi], np_dt,
-                            values=ov) for h in range(Hkv)] for bi in range(B)]
+                            values=ov, k_value=None if kvs is None else kvs[bi])
+           for h in range(Hkv)] for bi in range(B)]
+    if c["change"] is not None:
+        ks1, kvs1 = c["change"]
+        cache.change_k(ks1, kvs1)
+        oc = [[O.change_k_cache(u, ks1[bi], None if kvs1 is None else kvs1[bi]) for u in oc[bi]]
+              for bi in range(B)]
     for bi in range(B):
         h = bi % Hkv
         C.compare_unit(cache, oc[bi][h], bi, h, Ls[bi], np_dt, values=c["values"])
