@@ -119,8 +119,8 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
   const int nsb = a.tab.nsplit[b];
   const int ns = np < nsb ? np : nsb;
   if (split >= ns) return;  // uniform over the block
-  const int pbeg = split_begin(split, ns, np);
-  const int pend = split_begin(split + 1, ns, np);
+  const int pbeg = split_begin(split, ns, np, a.tab.flat[b] != 0);
+  const int pend = split_begin(split + 1, ns, np, a.tab.flat[b] != 0);
   // the page size and loaded groups of this wave's role
   const int role = kAsym ? wave : 0;
   const int64_t pbytes = page_bytes_of(Fmt<T>::kValBytes, a.tab.kact[role][b]);

@@ -132,8 +132,8 @@ __global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup g) {
   const int nsb = a.tab.nsplit[b];
   const int ns = np < nsb ? np : nsb;
   if (split >= ns) return;
-  const int pbeg = split_begin(split, ns, np);
-  const int pend = split_begin(split + 1, ns, np);
+  const int pbeg = split_begin(split, ns, np, a.tab.flat[b] != 0);
+  const int pend = split_begin(split + 1, ns, np, a.tab.flat[b] != 0);
   UnitPages u;
   u.kbytes = page_bytes_of(Fmt<T>::kValBytes, a.tab.kact[0][b]);
   u.vbytes = kAsym ? page_bytes_of(Fmt<T>::kValBytes, a.tab.kact[1][b]) : u.kbytes;

@@ -111,6 +111,7 @@ void fill_layout(const swan_cache* c, const int32_t* k_active_host, const int32_
     tab.len[b] = 0;
     tab.nnew[b] = 0;
     tab.nsplit[b] = 1;
+    tab.flat[b] = 0;
   }
   for (int r = 0; r < 2; ++r) {
     int64_t off = 0;
@@ -131,7 +132,7 @@ void fill_layout(const swan_cache* c, const int32_t* k_active_host, const int32_
 // size (split_begin), and their count is capped so that every split keeps a
 // page.  Fills nsplit[b] (may be NULL); returns the largest.
 int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t* k_active_host,
-                const int32_t* k_value_host, int32_t* nsplit) {
+                const int32_t* k_value_host, int32_t* nsplit, int8_t* flat = nullptr) {
   auto weight = [&](int b) {
     return swan::kpad_of(k_of(k_active_host, k_value_host, 0, b)) +
            swan::kpad_of(k_of(k_active_host, k_value_host, 1, b));
@@ -150,6 +151,14 @@ int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t*
     const long v = s ? atol(s) : 0;
     return (int64_t)(v > 0 ? v : 256 * 4 * 2);
   }();
+  // A sequence whose shrinking splits the one-page rule cuts to half the count
+  // wanted or fewer is short: its waves would each walk many pages one after
+  // another, so it gets equal splits of flat_pages pages instead.
+  static const int flat_pages = [] {
+    const char* s = getenv("SWAN_FLAT_PAGES");  // tuning override; 0: always shrinking
+    const long v = s ? atol(s) : 4;
+    return (int)(v > 0 ? v : 0);
+  }();
   int64_t per_wave = (total + target_waves - 1) / target_waves;
   if (per_wave < 1) per_wave = 1;
   int ns_max = 1;
@@ -157,11 +166,19 @@ int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t*
     const int S = seq_len_host[b] > c->buffer_tokens ? seq_len_host[b] - c->buffer_tokens : 0;
     const int np = swan::pages_for(S);
     const int64_t work = (int64_t)np * weight(b);
-    int ns = (int)((work + per_wave - 1) / per_wave);
+    const int want = (int)((work + per_wave - 1) / per_wave);
+    int ns = want;
     while (ns > 1 && (int64_t)ns * (ns + 1) / 2 > np) --ns;  // every split keeps a page
+    bool fl = false;
+    if (flat_pages > 0 && 2 * ns <= want) {
+      // short sequence: equal splits of about flat_pages pages instead
+      fl = true;
+      ns = np / flat_pages < want ? np / flat_pages : want;
+    }
     if (ns > swan::kMaxSplits) ns = swan::kMaxSplits;
     if (ns < 1) ns = 1;
     if (nsplit) nsplit[b] = ns;
+    if (flat) flat[b] = fl ? 1 : 0;
     if (ns > ns_max) ns_max = ns;
   }
   return ns_max;
@@ -358,7 +375,8 @@ swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_ho
   swan::DecodeLaunch a;
   int64_t role_bytes[2];
   fill_layout(c, k_active_host, k_value_host, a.tab, role_bytes);
-  const int ns = plan_splits(c, seq_len_host, k_active_host, k_value_host, a.tab.nsplit);
+  const int ns = plan_splits(c, seq_len_host, k_active_host, k_value_host, a.tab.nsplit,
+                            a.tab.flat);
   const size_t need = decode_ws_bytes(c, ns);
   if (!workspace || workspace_bytes < need)
     return fail(SWAN_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, need);

@@ -22,6 +22,7 @@ struct SeqTab {
   int64_t page_off[2][SWAN_MAX_BATCH];  // byte offset of the sequence's first key / value page
   int32_t nnew[SWAN_MAX_BATCH];         // compress: tokens appended to the sequence
   int32_t nsplit[SWAN_MAX_BATCH];       // decode: token splits of the sequence's launch
+  int8_t flat[SWAN_MAX_BATCH];          // decode: 1 = splits of equal size (short sequences)
 };
 
 __host__ __device__ inline int kpad_of(int k) { return (k + 7) & ~7; }
@@ -30,8 +31,11 @@ __host__ __device__ inline int kpad_of(int k) { return (k + 7) & ~7; }
 // shrinking size (weights ns, ns - 1, ..., 1): the grids are split-major, so
 // the longest splits are dispatched first and the last ones are short, which
 // shortens the tail.  Every split has at least one page when
-// ns (ns + 1) / 2 <= np (the planner keeps to that).
-__host__ __device__ inline int split_begin(int s, int ns, int np) {
+// ns (ns + 1) / 2 <= np (the planner keeps to that).  A short sequence, whose
+// pages that rule would leave in a few long splits, is cut into ns equal splits
+// instead (flat; every split has a page when ns <= np).
+__host__ __device__ inline int split_begin(int s, int ns, int np, bool flat = false) {
+  if (flat) return (int)((int64_t)s * np / ns);
   const int64_t before = (int64_t)s * ns - (int64_t)s * (s - 1) / 2;  // sum_{i<s} (ns - i)
   const int64_t total = (int64_t)ns * (ns + 1) / 2;
   return (int)(before * np / total);
