@@ -81,6 +81,7 @@ def test_page_and_cache_sizes():
     (dict(head_dim=64), swan.SWAN_ERR_UNSUPPORTED),
     (dict(buffer_tokens=-1), swan.SWAN_ERR_INVALID_ARG),
     (dict(buffer_tokens=5000), swan.SWAN_ERR_UNSUPPORTED),
+    (dict(buffer_tokens=4097), swan.SWAN_ERR_UNSUPPORTED),  # one past the largest buffer
     (dict(dtype=7), swan.SWAN_ERR_UNSUPPORTED),
     (dict(reserved=1), swan.SWAN_ERR_INVALID_ARG),
     (dict(k_pages=None), swan.SWAN_ERR_INVALID_ARG),
