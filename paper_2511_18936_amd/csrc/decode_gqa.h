@@ -190,13 +190,13 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
       load_page<T, KP8>(vb, vbase + p1 * pbytes, lane, n8);
       gqa_scatter<T, KP8>(va, p * kPage + lane < S, sh, lane);
       __syncthreads();
-      gqa_mfma<GH>(sh, (p - pbeg) & 1, lane, acc);
+      gqa_mfma<GH, T>(sh, (p - pbeg) & 1, lane, acc);
       const int p2 = p + 2 < plast ? p + 2 : plast;
       load_page<T, KP8>(va, vbase + p2 * pbytes, lane, n8);
       if (p + 1 < pend) {
         gqa_scatter<T, KP8>(vb, (p + 1) * kPage + lane < S, sh, lane);
         __syncthreads();
-        gqa_mfma<GH>(sh, (p + 1 - pbeg) & 1, lane, acc);
+        gqa_mfma<GH, T>(sh, (p + 1 - pbeg) & 1, lane, acc);
       }
     }
 #pragma unroll

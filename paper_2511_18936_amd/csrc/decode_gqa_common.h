@@ -14,6 +14,7 @@ typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int kVtStride = 68;    // halves per row of the value tile (64 + pad)
+constexpr int kVt8Stride = 68;   // bytes per row of the E4M3 value tile (64 + pad)
 constexpr int kPtStride = 68;    // halves per row of the probability tile (64 + pad)
 
 // replicas of the GH-head query rows (lane % R): 8 keep the gathers of 8
@@ -59,11 +60,32 @@ __device__ __forceinline__ void gather_scores(const PageRegs<T, KP8>& kr, const 
   }
 }
 
-// value wave, one page: zero the value tile, scatter the kept components
+// value wave, one page: zero the value tile, scatter the kept components.
+// E4M3 values go into a byte tile V8[dims][tokens] of their codes (code 0 is +0),
+// half the bytes to zero and to read back; the MFMA operand read decodes them.
 template <typename T, int KP8, typename Lds>
 __device__ __forceinline__ void gqa_scatter(const PageRegs<T, KP8>& vr, bool valid, Lds& sh,
                                             int lane) {
   wave_lds_fence();  // the previous page's tile reads come first
+  if constexpr (std::is_same<T, E4M3V>::value) {
+    constexpr int kRows = sizeof(sh.vt) / (kVtStride * 2);  // 128, or 129 with the spare row
+    constexpr int kChunks = (kRows * kVt8Stride + 15) / 16;
+    u32x4* z = (u32x4*)sh.vt;
+#pragma unroll
+    for (int c = lane; c < kChunks; c += 64) z[c] = u32x4{0u, 0u, 0u, 0u};
+    wave_lds_fence();
+    if (valid) {
+      uint8_t* vt8 = (uint8_t*)sh.vt + lane;
+#pragma unroll
+      for (int g = 0; g < KP8; ++g) {
+        const u32x2 c = vr.val[g];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          vt8[entry_idx(vr, g, u) * kVt8Stride] = (uint8_t)(((u < 4 ? c.x : c.y) >> (8 * (u & 3))) & 0xFFu);
+      }
+    }
+    return;
+  }
   {
     u32x4* z = (u32x4*)sh.vt;
     constexpr int kChunks = kD * kVtStride * 2 / 16;
@@ -84,7 +106,7 @@ __device__ __forceinline__ void gqa_scatter(const PageRegs<T, KP8>& vr, bool val
 
 // value wave, after the page barrier: rescale, then O += P . V on MFMA
 // (k-steps of 16 tokens, n-tiles of 16 dims)
-template <int GH, typename Lds>
+template <int GH, typename T, typename Lds>
 __device__ __forceinline__ void gqa_mfma(const Lds& sh, int par, int lane, f4* acc) {
   const int row = lane & 15;
   const int kq = 4 * (lane >> 4);
@@ -113,7 +135,17 @@ __device__ __forceinline__ void gqa_mfma(const Lds& sh, int par, int lane, f4* a
     const h4 alo = arow ? *(const h4*)&sh.pt[par][1][rr][16 * ks + kq] : zero;
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt) {
-      const h4 b = *(const h4*)(sh.vt + (16 * nt + row) * kVtStride + 16 * ks + kq);
+      h4 b;
+      if constexpr (std::is_same<T, E4M3V>::value) {
+        typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+        const uint32_t w = *(const uint32_t*)((const uint8_t*)sh.vt +
+                                              (16 * nt + row) * kVt8Stride + 16 * ks + kq);
+        const h2 lo = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 1.0f, false);
+        const h2 hi = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 1.0f, true);
+        b = h4{lo.x, lo.y, hi.x, hi.y};
+      } else {
+        b = *(const h4*)(sh.vt + (16 * nt + row) * kVtStride + 16 * ks + kq);
+      }
       acc[nt] = __builtin_amdgcn_mfma_f32_16x16x16f16(ahi, b, acc[nt], 0, 0, 0);
       acc[nt] = __builtin_amdgcn_mfma_f32_16x16x16f16(alo, b, acc[nt], 0, 0, 0);
     }
