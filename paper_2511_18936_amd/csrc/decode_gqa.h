@@ -74,9 +74,8 @@ __device__ __forceinline__ void gqa_scores(const PageRegs<T, KP8>& kr, bool vali
   if (lane < GH) sh.fr[par][lane] = frl;
 }
 
-// Grid: n * Hq dense-buffer blocks (wave 0 serves one query head), then
-// n * Hkv * (G / GH) * g.n_splits sparse blocks, each for GH query heads of
-// one KV head.  kAsym: keys and values have different k_pad, the larger being
+// Grid: n * Hkv * (G / GH) * g.n_splits sparse blocks, each for GH query heads
+// of one KV head, then n * Hq dense-buffer blocks (wave 0 serves one query head).  kAsym: keys and values have different k_pad, the larger being
 // 8 KP8; each wave then takes its role's page size and loaded groups at run
 // time, the rest being spare groups (load_page), for which q_rep and the value
 // tile get a spare row kSpareRow.
@@ -89,10 +88,13 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
   const int G = a.Hq / a.Hkv;
   const int pstride = a.n_splits + 1;
   int w = blockIdx.x;
-  const int NB = g.n * a.Hq;
-  if (w < NB) {  // dense-buffer block: one wave (scratch: the value tile)
+  const int HC = G / GH;               // head chunks per KV head
+  const int units = g.n * a.Hkv * HC;
+  const int nsparse = units * g.n_splits;
+  if (w >= nsparse) {  // dense-buffer block, after the sparse ones: one wave (scratch: the value tile)
     if (wave != 0) return;
-    const int b = g.seq[w / a.Hq], hq = w % a.Hq, h = hq / G;
+    const int wr = w - nsparse;
+    const int b = g.seq[wr / a.Hq], hq = wr % a.Hq, h = hq / G;
     const int bhq = b * a.Hq + hq;
     const int L = a.tab.len[b];
     const int nb = L < a.bb ? L : a.bb;
@@ -105,9 +107,6 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
                           scratch, scratch + kD, lane, part);
     return;
   }
-  w -= NB;
-  const int HC = G / GH;               // head chunks per KV head
-  const int units = g.n * a.Hkv * HC;
   const int split = w / units;
   const int ui = w % units;
   const int b = g.seq[ui / (a.Hkv * HC)];
