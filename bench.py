@@ -307,7 +307,10 @@ def main():
     kvs = si.k_value_for(w)  # None: values keep the keys' k
     kvs = None if kvs is None else [int(k) for k in kvs]
     kv_list = ks if kvs is None else kvs
-    n_extra = args.warmup + args.steps
+    # warm-up steps, timed steps, then a few steps that also time compress and decode
+    # apart (their events stay out of the timed region)
+    n_detail = min(args.steps, 10)
+    n_extra = args.warmup + args.steps + n_detail
     L0 = w.context - 1  # tokens cached before the first measured step
 
     # ---- rotations (Sec. 4.1.2), on the GPU ----
@@ -364,27 +367,36 @@ def main():
     assert ws.numel() >= ws_need
     out = torch.empty((w.batch, w.n_q_heads, 128), dtype=tdt, device=dev)
 
-    def step(i, evs=None):
-        if evs is not None:
+    def step(i, evs=None, breakdown=False):
+        """One decode step; evs[2] / evs[3] bracket the attention launches (recorded by
+        the library on their stream), and with breakdown evs[0], [1], [4] bracket the
+        compress-append and the whole decode call."""
+        if breakdown:
             evs[0].record()
         cache.append(step_k[i], step_v[i], Pqk, Pvo)
-        if evs is not None:
+        if breakdown:
             evs[1].record()
+        if evs is not None:
             swan.set_profile_events(evs[2], evs[3])
         swan.decode_attention(cache.desc, cache.seq_len, ks, qs[i], Pqk, Pvo, out, ws,
                               k_value=kvs)
         if evs is not None:
             swan.set_profile_events(None, None)
+        if breakdown:
             evs[4].record()
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
-    for e in evs:  # torch creates its events on first record; the library re-records these
-        e[2].record()
-        e[3].record()
+    def events(n):
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(n)]
+        for e in evs:  # torch creates its events on first record; the library re-records these
+            e[2].record()
+            e[3].record()
+        return evs
+
+    evs = events(args.steps)
     lens = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -393,11 +405,16 @@ def main():
         lens.append(list(cache.seq_len))
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    # untimed steps for the compress / decode breakdown
+    devs = events(n_detail)
+    for j in range(n_detail):
+        step(args.warmup + args.steps + j, devs[j], breakdown=True)
+    torch.cuda.synchronize()
 
     wall = t1 - t0
-    t_comp = [e[0].elapsed_time(e[1]) * 1e-3 for e in evs]
+    t_comp = [e[0].elapsed_time(e[1]) * 1e-3 for e in devs]
     t_attn = [e[2].elapsed_time(e[3]) * 1e-3 for e in evs]
-    t_dec = [e[1].elapsed_time(e[4]) * 1e-3 for e in evs]
+    t_dec = [e[1].elapsed_time(e[4]) * 1e-3 for e in devs]
     bytes_attn = [attention_bytes(w, L, ks, kv_list, esize) for L in lens]
     attn_avg = float(np.mean(t_attn))
     bytes_avg = float(np.mean(bytes_attn))
