@@ -29,7 +29,9 @@
  *    each, kept until the process ends), forked from and joined back into
  *    `stream` with events, so the call orders with `stream` like any other.
  *    Calls are made with the stream's device current; otherwise the launches
- *    run one after another on `stream`.
+ *    run one after another on `stream`.  It also holds, per GPU, the fixed
+ *    scratch array of swan_decode_attention_noalloc (a device global, not an
+ *    allocation).
  *  - All arguments are validated on the host before anything is enqueued, so
  *    a non-OK status means nothing was written.  Errors never abort, throw or
  *    exit; swan_last_error() returns a message for the calling thread.
@@ -213,6 +215,29 @@ swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_ho
                                   const void* q, const float* P_qk, const float* P_vo,
                                   float scale, void* out, void* workspace,
                                   size_t workspace_bytes, void* stream);
+
+/*
+ * swan_decode_attention without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Arguments, results and errors are those
+ * of swan_decode_attention.  The workspace (rotated queries and split
+ * partials) is instead a device array inside this library: SWAN_NOALLOC_SCRATCH_BYTES
+ * (16 MiB) per GPU, set up on the first call on a device (with the stream's
+ * device current) and held until the process ends.  A batch whose
+ * swan_decode_workspace_bytes exceeds it is rejected with SWAN_ERR_WORKSPACE
+ * before anything is enqueued.  The call allocates nothing: no hipMalloc, no
+ * stream or event creation (all launches go to `stream`, also for a batch that
+ * mixes k_pad).  Every call on one GPU shares that GPU's array, so calls that
+ * can overlap on one GPU (other streams, other threads) race and must be
+ * ordered by the caller; calls on one stream are ordered by it.
+ * `stream` must belong to the current device (SWAN_ERR_INVALID_ARG otherwise).
+ */
+#define SWAN_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+swan_status swan_decode_attention_noalloc(const swan_cache* c, const int32_t* seq_len_host,
+                                          const int32_t* k_active_host,
+                                          const int32_t* k_value_host, const void* q,
+                                          const float* P_qk, const float* P_vo, float scale,
+                                          void* out, void* stream);
 
 /*
  * Rotary position embedding, for the query and key rows of a layer before the

@@ -241,7 +241,7 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
                ? launch_attn_gqa_asym(ai, ls[i].g, ls[i].kp8)
                : launch_attn_asym(ai, ls[i].g, ls[i].kp8);
   };
-  SideStreams* ss = nl > 1 ? side_streams(a.stream) : nullptr;
+  SideStreams* ss = nl > 1 && !a.one_stream ? side_streams(a.stream) : nullptr;
   if (!ss) {  // one launch, or no side streams: back to back on the caller's stream
     for (int i = 0; i < nl; ++i)
       if ((e = launch_one(a, i)) != hipSuccess) return e;

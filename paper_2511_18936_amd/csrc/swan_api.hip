@@ -7,10 +7,21 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 
 #include "swan.h"
 #include "swan_internal.h"
+
+// ---------------------------------------------------------------------------
+// Scratch of swan_decode_attention_noalloc: the decode workspace (q_hat, then
+// the partials) in a device array of fixed size, one copy per GPU, held until
+// the process ends.  Host code only ever uses the address that
+// hipGetSymbolAddress returns for the current device: the array's name is a
+// host-side stand-in, not a device address.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = SWAN_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kScratchBytes];
 
 namespace {
 
@@ -199,13 +210,117 @@ swan_status hip_status(hipError_t e, const char* what) {
   return fail(SWAN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[swan::kMaxDevices] = {};
+
+// The scratch array's address on the device of `stream` (set up once per
+// device, with that device current).
+swan_status scratch_for_stream(hipStream_t stream, void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= swan::kMaxDevices)
+    return fail(SWAN_ERR_UNSUPPORTED, "device %d: the scratch table holds %d devices", dev,
+                swan::kMaxDevices);
+  if (stream) {
+    hipDevice_t sdev = -1;
+    e = hipStreamGetDevice(stream, &sdev);
+    if (e != hipSuccess) return hip_status(e, "hipStreamGetDevice");
+    if (sdev != dev)
+      return fail(SWAN_ERR_INVALID_ARG,
+                  "the stream belongs to device %d but device %d is current", (int)sdev, dev);
+  }
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+    if (!p || ((uintptr_t)p & 255) != 0)
+      return fail(SWAN_ERR_HIP, "scratch array at an unusable address");
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return SWAN_OK;
+}
+
+// Both decode entry points: validation, split plan, launches.  no_alloc: the
+// workspace is this library's scratch array (looked up after every host check
+// has passed), a plan that needs more than the array is rejected, and the
+// launches stay on `stream` (creating the side streams could allocate).
+swan_status decode_impl(const swan_cache* c, const int32_t* seq_len_host,
+                        const int32_t* k_active_host, const int32_t* k_value_host, const void* q,
+                        const float* P_qk, const float* P_vo, float scale, void* out,
+                        void* workspace, size_t workspace_bytes, void* stream, bool no_alloc) {
+  swan_status st = check_cache_shape(c);
+  if (st != SWAN_OK) return st;
+  if ((st = check_k(c, k_active_host, k_value_host)) != SWAN_OK) return st;
+  if ((st = check_cache_ptrs(c)) != SWAN_OK) return st;
+  if (!seq_len_host) return fail(SWAN_ERR_INVALID_ARG, "seq_len_host is NULL");
+  if (!q || !out || !P_qk) return fail(SWAN_ERR_INVALID_ARG, "q / out / P_qk is NULL");
+  if ((((uintptr_t)P_qk | (uintptr_t)P_vo) & 15) != 0)
+    return fail(SWAN_ERR_INVALID_ARG, "P_qk / P_vo must be 16-byte aligned");
+  for (int b = 0; b < c->batch; ++b) {
+    const int64_t L = seq_len_host[b];
+    if (L < 1) return fail(SWAN_ERR_INVALID_ARG, "seq_len[%d] = %lld: need L >= 1", b, (long long)L);
+    if (L - c->buffer_tokens > c->sparse_capacity)
+      return fail(SWAN_ERR_CAPACITY, "sequence %d has %lld sparse tokens, capacity %d", b,
+                  (long long)(L - c->buffer_tokens), c->sparse_capacity);
+  }
+  if (!(scale == scale) || isinf(scale)) return fail(SWAN_ERR_INVALID_ARG, "scale is not finite");
+  swan::DecodeLaunch a;
+  int64_t role_bytes[2];
+  fill_layout(c, k_active_host, k_value_host, a.tab, role_bytes);
+  const int ns = plan_splits(c, seq_len_host, k_active_host, k_value_host, a.tab.nsplit,
+                            a.tab.flat);
+  const size_t need = decode_ws_bytes(c, ns);
+  if (no_alloc) {
+    if (need > kScratchBytes)
+      return fail(SWAN_ERR_WORKSPACE,
+                  "this batch needs %zu bytes of decode scratch; swan_decode_attention_noalloc "
+                  "holds %zu (use swan_decode_attention with a workspace)", need, kScratchBytes);
+    const swan_status sst = scratch_for_stream((hipStream_t)stream, &workspace);
+    if (sst != SWAN_OK) return sst;
+    workspace_bytes = kScratchBytes;
+  }
+  if (!workspace || workspace_bytes < need)
+    return fail(SWAN_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, need);
+  if (((uintptr_t)workspace & 255) != 0)
+    return fail(SWAN_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  for (int b = 0; b < c->batch; ++b) a.tab.len[b] = seq_len_host[b];
+  const float sc = scale > 0.f ? scale : 1.0f / sqrtf((float)c->head_dim);
+  a.q = q;
+  a.P_qk = P_qk;
+  a.P_vo = P_vo;
+  a.out = out;
+  a.k_pages = c->k_pages;
+  a.v_pages = c->v_pages;
+  a.k_ring = c->k_ring;
+  a.v_ring = c->v_ring;
+  const size_t units = (size_t)c->batch * c->n_q_heads;
+  a.qhat = (float*)workspace;
+  a.part = (float*)((char*)workspace + round256(units * swan::kD * sizeof(float)));
+  a.B = c->batch;
+  a.Hq = c->n_q_heads;
+  a.Hkv = c->n_kv_heads;
+  a.bb = c->buffer_tokens;
+  a.n_pages_cap = swan::pages_for(c->sparse_capacity);
+  a.n_splits = ns;
+  a.qmult = sc * 1.4426950408889634f;
+  a.dtype = c->dtype;
+  a.stream = (hipStream_t)stream;
+  a.prof_start = g_prof_start;
+  a.prof_stop = g_prof_stop;
+  a.one_stream = no_alloc;
+  return hip_status(swan::launch_decode(a), "decode launch");
+}
+
 }  // namespace
 
 extern "C" {
 
 const char* swan_last_error(void) { return g_last_error.c_str(); }
 
-int32_t swan_version(void) { return 202; }
+int32_t swan_version(void) { return 203; }
 
 swan_status swan_page_bytes(int32_t dtype, int32_t k_active, size_t* bytes) {
   if (!bytes) return fail(SWAN_ERR_INVALID_ARG, "bytes is NULL");
@@ -356,57 +471,17 @@ swan_status swan_decode_attention(const swan_cache* c, const int32_t* seq_len_ho
                                   const void* q, const float* P_qk, const float* P_vo, float scale,
                                   void* out, void* workspace, size_t workspace_bytes,
                                   void* stream) {
-  swan_status st = check_cache_shape(c);
-  if (st != SWAN_OK) return st;
-  if ((st = check_k(c, k_active_host, k_value_host)) != SWAN_OK) return st;
-  if ((st = check_cache_ptrs(c)) != SWAN_OK) return st;
-  if (!seq_len_host) return fail(SWAN_ERR_INVALID_ARG, "seq_len_host is NULL");
-  if (!q || !out || !P_qk) return fail(SWAN_ERR_INVALID_ARG, "q / out / P_qk is NULL");
-  if ((((uintptr_t)P_qk | (uintptr_t)P_vo) & 15) != 0)
-    return fail(SWAN_ERR_INVALID_ARG, "P_qk / P_vo must be 16-byte aligned");
-  for (int b = 0; b < c->batch; ++b) {
-    const int64_t L = seq_len_host[b];
-    if (L < 1) return fail(SWAN_ERR_INVALID_ARG, "seq_len[%d] = %lld: need L >= 1", b, (long long)L);
-    if (L - c->buffer_tokens > c->sparse_capacity)
-      return fail(SWAN_ERR_CAPACITY, "sequence %d has %lld sparse tokens, capacity %d", b,
-                  (long long)(L - c->buffer_tokens), c->sparse_capacity);
-  }
-  if (!(scale == scale) || isinf(scale)) return fail(SWAN_ERR_INVALID_ARG, "scale is not finite");
-  swan::DecodeLaunch a;
-  int64_t role_bytes[2];
-  fill_layout(c, k_active_host, k_value_host, a.tab, role_bytes);
-  const int ns = plan_splits(c, seq_len_host, k_active_host, k_value_host, a.tab.nsplit,
-                            a.tab.flat);
-  const size_t need = decode_ws_bytes(c, ns);
-  if (!workspace || workspace_bytes < need)
-    return fail(SWAN_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, need);
-  if (((uintptr_t)workspace & 255) != 0)
-    return fail(SWAN_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
-  for (int b = 0; b < c->batch; ++b) a.tab.len[b] = seq_len_host[b];
-  const float sc = scale > 0.f ? scale : 1.0f / sqrtf((float)c->head_dim);
-  a.q = q;
-  a.P_qk = P_qk;
-  a.P_vo = P_vo;
-  a.out = out;
-  a.k_pages = c->k_pages;
-  a.v_pages = c->v_pages;
-  a.k_ring = c->k_ring;
-  a.v_ring = c->v_ring;
-  const size_t units = (size_t)c->batch * c->n_q_heads;
-  a.qhat = (float*)workspace;
-  a.part = (float*)((char*)workspace + round256(units * swan::kD * sizeof(float)));
-  a.B = c->batch;
-  a.Hq = c->n_q_heads;
-  a.Hkv = c->n_kv_heads;
-  a.bb = c->buffer_tokens;
-  a.n_pages_cap = swan::pages_for(c->sparse_capacity);
-  a.n_splits = ns;
-  a.qmult = sc * 1.4426950408889634f;
-  a.dtype = c->dtype;
-  a.stream = (hipStream_t)stream;
-  a.prof_start = g_prof_start;
-  a.prof_stop = g_prof_stop;
-  return hip_status(swan::launch_decode(a), "decode launch");
+  return decode_impl(c, seq_len_host, k_active_host, k_value_host, q, P_qk, P_vo, scale, out,
+                     workspace, workspace_bytes, stream, false);
+}
+
+swan_status swan_decode_attention_noalloc(const swan_cache* c, const int32_t* seq_len_host,
+                                          const int32_t* k_active_host,
+                                          const int32_t* k_value_host, const void* q,
+                                          const float* P_qk, const float* P_vo, float scale,
+                                          void* out, void* stream) {
+  return decode_impl(c, seq_len_host, k_active_host, k_value_host, q, P_qk, P_vo, scale, out,
+                     nullptr, 0, stream, true);
 }
 
 swan_status swan_change_k(const swan_cache* src, const int32_t* k_active_src,

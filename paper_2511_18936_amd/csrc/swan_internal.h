@@ -68,6 +68,7 @@ struct DecodeLaunch {
   hipStream_t stream;
   hipEvent_t prof_start;  // optional events around the attention launches
   hipEvent_t prof_stop;
+  bool one_stream;        // every launch on `stream` (no library side streams)
 };
 hipError_t launch_decode(const DecodeLaunch& a);
 constexpr int kSideStreams = 3;  // extra streams for the launches of a mixed-k batch

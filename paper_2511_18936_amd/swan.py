@@ -32,9 +32,10 @@ PAGE_TOKENS = 64
 EXPORTED = (
     "swan_last_error", "swan_version", "swan_page_bytes", "swan_cache_bytes",
     "swan_calibrate_workspace_bytes", "swan_calibrate_rotation", "swan_compress_append",
-    "swan_decode_workspace_bytes", "swan_decode_attention", "swan_change_k", "swan_rope",
-    "swan_set_profile_events",
+    "swan_decode_workspace_bytes", "swan_decode_attention", "swan_decode_attention_noalloc",
+    "swan_change_k", "swan_rope", "swan_set_profile_events",
 )
+NOALLOC_SCRATCH_BYTES = 16 << 20
 
 
 class SwanError(RuntimeError):
@@ -85,6 +86,8 @@ def _load() -> ctypes.CDLL:
         "swan_decode_workspace_bytes": [pdesc, pi32, pi32, pi32, psz],
         "swan_decode_attention": [pdesc, pi32, pi32, pi32, vp, vp, vp, ctypes.c_float, vp, vp, sz,
                                   vp],
+        "swan_decode_attention_noalloc": [pdesc, pi32, pi32, pi32, vp, vp, vp, ctypes.c_float,
+                                          vp, vp],
         "swan_change_k": [pdesc, pi32, pi32, pdesc, pi32, pi32, pi32, vp],
         "swan_rope": [vp, vp, i32, i32, i32, i32, i32, pi32, ctypes.c_double, vp],
         "swan_set_profile_events": [vp, vp],
@@ -210,6 +213,16 @@ def decode_attention(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence
                                       _i32_array(k_active), _opt_i32_array(k_value), _ptr(q),
                                       _ptr(P_qk), _ptr(P_vo), float(scale), _ptr(out),
                                       _ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+def decode_attention_noalloc(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence[int],
+                             q, P_qk, P_vo, out, scale: float = 0.0, stream=None,
+                             k_value: Optional[Sequence[int]] = None) -> None:
+    """swan_decode_attention with the library's own scratch instead of a workspace."""
+    _check(_lib.swan_decode_attention_noalloc(ctypes.byref(desc), _i32_array(seq_len),
+                                              _i32_array(k_active), _opt_i32_array(k_value),
+                                              _ptr(q), _ptr(P_qk), _ptr(P_vo), float(scale),
+                                              _ptr(out), _stream(stream)))
 
 
 def change_k(src: CacheDesc, k_active_src: Sequence[int], k_value_src: Optional[Sequence[int]],

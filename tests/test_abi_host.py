@@ -22,7 +22,7 @@ def _declared_functions():
 
 def test_header_and_binding_agree_on_exports():
     declared = _declared_functions()
-    assert len(declared) == 12
+    assert len(declared) == 13
     assert sorted(swan.EXPORTED) == declared
     lib = swan.lib()
     for name in declared:
@@ -30,8 +30,9 @@ def test_header_and_binding_agree_on_exports():
 
 
 def test_version_is_the_current_abi():
-    """2.02: keys and values with their own k (2.00), swan_change_k, swan_rope."""
-    assert swan.lib().swan_version() == 202
+    """2.03: swan_decode_attention_noalloc; 2.02: swan_change_k, swan_rope; 2.00: keys
+    and values with their own k."""
+    assert swan.lib().swan_version() == 203
 
 
 def test_nm_shows_exported_symbols():
@@ -233,3 +234,26 @@ def test_rope_rejects_bad_arguments():
     assert lib.swan_rope(FAKE, FAKE, swan.SWAN_F16, 2, 4, 3, 128, swan._i32_array([0, -1]), 1e4,
                          None) == E
     assert lib.swan_rope(None, None, swan.SWAN_F16, 2, 4, 0, 128, pos, 1e4, None) == swan.SWAN_OK
+
+
+def test_noalloc_decode_checks_arguments_and_its_scratch_limit_on_the_host():
+    """The allocation-free decode rejects bad arguments, and a batch whose partials
+    exceed its scratch array, before it looks the array up on a device."""
+    lib = swan.lib()
+    seq = swan._i32_array([10, 20])
+    kk = swan._i32_array([48, 64])
+    st = lib.swan_decode_attention_noalloc(ctypes.byref(_desc(batch=0)), seq, kk, None, FAKE,
+                                           FAKE, FAKE, 0.0, FAKE, None)
+    assert st == swan.SWAN_ERR_INVALID_ARG, swan.last_error()
+    st = lib.swan_decode_attention_noalloc(ctypes.byref(_desc()), seq, kk, None, None, FAKE,
+                                           FAKE, 0.0, FAKE, None)
+    assert st == swan.SWAN_ERR_INVALID_ARG, swan.last_error()
+    B, H = 64, 256
+    d = _desc(batch=B, n_q_heads=H, n_kv_heads=H, buffer_tokens=1, sparse_capacity=0)
+    lens, ks = [1] * B, [48] * B
+    assert swan.decode_workspace_bytes(d, lens, ks) > swan.NOALLOC_SCRATCH_BYTES
+    st = lib.swan_decode_attention_noalloc(ctypes.byref(d), swan._i32_array(lens),
+                                           swan._i32_array(ks), None, FAKE, FAKE, FAKE, 0.0,
+                                           FAKE, None)
+    assert st == swan.SWAN_ERR_WORKSPACE, swan.last_error()
+    assert "scratch" in swan.last_error()
