@@ -104,13 +104,14 @@ def kpad(k: int) -> int:
     return (k + 7) // 8 * 8
 
 
-def attention_launches(k_key, k_val):
+def attention_launches(k_key, k_val, merge_pct: int = 66):
     """The library's attention launches for these per-sequence k: [(kp8, same_k_pad)].
     Sequences are grouped by (key, value) k_pad; from the largest k_pad down, a group
-    joins the launch before it when its k_pad is at least SWAN_MERGE_PCT (default 66) %
-    of that launch's, and a launch whose sequences do not all have its k_pad for both
-    roles runs the instances for different k_pad."""
-    pct = int(os.environ.get("SWAN_MERGE_PCT", "66"))
+    joins the launch before it when its k_pad is at least merge_pct % of that
+    launch's (the library's default, 66; <= 0 merges nothing), and a launch whose
+    sequences do not all have its k_pad for both roles runs the instances for
+    different k_pad."""
+    pct = merge_pct
     groups = sorted({(kpad(a) // 8, kpad(b) // 8) for a, b in zip(k_key, k_val)},
                     key=lambda g: (-max(g), -g[0], -g[1]))
     launches = []

@@ -25,13 +25,17 @@
  *    sizes it with the *_bytes queries below.  The one resource it keeps: for
  *    a batch whose sequences use different k_pad, swan_decode_attention runs
  *    those attention launches side by side on up to three HIP streams of its
- *    own per device (default priority, created on first use with two events
- *    each, kept until the process ends), forked from and joined back into
- *    `stream` with events, so the call orders with `stream` like any other.
+ *    own per calling thread and device (default priority, created on that
+ *    thread's first such call with their events, kept until the process
+ *    ends), forked from and joined back into `stream` with events, so the
+ *    call orders with `stream` like any other and threads never share them.
  *    Calls are made with the stream's device current; otherwise the launches
  *    run one after another on `stream`.  It also holds, per GPU, the fixed
  *    scratch array of swan_decode_attention_noalloc (a device global, not an
  *    allocation).
+ *  - The decode split plan and launch grouping follow fixed rules, which
+ *    swan_set_decode_tuning can change for the calling thread; no environment
+ *    variable is read.
  *  - All arguments are validated on the host before anything is enqueued, so
  *    a non-OK status means nothing was written.  Errors never abort, throw or
  *    exit; swan_last_error() returns a message for the calling thread.
@@ -93,10 +97,12 @@ typedef enum swan_dtype {
  *     indices: k_pad / 8  chunks, each [64 slots][8 bytes] (uint8)
  * so entry e of slot t has its value at byte (e / GV) * 64 * CB + t * CB +
  * (e % GV) * VB and its index at byte 64 * k_pad * VB + (e / 8) * 512 + t * 8 +
- * (e % 8).  A page is 64 * k_pad * (VB + 1) bytes.  Entries 0..k-1 are the kept components in ascending index order;
- * entries k..k_pad-1 are padding with value +0 at the lowest dims that were not
- * kept, so the k_pad indices of a token are distinct (the decode kernel relies
- * on it).  The keys' pages live in k_pages and use the sequence's k_active; the
+ * (e % 8).  A page is 64 * k_pad * (VB + 1) bytes.  Entries 0..k-1 are the
+ * kept components in ascending index order (after swan_change_k raised k, the
+ * components kept at pruning in ascending order, then the raise's zero-valued
+ * pairs in ascending order); entries k..k_pad-1 are padding with value +0 at the
+ * lowest dims that were not kept, so the k_pad indices of a token are distinct
+ * (the decode kernel relies on it).  The keys' pages live in k_pages and use the sequence's k_active; the
  * values' pages live in v_pages and use its k_value (k_active when
  * k_value_host is NULL).  In each array, sequence s owns
  * n_kv_heads * ceil(sparse_capacity / 64) pages of that role's k, stored after
@@ -261,7 +267,7 @@ swan_status swan_rope(const void* x, void* y, int32_t dtype, int32_t batch, int3
  * k_value_src) out again in `dst` (laid out with k_active_dst / k_value_dst),
  * per sequence and role:
  *  - k' < k: each stored token keeps the k' largest of its k stored values,
- *    ties to the lower index.  For SWAN_F16 / SWAN_F32 values this is exactly
+ *    ties to the lower index, in ascending index order.  For SWAN_F16 / SWAN_F32 values this is exactly
  *    the token's top-k' (the top-k' of a top-k set, under one tie rule), so the
  *    result equals pruning at k' from the start; for SWAN_F16_E4M3 it ranks the
  *    stored 8-bit values.
@@ -284,6 +290,39 @@ swan_status swan_change_k(const swan_cache* src, const int32_t* k_active_src,
                           const int32_t* k_value_src, const swan_cache* dst,
                           const int32_t* k_active_dst, const int32_t* k_value_dst,
                           const int32_t* seq_len_host, void* stream);
+
+/*
+ * Tuning of swan_decode_workspace_bytes, swan_decode_attention and
+ * swan_decode_attention_noalloc on the calling thread (it holds until changed;
+ * NULL restores the defaults).  None of it changes what is computed: the
+ * softmax of Algorithm 1 runs over all cached tokens whatever the token axis is
+ * cut into, and only the order of floating-point additions differs.  The
+ * workspace size depends on the plan, so query it under the same tuning.
+ * Every field: 0 selects the default.
+ *  target_waves       sparse attention waves the split planner aims for over
+ *                     the batch (default 2048, two per wave slot of the GPU);
+ *                     each sequence's token splits follow its share of the
+ *                     bytes, every split keeps at least one page;
+ *  short_split_pages  a short sequence (whose shrinking splits would be at most
+ *                     half as many as its share asks for) is cut into equal
+ *                     splits of this many pages (default 4); -1: shrinking
+ *                     splits for every sequence;
+ *  merge_pct          for a batch mixing k_pad: from the largest k_pad down, a
+ *                     group of sequences joins the launch before it when its
+ *                     k_pad is at least this percentage of that launch's
+ *                     (default 66); -1: one launch per k_pad;
+ *  side_streams       library streams (per thread and device) for those
+ *                     launches, 1..3 (default 3); -1: all on the caller's stream.
+ * Errors: SWAN_ERR_INVALID_ARG for a value outside these ranges (the thread's
+ * tuning is then unchanged).
+ */
+typedef struct swan_decode_tuning {
+  int32_t target_waves;       /* 0 or 1..1048576 */
+  int32_t short_split_pages;  /* 0, -1 or 1..4096 */
+  int32_t merge_pct;          /* 0, -1 or 1..100 */
+  int32_t side_streams;       /* 0, -1 or 1..3 */
+} swan_decode_tuning;
+swan_status swan_set_decode_tuning(const swan_decode_tuning* tuning);
 
 /*
  * Profiling hook.  While both are non-NULL, swan_decode_attention on this

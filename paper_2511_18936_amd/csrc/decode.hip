@@ -6,8 +6,8 @@
 //                  sparse pages, plus one wave per (sequence, query head) over
 //                  the dense buffer; each writes a partial (m, l, acc[128]) in
 //                  the rotated space.  One launch per distinct k_pad of the
-//                  batch; several run side by side on library-owned streams,
-//                  joined back before the merge.  For fp16 GQA the launch is
+//                  batch; several run side by side on library-owned streams
+//                  of the calling thread, joined back before the merge.  For fp16 GQA the launch is
 //                  attn_gqa_kernel (decode_gqa.h) instead, one workgroup per
 //                  KV stream for several query heads.  Sequences whose keys and
 //                  values have different k_pad run the same kernels specialised
@@ -15,9 +15,6 @@
 //   merge_kernel   log-sum-exp merge of the partials, then o = o_hat . P_VO^T
 //                  (the inverse rotation that Sec. 4.2 absorbs into W_O)
 // The sparse attention wave itself is described in decode_mha.h.
-#include <cstdlib>
-#include <mutex>
-
 #include "decode_mha.h"
 
 namespace swan {
@@ -126,20 +123,22 @@ static hipError_t launch_group(const DecodeLaunch& a, const SeqGroup& g, int kp8
   }
 }
 
-// Side streams of one device for the attention launches of a batch that mixes
-// page formats: the launches are independent (disjoint sequences), so running
-// them side by side overlaps each one's ramp-up and tail.  Default priority.
+// Side streams of one device and thread for the attention launches of a
+// batch that mixes page formats: the launches are independent (disjoint
+// sequences), so running them side by side overlaps each one's ramp-up and
+// tail.  Default priority.  Each thread has its own, so that callers on other
+// threads (and streams) never wait on each other through them.
 struct SideStreams {
-  std::mutex mu;  // one fork/join at a time: the events are shared
-  bool tried = false, ok = false;
+  bool tried, ok;
   hipStream_t s[kSideStreams];
   hipEvent_t fork, join[kSideStreams];
 };
 
-// The side streams of the current device, or NULL (launch on the caller's
-// stream alone) when they cannot be made or `caller` belongs to another device.
+// The calling thread's side streams on the current device, or NULL (launch on
+// the caller's stream alone) when they cannot be made or `caller` belongs to
+// another device.
 static SideStreams* side_streams(hipStream_t caller) {
-  static SideStreams per_device[kMaxDevices];
+  static thread_local SideStreams per_device[kMaxDevices];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
   if (caller) {
@@ -147,7 +146,6 @@ static SideStreams* side_streams(hipStream_t caller) {
     if (hipStreamGetDevice(caller, &sdev) != hipSuccess || sdev != dev) return nullptr;
   }
   SideStreams* ss = &per_device[dev];
-  std::lock_guard<std::mutex> lk(ss->mu);
   if (!ss->tried) {
     ss->tried = true;
     bool ok = hipEventCreateWithFlags(&ss->fork, hipEventDisableTiming) == hipSuccess;
@@ -200,10 +198,6 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
       kp8v[ng] = pv;
       ++ng;
     }
-  static const int kMergePct = [] {
-    const char* s = getenv("SWAN_MERGE_PCT");  // tuning override; 0 merges nothing
-    return s ? atoi(s) : 66;
-  }();
   struct Launch {
     SeqGroup g;
     int kp8;
@@ -223,7 +217,7 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
     }
     used[best] = true;
     const bool sym = kp8k[best] == kp8v[best];
-    if (nl > 0 && kMergePct > 0 && bkp * 100 >= ls[nl - 1].kp8 * kMergePct) {
+    if (nl > 0 && a.merge_pct > 0 && bkp * 100 >= ls[nl - 1].kp8 * a.merge_pct) {
       Launch& l = ls[nl - 1];
       for (int j = 0; j < groups[best].n; ++j) l.g.seq[l.g.n++] = groups[best].seq[j];
       if (groups[best].n_splits > l.g.n_splits) l.g.n_splits = groups[best].n_splits;
@@ -241,13 +235,13 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
                ? launch_attn_gqa_asym(ai, ls[i].g, ls[i].kp8)
                : launch_attn_asym(ai, ls[i].g, ls[i].kp8);
   };
-  SideStreams* ss = nl > 1 && !a.one_stream ? side_streams(a.stream) : nullptr;
+  SideStreams* ss = nl > 1 && a.side_streams > 0 ? side_streams(a.stream) : nullptr;
   if (!ss) {  // one launch, or no side streams: back to back on the caller's stream
     for (int i = 0; i < nl; ++i)
       if ((e = launch_one(a, i)) != hipSuccess) return e;
   } else {
-    std::lock_guard<std::mutex> lk(ss->mu);
-    const int nside = nl - 1 < kSideStreams ? nl - 1 : kSideStreams;
+    const int nmax = a.side_streams < kSideStreams ? a.side_streams : kSideStreams;
+    const int nside = nl - 1 < nmax ? nl - 1 : nmax;
     if ((e = hipEventRecord(ss->fork, a.stream)) != hipSuccess) return e;
     for (int j = 0; j < nside; ++j)
       if ((e = hipStreamWaitEvent(ss->s[j], ss->fork, 0)) != hipSuccess) return e;

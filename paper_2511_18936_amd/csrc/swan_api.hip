@@ -29,6 +29,18 @@ thread_local std::string g_last_error;
 thread_local hipEvent_t g_prof_start = nullptr;
 thread_local hipEvent_t g_prof_stop = nullptr;
 
+// Decode tuning of this thread (swan_set_decode_tuning), with the defaults
+// resolved: about two sparse waves per wave slot of the GPU (measured best for
+// long contexts), short sequences in 4-page splits, launch merging at two
+// thirds of the k_pad, three side streams.
+struct Tuning {
+  int64_t target_waves = 256 * 4 * 2;
+  int short_split_pages = 4;  // 0: never
+  int merge_pct = 66;         // 0: never
+  int side_streams = swan::kSideStreams;
+};
+thread_local Tuning g_tuning;
+
 swan_status fail(swan_status st, const char* fmt, ...) {
   char buf[512];
   va_list ap;
@@ -136,12 +148,11 @@ void fill_layout(const swan_cache* c, const int32_t* k_active_host, const int32_
   }
 }
 
-// Token splits per (sequence, query head): about two waves per CU slot in total
-// (measured best for long contexts; SWAN_DECODE_WAVES overrides the target),
-// the split count of each sequence following its bytes (a page weighs the
-// k_pad of its keys plus that of its values); the splits themselves shrink in
-// size (split_begin), and their count is capped so that every split keeps a
-// page.  Fills nsplit[b] (may be NULL); returns the largest.
+// Token splits per (sequence, query head): about the thread's target number of
+// waves in total, the split count of each sequence following its bytes (a page
+// weighs the k_pad of its keys plus that of its values); the splits themselves
+// shrink in size (split_begin), and their count is capped so that every split
+// keeps a page.  Fills nsplit[b] (may be NULL); returns the largest.
 int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t* k_active_host,
                 const int32_t* k_value_host, int32_t* nsplit, int8_t* flat = nullptr) {
   auto weight = [&](int b) {
@@ -157,19 +168,11 @@ int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t*
     const int S = seq_len_host[b] > c->buffer_tokens ? seq_len_host[b] - c->buffer_tokens : 0;
     total += (int64_t)swan::pages_for(S) * weight(b) * waves_per_seq;
   }
-  static const int64_t target_waves = [] {
-    const char* s = getenv("SWAN_DECODE_WAVES");  // tuning override
-    const long v = s ? atol(s) : 0;
-    return (int64_t)(v > 0 ? v : 256 * 4 * 2);
-  }();
+  const int64_t target_waves = g_tuning.target_waves;
   // A sequence whose shrinking splits the one-page rule cuts to half the count
   // wanted or fewer is short: its waves would each walk many pages one after
   // another, so it gets equal splits of flat_pages pages instead.
-  static const int flat_pages = [] {
-    const char* s = getenv("SWAN_FLAT_PAGES");  // tuning override; 0: always shrinking
-    const long v = s ? atol(s) : 4;
-    return (int)(v > 0 ? v : 0);
-  }();
+  const int flat_pages = g_tuning.short_split_pages;
   int64_t per_wave = (total + target_waves - 1) / target_waves;
   if (per_wave < 1) per_wave = 1;
   int ns_max = 1;
@@ -310,7 +313,8 @@ swan_status decode_impl(const swan_cache* c, const int32_t* seq_len_host,
   a.stream = (hipStream_t)stream;
   a.prof_start = g_prof_start;
   a.prof_stop = g_prof_stop;
-  a.one_stream = no_alloc;
+  a.merge_pct = g_tuning.merge_pct;
+  a.side_streams = no_alloc ? 0 : g_tuning.side_streams;
   return hip_status(swan::launch_decode(a), "decode launch");
 }
 
@@ -320,7 +324,7 @@ extern "C" {
 
 const char* swan_last_error(void) { return g_last_error.c_str(); }
 
-int32_t swan_version(void) { return 203; }
+int32_t swan_version(void) { return 204; }
 
 swan_status swan_page_bytes(int32_t dtype, int32_t k_active, size_t* bytes) {
   if (!bytes) return fail(SWAN_ERR_INVALID_ARG, "bytes is NULL");
@@ -581,6 +585,28 @@ swan_status swan_rope(const void* x, void* y, int32_t dtype, int32_t batch, int3
   a.base = base;
   a.stream = (hipStream_t)stream;
   return hip_status(swan::launch_rope(a), "rope launch");
+}
+
+swan_status swan_set_decode_tuning(const swan_decode_tuning* t) {
+  Tuning n;
+  if (t) {
+    if (t->target_waves < 0 || t->target_waves > (1 << 20))
+      return fail(SWAN_ERR_INVALID_ARG, "target_waves %d outside 0..%d", t->target_waves, 1 << 20);
+    if (t->short_split_pages < -1 || t->short_split_pages > 4096)
+      return fail(SWAN_ERR_INVALID_ARG, "short_split_pages %d outside -1..4096",
+                  t->short_split_pages);
+    if (t->merge_pct < -1 || t->merge_pct > 100)
+      return fail(SWAN_ERR_INVALID_ARG, "merge_pct %d outside -1..100", t->merge_pct);
+    if (t->side_streams < -1 || t->side_streams > swan::kSideStreams)
+      return fail(SWAN_ERR_INVALID_ARG, "side_streams %d outside -1..%d", t->side_streams,
+                  swan::kSideStreams);
+    if (t->target_waves > 0) n.target_waves = t->target_waves;
+    if (t->short_split_pages != 0) n.short_split_pages = t->short_split_pages < 0 ? 0 : t->short_split_pages;
+    if (t->merge_pct != 0) n.merge_pct = t->merge_pct < 0 ? 0 : t->merge_pct;
+    if (t->side_streams != 0) n.side_streams = t->side_streams < 0 ? 0 : t->side_streams;
+  }
+  g_tuning = n;
+  return ok();
 }
 
 swan_status swan_set_profile_events(void* start_event, void* stop_event) {

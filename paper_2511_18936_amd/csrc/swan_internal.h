@@ -68,7 +68,8 @@ struct DecodeLaunch {
   hipStream_t stream;
   hipEvent_t prof_start;  // optional events around the attention launches
   hipEvent_t prof_stop;
-  bool one_stream;        // every launch on `stream` (no library side streams)
+  int merge_pct;          // launch grouping of a mixed-k batch (<= 0: none)
+  int side_streams;       // library streams for those launches, 0..kSideStreams
 };
 hipError_t launch_decode(const DecodeLaunch& a);
 constexpr int kSideStreams = 3;  // extra streams for the launches of a mixed-k batch

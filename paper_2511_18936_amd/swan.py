@@ -33,7 +33,7 @@ EXPORTED = (
     "swan_last_error", "swan_version", "swan_page_bytes", "swan_cache_bytes",
     "swan_calibrate_workspace_bytes", "swan_calibrate_rotation", "swan_compress_append",
     "swan_decode_workspace_bytes", "swan_decode_attention", "swan_decode_attention_noalloc",
-    "swan_change_k", "swan_rope", "swan_set_profile_events",
+    "swan_change_k", "swan_rope", "swan_set_decode_tuning", "swan_set_profile_events",
 )
 NOALLOC_SCRATCH_BYTES = 16 << 20
 
@@ -42,6 +42,15 @@ class SwanError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"swan status {status}: {message}")
         self.status = status
+
+
+class DecodeTuning(ctypes.Structure):
+    _fields_ = [
+        ("target_waves", ctypes.c_int32),
+        ("short_split_pages", ctypes.c_int32),
+        ("merge_pct", ctypes.c_int32),
+        ("side_streams", ctypes.c_int32),
+    ]
 
 
 class CacheDesc(ctypes.Structure):
@@ -90,6 +99,7 @@ def _load() -> ctypes.CDLL:
                                           vp, vp],
         "swan_change_k": [pdesc, pi32, pi32, pdesc, pi32, pi32, pi32, vp],
         "swan_rope": [vp, vp, i32, i32, i32, i32, i32, pi32, ctypes.c_double, vp],
+        "swan_set_decode_tuning": [ctypes.POINTER(DecodeTuning)],
         "swan_set_profile_events": [vp, vp],
     }
     for name, args in sigs.items():
@@ -134,6 +144,43 @@ def _stream(stream) -> Optional[int]:
     if stream is None:
         stream = torch.cuda.current_stream()
     return stream.cuda_stream
+
+
+def _elem_torch_dtype(code: int):
+    import torch
+
+    return torch.float32 if code == SWAN_F32 else torch.float16
+
+
+def _tensor(t, name: str, dtype, shape) -> None:
+    """The library sees only a device pointer: check what it assumes about the
+    tensor behind it (dtype, shape, dense row-major layout, a GPU) before the call.
+    A None entry of `shape` matches any size."""
+    if t is None:
+        raise SwanError(SWAN_ERR_INVALID_ARG, f"{name} is None")
+    if t.dtype != dtype:
+        raise SwanError(SWAN_ERR_INVALID_ARG, f"{name} has dtype {t.dtype}, expected {dtype}")
+    if t.dim() != len(shape) or any(w is not None and g != w for g, w in zip(t.shape, shape)):
+        want = "x".join("*" if w is None else str(w) for w in shape)
+        raise SwanError(SWAN_ERR_INVALID_ARG,
+                        f"{name} has shape {tuple(t.shape)}, expected [{want}]")
+    if not t.is_contiguous():
+        raise SwanError(SWAN_ERR_INVALID_ARG, f"{name} must be contiguous (row-major)")
+
+
+def _on_gpu(**tensors) -> None:
+    for name, t in tensors.items():
+        if t is not None and t.device.type != "cuda":
+            raise SwanError(SWAN_ERR_INVALID_ARG, f"{name} is on {t.device}, not on a GPU")
+
+
+def _rotations(desc: CacheDesc, P_qk, P_vo) -> None:
+    import torch
+
+    shape = (desc.n_kv_heads, desc.head_dim, desc.head_dim)
+    _tensor(P_qk, "P_qk", torch.float32, shape)
+    if P_vo is not None:
+        _tensor(P_vo, "P_vo", torch.float32, shape)
 
 
 def dtype_code(torch_dtype, sparse_values: str = "same") -> int:
@@ -190,6 +237,13 @@ def compress_append(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence[
                     v_new, P_qk, P_vo, n_new_per_seq: Optional[Sequence[int]] = None,
                     stream=None, k_value: Optional[Sequence[int]] = None) -> None:
     n_new = 0 if k_new is None else int(k_new.shape[2])
+    if k_new is not None or v_new is not None:
+        et = _elem_torch_dtype(desc.dtype)
+        shape = (desc.batch, desc.n_kv_heads, n_new, desc.head_dim)
+        _tensor(k_new, "k_new", et, shape)
+        _tensor(v_new, "v_new", et, shape)
+    _rotations(desc, P_qk, P_vo)
+    _on_gpu(k_new=k_new, v_new=v_new, P_qk=P_qk, P_vo=P_vo)
     per = None if n_new_per_seq is None else _i32_array(n_new_per_seq)
     _check(_lib.swan_compress_append(ctypes.byref(desc), _i32_array(seq_len),
                                      _i32_array(k_active), _opt_i32_array(k_value), _ptr(k_new),
@@ -209,16 +263,30 @@ def decode_workspace_bytes(desc: CacheDesc, seq_len: Sequence[int], k_active: Se
 def decode_attention(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence[int], q,
                      P_qk, P_vo, out, workspace, scale: float = 0.0, stream=None,
                      k_value: Optional[Sequence[int]] = None) -> None:
+    _decode_tensors(desc, q, P_qk, P_vo, out)
+    if workspace is None or workspace.device.type != "cuda" or not workspace.is_contiguous():
+        raise SwanError(SWAN_ERR_WORKSPACE, "workspace must be a contiguous GPU tensor")
+    ws_bytes = workspace.numel() * workspace.element_size()
     _check(_lib.swan_decode_attention(ctypes.byref(desc), _i32_array(seq_len),
                                       _i32_array(k_active), _opt_i32_array(k_value), _ptr(q),
                                       _ptr(P_qk), _ptr(P_vo), float(scale), _ptr(out),
-                                      _ptr(workspace), workspace.numel(), _stream(stream)))
+                                      _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def _decode_tensors(desc: CacheDesc, q, P_qk, P_vo, out) -> None:
+    et = _elem_torch_dtype(desc.dtype)
+    shape = (desc.batch, desc.n_q_heads, desc.head_dim)
+    _tensor(q, "q", et, shape)
+    _tensor(out, "out", et, shape)
+    _rotations(desc, P_qk, P_vo)
+    _on_gpu(q=q, out=out, P_qk=P_qk, P_vo=P_vo)
 
 
 def decode_attention_noalloc(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence[int],
                              q, P_qk, P_vo, out, scale: float = 0.0, stream=None,
                              k_value: Optional[Sequence[int]] = None) -> None:
     """swan_decode_attention with the library's own scratch instead of a workspace."""
+    _decode_tensors(desc, q, P_qk, P_vo, out)
     _check(_lib.swan_decode_attention_noalloc(ctypes.byref(desc), _i32_array(seq_len),
                                               _i32_array(k_active), _opt_i32_array(k_value),
                                               _ptr(q), _ptr(P_qk), _ptr(P_vo), float(scale),
@@ -247,6 +315,15 @@ def rope(x, pos0: Sequence[int], base: float, out=None, stream=None):
     _check(_lib.swan_rope(_ptr(x), _ptr(out), code, B, H, n, d, _i32_array(pos0), float(base),
                           _stream(stream)))
     return out
+
+
+def set_decode_tuning(target_waves: int = 0, short_split_pages: int = 0, merge_pct: int = 0,
+                      side_streams: int = 0) -> None:
+    """Split plan and launch grouping of the decode calls on this thread
+    (swan_set_decode_tuning; 0 = the default, -1 = off where the header allows it).
+    With every argument 0 the defaults are restored."""
+    t = DecodeTuning(target_waves, short_split_pages, merge_pct, side_streams)
+    _check(_lib.swan_set_decode_tuning(ctypes.byref(t)))
 
 
 def set_profile_events(start=None, stop=None) -> None:

@@ -22,7 +22,7 @@ def _declared_functions():
 
 def test_header_and_binding_agree_on_exports():
     declared = _declared_functions()
-    assert len(declared) == 13
+    assert len(declared) == 14
     assert sorted(swan.EXPORTED) == declared
     lib = swan.lib()
     for name in declared:
@@ -30,9 +30,9 @@ def test_header_and_binding_agree_on_exports():
 
 
 def test_version_is_the_current_abi():
-    """2.03: swan_decode_attention_noalloc; 2.02: swan_change_k, swan_rope; 2.00: keys
+    """2.04: swan_set_decode_tuning; 2.03: swan_decode_attention_noalloc; 2.02: swan_change_k, swan_rope; 2.00: keys
     and values with their own k."""
-    assert swan.lib().swan_version() == 203
+    assert swan.lib().swan_version() == 204
 
 
 def test_nm_shows_exported_symbols():
@@ -257,3 +257,65 @@ def test_noalloc_decode_checks_arguments_and_its_scratch_limit_on_the_host():
                                            FAKE, None)
     assert st == swan.SWAN_ERR_WORKSPACE, swan.last_error()
     assert "scratch" in swan.last_error()
+
+
+def test_decode_tuning_changes_the_plan_and_checks_its_ranges():
+    """swan_set_decode_tuning: the workspace follows the thread's split plan (one
+    split per sequence with a target of one wave), bad values are rejected and leave
+    the tuning as it was, and all-zero restores the defaults."""
+    d = _desc(batch=2, n_q_heads=4, n_kv_heads=4, buffer_tokens=16, sparse_capacity=40000)
+    lens, ks = [30000, 20000], [48, 48]
+    default = swan.decode_workspace_bytes(d, lens, ks)
+    try:
+        swan.set_decode_tuning(target_waves=1)
+        one = swan.decode_workspace_bytes(d, lens, ks)
+        units = 2 * 4
+        assert one == (units * 128 * 4 + 255) // 256 * 256 + units * 2 * 132 * 4
+        assert one < default
+        for kw in (dict(target_waves=-1), dict(short_split_pages=-2), dict(merge_pct=101),
+                   dict(side_streams=4), dict(side_streams=-2)):
+            with pytest.raises(swan.SwanError) as ei:
+                swan.set_decode_tuning(**kw)
+            assert ei.value.status == swan.SWAN_ERR_INVALID_ARG
+            assert swan.decode_workspace_bytes(d, lens, ks) == one
+        # a large target is capped by the one-page rule (30 splits for 469 pages)
+        swan.set_decode_tuning(target_waves=1 << 20)
+        assert swan.decode_workspace_bytes(d, lens, ks) == default
+    finally:
+        swan.set_decode_tuning()
+    assert swan.decode_workspace_bytes(d, lens, ks) == default
+
+
+def test_binding_checks_tensors_before_the_call():
+    """The library sees only device pointers, so the binding checks dtype, shape,
+    layout and device of every tensor against the descriptor first (CPU tensors
+    here: each case fails before any device pointer is taken)."""
+    import torch
+
+    d = _desc()  # batch 2, 8 query / 2 KV heads, fp16
+    P = torch.zeros((2, 128, 128), dtype=torch.float32)
+    k = torch.zeros((2, 2, 3, 128), dtype=torch.float16)
+    q = torch.zeros((2, 8, 128), dtype=torch.float16)
+    ws = torch.zeros(16, dtype=torch.uint8)
+
+    def rejects(fn, what):
+        with pytest.raises(swan.SwanError) as ei:
+            fn()
+        assert what in str(ei.value), str(ei.value)
+
+    app = lambda kn, vn, Pq=P, Pv=P: swan.compress_append(d, [0, 0], [48, 48], kn, vn, Pq, Pv)
+    rejects(lambda: app(k.float(), k), "dtype")
+    rejects(lambda: app(k, k[:, :1].contiguous()), "shape")
+    rejects(lambda: app(k, k.transpose(2, 3).contiguous().transpose(2, 3)), "contiguous")
+    rejects(lambda: app(k, k, P.double()), "P_qk")
+    rejects(lambda: app(k, k, P, P[:1]), "P_vo")
+    rejects(lambda: app(k, k), "not on a GPU")
+    dec = lambda qq, oo, Pq=P: swan.decode_attention(d, [5, 5], [48, 48], qq, Pq, P, oo, ws)
+    rejects(lambda: dec(q.float(), q), "dtype")
+    rejects(lambda: dec(q, q[:, :4].contiguous()), "shape")
+    rejects(lambda: dec(q, q.transpose(0, 1).contiguous().transpose(0, 1)), "contiguous")
+    rejects(lambda: dec(q, q, P.transpose(1, 2)), "P_qk")
+    rejects(lambda: dec(q, q), "not on a GPU")
+    rejects(lambda: swan.decode_attention_noalloc(d, [5, 5], [48, 48], q, P, P, q[:1]), "shape")
+    d32 = _desc(dtype=swan.SWAN_F32)
+    rejects(lambda: swan.decode_attention(d32, [5, 5], [48, 48], q, P, P, q, ws), "float32")

@@ -25,8 +25,7 @@ def test_attention_bytes_is_the_per_unit_byte_model():
         32 * (2 * 100 * 128 * 2) + 15 * 32 * (32640 * 128 * 3 + 2 * 128 * 128 * 2)
 
 
-def test_attention_launches_mirror_the_grouping(monkeypatch):
-    monkeypatch.delenv("SWAN_MERGE_PCT", raising=False)
+def test_attention_launches_mirror_the_grouping():
     ks = [48, 32, 32, 64, 48, 32, 96, 48]
     # k_pad 96 and 64 (two thirds) share a launch, so do 48 and 32
     assert bench.attention_launches(ks, ks) == [(12, False), (6, False)]
@@ -34,8 +33,7 @@ def test_attention_launches_mirror_the_grouping(monkeypatch):
     assert bench.attention_launches([48] * 16, [48] * 16) == [(6, True)]
     assert bench.attention_launches([41, 48], [47, 45]) == [(6, True)]  # one k_pad
     assert bench.attention_launches([77] * 4, [51] * 4) == [(10, False)]
-    monkeypatch.setenv("SWAN_MERGE_PCT", "0")
-    assert bench.attention_launches(ks, ks) == [(12, True), (8, True), (6, True), (4, True)]
+    assert bench.attention_launches(ks, ks, merge_pct=-1) == [(12, True), (8, True), (6, True), (4, True)]
 
 
 def test_bench_refuses_several_gpus():

@@ -84,11 +84,11 @@ def _run(device, name: str, n_units: int):
 
 
 def test_llama2_7b_32k_batch16(gpu_device):
-    _run(gpu_device, "llama2_7b_L32k_b16", 6)
+    _run(gpu_device, "llama2_7b_L32k_b16", 8)
 
 
 def test_llama3_8b_gqa_128k_batch4(gpu_device):
-    _run(gpu_device, "llama3_8b_gqa_L128k_b4", 3)
+    _run(gpu_device, "llama3_8b_gqa_L128k_b4", 8)
 
 
 def test_prefill16k_batch8_per_sequence_k(gpu_device):
@@ -96,12 +96,12 @@ def test_prefill16k_batch8_per_sequence_k(gpu_device):
 
 
 def test_llama2_7b_32k_batch16_e4m3_values(gpu_device):
-    _run(gpu_device, "llama2_7b_L32k_b16_e4m3", 4)
+    _run(gpu_device, "llama2_7b_L32k_b16_e4m3", 8)
 
 
 def test_llama2_7b_32k_batch16_keys77_values51(gpu_device):
-    _run(gpu_device, "llama2_7b_L32k_b16_k77_v51", 4)
+    _run(gpu_device, "llama2_7b_L32k_b16_k77_v51", 8)
 
 
 def test_llama3_8b_gqa_128k_batch4_keys77_values51(gpu_device):
-    _run(gpu_device, "llama3_8b_gqa_L128k_b4_k77_v51", 2)
+    _run(gpu_device, "llama3_8b_gqa_L128k_b4_k77_v51", 8)
