@@ -19,8 +19,9 @@
 // padding, straight from registers.  Lowering finds the k'-th largest
 // magnitude key by a bitwise search, counting the keys at or above a candidate
 // several at a time with packed integer arithmetic on the stored words; the
-// entries are then walked in index order, the destination page is assembled
-// in LDS and written with 16-byte stores.
+// kept pairs then go to the destination page in ascending index order (ties at
+// the k'-th magnitude to the lower index), assembled in LDS and written with
+// 16-byte stores.
 #include <utility>
 
 #include "swan_device.h"
@@ -229,31 +230,107 @@ __global__ __launch_bounds__(64) void change_k_kernel(ChangeKLaunch a) {
     need_eq = kd - (int)greater;
   }
 
-  // kept entries in index order; u0..u3 mark the dims they use (for the padding)
+  // The stored pairs are in ascending index order, except after a raise: its
+  // zero-valued pairs then follow the pairs kept at pruning.  In the first case
+  // the stored order is the index order, so ties at tau go to the lower index by
+  // taking them in stored order and the kept pairs are written in that order;
+  // otherwise the kept dims are first collected in a 128-bit mask (ties: the
+  // need_eq lowest tied dims) and each kept pair goes to its rank in the mask.
   const bool pad = kpd > kd;
   const int kv = valid ? ks : 0;
-  uint32_t u0 = 0u, u1 = 0u, u2 = 0u, u3 = 0u;
-  int j = 0;
+  bool asc = true;
+  {
+    uint32_t prev = 0u;
 #pragma unroll
-  for (int e = 0; e < KPS; ++e) {
-    const uint32_t v = (w[e / EPW] >> ((e % EPW) * VB * 8)) & VMASK;
-    const uint32_t key = MK::key(v);
-    const bool tie = key == tau;
-    const bool keep = e < kv && (key > tau || (tie && need_eq > 0));
-    if (keep) {
-      need_eq -= tie ? 1 : 0;
+    for (int e = 0; e < KPS; ++e) {
       const uint32_t d = (ix[e / 4] >> ((e % 4) * 8)) & 0xFFu;
-      write_val<F>(lds, val_off<F>(j, lane), v);
-      lds[idx_off(j, lane, kpd, VB)] = (char)d;
-      if (pad) {  // uniform
-        const uint32_t bit = 1u << (d & 31);
-        const uint32_t wd = d >> 5;  // indices are < 128 in a valid cache
-        u0 |= wd == 0u ? bit : 0u;
-        u1 |= wd == 1u ? bit : 0u;
-        u2 |= wd == 2u ? bit : 0u;
-        u3 |= wd == 3u ? bit : 0u;
+      asc = asc && (e == 0 || e >= kv || d > prev);
+      prev = d;
+    }
+  }
+  uint32_t u0 = 0u, u1 = 0u, u2 = 0u, u3 = 0u;  // the kept dims (for the padding)
+  int j = 0;
+  if (__ballot(!asc) == 0) {  // uniform: every lane's pairs are in index order
+#pragma unroll
+    for (int e = 0; e < KPS; ++e) {
+      const uint32_t v = (w[e / EPW] >> ((e % EPW) * VB * 8)) & VMASK;
+      const uint32_t key = MK::key(v);
+      const bool tie = key == tau;
+      const bool keep = e < kv && (key > tau || (tie && need_eq > 0));
+      if (keep) {
+        need_eq -= tie ? 1 : 0;
+        const uint32_t d = (ix[e / 4] >> ((e % 4) * 8)) & 0xFFu;
+        write_val<F>(lds, val_off<F>(j, lane), v);
+        lds[idx_off(j, lane, kpd, VB)] = (char)d;
+        if (pad) {  // uniform
+          const uint32_t bit = 1u << (d & 31);
+          const uint32_t wd = d >> 5;  // indices are < 128 in a valid cache
+          u0 |= wd == 0u ? bit : 0u;
+          u1 |= wd == 1u ? bit : 0u;
+          u2 |= wd == 2u ? bit : 0u;
+          u3 |= wd == 3u ? bit : 0u;
+        }
+        ++j;
       }
-      ++j;
+    }
+  } else {
+    // dims above tau and dims at tau
+    uint32_t g0 = 0u, g1 = 0u, g2 = 0u, g3 = 0u, t0 = 0u, t1 = 0u, t2 = 0u, t3 = 0u;
+#pragma unroll
+    for (int e = 0; e < KPS; ++e) {
+      const uint32_t v = (w[e / EPW] >> ((e % EPW) * VB * 8)) & VMASK;
+      const uint32_t key = MK::key(v);
+      const uint32_t d = (ix[e / 4] >> ((e % 4) * 8)) & 0x7Fu;
+      const uint32_t bit = 1u << (d & 31);
+      const uint32_t wd = d >> 5;
+      const uint32_t gb = e < kv && key > tau ? bit : 0u;
+      const uint32_t tb = e < kv && key == tau ? bit : 0u;
+      g0 |= wd == 0u ? gb : 0u;
+      g1 |= wd == 1u ? gb : 0u;
+      g2 |= wd == 2u ? gb : 0u;
+      g3 |= wd == 3u ? gb : 0u;
+      t0 |= wd == 0u ? tb : 0u;
+      t1 |= wd == 1u ? tb : 0u;
+      t2 |= wd == 2u ? tb : 0u;
+      t3 |= wd == 3u ? tb : 0u;
+    }
+    // keep the need_eq lowest tied dims
+    uint32_t tw[4] = {t0, t1, t2, t3};
+    int need = need_eq;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int c = __builtin_popcount(tw[q]);
+      if (c <= need) {
+        need -= c;
+      } else {
+        uint32_t rest = tw[q], keep = 0u;
+        for (int i = 0; i < need; ++i) {
+          keep |= rest & (0u - rest);
+          rest &= rest - 1u;
+        }
+        tw[q] = keep;
+        need = 0;
+      }
+    }
+    u0 = g0 | tw[0];
+    u1 = g1 | tw[1];
+    u2 = g2 | tw[2];
+    u3 = g3 | tw[3];
+    const int c0 = __builtin_popcount(u0), c1 = c0 + __builtin_popcount(u1),
+              c2 = c1 + __builtin_popcount(u2);
+    j = c2 + __builtin_popcount(u3);
+#pragma unroll
+    for (int e = 0; e < KPS; ++e) {
+      const uint32_t v = (w[e / EPW] >> ((e % EPW) * VB * 8)) & VMASK;
+      const uint32_t d = (ix[e / 4] >> ((e % 4) * 8)) & 0x7Fu;
+      const uint32_t wd = d >> 5;
+      const uint32_t m = wd == 0u ? u0 : wd == 1u ? u1 : wd == 2u ? u2 : u3;
+      const int before = wd == 0u ? 0 : wd == 1u ? c0 : wd == 2u ? c1 : c2;
+      if (e < kv && ((m >> (d & 31)) & 1u)) {
+        const int slot = before + __builtin_popcount(m & ((1u << (d & 31)) - 1u));
+        write_val<F>(lds, val_off<F>(slot, lane), v);
+        lds[idx_off(slot, lane, kpd, VB)] = (char)d;
+      }
     }
   }
   // value 0 at the lowest free dims (at most 128 - j dims are used, so they never

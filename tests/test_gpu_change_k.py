@@ -14,6 +14,7 @@ import pytest
 import swan_inputs as si
 from oracle import swan_oracle as O
 from tests import swan_cases as C
+from tests import swan_layout as lay
 from tests.test_gpu_parity import _build, _decode_check
 
 pytestmark = pytest.mark.gpu
@@ -129,3 +130,82 @@ def test_lower_then_raise(gpu_device, swan_mod, torch_mod):
         for h in range(2):
             C.compare_unit(cache, oc2[bi][h], bi, h, L, np.float16)
     _decode_check(swan_mod, torch_mod, gpu_device, cache, oc2, Pqk, Pvo, tqk, tvo, "f16")
+
+
+@pytest.mark.parametrize("fmt,k0,k1,k2", [
+    ("f16", 32, 64, 48),     # lowering keeps the 32 pairs and the 16 lowest zero fills
+    ("f16", 32, 64, 33),
+    ("f32", 24, 60, 30),
+    ("e4m3", 48, 96, 64),
+])
+def test_raise_then_lower(gpu_device, swan_mod, torch_mod, fmt, k0, k1, k2):
+    """After a raise the stored pairs are the pairs kept at pruning, then the zero
+    fills; lowering must still rank ties by index and write ascending indices."""
+    _log(f"raise then lower fmt={fmt} {k0} -> {k1} -> {k2}")
+    dtype, vals = _dt(fmt)
+    Ls = [900, 333]
+    cache, oc, Pqk, Pvo, tqk, tvo, *_ = _build(swan_mod, torch_mod, gpu_device, B=2, Hq=4,
+                                                Hkv=2, L=Ls, b=16, k_active=[k0, k0],
+                                                dtype=dtype, values=vals, seed=5)
+    cache.change_k([k1, k1])
+    cache.change_k([k2, k2])
+    oc2 = [[O.change_k_cache(O.change_k_cache(u, k1), k2) for u in row] for row in oc]
+    for bi, L in enumerate(Ls):
+        for h in range(2):
+            C.compare_unit(cache, oc2[bi][h], bi, h, L, si.np_dtype(dtype), values=vals)
+            assert np.all(np.diff(oc2[bi][h]["k_idx"], axis=1) > 0)  # ascending indices
+    _decode_check(swan_mod, torch_mod, gpu_device, cache, oc2, Pqk, Pvo, tqk, tvo, dtype)
+
+
+@pytest.mark.parametrize("dtype,k0,steps", [
+    (np.float16, 40, [(80, False), (50, True)]),   # raise, then lower into the fills
+    (np.float16, 40, [(33, True)]),                # lower with ties at zero
+    (np.float32, 24, [(64, False), (30, True)]),
+    (np.float16, 8, [(128, False), (9, True)]),
+])
+def test_change_k_zero_ties_on_host_packed_pages(gpu_device, swan_mod, torch_mod, dtype, k0,
+                                                 steps):
+    """Pages packed on the host from pairs with many zero (+0 and -0) and equal
+    magnitudes, so that the k'-th magnitude is tied between pairs kept at pruning
+    and the zero fills of a raise: the converted pages equal the oracle's."""
+    torch = torch_mod
+    B, Hkv, S, b = 2, 2, 300, 4
+    L = S + b
+    rng = si.rng_for(4712, k0, len(steps))
+    esize = np.dtype(dtype).itemsize
+    cache = swan_mod.SwanCache(B, 2, Hkv, b, S, [k0] * B, torch.float16 if esize == 2
+                               else torch.float32, gpu_device)
+    npc = (S + 63) // 64
+    kp_bytes = np.zeros(cache.k_pages.numel(), np.uint8)
+    vp_bytes = np.zeros(cache.v_pages.numel(), np.uint8)
+    oc = []
+    for bi in range(B):
+        row = []
+        for h in range(Hkv):
+            c = {"n_sparse": S, "k_buf": np.zeros((b, 128), dtype),
+                 "v_buf": np.zeros((b, 128), dtype)}
+            for r in ("k", "v"):
+                idx = np.sort(np.stack([rng.choice(128, k0, replace=False) for _ in range(S)]),
+                              axis=1)
+                # magnitudes from a small set (many ties), a third of them zero, random signs
+                mag = rng.choice([0.0, 0.0, 0.5, 1.0, 0.25, 2.0], size=(S, k0))
+                val = (mag * rng.choice([-1.0, 1.0], size=(S, k0))).astype(dtype)
+                c[f"{r}_idx"], c[f"{r}_val"] = idx, val
+                s0, e0 = lay.unit_slice([k0] * B, Hkv, S, esize, bi, h)
+                (kp_bytes if r == "k" else vp_bytes)[s0:e0] = lay.pack(idx, val, dtype, k0, npc)
+            row.append(c)
+        oc.append(row)
+    cache.k_pages.copy_(torch.tensor(kp_bytes, device=gpu_device))
+    cache.v_pages.copy_(torch.tensor(vp_bytes, device=gpu_device))
+    cache.seq_len = [L] * B
+    for k, _ in steps:
+        cache.change_k([k] * B)
+        oc = [[O.change_k_cache(u, k) for u in row] for row in oc]
+    torch.cuda.synchronize()
+    for bi in range(B):
+        for h in range(Hkv):
+            for role, r in enumerate(("k", "v")):
+                idx, val, _, _ = C.unit_pages(cache, bi, h, role, S, dtype)
+                assert np.array_equal(idx, oc[bi][h][f"{r}_idx"]), (bi, h, r)
+                assert np.array_equal(val.view(np.uint8),
+                                      np.asarray(oc[bi][h][f"{r}_val"], dtype).view(np.uint8))
