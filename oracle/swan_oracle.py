@@ -116,8 +116,10 @@ def calibrate(S: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
     no mean is removed.  Returns (P [d][d] float64, sigma [d] float64).
     """
     S = np.asarray(S, dtype=F64)
-    d = S.shape[1]
-    _, sig, vt = np.linalg.svd(S, full_matrices=True)
+    n, d = S.shape
+    # the right singular matrix is d x d either way; the thin factorisation skips
+    # the n x n left factor, which only a short S (n < d) needs for a square V
+    _, sig, vt = np.linalg.svd(S, full_matrices=n < d)
     sigma = np.zeros(d, dtype=F64)
     sigma[: sig.shape[0]] = sig
     P = vt.T  # columns are the right singular vectors, already in descending sigma
