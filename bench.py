@@ -23,6 +23,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+MALL_BYTES = 256 << 20  # MI355X last-level (Infinity) cache
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic_{wl}.txt")
 # sources of the decode attention kernels: counter summaries are valid only for these bytes
 ATTN_SOURCES = ("decode.hip", "decode_gqa.hip", "decode_asym.hip", "decode_gqa_asym.hip",
@@ -41,12 +42,15 @@ def parse_args():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama2_7b_L32k_b16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-units", type=int, default=3,
-                    help="(sequence, head) units in the oracle's timed sample")
+    ap.add_argument("--cpu-seconds", type=float, default=8.0,
+                    help="seconds of oracle work per host core in the CPU baseline")
     ap.add_argument("--change-k", type=int, default=0,
                     help="also time swan_change_k of the cache from the workload's k to this k")
     ap.add_argument("--layer", action="store_true",
                     help="also time decode steps of the whole attention layer (synthetic weights)")
+    ap.add_argument("--replicas", type=int, default=0,
+                    help="caches the steps rotate over (0: 8 when one step's attention bytes "
+                         "fit the GPU's 256 MB last-level cache, else 1)")
     ap.add_argument("--probe-copy", type=int, default=0,
                     help="also run a device copy of this many bytes (HBM counter calibration)")
     return ap.parse_args()
@@ -217,6 +221,46 @@ def time_layer(swan, torch, si, w, Pqk, Pvo, ks, kvs, dev, warmup, steps):
             "weights_bytes": 2 * hidden * d * (2 * w.n_q_heads + 2 * w.n_kv_heads)}
 
 
+def streaming_ceiling(torch, caches, dev, reps: int = 5):
+    """Bandwidth of a read-only streaming kernel over the caches' page arrays (the
+    bytes the attention kernels stream), with their load form: swan_stream_read of
+    libswanbench.so, timed with HIP events on the current stream; the best of a
+    sweep over wave counts and loads in flight."""
+    import ctypes
+
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2511_18936_amd", "libswanbench.so"))
+    lib.swan_stream_read.restype = ctypes.c_int32
+    lib.swan_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32,
+                                     ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    sink = torch.empty(16384, dtype=torch.int32, device=dev)
+    arrays = [t for c in caches for t in (c.k_pages, c.v_pages)]
+    stream = torch.cuda.current_stream().cuda_stream
+    nbytes = sum(t.numel() // 1024 * 1024 for t in arrays)
+
+    def one_pass(waves, u):
+        for t in arrays:
+            st = lib.swan_stream_read(t.data_ptr(), t.numel(), waves, u, sink.data_ptr(), stream)
+            if st != 0:
+                raise RuntimeError(f"swan_stream_read returned {st}")
+
+    best = None
+    for waves in (1024, 2048, 4096, 8192, 16384):
+        for u in (8, 16):
+            one_pass(waves, u)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                one_pass(waves, u)
+            e1.record()
+            torch.cuda.synchronize()
+            t = e0.elapsed_time(e1) * 1e-3 / reps
+            if best is None or t < best[0]:
+                best = (t, waves, u)
+    t, waves, u = best
+    return {"gbps": nbytes / t / 1e9, "bytes": nbytes, "ms": t * 1e3, "waves": waves,
+            "loads_in_flight": u, "launches_per_pass": len(arrays)}
+
+
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -228,61 +272,124 @@ def cpu_model() -> str:
     return platform.machine()
 
 
-def cpu_baseline(w, n_units: int):
-    """The oracle, as it stands, timed on the host on a bounded sample of units."""
+def _oracle_unit(args):
+    """One (sequence, KV head) unit for the oracle's timing: its caches after the
+    step's append (the attention input) and just before it (the append input)."""
     import numpy as np
-    from threadpoolctl import threadpool_limits
 
     import swan_inputs as si
     from oracle import swan_oracle as O
 
+    wname, u = args
+    w = si.WORKLOADS[wname]
     ks = si.k_active_for(w)
     kvs = si.k_value_for(w)
     kvs = ks if kvs is None else kvs
     np_dt = si.np_dtype(w.dtype)
     vals = "e4m3" if w.sparse_values == "e4m3" else "t"
     L = w.context
-    units = []
-    for u in range(n_units):
-        b, h = (u // w.n_kv_heads) % w.batch, u % w.n_kv_heads
-        Pqk, _ = O.calibrate_f32(si.calibration_rows(w.wid, h, si.ROLE_K))
-        Pvo, _ = O.calibrate_f32(si.calibration_rows(w.wid, h, si.ROLE_V))
-        K = si.kv_rows_host(w.wid, b, h, si.ROLE_K, L, w.dtype)
-        V = si.kv_rows_host(w.wid, b, h, si.ROLE_V, L, w.dtype)
-        # cache state after the step's append (the attention input) ...
-        c = O.compress_block(K, V, Pqk, Pvo, w.buffer, int(ks[b]), np_dt, values=vals,
-                             k_value=int(kvs[b]))
-        # ... and the buffer just before it (the append input)
-        c_prev = O.compress_block(K[L - 1 - w.buffer:L - 1], V[L - 1 - w.buffer:L - 1], Pqk, Pvo,
-                                  w.buffer, int(ks[b]), np_dt, values=vals, k_value=int(kvs[b]))
-        q = si.queries_host(w.wid, 1, 1, w.dtype)[0, 0].astype(np.float64)
-        units.append((Pqk, Pvo, c, c_prev, K[L - 1], V[L - 1], q, int(ks[b]), int(kvs[b])))
-    t_append, t_attend = [], []
+    b, h = (u // w.n_kv_heads) % w.batch, u % w.n_kv_heads
+    Pqk, _ = O.calibrate_f32(si.calibration_rows(w.wid, h, si.ROLE_K))
+    Pvo, _ = O.calibrate_f32(si.calibration_rows(w.wid, h, si.ROLE_V))
+    K = si.kv_rows_host(w.wid, b, h, si.ROLE_K, L, w.dtype)
+    V = si.kv_rows_host(w.wid, b, h, si.ROLE_V, L, w.dtype)
+    c = O.compress_block(K, V, Pqk, Pvo, w.buffer, int(ks[b]), np_dt, values=vals,
+                         k_value=int(kvs[b]))
+    c_prev = O.compress_block(K[L - 1 - w.buffer:L - 1], V[L - 1 - w.buffer:L - 1], Pqk, Pvo,
+                              w.buffer, int(ks[b]), np_dt, values=vals, k_value=int(kvs[b]))
+    qs = si.queries_host(w.wid, 1, w.group, w.dtype)[0].astype(np.float64)
+    return (Pqk, Pvo, c, c_prev, K[L - 1], V[L - 1], qs, int(ks[b]), int(kvs[b]), np_dt, vals,
+            w.buffer)
+
+
+def _oracle_unit_steps(unit, reps: int):
+    """reps decode steps of one unit with the oracle: append the current token
+    (Algorithm 1: rotate, buffer, evict and prune the oldest) and attend for each of
+    the unit's query heads.  Returns (append seconds, attention seconds) in total."""
+    import time as _t
+
+    from oracle import swan_oracle as O
+
+    Pqk, Pvo, c, c_prev, kl, vl, qs, k, kv, np_dt, vals, bb = unit
+    t_app = t_att = 0.0
+    for _ in range(reps):
+        uc = O.UnitCache(Pqk, Pvo, bb, k, np_dt, values=vals, k_value=kv)
+        uc.k_buf.extend(list(c_prev["k_buf"]))
+        uc.v_buf.extend(list(c_prev["v_buf"]))
+        t0 = _t.perf_counter()
+        uc.append(kl, vl)
+        t1 = _t.perf_counter()
+        for q in qs:
+            O.attend_arrays(q, Pqk, Pvo, c)
+        t2 = _t.perf_counter()
+        t_app += t1 - t0
+        t_att += t2 - t1
+    return t_app, t_att
+
+
+def _oracle_worker(args):
+    """Pool worker: build a unit, wait for every worker, then time `reps` steps on
+    one thread; returns (start, end, reps) on the shared monotonic clock."""
+    import numpy  # noqa: F401  (loaded before the limit, which covers loaded libraries only)
+    from threadpoolctl import threadpool_limits
+
+    import swan_inputs  # noqa: F401
+    from oracle import swan_oracle  # noqa: F401
+
+    wname, u, reps, barrier = args
     with threadpool_limits(limits=1):
-        for rep in range(2):
-            for Pqk, Pvo, c, c_prev, kl, vl, q, k, kv in units:
-                uc = O.UnitCache(Pqk, Pvo, w.buffer, k, np_dt, values=vals, k_value=kv)
-                uc.k_buf.extend(list(c_prev["k_buf"]))
-                uc.v_buf.extend(list(c_prev["v_buf"]))
-                t0 = time.perf_counter()
-                uc.append(kl, vl)  # Algorithm 1: rotate, buffer, evict and prune the oldest
-                t1 = time.perf_counter()
-                O.attend_arrays(q, Pqk, Pvo, c)
-                t2 = time.perf_counter()
-                t_append.append(t1 - t0)
-                t_attend.append(t2 - t1)
-    ta = float(np.median(t_append))
-    tt = float(np.median(t_attend))
-    t_step = w.batch * w.n_kv_heads * ta + w.batch * w.n_q_heads * tt
+        unit = _oracle_unit((wname, u))
+        barrier.wait()
+        t0 = time.perf_counter()
+        _oracle_unit_steps(unit, reps)
+        t1 = time.perf_counter()
+    return t0, t1, reps
+
+
+def cpu_baseline(w, seconds: float = 8.0):
+    """The oracle, as it stands, timed on the host's cores on a bounded sample of the
+    workload: one (sequence, KV head) unit per worker process, each worker doing
+    whole decode steps of its unit (append + attention for the unit's query heads)
+    on one thread for about `seconds`; all workers start together and the rate is
+    their steps over the wall time.  A one-thread run of the same unit comes first
+    and sets the repetition count."""
+    import multiprocessing as mp
+
+    import numpy  # noqa: F401  (loaded before the limit, which covers loaded libraries only)
+    from threadpoolctl import threadpool_limits
+
+    import swan_inputs  # noqa: F401
+    from oracle import swan_oracle  # noqa: F401
+
+    cores = max(1, min(len(os.sched_getaffinity(0)), 16))
+    units_per_step = w.batch * w.n_kv_heads  # one append + G attentions each
+    with threadpool_limits(limits=1):
+        unit = _oracle_unit((w.name, 0))
+        _oracle_unit_steps(unit, 1)  # warm-up
+        t0 = time.perf_counter()
+        ta, tt = _oracle_unit_steps(unit, 3)
+        one = (time.perf_counter() - t0) / 3
+    reps = max(1, int(seconds / one))
+    one_thread = w.batch / (units_per_step * one)
+    ctx = mp.get_context("spawn")
+    with ctx.Manager() as mgr:
+        barrier = mgr.Barrier(cores)
+        with ctx.Pool(cores) as pool:
+            res = pool.map(_oracle_worker, [(w.name, u, reps, barrier) for u in range(cores)])
+    wall = max(r[1] for r in res) - min(r[0] for r in res)
+    unit_steps = sum(r[2] for r in res)
+    value = w.batch * unit_steps / (units_per_step * wall)
     return {
-        "value": w.batch / t_step,
+        "value": value,
         "unit": "decode tokens/s",
-        "cores": 1,
+        "cores": cores,
         "kind": "oracle",
-        "sample": (f"{n_units} (sequence, head) units at L={L}: oracle append of the current "
-                   f"token ({ta * 1e3:.2f} ms median) and attention ({tt * 1e3:.1f} ms median), "
-                   f"scaled to {w.batch}x{w.n_kv_heads} appends + {w.batch}x{w.n_q_heads} "
-                   f"attentions per step; numpy float64, one thread"),
+        "sample": (f"{cores} (sequence, KV head) units at L={w.context}, one per worker process "
+                   f"on one thread each, {reps} decode steps per unit (append of the current "
+                   f"token {ta / 3 * 1e3:.2f} ms + {w.group} attention(s) {tt / 3 * 1e3:.1f} ms "
+                   f"on one thread), {wall:.1f} s wall; scaled to the step's "
+                   f"{units_per_step} units; numpy float64"),
+        "one_thread": {"value": one_thread, "unit": "decode tokens/s", "cores": 1},
         "host_cpu": cpu_model(),
         "host_threads_available": len(os.sched_getaffinity(0)),
     }
@@ -337,8 +444,15 @@ def main():
     qs = [si.queries_device(w.wid, w.batch, w.n_q_heads, w.dtype, dev, step=i)
           for i in range(n_extra)]
     capacity = max(w.context + n_extra - w.buffer, 1)
-    cache = swan.SwanCache(w.batch, w.n_q_heads, w.n_kv_heads, w.buffer, capacity, ks, tdt, dev,
-                           sparse_values=w.sparse_values, k_value=kvs)
+    # A step whose bytes fit the 256 MB last-level (MALL) cache would be timed
+    # partly out of that cache if it read the same cache every step; the steps then
+    # rotate over replicas, whose pages together exceed it.
+    step_bytes = attention_bytes(w, [w.context] * w.batch, ks, kv_list, esize)
+    n_rep = args.replicas or (8 if step_bytes < MALL_BYTES else 1)
+    caches = [swan.SwanCache(w.batch, w.n_q_heads, w.n_kv_heads, w.buffer, capacity, ks, tdt,
+                             dev, sparse_values=w.sparse_values, k_value=kvs)
+              for _ in range(n_rep)]
+    cache = caches[0]
     torch.cuda.synchronize()
     log(f"[bench] inputs ready in {time.perf_counter() - t:.1f}s "
         f"(raw K/V {2 * Kp.numel() * esize / 1e9:.2f} GB, "
@@ -356,11 +470,13 @@ def main():
         for k, kv in zip(ks, kv_list))
     log(f"[bench] prefill compress of {L0} tokens: {t_prefill * 1e3:.2f} ms "
         f"({prefill_bytes / t_prefill / 1e9:.0f} GB/s algorithmic)")
+    for c in caches[1:]:
+        c.append(Kp, Vp, Pqk, Pvo)
     del Kp, Vp
     torch.cuda.empty_cache()
 
     # workspace sized for the longest step, allocated before timing
-    final_len = [L + n_extra for L in cache.seq_len]
+    final_len = [L + n_extra for L in cache.seq_len]  # every replica appends at most n_extra
     ws = torch.empty(swan.decode_workspace_bytes(cache.desc, final_len, ks, kvs),
                      dtype=torch.uint8, device=dev)
     ws_need = max(swan.decode_workspace_bytes(cache.desc, [L + i for L in cache.seq_len], ks, kvs)
@@ -369,9 +485,10 @@ def main():
     out = torch.empty((w.batch, w.n_q_heads, 128), dtype=tdt, device=dev)
 
     def step(i, evs=None, breakdown=False):
-        """One decode step; evs[2] / evs[3] bracket the attention launches (recorded by
-        the library on their stream), and with breakdown evs[0], [1], [4] bracket the
-        compress-append and the whole decode call."""
+        """One decode step on replica i % n_rep; evs[2] / evs[3] bracket the attention
+        launches (recorded by the library on their stream), and with breakdown evs[0],
+        [1], [4] bracket the compress-append and the whole decode call."""
+        cache = caches[i % n_rep]
         if breakdown:
             evs[0].record()
         cache.append(step_k[i], step_v[i], Pqk, Pvo)
@@ -403,7 +520,7 @@ def main():
     t0 = time.perf_counter()
     for j in range(args.steps):
         step(args.warmup + j, evs[j])
-        lens.append(list(cache.seq_len))
+        lens.append(list(caches[(args.warmup + j) % n_rep].seq_len))
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     # untimed steps for the compress / decode breakdown
@@ -426,6 +543,10 @@ def main():
     log(f"[bench] step {wall / args.steps * 1e3:.3f} ms wall; compress {np.mean(t_comp) * 1e3:.3f} ms, "
         f"decode {dec_avg * 1e3:.3f} ms, attention kernel {attn_avg * 1e3:.3f} ms "
         f"= {achieved:.0f} GB/s ({achieved / HBM_PEAK_GBPS * 100:.1f}% of 8 TB/s)")
+    ceiling = streaming_ceiling(torch, caches, dev)
+    log(f"[bench] streaming-read ceiling over the same page arrays: {ceiling['gbps']:.0f} GB/s "
+        f"({ceiling['gbps'] / HBM_PEAK_GBPS * 100:.1f}% of 8 TB/s); attention kernel at "
+        f"{achieved / ceiling['gbps'] * 100:.1f}% of it")
 
     if args.probe_copy:
         n = args.probe_copy // 4
@@ -451,7 +572,7 @@ def main():
 
     layer = None
     if args.layer:
-        del cache
+        del cache, caches
         torch.cuda.empty_cache()
         layer = time_layer(swan, torch, si, w, Pqk, Pvo, ks, kvs, dev, args.warmup, args.steps)
         log(f"[bench] layer decode step (hidden {layer['hidden']}): {layer['step_ms']:.3f} ms, "
@@ -460,7 +581,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         t = time.perf_counter()
-        cpu = cpu_baseline(w, args.cpu_units)
+        cpu = cpu_baseline(w, args.cpu_seconds)
         log(f"[bench] cpu baseline in {time.perf_counter() - t:.1f}s: {cpu['value']:.2f} tokens/s")
 
     result = {
@@ -474,7 +595,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f32",  # the arithmetic: scores, softmax and accumulation in float32
+        "storage_dtype": w.dtype if w.sparse_values != "e4m3" else f"{w.dtype}+e4m3",
         "data": "synthetic (seeded low-rank K/V recipe, N(0,1) queries; no dataset or weights)",
         "config": {
             "workload": w.name, "batch": w.batch, "n_q_heads": w.n_q_heads,
@@ -498,6 +620,14 @@ def main():
             "algorithmic_bytes_per_launch": bytes_avg,
             "avg_launch_ms": attn_avg * 1e3,
             "source_digest": digest,
+            "replicas": n_rep,
+            # the same page arrays read by a kernel that only streams them with the
+            # attention kernels' load form (libswanbench.so, swan_stream_read)
+            "ceiling_gbps": ceiling["gbps"],
+            "frac_of_ceiling": achieved / ceiling["gbps"],
+            "ceiling_bytes": ceiling["bytes"],
+            "ceiling_shape": {k: ceiling[k] for k in ("waves", "loads_in_flight",
+                                                     "launches_per_pass")},
         },
         "cpu_baseline": cpu,
         "detail": {

@@ -1,4 +1,5 @@
-"""Build libswan.so (the HIP kernels and the C ABI) for gfx950 with hipcc.
+"""Build libswan.so (the HIP kernels and the C ABI) for gfx950 with hipcc, and
+libswanbench.so (the streaming-read ceiling that bench.py measures beside it).
 
 Usage: python -m paper_2511_18936_amd.build   (or build() from Python)
 The library is written next to this file, in-tree.
@@ -13,6 +14,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libswan.so")
+# measurement support (the streaming-read ceiling), a library of its own
+BENCH_LIB = os.path.join(HERE, "libswanbench.so")
+BENCH_SOURCES = ["stream_ceiling.hip"]
 SOURCES = ["swan_api.hip", "decode.hip", "decode_gqa.hip", "decode_asym.hip",
            "decode_gqa_asym.hip", "compress.hip", "prefill.hip", "change_k.hip", "rope.hip",
            "calibrate.hip"]
@@ -62,6 +66,10 @@ def build(verbose: bool = False, extra=()) -> str:
     _run([hipcc(), *FLAGS, *extra, *[obj for _, obj in jobs], "-o", tmp,
           "-Wl,-rpath,/opt/rocm/lib"], verbose)
     os.replace(tmp, LIB)
+    tmp = BENCH_LIB + ".tmp"
+    _run([hipcc(), *FLAGS, *extra, f"-I{INCLUDE}", *[os.path.join(CSRC, s) for s in BENCH_SOURCES],
+          "-o", tmp, "-Wl,-rpath,/opt/rocm/lib"], verbose)
+    os.replace(tmp, BENCH_LIB)
     return LIB
 
 

@@ -155,12 +155,12 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
     PageRegs<T, KP8> ka, kb;
     load_page<T, KP8>(ka, kbase + pbeg * pbytes, lane, n8);
     for (int p = pbeg; p < pend; p += 2) {
-      const int p1 = p + 1 < plast ? p + 1 : plast;
-      load_page<T, KP8>(kb, kbase + p1 * pbytes, lane, n8);
+      const bool in1 = p + 1 <= plast;  // past the split: the resident spare arrays
+      load_page<T, KP8>(kb, kbase + (in1 ? p + 1 : plast) * pbytes, lane, in1 ? n8 : 0);
       gqa_scores<T, KP8, GH>(ka, p * kPage + lane < S, sh, (p - pbeg) & 1, lane, m, l, first);
       __syncthreads();
-      const int p2 = p + 2 < plast ? p + 2 : plast;
-      load_page<T, KP8>(ka, kbase + p2 * pbytes, lane, n8);
+      const bool in2 = p + 2 <= plast;
+      load_page<T, KP8>(ka, kbase + (in2 ? p + 2 : plast) * pbytes, lane, in2 ? n8 : 0);
       if (p + 1 < pend) {
         gqa_scores<T, KP8, GH>(kb, (p + 1) * kPage + lane < S, sh, (p + 1 - pbeg) & 1, lane, m, l,
                                first);
@@ -185,13 +185,13 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
     PageRegs<T, KP8> va, vb;
     load_page<T, KP8>(va, vbase + pbeg * pbytes, lane, n8);
     for (int p = pbeg; p < pend; p += 2) {
-      const int p1 = p + 1 < plast ? p + 1 : plast;
-      load_page<T, KP8>(vb, vbase + p1 * pbytes, lane, n8);
+      const bool in1 = p + 1 <= plast;  // past the split: the resident spare arrays
+      load_page<T, KP8>(vb, vbase + (in1 ? p + 1 : plast) * pbytes, lane, in1 ? n8 : 0);
       gqa_scatter<T, KP8>(va, p * kPage + lane < S, sh, lane);
       __syncthreads();
       gqa_mfma<GH, T>(sh, (p - pbeg) & 1, lane, acc);
-      const int p2 = p + 2 < plast ? p + 2 : plast;
-      load_page<T, KP8>(va, vbase + p2 * pbytes, lane, n8);
+      const bool in2 = p + 2 <= plast;
+      load_page<T, KP8>(va, vbase + (in2 ? p + 2 : plast) * pbytes, lane, in2 ? n8 : 0);
       if (p + 1 < pend) {
         gqa_scatter<T, KP8>(vb, (p + 1) * kPage + lane < S, sh, lane);
         __syncthreads();

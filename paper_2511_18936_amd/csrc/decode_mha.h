@@ -49,8 +49,10 @@ struct UnitPages {
 };
 
 // One wave: pages [pbeg, pend) of one (sequence, kv head), for one query head.
-// The next page is always loaded (clamped to the last page) so that no load
-// sits under a branch and the compiler can keep one page in flight.
+// The next page is always loaded so that no load sits under a branch and the
+// compiler can keep one page in flight; past the split's last page that load
+// reads the small resident spare arrays instead (n8 = 0: value 0, index
+// kSpareRow), which stay in cache, and its registers are never used.
 template <typename T, int KP8>
 __device__ void sparse_split(const UnitPages& u, int pbeg, int pend, int S, float* qrep,
                              float* acc, int lane, float* __restrict__ part) {
@@ -65,13 +67,15 @@ __device__ void sparse_split(const UnitPages& u, int pbeg, int pend, int S, floa
     load_page<T, KP8>(ka, u.kbase + pbeg * u.kbytes, lane, u.nk8);
     load_page<T, KP8>(va, u.vbase + pbeg * u.vbytes, lane, u.nv8);
     for (int p = pbeg; p < pend; p += 2) {
-      const int p1 = p + 1 < plast ? p + 1 : plast;
-      load_page<T, KP8>(kb, u.kbase + p1 * u.kbytes, lane, u.nk8);
-      load_page<T, KP8>(vb, u.vbase + p1 * u.vbytes, lane, u.nv8);
+      const bool in1 = p + 1 <= plast;  // uniform
+      const int p1 = in1 ? p + 1 : plast;
+      load_page<T, KP8>(kb, u.kbase + p1 * u.kbytes, lane, in1 ? u.nk8 : 0);
+      load_page<T, KP8>(vb, u.vbase + p1 * u.vbytes, lane, in1 ? u.nv8 : 0);
       process_page<T, KP8>(ka, va, p * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
-      const int p2 = p + 2 < plast ? p + 2 : plast;
-      load_page<T, KP8>(ka, u.kbase + p2 * u.kbytes, lane, u.nk8);
-      load_page<T, KP8>(va, u.vbase + p2 * u.vbytes, lane, u.nv8);
+      const bool in2 = p + 2 <= plast;
+      const int p2 = in2 ? p + 2 : plast;
+      load_page<T, KP8>(ka, u.kbase + p2 * u.kbytes, lane, in2 ? u.nk8 : 0);
+      load_page<T, KP8>(va, u.vbase + p2 * u.vbytes, lane, in2 ? u.nv8 : 0);
       if (p + 1 < pend)
         process_page<T, KP8>(kb, vb, (p + 1) * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
     }

@@ -319,3 +319,18 @@ def test_binding_checks_tensors_before_the_call():
     rejects(lambda: swan.decode_attention_noalloc(d, [5, 5], [48, 48], q, P, P, q[:1]), "shape")
     d32 = _desc(dtype=swan.SWAN_F32)
     rejects(lambda: swan.decode_attention(d32, [5, 5], [48, 48], q, P, P, q, ws), "float32")
+
+
+def test_bench_library_exports_its_header():
+    """libswanbench.so (the streaming-read ceiling bench.py measures) exports what
+    include/swan_bench.h declares."""
+    import subprocess
+
+    with open(os.path.join(ROOT, "include", "swan_bench.h")) as f:
+        declared = re.findall(r"^\s*int32_t\s+(swan_\w+)\(", f.read(), re.M)
+    assert declared == ["swan_stream_read"]
+    path = os.path.join(ROOT, "paper_2511_18936_amd", "libswanbench.so")
+    out = subprocess.run(["nm", "-D", "--defined-only", path], capture_output=True, text=True,
+                         check=True).stdout
+    for name in declared:
+        assert re.search(rf"\bT {name}\b", out), name
