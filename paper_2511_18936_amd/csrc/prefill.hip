@@ -2,23 +2,39 @@
 // values fp16 or E4M3).
 //
 // Same result as token-by-token Algorithm 1 (and as insert_kernel): each new
-// key/value is rotated exactly (float64 products and sums) and rounded once
-// to fp16; tokens that stay in the buffer go to their ring slot, the others
-// are pruned to their top-k magnitudes (ties: lower index) and packed.
+// key/value x is rotated, x_hat = x . P, and the exact x_hat is rounded once to
+// fp16; tokens that stay in the buffer go to their ring slot, the others are
+// pruned to their top-k magnitudes (ties: lower index) and packed.
 //
-// One wave handles 64-position blocks of one (sequence, kv head, role):
-//   rotation   on MFMA in float64 (v_mfma_f64_16x16x4f64): 16 tokens x 32
-//              output dims per pass, the contraction dim permuted so that a
-//              lane reads 32 contiguous input values of its token row; the
-//              lane's B operands (its 2 x 32 entries of P for one quarter of
-//              the output dims) are held in registers across the block's 4
-//              passes of 16 tokens
+// The rotation runs on int8 MFMA (v_mfma_i32_16x16x64_i8) with exact integer
+// arithmetic.  Each token row is a fixed-point integer X (30 bits below a
+// power of two above the row's largest magnitude) and P a fixed-point integer
+// Y (38 bits below a power of two above its largest entry), each split into
+// balanced base-256 digits (4 for X, 5 for Y, every digit in [-128, 127]).
+// The digit products are accumulated exactly in int32, one accumulator per
+// digit weight; the 17 digit pairs whose weight is within 5 digits of the top
+// give x_hat up to a bounded remainder: the 3 dropped pairs (below 2^-38 of
+// the two powers of two's product), plus the truncation of tiny entries of x
+// (counted per row) or of P (bounded per column).  An element is certified
+// when no fp16 rounding boundary lies within that bound of the computed
+// value; the rare rest (about 7 in 10^6 elements on the benchmark inputs) is
+// recomputed in float64.  Either way the stored value is the exact x_hat
+// rounded once to fp16.
+//
+// A workgroup of 4 waves serves one (sequence, kv head, role): it first
+// writes P's digits, in the MFMA operand layout, to LDS (80 KiB), then each
+// wave handles its own 64-position blocks:
+//   rotation   per pair of 16-token tiles: x digits in registers (A
+//              operands), per 16 output dims the 5 P digits from LDS (B
+//              operands) and 68 MFMAs, then the certified fp16 values into
+//              an LDS row per token
 //   selection  one token per lane on its 128 stored values: a radix select
-//              on bit planes of the magnitudes finds the k-th largest, then
-//              one in-order pass emits the kept pairs (and the padding) into
-//              an LDS copy of the page
-//   output     each lane stores its own 16-byte slot chunks of the page (a
-//              wave store is 1 KiB contiguous), or its dense row to the ring
+//              on bit planes of the magnitudes finds the kept dims (a 128-bit
+//              mask; ties at the k-th largest to the lower dim)
+//   output     each lane walks its kept dims in ascending order, reads their
+//              values from its LDS row and stores its page slot chunk by
+//              chunk (a wave store is 1 KiB contiguous), or its dense row to
+//              the ring
 #include <type_traits>
 
 #include "swan_device.h"
@@ -26,14 +42,26 @@
 
 namespace swan {
 
-typedef double d4 __attribute__((ext_vector_type(4)));
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kRowHalves = 136;                // LDS row of one token's 128 fp16 values (+ pad)
-constexpr int kPrefillBlocksPerWave = 4;       // 64-position blocks per wave
+constexpr int kPrefillBlocksPerWave = 8;       // 64-position blocks per wave
+constexpr int kPrefillWaves = 4;               // waves per workgroup, sharing P's digits
 constexpr int kXcds = 8;                       // MI355X: 8 XCDs, each with its own L2
-constexpr int kStageBytes = 64 * kRowHalves * 2;  // the rows, then the page copy
-// a page (64 * k_pad * 3 bytes) fits the copy up to k_pad 88; above, values and
-// indices are emitted and stored in two rounds
+constexpr int kStageBytes = 64 * kRowHalves * 2;  // the rows of one wave
+// digit arithmetic of the rotation
+constexpr int kXDigits = 4;                    // x: balanced base-256 digits
+constexpr int kPDigits = 5;                    // P: balanced base-256 digits
+constexpr int kXFix = 8 * kXDigits - 2;        // |X| < 2^30
+constexpr int kPFix = 8 * kPDigits - 2;        // |Y| < 2^38
+constexpr int kTopLevel = 5;                   // digit pairs (s, t) with s + t <= 5 ...
+constexpr int kLevels = kTopLevel + 1;         // ... accumulated per weight s + t
+// The 3 dropped pairs, (2,4) and (3,3) of weight 2^8 and (3,4) of weight 1 in
+// units of the lowest digit product: each sums 128 products of at most 2^14.
+constexpr double kDroppedUnits = (2.0 * 256.0 + 1.0) * 128.0 * 16384.0;
+constexpr int kBDigBytes = 8 * 2 * kPDigits * 1024;   // [out tile][k step][digit][lane][16 B]
+constexpr int kPrefillLds = kBDigBytes + kPrefillWaves * kStageBytes + 128 * 4 + 64;
+constexpr uint16_t kUncertain = 0xFFFFu;       // a NaN pattern: never a rounded x_hat
 
 // One step of a 16x16 bit-matrix transpose applied to both 16-bit halves of
 // 16 words at once (row i of each matrix = half of w[i], column b = bit b):
@@ -49,14 +77,26 @@ __device__ __forceinline__ void transpose_step(uint32_t* w, uint32_t mask) {
   }
 }
 
-// k-th largest of the 128 fp16 magnitudes in v (two per dword), and how many
-// elements equal to it are kept (the rest of the k are strictly larger).
-// Radix select on bit planes: the magnitudes of each 32-element chunk c are
-// transposed so that pl[b][c] holds bit b of each element (bits 0-15: the
-// chunk's even elements, 16-31: its odd ones); from the top bit down, the
-// candidates still equal to the threshold prefix are split by the next bit.
-__device__ __forceinline__ void kth_magnitude(const uint32_t* v, int k, uint32_t& tau,
-                                              int& need_eq) {
+// Bits 0-15 of a bit-plane word stand for a chunk's even dims, bits 16-31 for
+// its odd ones; this puts them in dim order (bit i = dim 32 c + i).
+__device__ __forceinline__ uint32_t spread16(uint32_t x) {
+  x = (x | (x << 8)) & 0x00FF00FFu;
+  x = (x | (x << 4)) & 0x0F0F0F0Fu;
+  x = (x | (x << 2)) & 0x33333333u;
+  return (x | (x << 1)) & 0x55555555u;
+}
+__device__ __forceinline__ uint32_t dim_order(uint32_t w) {
+  return spread16(w & 0xFFFFu) | (spread16(w >> 16) << 1);
+}
+
+// The k dims kept from the 128 fp16 magnitudes in v (two per dword): the k
+// largest, ties at the k-th largest to the lower dim, as a 128-bit mask in dim
+// order.  Radix select on bit planes: the magnitudes of each 32-element chunk
+// c are transposed so that pl[b][c] holds bit b of each element (bits 0-15:
+// the chunk's even elements, 16-31: its odd ones); from the top bit down, the
+// candidates still equal to the threshold prefix are split by the next bit,
+// and those above it are collected.
+__device__ __forceinline__ void kept_dims(const uint32_t* v, int k, uint32_t* kept) {
   uint32_t pl[15][4];
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
@@ -70,9 +110,8 @@ __device__ __forceinline__ void kth_magnitude(const uint32_t* v, int k, uint32_t
 #pragma unroll
     for (int b = 0; b < 15; ++b) pl[b][c] = w[b];  // plane 15 (the sign) is zero
   }
-  uint32_t eq[4] = {~0u, ~0u, ~0u, ~0u};
-  int gt = 0;
-  uint32_t t = 0;
+  uint32_t eq[4] = {~0u, ~0u, ~0u, ~0u}, gt[4] = {0u, 0u, 0u, 0u};
+  int ngt = 0;
 #pragma unroll
   for (int b = 14; b >= 0; --b) {
     uint32_t hi[4];
@@ -82,59 +121,155 @@ __device__ __forceinline__ void kth_magnitude(const uint32_t* v, int k, uint32_t
       hi[c] = eq[c] & pl[b][c];
       cnt += __popc(hi[c]);
     }
-    const bool one = gt + cnt >= k;  // the k-th largest has this bit set
-    t |= one ? (1u << b) : 0u;
-    gt += one ? 0 : cnt;
+    const bool one = ngt + cnt >= k;  // the k-th largest has this bit set
+    ngt += one ? 0 : cnt;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) eq[c] = one ? hi[c] : (eq[c] & ~pl[b][c]);
-  }
-  tau = t;
-  need_eq = k - gt;
-}
-
-// One token per lane: its kept (value, index) pairs in ascending index
-// order, then the padding (value +0 at the lowest unselected dims), written
-// into the LDS page copy at the lane's offsets: values [kp/8][64][CB] at sv
-// (fp16 bits, or their E4M3 codes), indices [kp/8][64][8 B] at si.
-template <typename F, bool kVals, bool kIdx>
-__device__ __forceinline__ void emit_slots(const uint32_t* v, uint32_t tau, int need_eq, int k,
-                                           int npad, char* sv, uint8_t* si) {
-  constexpr bool kE4M3 = std::is_same<F, E4M3V>::value;
-  auto put = [&](int e, uint32_t hb) {
-    if constexpr (kE4M3)
-      ((uint8_t*)sv)[(e >> 3) * 512 + (e & 7)] = (uint8_t)f16_bits_to_e4m3(hb);
-    else
-      ((uint16_t*)sv)[(e >> 3) * 512 + (e & 7)] = (uint16_t)hb;
-  };
-  int e = 0, eq = 0, pad = 0;
-#pragma unroll
-  for (int j = 0; j < kD; ++j) {
-    const uint32_t hb = (v[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu;
-    const uint32_t m = hb & 0x7FFFu;
-    const bool tie = m == tau;
-    const bool sel = m > tau || (tie && eq < need_eq);
-    eq += tie ? 1 : 0;
-    if (sel) {
-      if (kVals) put(e, hb);
-      if (kIdx) si[(e >> 3) * 512 + (e & 7)] = (uint8_t)j;
-      ++e;
-    } else if (pad < npad) {
-      const int ep = k + pad;
-      if (kVals) put(ep, 0u);
-      if (kIdx) si[(ep >> 3) * 512 + (ep & 7)] = (uint8_t)j;
-      ++pad;
+    for (int c = 0; c < 4; ++c) {
+      gt[c] |= one ? 0u : hi[c];
+      eq[c] = one ? hi[c] : (eq[c] & ~pl[b][c]);
     }
   }
+  // eq: the elements equal to the k-th largest; k - ngt of them are kept,
+  // lowest dims first
+  int need = k - ngt;
+  int neq = 0;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    eq[c] = dim_order(eq[c]);
+    neq += __popc(eq[c]);
+  }
+  if (neq > need) {  // ties: keep the lowest need of them
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      uint32_t keep = 0u, rest = eq[c];
+      while (need > 0 && rest != 0u) {
+        keep |= rest & (0u - rest);
+        rest &= rest - 1u;
+        --need;
+      }
+      eq[c] = keep;
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < 4; ++c) kept[c] = dim_order(gt[c]) | eq[c];
+}
+
+// The lowest set dim of the 128-bit mask (lo: dims 0-63, hi: 64-127), cleared.
+__device__ __forceinline__ int pop_lowest(uint64_t& lo, uint64_t& hi) {
+  const bool in_lo = lo != 0ull;
+  const int d = in_lo ? __builtin_ctzll(lo) : 64 + __builtin_ctzll(hi);
+  lo = in_lo ? lo & (lo - 1ull) : lo;
+  hi = in_lo ? hi : hi & (hi - 1ull);
+  return d;
+}
+
+// One token per lane: its page slot, written to global memory chunk by chunk
+// (a wave's chunk store is 1 KiB, or 512 B, contiguous).  Entries 0..k-1 are
+// the kept dims in ascending order with their values, read from the lane's
+// LDS row; entries k..kp-1 the padding, value +0 at the lowest dims not kept.
+template <typename F>
+__device__ __forceinline__ void store_slot(const uint16_t* row, const uint32_t* kept, int k,
+                                           int kp, char* page, int lane) {
+  constexpr int VB = Fmt<F>::kValBytes;
+  constexpr bool kE4M3 = std::is_same<F, E4M3V>::value;
+  uint64_t klo = kept[0] | ((uint64_t)kept[1] << 32), khi = kept[2] | ((uint64_t)kept[3] << 32);
+  uint64_t flo = ~klo, fhi = ~khi;
+  char* ipage = page + 64 * kp * VB;
+  for (int c = 0; c < kp / 8; ++c) {
+    uint32_t val[4] = {0u, 0u, 0u, 0u}, idx[2] = {0u, 0u};
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int e = 8 * c + q;  // uniform
+      uint32_t hb = 0u, d;
+      if (e < k) {
+        d = (uint32_t)pop_lowest(klo, khi);
+        hb = row[d];
+      } else {
+        d = (uint32_t)pop_lowest(flo, fhi);
+      }
+      idx[q >> 2] |= d << (8 * (q & 3));
+      if constexpr (kE4M3)
+        val[q >> 2] |= f16_bits_to_e4m3(hb) << (8 * (q & 3));
+      else
+        val[q >> 1] |= hb << (16 * (q & 1));
+    }
+    if constexpr (kE4M3)
+      *(u32x2*)(page + c * 512 + lane * 8) = u32x2{val[0], val[1]};
+    else
+      *(u32x4*)(page + c * 1024 + lane * 16) = u32x4{val[0], val[1], val[2], val[3]};
+    *(u32x2*)(ipage + c * 512 + lane * 8) = u32x2{idx[0], idx[1]};
+  }
+}
+
+// v_perm_b32: byte i of the result is byte sel_i of the 8 bytes {hi : lo}
+__device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel) {
+  return __builtin_amdgcn_perm(hi, lo, sel);
+}
+
+// The balanced base-256 digits of four fixed-point values, as four int8 words
+// (digit 0 = the top one).  yb = X + 0x808080: its low three bytes are the low
+// digits plus 128, its top byte the top digit (two's complement).
+__device__ __forceinline__ void digit_words(uint32_t a, uint32_t b, uint32_t c, uint32_t d,
+                                            uint32_t* w) {
+  const uint32_t ab_lo = perm(b, a, 0x05010400u), ab_hi = perm(b, a, 0x07030602u);
+  const uint32_t cd_lo = perm(d, c, 0x05010400u), cd_hi = perm(d, c, 0x07030602u);
+  w[3] = perm(cd_lo, ab_lo, 0x05040100u) ^ 0x80808080u;
+  w[2] = perm(cd_lo, ab_lo, 0x07060302u) ^ 0x80808080u;
+  w[1] = perm(cd_hi, ab_hi, 0x05040100u) ^ 0x80808080u;
+  w[0] = perm(cd_hi, ab_hi, 0x07060302u);
+}
+
+// fixed-point value of one fp16 element: trunc(x * 2^shift) + 0x808080
+__device__ __forceinline__ uint32_t fixed_biased(uint32_t hbits, int shift) {
+  const float f = f16_bits_to_f32(hbits);
+  return (uint32_t)(int32_t)__builtin_ldexpf(f, shift) + 0x00808080u;
+}
+
+// The fp16 rounding of a value y known to within E: y's own rounding when no
+// fp16 rounding boundary lies within E of it, else kUncertain.  Branch-free:
+// y is rounded to float32 with round-to-odd (round to nearest, then back
+// toward zero and the last bit set when that was inexact), which keeps the
+// information that the hardware float32 -> fp16 rounding needs to round y
+// itself correctly; the distance to the boundary is measured in float64.
+__device__ __forceinline__ uint32_t certified_f16(double y, double E) {
+  const float yn = (float)y;
+  const double back = (double)yn;
+  const bool inexact = back != y;
+  const bool away = fabs(back) > fabs(y);
+  float y32 = __uint_as_float((__float_as_uint(yn) - (inexact && away ? 1u : 0u)) |
+                              (inexact ? 1u : 0u));
+  asm("" : "+v"(y32));  // two hardware conversions, not one software f64 -> f16
+  const uint32_t hb = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)y32);
+  const uint32_t ex = (hb >> 10) & 31u;
+  const double hd = (double)f16_bits_to_f32(hb);
+  const double dist = fabs(y - hd);  // exact
+  // half the spacing of fp16 values at hb on y's side: below a power of two the
+  // spacing halves.  (E < half / 2 keeps the other side's boundary out of reach
+  // too.)
+  const double half = ex ? __builtin_ldexp(1.0, (int)ex - 26) : 0x1p-25;
+  const bool below_pow2 = (hb & 0x3FFu) == 0u && ex > 1u && fabs(y) < fabs(hd);
+  const double side = below_pow2 ? 0.5 * half : half;
+  const bool ok = (ex != 31u) & (dist + E + fabs(y) * 0x1p-50 < side) & (E < 0.25 * half);
+  return ok ? hb : kUncertain;
+}
+
+__device__ __forceinline__ double wave_sum_f64(double v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
 }
 
 template <typename F>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void prefill_kernel(CompressLaunch a) {
   constexpr int VB = Fmt<F>::kValBytes, CB = Fmt<F>::kChunkBytes;
-  __shared__ __attribute__((aligned(16))) char lds[kStageBytes];
-  _Float16* rows = (_Float16*)lds;  // [64 tokens][kRowHalves], then reused as the page copy
-  const int lane = threadIdx.x;
-  const int q = lane >> 4, r16 = lane & 15;
+  extern __shared__ __attribute__((aligned(16))) char lds_all[];
+  char* bdig = lds_all;
+  float* colDY = (float*)(lds_all + kBDigBytes + kPrefillWaves * kStageBytes);  // [128]
+  float* wgred = colDY + 128;                                                  // [4]
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  char* lds = lds_all + kBDigBytes + wave * kStageBytes;  // this wave's rows / page copy
+  _Float16* rows = (_Float16*)lds;  // [64 tokens][kRowHalves]
+  const int m16 = lane & 15, g4 = lane >> 4;
   // grid: (b, h, role, block group)
   // Workgroups go to the 8 XCDs round-robin by id, so XCD id % 8 gets the
   // (head, role) pairs u = xcd, xcd + 8, ...: its L2 then holds 1/8 of the P
@@ -155,15 +290,57 @@ void prefill_kernel(CompressLaunch a) {
   const int len_new = len_old + nnew;
   const int blk0 = len_old / kPage;
   const int blk1 = (len_new - 1) / kPage;  // inclusive
-  const int bbeg = blk0 + grp * kPrefillBlocksPerWave;
-  if (bbeg > blk1) return;
-  const int bend = min(bbeg + kPrefillBlocksPerWave, blk1 + 1);
+  if (blk0 + grp * kPrefillWaves * kPrefillBlocksPerWave > blk1) return;  // uniform
 
   const _Float16* x = (const _Float16*)(role ? a.v_new : a.k_new) +
                       ((int64_t)b * a.Hkv + h) * a.n_new * kD;
-  // NULL P_vo: values already in the rotated basis; the rotation is then by I
+  // NULL P_vo: values already in the rotated basis, stored as given
   const float* Prole = role ? a.P_vo : a.P_qk;
   const float* P = Prole ? Prole + (int64_t)h * kD * kD : nullptr;
+
+  // ---- P's digits (once per workgroup) ----
+  int G = 0;         // Y = trunc(P * 2^G), |Y| < 2^38
+  float pmax = 0.f;  // largest |P|
+  if (P) {
+    float pm = 0.f;
+    for (int r = 0; r < kD * kD / 256; ++r) pm = fmaxf(pm, fabsf(P[tid + 256 * r]));
+    pm = wave_max(pm);
+    if (lane == 0) wgred[wave] = pm;
+    if (tid < kD) colDY[tid] = 0.f;
+    __syncthreads();
+    pmax = fmaxf(fmaxf(wgred[0], wgred[1]), fmaxf(wgred[2], wgred[3]));
+    int pe = 0;
+    if (pmax > 0.f) (void)__builtin_frexpf(pmax, &pe);  // pmax < 2^pe
+    G = kPFix - pe;
+    // vector v: 16 entries P[k][col], k = 64 ks + 16 g + j, as the 16 bytes of
+    // lane (col % 16) + 16 g of the B operand of output tile col / 16, step ks
+    for (int r = 0; r < 4; ++r) {
+      const int v = tid + 256 * r;
+      const int n = v & 15, g = (v >> 4) & 3, ks = (v >> 6) & 1, o = v >> 7;
+      const int col = 16 * o + n;
+      uint32_t dw[kPDigits][4] = {};
+      double dy = 0.0;
+      for (int j = 0; j < 16; ++j) {
+        const double p = (double)P[(64 * ks + 16 * g + j) * kD + col];
+        double yv = trunc(__builtin_ldexp(p, G));
+        dy = fmax(dy, fabs(p - __builtin_ldexp(yv, -G)));  // exact
+        for (int t = kPDigits - 1; t >= 1; --t) {
+          const double q = floor((yv + 128.0) * (1.0 / 256.0));
+          const int dgt = (int)(yv - 256.0 * q);  // in [-128, 127]
+          dw[t][j >> 2] |= ((uint32_t)dgt & 0xFFu) << (8 * (j & 3));
+          yv = q;
+        }
+        dw[0][j >> 2] |= ((uint32_t)(int)yv & 0xFFu) << (8 * (j & 3));  // |top| <= 64
+      }
+      for (int t = 0; t < kPDigits; ++t)
+        *(u32x4*)(bdig + ((o * 2 + ks) * kPDigits + t) * 1024 + (n + 16 * g) * 16) =
+            u32x4{dw[t][0], dw[t][1], dw[t][2], dw[t][3]};
+      uint32_t dyb = __float_as_uint((float)dy);  // rounded up: a bound
+      if ((double)__uint_as_float(dyb) < dy) dyb += 1u;
+      atomicMax((unsigned int*)&colDY[col], dyb);
+    }
+    __syncthreads();
+  }
 
   const int k = a.tab.kact[role][b];
   const int kp = kpad_of(k);
@@ -171,159 +348,271 @@ void prefill_kernel(CompressLaunch a) {
   char* pages = (char*)(role ? a.v_pages : a.k_pages) + a.tab.page_off[role][b] +
                 (int64_t)h * a.n_pages_cap * pbytes;
   uint16_t* ring = (uint16_t*)(role ? a.v_ring : a.k_ring) + ((int64_t)b * a.Hkv + h) * a.bb * kD;
+  const int bbeg = blk0 + (grp * kPrefillWaves + wave) * kPrefillBlocksPerWave;
+  const int bend = min(bbeg + kPrefillBlocksPerWave, blk1 + 1);
 
   for (int blk = bbeg; blk < bend; ++blk) {
     const int pos0 = blk * kPage;
-    // ---- rotation: 4 quarters of the output dims x 4 passes of 16 tokens,
-    //      results rounded to fp16 into LDS rows ----
+    bool uncertain = false;  // some element of the block needs the float64 path
+    if (P) {
+      // ---- rotation: two 16-token tiles at a time ----
 #pragma unroll 1
-    for (int nh = 0; nh < 4; ++nh) {
-      // B operands of this quarter: pb[nt][ks] = P[32 q + ks][32 nh + 16 nt + r16]
-      float pb[2][32];
+      for (int tp = 0; tp < 2; ++tp) {
+        i32x4 A[2][2][kXDigits];  // [tile][k step][digit]
+        double Eb[2][4];          // per token of the result rows: bound without the P term
+        double Ey[2][4];          // factor of the column's P truncation term
+        double sc[2][4];          // y = H * sc (a power of two)
 #pragma unroll
-      for (int ks = 0; ks < 32; ++ks)
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-          pb[nt][ks] = P ? P[(32 * q + ks) * kD + 32 * nh + 16 * nt + r16]
-                         : (32 * q + ks == 32 * nh + 16 * nt + r16 ? 1.f : 0.f);
-#pragma unroll 1
-      for (int mt = 0; mt < 4; ++mt) {
-        const int tp0 = pos0 + 16 * mt - len_old;  // token index of the pass's first row
-        if (tp0 + 15 < 0 || tp0 >= nnew) continue;  // no new token in this pass (uniform)
-        // A operands: lane (q, r16) holds x[token 16 mt + r16][32 q .. 32 q + 31]
-        u32x4 xv[4];
-        {
-          const int t = tp0 + r16;
+        for (int T = 0; T < 2; ++T) {
+          // lane (m16, g4): token 16 (2 tp + T) + m16, dims 64 ks + 16 g4 + j
+          const int tok = 16 * (2 * tp + T) + m16;
+          const int t = pos0 + tok - len_old;
+          u32x4 xv[2][2];
           if (t >= 0 && t < nnew) {
-            const u32x4* src = (const u32x4*)(x + (int64_t)t * kD + 32 * q);
+            const u32x4* src = (const u32x4*)(x + (int64_t)t * kD + 16 * g4);
 #pragma unroll
-            for (int c = 0; c < 4; ++c) xv[c] = src[c];
+            for (int ks = 0; ks < 2; ++ks) {
+              xv[ks][0] = src[8 * ks];
+              xv[ks][1] = src[8 * ks + 1];
+            }
           } else {
 #pragma unroll
-            for (int c = 0; c < 4; ++c) xv[c] = u32x4{0u, 0u, 0u, 0u};
+            for (int ks = 0; ks < 2; ++ks) xv[ks][0] = xv[ks][1] = u32x4{0u, 0u, 0u, 0u};
           }
-        }
-        d4 acc[2];
+          // the row's largest magnitude (fp16 bits) and the sum of its magnitudes
+          uint32_t mx = 0u;
+          float l1 = 0.f;
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt) acc[nt] = d4{0.0, 0.0, 0.0, 0.0};
+          for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-        for (int ks = 0; ks < 32; ++ks) {
-          const uint32_t wv = xv[ks >> 3][(ks >> 1) & 3];
-          const double av = (double)f16_bits_to_f32((ks & 1) ? (wv >> 16) : (wv & 0xFFFFu));
+            for (int c = 0; c < 2; ++c)
 #pragma unroll
-          for (int nt = 0; nt < 2; ++nt)
-          {
-            float pv = pb[nt][ks];
-            asm volatile("" : "+v"(pv));  // convert per use: as doubles pb would not fit
-            acc[nt] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, (double)pv, acc[nt], 0, 0, 0);
+              for (int q = 0; q < 4; ++q) {
+                const uint32_t wv = xv[ks][c][q];
+                const uint32_t lo = wv & 0x7FFFu, hi = (wv >> 16) & 0x7FFFu;
+                mx = max(mx, max(lo, hi));
+                l1 += f16_bits_to_f32(lo) + f16_bits_to_f32(hi);
+              }
+          mx = max(mx, (uint32_t)__shfl_xor((int)mx, 16));
+          mx = max(mx, (uint32_t)__shfl_xor((int)mx, 32));
+          l1 += __shfl_xor(l1, 16);
+          l1 += __shfl_xor(l1, 32);
+          // max|x| < 2^e
+          const int e = mx == 0u ? 0
+                        : (mx >> 10) ? (int)(mx >> 10) - 14
+                                     : 8 - __builtin_clz(mx);  // (32 - clz) - 24
+          const int shift = kXFix - e;
+          // |x| >= 2^(e - 20) is exact in 30 bits below 2^e; each smaller nonzero
+          // element is truncated by less than 2^(e - 30): count them.  thr: the
+          // fp16 bits of 2^(e - 20), or 0 below the fp16 range (none truncated)
+          const int te = e - kXFix + 10;
+          const uint32_t thr = te >= -14 ? (uint32_t)(te + 15) << 10
+                               : te >= -24 ? 1u << (te + 24) : 0u;
+          int ntr = 0;
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const uint32_t wv = xv[ks][c][q];
+                ntr += ((wv & 0x7FFFu) - 1u < thr - 1u) ? 1 : 0;  // 0 < |x| < 2^(e - 20)
+                ntr += (((wv >> 16) & 0x7FFFu) - 1u < thr - 1u) ? 1 : 0;
+              }
+          ntr += __shfl_xor(ntr, 16);
+          ntr += __shfl_xor(ntr, 32);
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks) {
+            uint32_t dg[kXDigits][4];
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+#pragma unroll
+              for (int q2 = 0; q2 < 2; ++q2) {
+                // values 8 c + 4 q2 .. + 3
+                const uint32_t w0 = xv[ks][c][2 * q2], w1 = xv[ks][c][2 * q2 + 1];
+                uint32_t wd[kXDigits];
+                digit_words(fixed_biased(w0 & 0xFFFFu, shift), fixed_biased(w0 >> 16, shift),
+                            fixed_biased(w1 & 0xFFFFu, shift), fixed_biased(w1 >> 16, shift), wd);
+#pragma unroll
+                for (int s = 0; s < kXDigits; ++s) dg[s][2 * c + q2] = wd[s];
+              }
+#pragma unroll
+            for (int s = 0; s < kXDigits; ++s)
+              A[T][ks][s] = i32x4{(int)dg[s][0], (int)dg[s][1], (int)dg[s][2], (int)dg[s][3]};
           }
-        }
-        // f64 MFMA result layout: register v of lane l holds D[l / 16 + 4 v][l % 16],
-        // i.e. token row q + 4 v of the pass, output dim 32 nh + 16 nt + r16
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
+          // the bound's row terms, for the result lanes: token tok's scale,
+          // dropped-pair bound and truncated-x bound
+          const double sce = __builtin_ldexp(1.0, 16 + e - kXFix - G);
+          const double eb = (kDroppedUnits * __builtin_ldexp(1.0, e - kXFix - G) +
+                             (double)ntr * (double)pmax * __builtin_ldexp(1.0, e - kXFix)) *
+                            (1.0 + 0x1p-40);
+          // sum |x_i|, with room for the float32 additions' rounding (128 terms)
+          const double ey = (double)l1 * (1.0 + 0x1p-15);
+          // move them to the lanes holding the token's results: row r = 4 g + v
+          // of the tile is token m16 = r of the tile
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
-            const uint16_t hb = f64_to_f16_bits_fast(acc[nt][v]);
-            ((uint16_t*)rows)[(16 * mt + q + 4 * v) * kRowHalves + 32 * nh + 16 * nt + r16] = hb;
+            const int src_lane = 4 * g4 + v;  // lane (m16 = 4 g4 + v, g4 = 0) has token 4 g4 + v
+            sc[T][v] = __shfl(sce, src_lane);
+            Eb[T][v] = __shfl(eb, src_lane);
+            Ey[T][v] = __shfl(ey, src_lane);
           }
+        }
+        // ---- MFMA per 16 output dims, then certified fp16 values to the rows;
+        //      the results of tile o are turned into fp16 while the MFMAs of
+        //      tile o + 1 run ----
+        auto mfma_tile = [&](int o, i32x4 (&acc)[2][kLevels]) {
+#pragma unroll
+          for (int T = 0; T < 2; ++T)
+#pragma unroll
+            for (int l = 0; l < kLevels; ++l) acc[T][l] = i32x4{0, 0, 0, 0};
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks) {
+            i32x4 Bd[kPDigits];
+#pragma unroll
+            for (int t = 0; t < kPDigits; ++t)
+              Bd[t] = *(const i32x4*)(bdig + ((o * 2 + ks) * kPDigits + t) * 1024 + lane * 16);
+#pragma unroll
+            for (int T = 0; T < 2; ++T)
+#pragma unroll
+              for (int s = 0; s < kXDigits; ++s)
+#pragma unroll
+                for (int t = 0; t < kPDigits; ++t)
+                  if (s + t <= kTopLevel)
+                    acc[T][s + t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[T][ks][s], Bd[t],
+                                                                          acc[T][s + t], 0, 0, 0);
+          }
+        };
+        // result layout: register v of lane l is row 4 (l / 16) + v (token),
+        // column l % 16 (output dim 16 o + l % 16)
+        auto to_rows = [&](int o, const i32x4 (&acc)[2][kLevels]) {
+          const int col = 16 * o + m16;
+          const double dyc = (double)colDY[col];
+#pragma unroll
+          for (int T = 0; T < 2; ++T)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              // H = sum_l C_l 256^(5 - l): levels 0-1 and 2-3 combine exactly
+              // in int32 (|C_0| <= 2^21, |C_2| <= 3 * 2^21, |C_l| <= 2^23), the
+              // rest in float64 (exact below 2^53, else within 2^-52 |H|)
+              const int t01 = acc[T][0][v] * 256 + acc[T][1][v];
+              const int t23 = acc[T][2][v] * 256 + acc[T][3][v];
+              double H = fma((double)t01, 65536.0, (double)t23);
+              H = fma(H, 256.0, (double)acc[T][4][v]);
+              H = fma(H, 256.0, (double)acc[T][5][v]);
+              const double y = H * sc[T][v];
+              const double E = fma(dyc, Ey[T][v], Eb[T][v]) * (1.0 + 0x1p-40);
+              const uint32_t hb = certified_f16(y, E);
+              uncertain |= hb == kUncertain;
+              const int tok = 16 * (2 * tp + T) + 4 * g4 + v;
+              ((uint16_t*)rows)[tok * kRowHalves + col] = (uint16_t)hb;
+            }
+        };
+        i32x4 accA[2][kLevels], accB[2][kLevels];
+        mfma_tile(0, accA);
+#pragma unroll 1
+        for (int o = 0; o < 8; o += 2) {
+          mfma_tile(o + 1, accB);
+          to_rows(o, accA);
+          if (o + 2 < 8) mfma_tile(o + 2, accA);
+          to_rows(o + 1, accB);
+        }
+      }
+    } else {
+      // values given in the rotated basis: the rows are the input
+      const int t = pos0 + lane - len_old;
+      u32x4* dst = (u32x4*)(rows + lane * kRowHalves);
+      if (t >= 0 && t < nnew) {
+        const u32x4* src = (const u32x4*)(x + (int64_t)t * kD);
+#pragma unroll
+        for (int c = 0; c < 16; ++c) dst[c] = src[c];
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
+    if (__ballot(uncertain) != 0) {
+      // The rare uncertain elements: x_hat in float64 over the input row and P,
+      // rounded once.  The wave takes them one at a time, each lane summing the
+      // products of two input dims.
+      const int t = pos0 + lane - len_old;
+      uint16_t* myrow = (uint16_t*)(rows + lane * kRowHalves);
+      uint32_t um[4] = {0u, 0u, 0u, 0u};  // this lane's uncertain dims
+      if (t >= 0 && t < nnew)
+        for (int j = 0; j < kD; ++j)
+          if (myrow[j] == kUncertain) um[j >> 5] |= 1u << (j & 31);
+      for (uint64_t act = __ballot((um[0] | um[1] | um[2] | um[3]) != 0u); act != 0u;
+           act = __ballot((um[0] | um[1] | um[2] | um[3]) != 0u)) {
+        const int L = __builtin_ctzll(act);
+        const int jl = um[0] ? __builtin_ctz(um[0])
+                       : um[1] ? 32 + __builtin_ctz(um[1])
+                       : um[2] ? 64 + __builtin_ctz(um[2])
+                       : um[3] ? 96 + __builtin_ctz(um[3]) : 0;
+        const int j = __shfl(jl, L);
+        const int tl = __shfl(t, L);
+        const uint32_t xw = *(const uint32_t*)(x + (int64_t)tl * kD + 2 * lane);
+        double part = (double)f16_bits_to_f32(xw & 0xFFFFu) * (double)P[(2 * lane) * kD + j];
+        part = fma((double)f16_bits_to_f32(xw >> 16), (double)P[(2 * lane + 1) * kD + j], part);
+        part = wave_sum_f64(part);
+        if (lane == L) {
+          myrow[j] = f64_to_f16_bits(part);
+          um[j >> 5] &= ~(1u << (j & 31));
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+    }
 
     // ---- one token per lane ----
     const int pos = pos0 + lane;
     const int t = pos - len_old;
     const bool mine = t >= 0 && t < nnew;
     const bool dense = pos >= len_new - a.bb;
-    uint32_t v[64];
-    if (mine) {
-      const u32x4* rp = (const u32x4*)(rows + lane * kRowHalves);
+    const uint16_t* row = (const uint16_t*)(rows + lane * kRowHalves);
+    if (mine && dense) {  // stays in the buffer: ring slot pos % b
+      u32x4* dst = (u32x4*)(ring + (int64_t)(pos % a.bb) * kD);
+#pragma unroll
+      for (int c = 0; c < 16; ++c) dst[c] = ((const u32x4*)row)[c];
+    } else if (mine) {
+      uint32_t v[64];
 #pragma unroll
       for (int c = 0; c < 16; ++c) {
-        const u32x4 c4 = rp[c];
+        const u32x4 c4 = ((const u32x4*)row)[c];
         v[4 * c] = c4.x;
         v[4 * c + 1] = c4.y;
         v[4 * c + 2] = c4.z;
         v[4 * c + 3] = c4.w;
       }
+      uint32_t kept[4];
+      kept_dims(v, k, kept);
+      store_slot<F>(row, kept, k, kp, pages + (int64_t)blk * pbytes, lane);
     }
+    // the rows are rewritten by the next block
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
-    if (mine && dense) {  // stays in the buffer: ring slot pos % b
-      u32x4* dst = (u32x4*)(ring + (int64_t)(pos % a.bb) * kD);
-#pragma unroll
-      for (int c = 0; c < 16; ++c) dst[c] = u32x4{v[4 * c], v[4 * c + 1], v[4 * c + 2], v[4 * c + 3]};
-    }
-    const bool sparse = mine && !dense;
-    // uniform; never for one-byte values (64 * 128 * 2 bytes fit)
-    const bool two_rounds = VB > 1 && 64 * kp * (VB + 1) > kStageBytes;
-    const int vregion = 64 * kp * VB;                            // value bytes of a page
-    uint32_t tau_keep = 0;
-    int need_keep = 0, npad = 0;
-    if (sparse) {
-      // k-th largest magnitude; ties at it are taken lowest dim first
-      uint32_t tau;
-      int need_eq;
-      kth_magnitude(v, k, tau, need_eq);
-      npad = kp - k;
-      if (!two_rounds)
-        emit_slots<F, true, true>(v, tau, need_eq, k, npad, lds + lane * CB,
-                                  (uint8_t*)lds + vregion + lane * 8);
-      else
-        emit_slots<F, true, false>(v, tau, need_eq, k, npad, lds + lane * CB, nullptr);
-      tau_keep = tau;
-      need_keep = need_eq;
-    }
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    char* page = pages + (int64_t)blk * pbytes;
-    const int nch = kp >> 3;
-    if (sparse) {  // this lane's slot chunks of the page
-      for (int c = 0; c < nch; ++c) {
-        if constexpr (CB == 16)
-          *(u32x4*)(page + c * 1024 + lane * 16) = *(const u32x4*)(lds + c * 1024 + lane * 16);
-        else
-          *(u32x2*)(page + c * 512 + lane * 8) = *(const u32x2*)(lds + c * 512 + lane * 8);
-      }
-      if (!two_rounds)
-        for (int c = 0; c < nch; ++c)
-          *(u32x2*)(page + vregion + c * 512 + lane * 8) =
-              *(const u32x2*)(lds + vregion + c * 512 + lane * 8);
-    }
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    if (two_rounds) {  // indices: the same selection again, then their chunks
-      if (sparse)
-        emit_slots<F, false, true>(v, tau_keep, need_keep, k, npad, nullptr,
-                                   (uint8_t*)lds + lane * 8);
-      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      if (sparse)
-        for (int c = 0; c < nch; ++c)
-          *(u32x2*)(page + vregion + c * 512 + lane * 8) =
-              *(const u32x2*)(lds + c * 512 + lane * 8);
-      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-    }
   }
 }
 
 int prefill_groups(int max_new_tokens, int min_len_old) {
   (void)min_len_old;
   const int max_blocks = (max_new_tokens + kPage - 1) / kPage + 1;
-  return (max_blocks + kPrefillBlocksPerWave - 1) / kPrefillBlocksPerWave;
+  const int per_wg = kPrefillBlocksPerWave * kPrefillWaves;
+  return (max_blocks + per_wg - 1) / per_wg;
+}
+
+template <typename F>
+static hipError_t launch_prefill_f(const CompressLaunch& a, dim3 grid) {
+  const hipError_t e = hipFuncSetAttribute((const void*)prefill_kernel<F>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, kPrefillLds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(prefill_kernel<F>, grid, dim3(64 * kPrefillWaves), kPrefillLds, a.stream, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_prefill(const CompressLaunch& a) {
   const int pairs = (2 * a.Hkv + kXcds - 1) / kXcds * kXcds;  // (head, role), padded
   const dim3 grid((int64_t)pairs * a.B * a.prefill_groups);
-  if (a.dtype == SWAN_F16_E4M3)
-    hipLaunchKernelGGL(prefill_kernel<E4M3V>, grid, dim3(64), 0, a.stream, a);
-  else
-    hipLaunchKernelGGL(prefill_kernel<_Float16>, grid, dim3(64), 0, a.stream, a);
-  return hipGetLastError();
+  if (a.dtype == SWAN_F16_E4M3) return launch_prefill_f<E4M3V>(a, grid);
+  return launch_prefill_f<_Float16>(a, grid);
 }
 
 }  // namespace swan
