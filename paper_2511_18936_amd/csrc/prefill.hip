@@ -15,26 +15,30 @@
 // digit weight; the 17 digit pairs whose weight is within 5 digits of the top
 // give x_hat up to a bounded remainder: the 3 dropped pairs (below 2^-38 of
 // the two powers of two's product), plus the truncation of tiny entries of x
-// (counted per row) or of P (bounded per column).  An element is certified
-// when no fp16 rounding boundary lies within that bound of the computed
-// value; the rare rest (about 7 in 10^6 elements on the benchmark inputs) is
-// recomputed in float64.  Either way the stored value is the exact x_hat
-// rounded once to fp16.
+// (counted per row) or of P (bounded per column).  Each element is rounded to
+// fp16 in two ways that must agree: both ends of its error interval (widened
+// by the float64 and float32 roundings) are rounded through float32; about 7
+// elements in 10^4 disagree and get an exact certification in float64 (no
+// fp16 rounding boundary within the bound of the computed value), and the
+// few that fail that are recomputed in float64 from x and P.  Either way the
+// stored value is the exact x_hat rounded once to fp16.
 //
 // A workgroup of 4 waves serves one (sequence, kv head, role): it first
 // writes P's digits, in the MFMA operand layout, to LDS (80 KiB), then each
-// wave handles its own 64-position blocks:
-//   rotation   per pair of 16-token tiles: x digits in registers (A
-//              operands), per 16 output dims the 5 P digits from LDS (B
-//              operands) and 68 MFMAs, then the certified fp16 values into
-//              an LDS row per token
+// wave handles its own 64-position blocks, one wave per SIMD:
+//   rotation   per pair of 16-token tiles (their x rows loaded one pair
+//              ahead): x digits in registers (A operands); 16 steps (16
+//              output dims x 64 input dims) of 34 MFMAs on P digits read
+//              from LDS one step ahead (B operands), each MFMA followed by
+//              VALU work of the previous tile's conversion into the LDS row
+//              of its token
 //   selection  one token per lane on its 128 stored values: a radix select
 //              on bit planes of the magnitudes finds the kept dims (a 128-bit
 //              mask; ties at the k-th largest to the lower dim)
-//   output     each lane walks its kept dims in ascending order, reads their
-//              values from its LDS row and stores its page slot chunk by
-//              chunk (a wave store is 1 KiB contiguous), or its dense row to
-//              the ring
+//   output     each lane walks its kept dims in ascending order, 8 per page
+//              chunk, reads their values from its LDS row and stores its page
+//              slot chunk by chunk (a wave store is 1 KiB contiguous), or its
+//              dense row to the ring
 #include <type_traits>
 
 #include "swan_device.h"
@@ -154,12 +158,15 @@ __device__ __forceinline__ void kept_dims(const uint32_t* v, int k, uint32_t* ke
   for (int c = 0; c < 4; ++c) kept[c] = dim_order(gt[c]) | eq[c];
 }
 
-// The lowest set dim of the 128-bit mask (lo: dims 0-63, hi: 64-127), cleared.
-__device__ __forceinline__ int pop_lowest(uint64_t& lo, uint64_t& hi) {
+// The lowest set dim of the 128-bit mask (lo: dims 0-63, hi: 64-127), cleared;
+// branch-free.
+__device__ __forceinline__ uint32_t pop_lowest(uint64_t& lo, uint64_t& hi) {
   const bool in_lo = lo != 0ull;
-  const int d = in_lo ? __builtin_ctzll(lo) : 64 + __builtin_ctzll(hi);
-  lo = in_lo ? lo & (lo - 1ull) : lo;
-  hi = in_lo ? hi : hi & (hi - 1ull);
+  const uint64_t m = in_lo ? lo : hi;
+  const uint32_t d = (uint32_t)__builtin_ctzll(m) + (in_lo ? 0u : 64u);
+  const uint64_t rest = m & (m - 1ull);
+  lo = in_lo ? rest : lo;
+  hi = in_lo ? hi : rest;
   return d;
 }
 
@@ -167,6 +174,8 @@ __device__ __forceinline__ int pop_lowest(uint64_t& lo, uint64_t& hi) {
 // (a wave's chunk store is 1 KiB, or 512 B, contiguous).  Entries 0..k-1 are
 // the kept dims in ascending order with their values, read from the lane's
 // LDS row; entries k..kp-1 the padding, value +0 at the lowest dims not kept.
+// Per chunk the 8 dims are found first, then their 8 values read together;
+// the padding lies in the last chunk (kp - k < 8).
 template <typename F>
 __device__ __forceinline__ void store_slot(const uint16_t* row, const uint32_t* kept, int k,
                                            int kp, char* page, int lane) {
@@ -176,22 +185,28 @@ __device__ __forceinline__ void store_slot(const uint16_t* row, const uint32_t* 
   uint64_t flo = ~klo, fhi = ~khi;
   char* ipage = page + 64 * kp * VB;
   for (int c = 0; c < kp / 8; ++c) {
+    // kept entries in this chunk (uniform): 8 but in the last chunk, which
+    // also holds the padding when k is not a multiple of 8
+    const int nk = min(k - 8 * c, 8);
+    uint32_t d[8], hb[8];
+    if (nk == 8) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) d[q] = pop_lowest(klo, khi);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) d[q] = q < nk ? pop_lowest(klo, khi) : pop_lowest(flo, fhi);
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) hb[q] = row[d[q] & 127u];
     uint32_t val[4] = {0u, 0u, 0u, 0u}, idx[2] = {0u, 0u};
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-      const int e = 8 * c + q;  // uniform
-      uint32_t hb = 0u, d;
-      if (e < k) {
-        d = (uint32_t)pop_lowest(klo, khi);
-        hb = row[d];
-      } else {
-        d = (uint32_t)pop_lowest(flo, fhi);
-      }
-      idx[q >> 2] |= d << (8 * (q & 3));
+      const uint32_t h = q < nk ? hb[q] : 0u;
+      idx[q >> 2] |= d[q] << (8 * (q & 3));
       if constexpr (kE4M3)
-        val[q >> 2] |= f16_bits_to_e4m3(hb) << (8 * (q & 3));
+        val[q >> 2] |= f16_bits_to_e4m3(h) << (8 * (q & 3));
       else
-        val[q >> 1] |= hb << (16 * (q & 1));
+        val[q >> 1] |= h << (16 * (q & 1));
     }
     if constexpr (kE4M3)
       *(u32x2*)(page + c * 512 + lane * 8) = u32x2{val[0], val[1]};
@@ -251,6 +266,15 @@ __device__ __forceinline__ uint32_t certified_f16(double y, double E) {
   const double side = below_pow2 ? 0.5 * half : half;
   const bool ok = (ex != 31u) & (dist + E + fabs(y) * 0x1p-50 < side) & (E < 0.25 * half);
   return ok ? hb : kUncertain;
+}
+
+// x rounded to float32 and that rounded to fp16, both by the hardware (the
+// empty asm keeps the compiler from fusing them into one software f64 -> f16
+// conversion)
+__device__ __forceinline__ uint32_t f16_via_f32(double x) {
+  float f = (float)x;
+  asm("" : "+v"(f));
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);
 }
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
@@ -351,6 +375,29 @@ void prefill_kernel(CompressLaunch a) {
   const int bbeg = blk0 + (grp * kPrefillWaves + wave) * kPrefillBlocksPerWave;
   const int bend = min(bbeg + kPrefillBlocksPerWave, blk1 + 1);
 
+  // The x rows of a pair of 16-token tiles (lane (m16, g4): token 16 (2 tp +
+  // T) + m16, dims 64 ks + 16 g4 + j), zero past the wave's blocks and the new
+  // tokens.  They are loaded one tile pair ahead of their use.
+  auto load_x = [&](int blk_, int tp_, u32x4 (&xv)[2][2][2]) {
+#pragma unroll
+    for (int T = 0; T < 2; ++T) {
+      const int t = blk_ * kPage + 16 * (2 * tp_ + T) + m16 - len_old;
+      if (blk_ < bend && t >= 0 && t < nnew) {
+        const u32x4* src = (const u32x4*)(x + (int64_t)t * kD + 16 * g4);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          xv[T][ks][0] = src[8 * ks];
+          xv[T][ks][1] = src[8 * ks + 1];
+        }
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) xv[T][ks][0] = xv[T][ks][1] = u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+  };
+  u32x4 xnext[2][2][2];
+  if (P) load_x(bbeg, 0, xnext);
+
   for (int blk = bbeg; blk < bend; ++blk) {
     const int pos0 = blk * kPage;
     bool uncertain = false;  // some element of the block needs the float64 path
@@ -359,26 +406,21 @@ void prefill_kernel(CompressLaunch a) {
 #pragma unroll 1
       for (int tp = 0; tp < 2; ++tp) {
         i32x4 A[2][2][kXDigits];  // [tile][k step][digit]
-        double Eb[2][4];          // per token of the result rows: bound without the P term
-        double Ey[2][4];          // factor of the column's P truncation term
-        double sc[2][4];          // y = H * sc (a power of two)
+        float Eb[2][4];           // per token of the result rows: bound without the P term
+        float Ey[2][4];           // factor of the column's P truncation term
+        int sx[2][4];             // y = H * 2^sx
+        u32x4 xcur[2][2][2];
+#pragma unroll
+        for (int T = 0; T < 2; ++T)
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks) {
+            xcur[T][ks][0] = xnext[T][ks][0];
+            xcur[T][ks][1] = xnext[T][ks][1];
+          }
+        load_x(tp ? blk + 1 : blk, tp ^ 1, xnext);
 #pragma unroll
         for (int T = 0; T < 2; ++T) {
-          // lane (m16, g4): token 16 (2 tp + T) + m16, dims 64 ks + 16 g4 + j
-          const int tok = 16 * (2 * tp + T) + m16;
-          const int t = pos0 + tok - len_old;
-          u32x4 xv[2][2];
-          if (t >= 0 && t < nnew) {
-            const u32x4* src = (const u32x4*)(x + (int64_t)t * kD + 16 * g4);
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-              xv[ks][0] = src[8 * ks];
-              xv[ks][1] = src[8 * ks + 1];
-            }
-          } else {
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks) xv[ks][0] = xv[ks][1] = u32x4{0u, 0u, 0u, 0u};
-          }
+          const u32x4 (&xv)[2][2] = xcur[T];
           // the row's largest magnitude (fp16 bits) and the sum of its magnitudes
           uint32_t mx = 0u;
           float l1 = 0.f;
@@ -442,80 +484,129 @@ void prefill_kernel(CompressLaunch a) {
           }
           // the bound's row terms, for the result lanes: token tok's scale,
           // dropped-pair bound and truncated-x bound
-          const double sce = __builtin_ldexp(1.0, 16 + e - kXFix - G);
-          const double eb = (kDroppedUnits * __builtin_ldexp(1.0, e - kXFix - G) +
-                             (double)ntr * (double)pmax * __builtin_ldexp(1.0, e - kXFix)) *
-                            (1.0 + 0x1p-40);
-          // sum |x_i|, with room for the float32 additions' rounding (128 terms)
-          const double ey = (double)l1 * (1.0 + 0x1p-15);
+          // (float32, rounded up: the factors 1 + 2^-15 leave room for that
+          // rounding, for the float32 additions of l1 (128 terms) and for the
+          // rounding of the float32 fma that combines them per element)
+          const int sxe = 16 + e - kXFix - G;
+          const float eb = (float)(kDroppedUnits * __builtin_ldexp(1.0, e - kXFix - G) +
+                                   (double)ntr * (double)pmax * __builtin_ldexp(1.0, e - kXFix)) *
+                           (1.0f + 0x1p-15f);
+          // sum |x_i|
+          const float ey = l1 * (1.0f + 0x1p-14f);
           // move them to the lanes holding the token's results: row r = 4 g + v
           // of the tile is token m16 = r of the tile
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             const int src_lane = 4 * g4 + v;  // lane (m16 = 4 g4 + v, g4 = 0) has token 4 g4 + v
-            sc[T][v] = __shfl(sce, src_lane);
+            sx[T][v] = __shfl(sxe, src_lane);
             Eb[T][v] = __shfl(eb, src_lane);
             Ey[T][v] = __shfl(ey, src_lane);
           }
         }
         // ---- MFMA per 16 output dims, then certified fp16 values to the rows;
         //      the results of tile o are turned into fp16 while the MFMAs of
-        //      tile o + 1 run ----
-        auto mfma_tile = [&](int o, i32x4 (&acc)[2][kLevels]) {
+        //      tile o + 1 run (the loop is unrolled so that one scheduling
+        //      region holds both) ----
+        // step j = 2 o + ks: output tile o, k step ks.  The P digits of a step
+        // are read from LDS into registers one step ahead of their MFMAs.
+        auto load_b = [&](int j, i32x4 (&B)[kPDigits]) {
 #pragma unroll
-          for (int T = 0; T < 2; ++T)
-#pragma unroll
-            for (int l = 0; l < kLevels; ++l) acc[T][l] = i32x4{0, 0, 0, 0};
-#pragma unroll
-          for (int ks = 0; ks < 2; ++ks) {
-            i32x4 Bd[kPDigits];
-#pragma unroll
-            for (int t = 0; t < kPDigits; ++t)
-              Bd[t] = *(const i32x4*)(bdig + ((o * 2 + ks) * kPDigits + t) * 1024 + lane * 16);
+          for (int t = 0; t < kPDigits; ++t)
+            B[t] = *(const i32x4*)(bdig + (j * kPDigits + t) * 1024 + lane * 16);
+        };
+        auto mfma_step = [&](int j, i32x4 (&acc)[2][kLevels], const i32x4 (&B)[kPDigits]) {
+          const int ks = j & 1;
+          if (ks == 0) {
 #pragma unroll
             for (int T = 0; T < 2; ++T)
 #pragma unroll
-              for (int s = 0; s < kXDigits; ++s)
-#pragma unroll
-                for (int t = 0; t < kPDigits; ++t)
-                  if (s + t <= kTopLevel)
-                    acc[T][s + t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[T][ks][s], Bd[t],
-                                                                          acc[T][s + t], 0, 0, 0);
+              for (int l = 0; l < kLevels; ++l) acc[T][l] = i32x4{0, 0, 0, 0};
           }
-        };
-        // result layout: register v of lane l is row 4 (l / 16) + v (token),
-        // column l % 16 (output dim 16 o + l % 16)
-        auto to_rows = [&](int o, const i32x4 (&acc)[2][kLevels]) {
-          const int col = 16 * o + m16;
-          const double dyc = (double)colDY[col];
 #pragma unroll
           for (int T = 0; T < 2; ++T)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-              // H = sum_l C_l 256^(5 - l): levels 0-1 and 2-3 combine exactly
-              // in int32 (|C_0| <= 2^21, |C_2| <= 3 * 2^21, |C_l| <= 2^23), the
-              // rest in float64 (exact below 2^53, else within 2^-52 |H|)
-              const int t01 = acc[T][0][v] * 256 + acc[T][1][v];
-              const int t23 = acc[T][2][v] * 256 + acc[T][3][v];
-              double H = fma((double)t01, 65536.0, (double)t23);
-              H = fma(H, 256.0, (double)acc[T][4][v]);
-              H = fma(H, 256.0, (double)acc[T][5][v]);
-              const double y = H * sc[T][v];
-              const double E = fma(dyc, Ey[T][v], Eb[T][v]) * (1.0 + 0x1p-40);
+            for (int s = 0; s < kXDigits; ++s)
+#pragma unroll
+              for (int t = 0; t < kPDigits; ++t)
+                if (s + t <= kTopLevel)
+                  acc[T][s + t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[T][ks][s], B[t],
+                                                                        acc[T][s + t], 0, 0, 0);
+        };
+        // result layout: register v of lane l is row 4 (l / 16) + v (token),
+        // column l % 16 (output dim 16 o + l % 16).
+        // H = sum_l C_l 256^(5 - l), combined as ((t01 2^16 + t23) 2^16 + t45)
+        // with t01 = C_0 256 + C_1 etc. exact in int32: a top digit of x or P
+        // lies in [-64, 64], so over 128 products |C_0| <= 2^19, |C_1| <= 2^21,
+        // |C_2| <= 2^22, |C_3| <= 3 * 2^21, |C_4| <= 7 * 2^20, |C_5| <= 3 * 2^21.
+        // The float64 sums are exact below 2^53, else within 2^-53 |H|.
+        auto result = [&](const i32x4 (&acc)[2][kLevels], int T, int v) {
+          const int t01 = acc[T][0][v] * 256 + acc[T][1][v];
+          const int t23 = acc[T][2][v] * 256 + acc[T][3][v];
+          const int t45 = acc[T][4][v] * 256 + acc[T][5][v];
+          const double H = fma(fma((double)t01, 65536.0, (double)t23), 65536.0, (double)t45);
+          return __builtin_ldexp(H, sx[T][v]);
+        };
+        // Fast check: both ends of [y - E1, y + E1], E1 = E + 2^-22 |y|,
+        // rounded to fp16 through float32.  The margin 2^-22 |y| covers the
+        // float64 and float32 roundings of the ends, so the two conversions
+        // bracket every value within E of y; rounding is monotone, so when
+        // they agree that is the fp16 rounding of x_hat.  Elements whose ends
+        // disagree (about 1 in 10^3) get the exact certification.  One half
+        // (4 tokens) of tile o per call; returns the open elements as bits.
+        auto to_rows = [&](int o, int T, const i32x4 (&acc)[2][kLevels]) {
+          const int col = 16 * o + m16;
+          const float dyc = colDY[col];
+          uint32_t need = 0u;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const double y = result(acc, T, v);
+            const double E1 = fma(fabs(y), 0x1p-22, (double)fmaf(dyc, Ey[T][v], Eb[T][v]));
+            const uint32_t lo = f16_via_f32(y - E1), hi = f16_via_f32(y + E1);
+            need |= (lo != hi ? 1u : 0u) << v;
+            const int tok = 16 * (2 * tp + T) + 4 * g4 + v;
+            ((uint16_t*)rows)[tok * kRowHalves + col] = (uint16_t)lo;
+          }
+          return need;
+        };
+        // the exact certification of the elements the fast check left open
+        auto fix_rows = [&](int o, int T, const i32x4 (&acc)[2][kLevels], uint32_t need) {
+          const int col = 16 * o + m16;
+          const float dyc = colDY[col];
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            if (need & (1u << v)) {
+              const double y = result(acc, T, v);
+              const double E = (double)fmaf(dyc, Ey[T][v], Eb[T][v]);
               const uint32_t hb = certified_f16(y, E);
               uncertain |= hb == kUncertain;
               const int tok = 16 * (2 * tp + T) + 4 * g4 + v;
               ((uint16_t*)rows)[tok * kRowHalves + col] = (uint16_t)hb;
             }
         };
-        i32x4 accA[2][kLevels], accB[2][kLevels];
-        mfma_tile(0, accA);
-#pragma unroll 1
-        for (int o = 0; o < 8; o += 2) {
-          mfma_tile(o + 1, accB);
-          to_rows(o, accA);
-          if (o + 2 < 8) mfma_tile(o + 2, accA);
-          to_rows(o + 1, accB);
+        // 16 steps j = 2 o + ks (+ two to drain): step j issues the LDS reads
+        // of step j + 1's P digits, then its 34 MFMAs, each followed by three
+        // VALU instructions of half a tile of tile o - 1's conversion (the
+        // scheduling barriers keep that order and the steps apart).
+        i32x4 acc[2][2][kLevels];
+        i32x4 Bq[2][kPDigits];
+        load_b(0, Bq[0]);
+#pragma unroll
+        for (int j = 0; j < 18; ++j) {
+          const int o = j >> 1, ks = j & 1;
+          if (j + 1 < 16) load_b(j + 1, Bq[(j + 1) & 1]);
+          if (j < 16) mfma_step(j, acc[o & 1], Bq[j & 1]);
+          uint32_t need = 0u;
+          if (j >= 2) need = to_rows(o - 1, ks, acc[(o - 1) & 1]);
+          if (j + 1 < 16) __builtin_amdgcn_sched_group_barrier(0x100, kPDigits, 0);  // DS read
+          if (j < 16) {
+#pragma unroll
+            for (int i = 0; i < 34; ++i) {
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+              __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // VALU
+            }
+          }
+          __builtin_amdgcn_sched_barrier(0);
+          if (j >= 2 && __ballot(need != 0u) != 0u) fix_rows(o - 1, ks, acc[(o - 1) & 1], need);
         }
       }
     } else {
