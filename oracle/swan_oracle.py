@@ -10,6 +10,10 @@ paper states the method (SWAN: Sparse Winnowed Attention, arXiv 2511.18936):
 * ``calibrate``            Sec. 4.1.2: the projection is the right singular
                            matrix of the joint activation matrix S, columns in
                            descending singular value.
+* ``joint_matrices`` / ``calibrate_joint``  Sec. 4.1.1-4.1.2: per KV head, S_QK
+                           stacks the grouped queries over the keys and S_VO the
+                           values over the group's transposed W_O head blocks
+                           (reading 14).
 * ``rotate`` / ``to_storage``  Algorithm 1 (project the key; the value arrives
                            projected): x_hat = x . P, rounded once to the
                            storage type T when it enters the dense buffer.
@@ -74,7 +78,12 @@ Readings of the paper used here (where it is silent or ambiguous):
      each rounded once to T from a float64 product; W_V_hat = W_V . P_VO and
      W_O_hat = P_VO^T . W_O per head are formed in float64; the values enter
      the cache without a further rotation and the attention output leaves it
-     rotated, straight into W_O_hat.
+     rotated, straight into W_O_hat;
+ 14. the joint matrices (Sec. 4.1.1-4.1.2): KV head j serves query heads
+     jG .. jG + G - 1 (the reshape of Q to N_kv x nG x d_h keeps consecutive
+     heads together); W_O's head blocks are its consecutive d_h-row blocks; the
+     tensors are stacked as they are, without scaling or mean removal, and the
+     row order inside S does not change its right singular vectors.
 
 Parity status: every function above is pinned by tests/test_oracle_pins.py;
 nothing here is "parity unpinned" except the end-task accuracy of Tables 1-3,
@@ -130,6 +139,46 @@ def calibrate_f32(S: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
     """The fp32 rotation that both the oracle and the GPU path then consume."""
     P, sigma = calibrate(S)
     return P.astype(np.float32), sigma.astype(np.float32)
+
+
+# --------------------------------------------------------------------------- #
+# Sec. 4.1.1-4.1.2: the joint matrices of a layer's calibration activations
+# --------------------------------------------------------------------------- #
+def joint_matrices(Q: np.ndarray, K: np.ndarray, V: np.ndarray, W_o: np.ndarray,
+                   n_kv_heads: int) -> Tuple[List[np.ndarray], List[np.ndarray]]:
+    """S_QK and S_VO of every KV head j (Sec. 4.1.1-4.1.2), float64.
+
+    Q [N_q][n][d_h]: post-RoPE queries of the calibration tokens, K [N_kv][n][d_h]
+    post-RoPE keys, V [N_kv][n][d_h] values, W_o [N_q d_h][d] the output weights.
+    The G = N_q / N_kv query heads of KV head j are heads jG .. jG + G - 1.  The
+    query tensor is reshaped to Q_grouped [N_kv][n G][d_h]; W_O is sliced into
+    its N_q head blocks W_O^(h) [d_h][d] (rows h d_h .. (h + 1) d_h - 1), grouped
+    the same way.  S_QK^(j) stacks Q_grouped^(j) over K^(j); S_VO^(j) stacks V^(j)
+    over the transposed blocks W_O^(h)^T [d][d_h] of the group's heads.
+    """
+    Q = np.asarray(Q, dtype=F64)
+    K = np.asarray(K, dtype=F64)
+    V = np.asarray(V, dtype=F64)
+    W_o = np.asarray(W_o, dtype=F64)
+    n_q, n, d_h = Q.shape
+    G = n_q // n_kv_heads
+    Q_grouped = Q.reshape(n_kv_heads, n * G, d_h)
+    blocks = W_o.reshape(n_q, d_h, W_o.shape[1])  # W_O^(h)
+    S_qk, S_vo = [], []
+    for j in range(n_kv_heads):
+        S_qk.append(np.concatenate([Q_grouped[j], K[j]], axis=0))
+        wo_t = [blocks[h].T for h in range(j * G, (j + 1) * G)]
+        S_vo.append(np.concatenate([V[j]] + wo_t, axis=0))
+    return S_qk, S_vo
+
+
+def calibrate_joint(Q: np.ndarray, K: np.ndarray, V: np.ndarray, W_o: np.ndarray,
+                    n_kv_heads: int) -> Tuple[np.ndarray, np.ndarray]:
+    """P_QK, P_VO [N_kv][d_h][d_h] (float64): the right singular matrices of each
+    KV head's joint matrices (Sec. 4.1.2)."""
+    S_qk, S_vo = joint_matrices(Q, K, V, W_o, n_kv_heads)
+    return (np.stack([calibrate(S)[0] for S in S_qk]),
+            np.stack([calibrate(S)[0] for S in S_vo]))
 
 
 # --------------------------------------------------------------------------- #
@@ -281,20 +330,23 @@ class UnitCache:
         return len(self.k_idx) + len(self.k_buf)
 
     def append(self, k_row: np.ndarray, v_row: np.ndarray) -> None:
-        """One token of Algorithm 1: project, append to the buffer, evict-and-prune if > b."""
-        k_hat = to_storage(rotate(k_row, self.P_qk), self.dtype)
-        v_hat = to_storage(rotate(v_row, self.P_vo), self.dtype)
-        self.k_buf.append(k_hat)
-        self.v_buf.append(v_hat)
+        """Admit one token (Algorithm 1): its rotated key and value, rounded once
+        to T, join the dense buffer, which keeps the b most recent tokens; a token
+        pushed out of it is retired into the sparse cache."""
+        self.k_buf.append(to_storage(rotate(k_row, self.P_qk), self.dtype))
+        self.v_buf.append(to_storage(rotate(v_row, self.P_vo), self.dtype))
         while len(self.k_buf) > self.b:
-            k_old = self.k_buf.popleft()
-            v_old = self.v_buf.popleft()
-            i_k = topk_indices(k_old, self.k)
-            self.k_idx.append(i_k)
-            self.k_val.append(self._sparse_value(k_old[i_k]))
-            i_v = topk_indices(v_old, self.kv)
-            self.v_idx.append(i_v)
-            self.v_val.append(self._sparse_value(v_old[i_v]))
+            self._retire(self.k_buf.popleft(), self.v_buf.popleft())
+
+    def _retire(self, k_old: np.ndarray, v_old: np.ndarray) -> None:
+        """A token leaving the buffer keeps, per role, the (index, value) pairs of
+        its largest stored magnitudes (Sec. 4.3): k of them for the key, k_value
+        for the value (reading 10)."""
+        for vec, keep, idx_l, val_l in ((k_old, self.k, self.k_idx, self.k_val),
+                                        (v_old, self.kv, self.v_idx, self.v_val)):
+            i = topk_indices(vec, keep)
+            idx_l.append(i)
+            val_l.append(self._sparse_value(vec[i]))
 
     def change_k(self, k_new: int, k_value_new: Optional[int] = None) -> None:
         """Reading 11: the stored tokens laid out again for the new k, which the

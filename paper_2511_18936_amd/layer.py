@@ -25,6 +25,39 @@ from . import swan
 HEAD_DIM = swan.HEAD_DIM
 
 
+def calibrate_joint(q, k, v, W_o, n_kv_heads: int, P_qk_out, P_vo_out, stream=None) -> None:
+    """The layer's rotations from calibration activations (Sec. 4.1.1-4.1.2).
+
+    q [N_q][n][128]: post-RoPE queries of n calibration tokens; k [N_kv][n][128]
+    post-RoPE keys; v [N_kv][n][128] values (x . W_V, before any rotation);
+    W_o [N_q 128][hidden] (cuda tensors, float16 or float32).  For each KV head j
+    (query heads jG .. jG + G - 1) the joint matrices are stacked in device
+    memory as float32, S_QK = [Q_grouped^(j); K^(j)] and S_VO = [V^(j); W_O^(h)^T
+    for the group's heads], W_O^(h) being rows 128 h .. 128 h + 127 of W_o, and
+    swan_calibrate_rotation writes their right singular matrices to P_qk_out[j]
+    and P_vo_out[j] ([N_kv][128][128] float32)."""
+    import torch
+
+    n_q, n, d = q.shape
+    if d != HEAD_DIM or n_q % n_kv_heads != 0:
+        raise ValueError("q must be [N_q][n][128] with N_q a multiple of n_kv_heads")
+    if tuple(k.shape) != (n_kv_heads, n, d) or tuple(v.shape) != (n_kv_heads, n, d):
+        raise ValueError("k and v must be [n_kv_heads][n][128]")
+    if W_o.dim() != 2 or W_o.shape[0] != n_q * d:
+        raise ValueError("W_o must be [N_q * 128][hidden]")
+    G = n_q // n_kv_heads
+    hidden = W_o.shape[1]
+    q_grouped = q.reshape(n_kv_heads, n * G, d)
+    blocks = W_o.reshape(n_q, d, hidden)  # W_O^(h)
+    ws = torch.empty(swan.calibrate_workspace_bytes(d), dtype=torch.uint8, device=q.device)
+    for j in range(n_kv_heads):
+        s_qk = torch.cat([q_grouped[j], k[j]], dim=0).float().contiguous()
+        swan.calibrate_rotation(s_qk, P_qk_out[j], workspace=ws, stream=stream)
+        wo_t = blocks[j * G:(j + 1) * G].transpose(1, 2).reshape(G * hidden, d)
+        s_vo = torch.cat([v[j], wo_t], dim=0).float().contiguous()
+        swan.calibrate_rotation(s_vo, P_vo_out[j], workspace=ws, stream=stream)
+
+
 class SwanAttentionLayer:
     def __init__(self, W_q, W_k, W_v, W_o, P_qk, P_vo, n_heads: int, n_kv_heads: int,
                  rope_base: float, batch: int, buffer_tokens: int, capacity: int,

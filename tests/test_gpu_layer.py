@@ -105,12 +105,63 @@ def _weights(seed, hidden, Hq, Hkv):
 
 @pytest.mark.parametrize("Hq,Hkv,base,k", [(8, 8, 10000.0, 48), (8, 2, 500000.0, 64)])
 def test_layer_decode_steps(gpu_device, swan_mod, torch_mod, Hq, Hkv, base, k):
+    _log(f"layer Hq={Hq} Hkv={Hkv} base={base} k={k}")
+    W_q, W_k, W_v, W_o, P_qk, P_vo = _weights(Hq + Hkv, 512, Hq, Hkv)
+    _layer_steps(gpu_device, swan_mod, torch_mod, Hq, Hkv, base, k, W_q, W_k, W_v, W_o, P_qk,
+                 P_vo)
+
+
+@pytest.mark.parametrize("Hq,Hkv,base,k", [(8, 8, 10000.0, 48), (8, 2, 500000.0, 64)])
+def test_layer_with_joint_calibration(gpu_device, swan_mod, torch_mod, Hq, Hkv, base, k):
+    """Sec. 4.1.1-4.1.2: the rotations calibrated on the GPU from the layer's own
+    post-RoPE queries and keys, its values and W_O (layer.calibrate_joint) match
+    the oracle's calibrate_joint on the same tensors, and the layer built on them
+    decodes like the oracle's."""
+    torch = torch_mod
+    from paper_2511_18936_amd.layer import SwanAttentionLayer, calibrate_joint
+
+    _log(f"joint calibration Hq={Hq} Hkv={Hkv} base={base} k={k}")
+    hidden, n_cal = 512, 256
+    W_q, W_k, W_v, W_o, _, _ = _weights(Hq + Hkv + 100, hidden, Hq, Hkv)
+    t16 = lambda a: torch.tensor(a, dtype=torch.float16, device=gpu_device)
+    eye = torch.eye(128, dtype=torch.float32, device=gpu_device).repeat(Hkv, 1, 1).contiguous()
+    # identity rotations: project() then gives the raw post-RoPE q, k and v = x . W_V
+    raw = SwanAttentionLayer(t16(W_q), t16(W_k), t16(W_v), t16(W_o), eye, eye, Hq, Hkv, base,
+                             1, 0, n_cal, [128])
+    X = si.rng_for(709, Hq).standard_normal((1, n_cal, hidden)).astype(np.float16)
+    q, kk, vv = raw.project(t16(X))
+    Pqk = torch.empty((Hkv, 128, 128), dtype=torch.float32, device=gpu_device)
+    Pvo = torch.empty_like(Pqk)
+    calibrate_joint(q[0], kk[0], vv[0], raw.W_o_hat, Hkv, Pqk, Pvo)
+    torch.cuda.synchronize()
+    Pqk_g = Pqk.double().cpu().numpy()
+    Pvo_g = Pvo.double().cpu().numpy()
+    Q, K, V = (t[0].double().cpu().numpy() for t in (q, kk, vv))
+    Wo = raw.W_o_hat.double().cpu().numpy()  # = W_O (identity P_VO), as float16
+    S_qk, S_vo = O.joint_matrices(Q, K, V, Wo, Hkv)
+    for j in range(Hkv):
+        for S, Pg in ((S_qk[j], Pqk_g[j]), (S_vo[j], Pvo_g[j])):
+            Po, so = O.calibrate(S)
+            assert np.max(np.abs(Pg.T @ Pg - np.eye(128))) < 2e-6
+            # columns with a clear spectral gap agree with the oracle's, signs included
+            gap = np.minimum(np.r_[np.inf, so[:-1] - so[1:]], np.r_[so[:-1] - so[1:], np.inf])
+            sep = gap > 1e-3 * so
+            assert sep.sum() > 64, sep.sum()
+            err = np.max(np.abs(Pg[:, sep] - Po[:, sep]))
+            _log(f"  head {j}: {int(sep.sum())} separated columns, max diff {err:.1e}")
+            assert err < 1e-4
+    _layer_steps(gpu_device, swan_mod, torch_mod, Hq, Hkv, base, k, W_q, W_k, W_v, W_o, Pqk_g,
+                 Pvo_g)
+
+
+def _layer_steps(gpu_device, swan_mod, torch_mod, Hq, Hkv, base, k, W_q, W_k, W_v, W_o, P_qk,
+                 P_vo):
+    """Prompt then decode steps of the layer on the GPU against the oracle (P_qk,
+    P_vo: float64 copies of float32 rotations)."""
     torch = torch_mod
     from paper_2511_18936_amd.layer import SwanAttentionLayer
 
-    _log(f"layer Hq={Hq} Hkv={Hkv} base={base} k={k}")
-    B, hidden, L0, steps, b = 2, 512, 300, 3, 32
-    W_q, W_k, W_v, W_o, P_qk, P_vo = _weights(Hq + Hkv, hidden, Hq, Hkv)
+    B, hidden, L0, steps, b = 2, W_q.shape[0], 300, 3, 32
     W16 = [w.astype(np.float16).astype(np.float64) for w in (W_q, W_k, W_v, W_o)]
     t16 = lambda a: torch.tensor(a, dtype=torch.float16, device=gpu_device)
     layer = SwanAttentionLayer(t16(W_q), t16(W_k), t16(W_v), t16(W_o),

@@ -130,6 +130,83 @@ def _brute_topk(y, k):
     return sorted(order[:k])
 
 
+# --------------------------------------------------------------------------- #
+# Sec. 4.1.1-4.1.2: the joint matrices of a layer (reading 14)
+# --------------------------------------------------------------------------- #
+@pytest.mark.parametrize("n_q,n_kv", [(8, 2), (4, 4), (6, 3)])
+def test_joint_matrices_brute_force_grouping(n_q, n_kv):
+    """Each KV head's matrices, assembled row by row with explicit head and token
+    loops: query head h belongs to KV head h // G, and W_O^(h) is rows h d_h ..
+    (h + 1) d_h - 1 of W_O, entering S_VO transposed."""
+    d_h, n, d = 8, 5, 6
+    r = si.rng_for(9001, n_q, n_kv)
+    Q = r.standard_normal((n_q, n, d_h))
+    K = r.standard_normal((n_kv, n, d_h))
+    V = r.standard_normal((n_kv, n, d_h))
+    W_o = r.standard_normal((n_q * d_h, d))
+    S_qk, S_vo = O.joint_matrices(Q, K, V, W_o, n_kv)
+    G = n_q // n_kv
+    for j in range(n_kv):
+        rows = []
+        for h in range(n_q):
+            if h // G == j:
+                for t in range(n):
+                    rows.append([Q[h][t][c] for c in range(d_h)])
+        for t in range(n):
+            rows.append([K[j][t][c] for c in range(d_h)])
+        assert np.array_equal(S_qk[j], np.array(rows))
+        rows = [[V[j][t][c] for c in range(d_h)] for t in range(n)]
+        for h in range(n_q):
+            if h // G == j:
+                for col in range(d):  # row col of W_O^(h)^T
+                    rows.append([W_o[h * d_h + i][col] for i in range(d_h)])
+        assert np.array_equal(S_vo[j], np.array(rows))
+
+
+def test_joint_matrices_mark_each_head():
+    """Constant marker rows: query head h's rows are (h + 1) e_h, W_O block h holds
+    1000 (h + 1) + row; each KV head's matrices hold exactly its group's marks."""
+    n_q, n_kv, d_h, n, d = 8, 2, 8, 3, 4
+    Q = np.zeros((n_q, n, d_h))
+    for h in range(n_q):
+        Q[h, :, h] = h + 1
+    K = np.zeros((n_kv, n, d_h))
+    V = np.zeros((n_kv, n, d_h))
+    W_o = np.zeros((n_q * d_h, d))
+    for h in range(n_q):
+        W_o[h * d_h:(h + 1) * d_h, :] = 1000 * (h + 1) + np.arange(d_h)[:, None]
+    S_qk, S_vo = O.joint_matrices(Q, K, V, W_o, n_kv)
+    for j, heads in enumerate(([0, 1, 2, 3], [4, 5, 6, 7])):
+        marks = sorted({int(x) for x in S_qk[j].ravel() if x})
+        assert marks == [h + 1 for h in heads]
+        wo_part = S_vo[j][n:]
+        assert wo_part.shape == (len(heads) * d, d_h)
+        for gi, h in enumerate(heads):
+            block = wo_part[gi * d:(gi + 1) * d]
+            assert np.array_equal(block, np.tile(1000 * (h + 1) + np.arange(d_h), (d, 1)))
+
+
+def test_joint_calibration_reduces_to_single_tensor_calibration():
+    """Special cases with a plain answer: queries equal to the keys (each row
+    twice) and zero output weights leave the right singular vectors of K and V
+    alone, so calibrate_joint equals calibrate on K and on V; and the row order
+    inside S does not matter."""
+    n_kv, n, d_h = 2, 300, 16
+    r = si.rng_for(9002)
+    scales = np.exp(-np.arange(d_h) / 3.0)
+    K = r.standard_normal((n_kv, n, d_h)) * scales
+    V = r.standard_normal((n_kv, n, d_h)) * scales[::-1]
+    Q = K.copy()  # G = 1, MHA
+    W_o = np.zeros((n_kv * d_h, 7))
+    P_qk, P_vo = O.calibrate_joint(Q, K, V, W_o, n_kv)
+    for j in range(n_kv):
+        assert np.allclose(P_qk[j], O.calibrate(K[j])[0], atol=1e-9)
+        assert np.allclose(P_vo[j], O.calibrate(V[j])[0], atol=1e-9)
+        S_qk, _ = O.joint_matrices(Q, K, V, W_o, n_kv)
+        perm = r.permutation(S_qk[j].shape[0])
+        assert np.allclose(O.calibrate(S_qk[j][perm])[0], P_qk[j], atol=1e-9)
+
+
 @pytest.mark.parametrize("d", [4, 8, 16, 128])
 def test_topk_brute_force_with_many_ties(d):
     r = si.rng_for(11, d)
