@@ -125,6 +125,16 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
   const int64_t pbytes = page_bytes_of(Fmt<T>::kValBytes, a.tab.kact[role][b]);
   const int n8 = kAsym ? kpad_of(a.tab.kact[role][b]) / 8 : KP8;
   const int64_t head_off = (int64_t)h * a.n_pages_cap * pbytes;
+  // this wave's role pages.  Pages up to 192 bytes per lane (fp16 up to k_pad
+  // 64) load the first page before the query replicas are filled, so that its
+  // latency overlaps the fill and the barrier; larger pages keep their
+  // registers free of it there (two waves per SIMD need the kernel within 256
+  // registers).
+  constexpr bool kEarly = sizeof(PageRegs<T, KP8>) <= 192;
+  const char* rbase = wave == 0 ? (const char*)a.k_pages + a.tab.page_off[0][b] + head_off
+                                : (const char*)a.v_pages + a.tab.page_off[1][b] + head_off;
+  PageRegs<T, KP8> ra, rb;  // the wave's two page register sets
+  if constexpr (kEarly) load_page<T, KP8>(ra, rbase + pbeg * pbytes, lane, n8);
 
   // q_rep[dim][r][head]: thread t writes dim t, all replicas
   {
@@ -144,7 +154,7 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
   const int plast = pend - 1;
   if (wave == 0) {
     // ---- score wave ----
-    const char* kbase = (const char*)a.k_pages + a.tab.page_off[0][b] + head_off;
+    const char* kbase = rbase;
     float m[GH], l[GH];
     bool first = true;
 #pragma unroll
@@ -152,8 +162,9 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
       m[j] = 0.f;
       l[j] = 0.f;
     }
-    PageRegs<T, KP8> ka, kb;
-    load_page<T, KP8>(ka, kbase + pbeg * pbytes, lane, n8);
+    PageRegs<T, KP8>& ka = ra;
+    PageRegs<T, KP8>& kb = rb;
+    if constexpr (!kEarly) load_page<T, KP8>(ka, kbase + pbeg * pbytes, lane, n8);
     for (int p = pbeg; p < pend; p += 2) {
       const bool in1 = p + 1 <= plast;  // past the split: the resident spare arrays
       load_page<T, KP8>(kb, kbase + (in1 ? p + 1 : plast) * pbytes, lane, in1 ? n8 : 0);
@@ -178,12 +189,13 @@ __global__ __launch_bounds__(128) void attn_gqa_kernel(DecodeLaunch a, SeqGroup 
     }
   } else {
     // ---- value wave ----
-    const char* vbase = (const char*)a.v_pages + a.tab.page_off[1][b] + head_off;
+    const char* vbase = rbase;
     f4 acc[8];
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt) acc[nt] = f4{0.f, 0.f, 0.f, 0.f};
-    PageRegs<T, KP8> va, vb;
-    load_page<T, KP8>(va, vbase + pbeg * pbytes, lane, n8);
+    PageRegs<T, KP8>& va = ra;
+    PageRegs<T, KP8>& vb = rb;
+    if constexpr (!kEarly) load_page<T, KP8>(va, vbase + pbeg * pbytes, lane, n8);
     for (int p = pbeg; p < pend; p += 2) {
       const bool in1 = p + 1 <= plast;  // past the split: the resident spare arrays
       load_page<T, KP8>(vb, vbase + (in1 ? p + 1 : plast) * pbytes, lane, in1 ? n8 : 0);
