@@ -21,36 +21,50 @@ namespace swan {
 
 // ---------------------------------------------------------------------------
 // q rotation: q_hat[b][h][j] = mult * sum_i q[b][h][i] * P_qk[g][i][j]
+// 512 threads per (b, h): thread (j, s) sums rows i = 32 s .. 32 s + 31 (two
+// independent accumulators, 32 loads in flight), the four quarters meet in LDS
 // ---------------------------------------------------------------------------
+constexpr int kRotQuarters = 4;
 template <typename T>
-__global__ __launch_bounds__(128) void qrot_kernel(const T* __restrict__ q,
-                                                   const float* __restrict__ Pqk,
-                                                   float* __restrict__ qhat, int Hq, int G,
-                                                   float mult) {
+__global__ __launch_bounds__(kD * kRotQuarters) void qrot_kernel(const T* __restrict__ q,
+                                                                 const float* __restrict__ Pqk,
+                                                                 float* __restrict__ qhat, int Hq,
+                                                                 int G, float mult) {
   __shared__ float qs[kD];
+  __shared__ float part[kRotQuarters][kD];
   const int bh = blockIdx.x;
   const int g = (bh % Hq) / G;
-  const int j = threadIdx.x;
-  qs[j] = (float)q[(int64_t)bh * kD + j];
+  const int j = threadIdx.x & (kD - 1), sq = threadIdx.x / kD;
+  if (sq == 0) qs[j] = (float)q[(int64_t)bh * kD + j];
   __syncthreads();
-  const float* P = Pqk + (int64_t)g * kD * kD;
-  float acc = 0.f;
-#pragma unroll 32
-  for (int i = 0; i < kD; ++i) acc = fmaf(qs[i], P[i * kD + j], acc);
-  qhat[(int64_t)bh * kD + j] = acc * mult;
+  const float* P = Pqk + (int64_t)g * kD * kD + (int64_t)(32 * sq) * kD + j;
+  float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+  for (int i = 0; i < 32; i += 2) {
+    a0 = fmaf(qs[32 * sq + i], P[i * kD], a0);
+    a1 = fmaf(qs[32 * sq + i + 1], P[(i + 1) * kD], a1);
+  }
+  part[sq][j] = a0 + a1;
+  __syncthreads();
+  if (sq == 0)
+    qhat[(int64_t)bh * kD + j] = ((part[0][j] + part[1][j]) + (part[2][j] + part[3][j])) * mult;
 }
 
 // ---------------------------------------------------------------------------
 // merge partials (log-sum-exp, fixed order) and rotate back: o = o_hat . P_vo^T
 // ---------------------------------------------------------------------------
+constexpr int kMergeThreads = kD * kRotQuarters;
 template <typename T>
-__global__ __launch_bounds__(128) void merge_kernel(DecodeLaunch a) {
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeLaunch a) {
+  constexpr int kWaves = kMergeThreads / 64;
   __shared__ float oh[kD];
   __shared__ float wts[kMaxSplits + 1];
-  __shared__ float red[4];
+  __shared__ float red[2 * kWaves];
+  __shared__ float rq[kRotQuarters][kD];
   const int bhq = blockIdx.x;
   const int b = bhq / a.Hq, hq = bhq % a.Hq, h = hq / (a.Hq / a.Hkv);
   const int t = threadIdx.x;
+  const int sq = t / kD, tt = t & (kD - 1);  // quarter and dim of this thread
   const int L = a.tab.len[b];
   const int S = L > a.bb ? L - a.bb : 0;
   const int np = pages_for(S);
@@ -62,41 +76,62 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeLaunch a) {
   const int np_all = ns + (has_buf ? 1 : 0);
   auto slot = [&](int i) { return i < ns ? i : a.n_splits; };
   float mloc = -INFINITY;
-  for (int i = t; i < np_all; i += 128) mloc = fmaxf(mloc, part[slot(i) * kPartFloats]);
+  for (int i = t; i < np_all; i += kMergeThreads) mloc = fmaxf(mloc, part[slot(i) * kPartFloats]);
   mloc = wave_max(mloc);
   if ((t & 63) == 0) red[t >> 6] = mloc;
   __syncthreads();
-  const float m = fmaxf(red[0], red[1]);
+  float m = red[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red[w]);
   float lloc = 0.f;
-  for (int i = t; i < np_all; i += 128) {
+  for (int i = t; i < np_all; i += kMergeThreads) {
     const float* pi = part + slot(i) * kPartFloats;
     const float wgt = exp2f(pi[0] - m);
     wts[i] = wgt;
     lloc += wgt * pi[1];
   }
   lloc = wave_sum(lloc);
-  if ((t & 63) == 0) red[2 + (t >> 6)] = lloc;
+  if ((t & 63) == 0) red[kWaves + (t >> 6)] = lloc;
   __syncthreads();
-  const float inv = 1.f / (red[2] + red[3]);
+  float lsum = 0.f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) lsum += red[kWaves + w];
+  const float inv = 1.f / lsum;
+  // the weighted sum of the partial accumulators: quarter sq takes partials
+  // i = sq, sq + 4, ...; the quarters add in a fixed order
   float o = 0.f;
-  for (int i = 0; i < np_all; ++i) o = fmaf(wts[i], part[slot(i) * kPartFloats + 4 + t], o);
-  oh[t] = o * inv;
+  for (int i = sq; i < np_all; i += kRotQuarters)
+    o = fmaf(wts[i], part[slot(i) * kPartFloats + 4 + tt], o);
+  rq[sq][tt] = o;
+  __syncthreads();
+  if (sq == 0) oh[tt] = ((rq[0][tt] + rq[1][tt]) + (rq[2][tt] + rq[3][tt])) * inv;
   if (!a.P_vo) {  // the output stays in the rotated basis (P_VO absorbed into W_O)
-    ((T*)a.out)[(int64_t)bhq * kD + t] = (T)oh[t];
+    if (sq == 0) ((T*)a.out)[(int64_t)bhq * kD + tt] = (T)oh[tt];
     return;
   }
   __syncthreads();
-  const float4* P = (const float4*)(a.P_vo + ((int64_t)h * kD + t) * kD);
-  float r = 0.f;
-#pragma unroll 8
-  for (int j4 = 0; j4 < kD / 4; ++j4) {
-    const float4 p = P[j4];
-    r = fmaf(p.x, oh[4 * j4], r);
-    r = fmaf(p.y, oh[4 * j4 + 1], r);
-    r = fmaf(p.z, oh[4 * j4 + 2], r);
-    r = fmaf(p.w, oh[4 * j4 + 3], r);
+  // o[t] = sum_j o_hat[j] P_vo[t][j]: the four 32-column quarters of row t in
+  // flight at once, one per 128 threads
+  const float4* P = (const float4*)(a.P_vo + ((int64_t)h * kD + tt) * kD + 32 * sq);
+  float r0 = 0.f, r1 = 0.f;
+#pragma unroll
+  for (int j4 = 0; j4 < 8; j4 += 2) {
+    const float4 p = P[j4], u = P[j4 + 1];
+    const float* o0 = oh + 32 * sq + 4 * j4;
+    r0 = fmaf(p.x, o0[0], r0);
+    r0 = fmaf(p.y, o0[1], r0);
+    r0 = fmaf(p.z, o0[2], r0);
+    r0 = fmaf(p.w, o0[3], r0);
+    r1 = fmaf(u.x, o0[4], r1);
+    r1 = fmaf(u.y, o0[5], r1);
+    r1 = fmaf(u.z, o0[6], r1);
+    r1 = fmaf(u.w, o0[7], r1);
   }
-  ((T*)a.out)[(int64_t)bhq * kD + t] = (T)r;
+  __syncthreads();  // rq is reused
+  rq[sq][tt] = r0 + r1;
+  __syncthreads();
+  if (sq == 0)
+    ((T*)a.out)[(int64_t)bhq * kD + tt] = (T)((rq[0][tt] + rq[1][tt]) + (rq[2][tt] + rq[3][tt]));
 }
 
 template <typename T, int KP8>
@@ -161,8 +196,8 @@ template <typename T>
 static hipError_t launch_decode_t(const DecodeLaunch& a) {
   const int BH = a.B * a.Hq;
   using E = typename Fmt<T>::Elem;
-  hipLaunchKernelGGL(qrot_kernel<E>, dim3(BH), dim3(128), 0, a.stream, (const E*)a.q, a.P_qk,
-                     a.qhat, a.Hq, a.Hq / a.Hkv, a.qmult);
+  hipLaunchKernelGGL(qrot_kernel<E>, dim3(BH), dim3(kD * kRotQuarters), 0, a.stream,
+                     (const E*)a.q, a.P_qk, a.qhat, a.Hq, a.Hq / a.Hkv, a.qmult);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (a.prof_start) {
@@ -260,7 +295,7 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
     e = hipEventRecord(a.prof_stop, a.stream);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(merge_kernel<E>, dim3(BH), dim3(128), 0, a.stream, a);
+  hipLaunchKernelGGL(merge_kernel<E>, dim3(BH), dim3(kMergeThreads), 0, a.stream, a);
   return hipGetLastError();
 }
 

@@ -125,9 +125,15 @@ def _check(status: int) -> None:
         raise SwanError(status, last_error())
 
 
+_I32_TYPES: dict = {}
+
+
 def _i32_array(values: Sequence[int]):
-    arr = (ctypes.c_int32 * len(values))(*[int(v) for v in values])
-    return arr
+    n = len(values)
+    ty = _I32_TYPES.get(n)
+    if ty is None:
+        ty = _I32_TYPES[n] = ctypes.c_int32 * n
+    return ty(*values)
 
 
 def _opt_i32_array(values: Optional[Sequence[int]]):
@@ -138,12 +144,17 @@ def _ptr(t) -> Optional[int]:
     return None if t is None else t.data_ptr()
 
 
-def _stream(stream) -> Optional[int]:
+def _stream(stream, device_index: Optional[int] = None) -> Optional[int]:
+    """The HIP stream handle: the given torch stream's, else the current stream of
+    device_index (default: the current device)."""
     import torch
 
-    if stream is None:
-        stream = torch.cuda.current_stream()
-    return stream.cuda_stream
+    if stream is not None:
+        return stream.cuda_stream
+    raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+    if raw is not None:
+        return raw(torch.cuda.current_device() if device_index is None else device_index)
+    return torch.cuda.current_stream().cuda_stream
 
 
 def _elem_torch_dtype(code: int):
@@ -160,17 +171,19 @@ def _tensor(t, name: str, dtype, shape) -> None:
         raise SwanError(SWAN_ERR_INVALID_ARG, f"{name} is None")
     if t.dtype != dtype:
         raise SwanError(SWAN_ERR_INVALID_ARG, f"{name} has dtype {t.dtype}, expected {dtype}")
-    if t.dim() != len(shape) or any(w is not None and g != w for g, w in zip(t.shape, shape)):
+    ts = tuple(t.shape)
+    if ts != shape and (len(ts) != len(shape) or
+                        any(w is not None and g != w for g, w in zip(ts, shape))):
         want = "x".join("*" if w is None else str(w) for w in shape)
         raise SwanError(SWAN_ERR_INVALID_ARG,
-                        f"{name} has shape {tuple(t.shape)}, expected [{want}]")
+                        f"{name} has shape {ts}, expected [{want}]")
     if not t.is_contiguous():
         raise SwanError(SWAN_ERR_INVALID_ARG, f"{name} must be contiguous (row-major)")
 
 
 def _on_gpu(**tensors) -> None:
     for name, t in tensors.items():
-        if t is not None and t.device.type != "cuda":
+        if t is not None and not t.is_cuda:
             raise SwanError(SWAN_ERR_INVALID_ARG, f"{name} is on {t.device}, not on a GPU")
 
 
@@ -248,7 +261,7 @@ def compress_append(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence[
     _check(_lib.swan_compress_append(ctypes.byref(desc), _i32_array(seq_len),
                                      _i32_array(k_active), _opt_i32_array(k_value), _ptr(k_new),
                                      _ptr(v_new), n_new, per, _ptr(P_qk), _ptr(P_vo),
-                                     _stream(stream)))
+                                     _stream(stream, P_qk.get_device())))
 
 
 def decode_workspace_bytes(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence[int],
@@ -264,13 +277,13 @@ def decode_attention(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence
                      P_qk, P_vo, out, workspace, scale: float = 0.0, stream=None,
                      k_value: Optional[Sequence[int]] = None) -> None:
     _decode_tensors(desc, q, P_qk, P_vo, out)
-    if workspace is None or workspace.device.type != "cuda" or not workspace.is_contiguous():
+    if workspace is None or not workspace.is_cuda or not workspace.is_contiguous():
         raise SwanError(SWAN_ERR_WORKSPACE, "workspace must be a contiguous GPU tensor")
     ws_bytes = workspace.numel() * workspace.element_size()
     _check(_lib.swan_decode_attention(ctypes.byref(desc), _i32_array(seq_len),
                                       _i32_array(k_active), _opt_i32_array(k_value), _ptr(q),
                                       _ptr(P_qk), _ptr(P_vo), float(scale), _ptr(out),
-                                      _ptr(workspace), ws_bytes, _stream(stream)))
+                                      _ptr(workspace), ws_bytes, _stream(stream, q.get_device())))
 
 
 def _decode_tensors(desc: CacheDesc, q, P_qk, P_vo, out) -> None:
@@ -290,7 +303,7 @@ def decode_attention_noalloc(desc: CacheDesc, seq_len: Sequence[int], k_active: 
     _check(_lib.swan_decode_attention_noalloc(ctypes.byref(desc), _i32_array(seq_len),
                                               _i32_array(k_active), _opt_i32_array(k_value),
                                               _ptr(q), _ptr(P_qk), _ptr(P_vo), float(scale),
-                                              _ptr(out), _stream(stream)))
+                                              _ptr(out), _stream(stream, q.get_device())))
 
 
 def change_k(src: CacheDesc, k_active_src: Sequence[int], k_value_src: Optional[Sequence[int]],
