@@ -53,18 +53,14 @@ __global__ __launch_bounds__(kD * kRotQuarters) void qrot_kernel(const T* __rest
 // ---------------------------------------------------------------------------
 // merge partials (log-sum-exp, fixed order) and rotate back: o = o_hat . P_vo^T
 // ---------------------------------------------------------------------------
-constexpr int kMergeThreads = kD * kRotQuarters;
 template <typename T>
-__global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeLaunch a) {
-  constexpr int kWaves = kMergeThreads / 64;
+__global__ __launch_bounds__(128) void merge_kernel(DecodeLaunch a) {
   __shared__ float oh[kD];
   __shared__ float wts[kMaxSplits + 1];
-  __shared__ float red[2 * kWaves];
-  __shared__ float rq[kRotQuarters][kD];
+  __shared__ float red[4];
   const int bhq = blockIdx.x;
   const int b = bhq / a.Hq, hq = bhq % a.Hq, h = hq / (a.Hq / a.Hkv);
   const int t = threadIdx.x;
-  const int sq = t / kD, tt = t & (kD - 1);  // quarter and dim of this thread
   const int L = a.tab.len[b];
   const int S = L > a.bb ? L - a.bb : 0;
   const int np = pages_for(S);
@@ -76,62 +72,41 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeLaunch a) {
   const int np_all = ns + (has_buf ? 1 : 0);
   auto slot = [&](int i) { return i < ns ? i : a.n_splits; };
   float mloc = -INFINITY;
-  for (int i = t; i < np_all; i += kMergeThreads) mloc = fmaxf(mloc, part[slot(i) * kPartFloats]);
+  for (int i = t; i < np_all; i += 128) mloc = fmaxf(mloc, part[slot(i) * kPartFloats]);
   mloc = wave_max(mloc);
   if ((t & 63) == 0) red[t >> 6] = mloc;
   __syncthreads();
-  float m = red[0];
-#pragma unroll
-  for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red[w]);
+  const float m = fmaxf(red[0], red[1]);
   float lloc = 0.f;
-  for (int i = t; i < np_all; i += kMergeThreads) {
+  for (int i = t; i < np_all; i += 128) {
     const float* pi = part + slot(i) * kPartFloats;
     const float wgt = exp2f(pi[0] - m);
     wts[i] = wgt;
     lloc += wgt * pi[1];
   }
   lloc = wave_sum(lloc);
-  if ((t & 63) == 0) red[kWaves + (t >> 6)] = lloc;
+  if ((t & 63) == 0) red[2 + (t >> 6)] = lloc;
   __syncthreads();
-  float lsum = 0.f;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) lsum += red[kWaves + w];
-  const float inv = 1.f / lsum;
-  // the weighted sum of the partial accumulators: quarter sq takes partials
-  // i = sq, sq + 4, ...; the quarters add in a fixed order
+  const float inv = 1.f / (red[2] + red[3]);
   float o = 0.f;
-  for (int i = sq; i < np_all; i += kRotQuarters)
-    o = fmaf(wts[i], part[slot(i) * kPartFloats + 4 + tt], o);
-  rq[sq][tt] = o;
-  __syncthreads();
-  if (sq == 0) oh[tt] = ((rq[0][tt] + rq[1][tt]) + (rq[2][tt] + rq[3][tt])) * inv;
+  for (int i = 0; i < np_all; ++i) o = fmaf(wts[i], part[slot(i) * kPartFloats + 4 + t], o);
+  oh[t] = o * inv;
   if (!a.P_vo) {  // the output stays in the rotated basis (P_VO absorbed into W_O)
-    if (sq == 0) ((T*)a.out)[(int64_t)bhq * kD + tt] = (T)oh[tt];
+    ((T*)a.out)[(int64_t)bhq * kD + t] = (T)oh[t];
     return;
   }
   __syncthreads();
-  // o[t] = sum_j o_hat[j] P_vo[t][j]: the four 32-column quarters of row t in
-  // flight at once, one per 128 threads
-  const float4* P = (const float4*)(a.P_vo + ((int64_t)h * kD + tt) * kD + 32 * sq);
-  float r0 = 0.f, r1 = 0.f;
-#pragma unroll
-  for (int j4 = 0; j4 < 8; j4 += 2) {
-    const float4 p = P[j4], u = P[j4 + 1];
-    const float* o0 = oh + 32 * sq + 4 * j4;
-    r0 = fmaf(p.x, o0[0], r0);
-    r0 = fmaf(p.y, o0[1], r0);
-    r0 = fmaf(p.z, o0[2], r0);
-    r0 = fmaf(p.w, o0[3], r0);
-    r1 = fmaf(u.x, o0[4], r1);
-    r1 = fmaf(u.y, o0[5], r1);
-    r1 = fmaf(u.z, o0[6], r1);
-    r1 = fmaf(u.w, o0[7], r1);
+  const float4* P = (const float4*)(a.P_vo + ((int64_t)h * kD + t) * kD);
+  float r = 0.f;
+#pragma unroll 8
+  for (int j4 = 0; j4 < kD / 4; ++j4) {
+    const float4 p = P[j4];
+    r = fmaf(p.x, oh[4 * j4], r);
+    r = fmaf(p.y, oh[4 * j4 + 1], r);
+    r = fmaf(p.z, oh[4 * j4 + 2], r);
+    r = fmaf(p.w, oh[4 * j4 + 3], r);
   }
-  __syncthreads();  // rq is reused
-  rq[sq][tt] = r0 + r1;
-  __syncthreads();
-  if (sq == 0)
-    ((T*)a.out)[(int64_t)bhq * kD + tt] = (T)((rq[0][tt] + rq[1][tt]) + (rq[2][tt] + rq[3][tt]));
+  ((T*)a.out)[(int64_t)bhq * kD + t] = (T)r;
 }
 
 template <typename T, int KP8>
@@ -295,7 +270,7 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
     e = hipEventRecord(a.prof_stop, a.stream);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(merge_kernel<E>, dim3(BH), dim3(kMergeThreads), 0, a.stream, a);
+  hipLaunchKernelGGL(merge_kernel<E>, dim3(BH), dim3(128), 0, a.stream, a);
   return hipGetLastError();
 }
 
