@@ -15,13 +15,14 @@
 // digit weight; the 17 digit pairs whose weight is within 5 digits of the top
 // give x_hat up to a bounded remainder: the 3 dropped pairs (below 2^-38 of
 // the two powers of two's product), plus the truncation of tiny entries of x
-// (counted per row) or of P (bounded per column).  Each element is rounded to
-// fp16 in two ways that must agree: both ends of its error interval (widened
-// by the float64 and float32 roundings) are rounded through float32; about 7
-// elements in 10^4 disagree and get an exact certification in float64 (no
-// fp16 rounding boundary within the bound of the computed value), and the
-// few that fail that are recomputed in float64 from x and P.  Either way the
-// stored value is the exact x_hat rounded once to fp16.
+// (counted per row) or of P (bounded per column).  Each
+// element is rounded to fp16 in two ways that must agree: both ends of its
+// error interval (widened by the float64 and float32 roundings) are rounded
+// through float32; about 7 elements in 10^4 disagree and get an exact
+// certification in float64 (no fp16 rounding boundary within the bound of the
+// computed value), and the few that fail that are recomputed in float64 from
+// x and P.  Either way the stored value is the exact x_hat rounded once to
+// fp16.
 //
 // A workgroup of 4 waves serves one (sequence, kv head, role): it first
 // writes P's digits, in the MFMA operand layout, to LDS (80 KiB), then each
@@ -514,23 +515,29 @@ void prefill_kernel(CompressLaunch a) {
           for (int t = 0; t < kPDigits; ++t)
             B[t] = *(const i32x4*)(bdig + (j * kPDigits + t) * 1024 + lane * 16);
         };
-        auto mfma_step = [&](int j, i32x4 (&acc)[2][kLevels], const i32x4 (&B)[kPDigits]) {
-          const int ks = j & 1;
-          if (ks == 0) {
+        // the 17 digit pairs (s, t), s + t <= 5, of one tile in s-major order;
+        // a step issues them for tile 0 then tile 1, in four parts of 9, 8, 9
+        // and 8 MFMAs (part q: tile q / 2, pairs 9 (q % 2) ..)
+        auto mfma_part = [&](int j, i32x4 (&acc)[2][kLevels], const i32x4 (&B)[kPDigits],
+                             int q) {
+          const int ks = j & 1, T = q >> 1;
+          int n = 0;
 #pragma unroll
-            for (int T = 0; T < 2; ++T)
+          for (int s = 0; s < kXDigits; ++s)
 #pragma unroll
-              for (int l = 0; l < kLevels; ++l) acc[T][l] = i32x4{0, 0, 0, 0};
-          }
+            for (int t = 0; t < kPDigits; ++t)
+              if (s + t <= kTopLevel) {
+                if ((n < 9) == ((q & 1) == 0))
+                  acc[T][s + t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[T][ks][s], B[t],
+                                                                        acc[T][s + t], 0, 0, 0);
+                ++n;
+              }
+        };
+        auto zero_acc = [&](i32x4 (&acc)[2][kLevels]) {
 #pragma unroll
           for (int T = 0; T < 2; ++T)
 #pragma unroll
-            for (int s = 0; s < kXDigits; ++s)
-#pragma unroll
-              for (int t = 0; t < kPDigits; ++t)
-                if (s + t <= kTopLevel)
-                  acc[T][s + t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[T][ks][s], B[t],
-                                                                        acc[T][s + t], 0, 0, 0);
+            for (int l = 0; l < kLevels; ++l) acc[T][l] = i32x4{0, 0, 0, 0};
         };
         // result layout: register v of lane l is row 4 (l / 16) + v (token),
         // column l % 16 (output dim 16 o + l % 16).
@@ -553,20 +560,16 @@ void prefill_kernel(CompressLaunch a) {
         // they agree that is the fp16 rounding of x_hat.  Elements whose ends
         // disagree (about 1 in 10^3) get the exact certification.  One half
         // (4 tokens) of tile o per call; returns the open elements as bits.
-        auto to_rows = [&](int o, int T, const i32x4 (&acc)[2][kLevels]) {
+        // (one element: register v of a lane's half tile, dyc the P truncation
+        // bound of its column; returns 1 when open)
+        auto to_row = [&](int o, int T, const i32x4 (&acc)[2][kLevels], int v, float dyc) {
           const int col = 16 * o + m16;
-          const float dyc = colDY[col];
-          uint32_t need = 0u;
-#pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const double y = result(acc, T, v);
-            const double E1 = fma(fabs(y), 0x1p-22, (double)fmaf(dyc, Ey[T][v], Eb[T][v]));
-            const uint32_t lo = f16_via_f32(y - E1), hi = f16_via_f32(y + E1);
-            need |= (lo != hi ? 1u : 0u) << v;
-            const int tok = 16 * (2 * tp + T) + 4 * g4 + v;
-            ((uint16_t*)rows)[tok * kRowHalves + col] = (uint16_t)lo;
-          }
-          return need;
+          const double y = result(acc, T, v);
+          const double E1 = fma(fabs(y), 0x1p-22, (double)fmaf(dyc, Ey[T][v], Eb[T][v]));
+          const uint32_t lo = f16_via_f32(y - E1), hi = f16_via_f32(y + E1);
+          const int tok = 16 * (2 * tp + T) + 4 * g4 + v;
+          ((uint16_t*)rows)[tok * kRowHalves + col] = (uint16_t)lo;
+          return lo != hi ? 1u : 0u;
         };
         // the exact certification of the elements the fast check left open
         auto fix_rows = [&](int o, int T, const i32x4 (&acc)[2][kLevels], uint32_t need) {
@@ -583,29 +586,44 @@ void prefill_kernel(CompressLaunch a) {
               ((uint16_t*)rows)[tok * kRowHalves + col] = (uint16_t)hb;
             }
         };
-        // 16 steps j = 2 o + ks (+ two to drain): step j issues the LDS reads
-        // of step j + 1's P digits, then its 34 MFMAs, each followed by three
-        // VALU instructions of half a tile of tile o - 1's conversion (the
-        // scheduling barriers keep that order and the steps apart).
+        // 16 steps j = 2 o + ks (+ two to drain): step j reads the P bound of
+        // the column it converts, issues the LDS reads of step j + 1's P
+        // digits, then its 34 MFMAs in four parts, each part
+        // followed by one element of half a tile of tile o - 1's conversion;
+        // the scheduling barriers interleave a part's MFMAs with that
+        // element's VALU work (4 instructions after each MFMA) and keep the
+        // parts apart, so the conversion runs while the MFMAs do.
         i32x4 acc[2][2][kLevels];
         i32x4 Bq[2][kPDigits];
         load_b(0, Bq[0]);
 #pragma unroll
         for (int j = 0; j < 18; ++j) {
           const int o = j >> 1, ks = j & 1;
+          const float dyc = j >= 2 ? colDY[16 * (o - 1) + m16] : 0.f;
           if (j + 1 < 16) load_b(j + 1, Bq[(j + 1) & 1]);
-          if (j < 16) mfma_step(j, acc[o & 1], Bq[j & 1]);
+          if (j < 16 && ks == 0) zero_acc(acc[o & 1]);
           uint32_t need = 0u;
-          if (j >= 2) need = to_rows(o - 1, ks, acc[(o - 1) & 1]);
-          if (j + 1 < 16) __builtin_amdgcn_sched_group_barrier(0x100, kPDigits, 0);  // DS read
-          if (j < 16) {
 #pragma unroll
-            for (int i = 0; i < 34; ++i) {
-              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-              __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // VALU
+          for (int q = 0; q < 4; ++q) {
+            if (j < 16) mfma_part(j, acc[o & 1], Bq[j & 1], q);
+            if (j >= 2) need |= to_row(o - 1, ks, acc[(o - 1) & 1], q, dyc) << q;
+            if (q == 0) {  // DS reads: the column bound, then the next step's P digits
+              if (j >= 2 && j + 1 < 16)
+                __builtin_amdgcn_sched_group_barrier(0x100, kPDigits + 1, 0);
+              else if (j + 1 < 16)
+                __builtin_amdgcn_sched_group_barrier(0x100, kPDigits, 0);
+              else
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             }
+            if (j < 16) {
+#pragma unroll
+              for (int i = 0; i < 9 - (q & 1); ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+                __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU
+              }
+            }
+            __builtin_amdgcn_sched_barrier(0);
           }
-          __builtin_amdgcn_sched_barrier(0);
           if (j >= 2 && __ballot(need != 0u) != 0u) fix_rows(o - 1, ks, acc[(o - 1) & 1], need);
         }
       }
