@@ -48,6 +48,8 @@
 namespace swan {
 
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kRowHalves = 136;                // LDS row of one token's 128 fp16 values (+ pad)
 constexpr int kPrefillBlocksPerWave = 8;       // 64-position blocks per wave
@@ -422,8 +424,10 @@ void prefill_kernel(CompressLaunch a) {
 #pragma unroll
         for (int T = 0; T < 2; ++T) {
           const u32x4 (&xv)[2][2] = xcur[T];
-          // the row's largest magnitude (fp16 bits) and the sum of its magnitudes
-          uint32_t mx = 0u;
+          // the row's largest magnitude (fp16 bits), the sum of its magnitudes
+          // and the smallest |x| - 1 (as 16-bit integers, so that 0 wraps to
+          // the largest), two elements per instruction
+          u16x2 mx2 = {0, 0}, tm2 = {0xFFFF, 0xFFFF};
           float l1 = 0.f;
 #pragma unroll
           for (int ks = 0; ks < 2; ++ks)
@@ -431,13 +435,18 @@ void prefill_kernel(CompressLaunch a) {
             for (int c = 0; c < 2; ++c)
 #pragma unroll
               for (int q = 0; q < 4; ++q) {
-                const uint32_t wv = xv[ks][c][q];
-                const uint32_t lo = wv & 0x7FFFu, hi = (wv >> 16) & 0x7FFFu;
-                mx = max(mx, max(lo, hi));
-                l1 += f16_bits_to_f32(lo) + f16_bits_to_f32(hi);
+                const uint32_t wa = xv[ks][c][q] & 0x7FFF7FFFu;
+                const u16x2 a2 = __builtin_bit_cast(u16x2, wa);
+                mx2 = __builtin_elementwise_max(mx2, a2);
+                tm2 = __builtin_elementwise_min(tm2, a2 - (u16x2){1, 1});
+                l1 = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, wa), (f16x2){1, 1}, l1, false);
               }
+          uint32_t mx = max((uint32_t)mx2.x, (uint32_t)mx2.y);
+          uint32_t tm = min((uint32_t)tm2.x, (uint32_t)tm2.y);
           mx = max(mx, (uint32_t)__shfl_xor((int)mx, 16));
           mx = max(mx, (uint32_t)__shfl_xor((int)mx, 32));
+          tm = min(tm, (uint32_t)__shfl_xor((int)tm, 16));
+          tm = min(tm, (uint32_t)__shfl_xor((int)tm, 32));
           l1 += __shfl_xor(l1, 16);
           l1 += __shfl_xor(l1, 32);
           // max|x| < 2^e
@@ -446,24 +455,27 @@ void prefill_kernel(CompressLaunch a) {
                                      : 8 - __builtin_clz(mx);  // (32 - clz) - 24
           const int shift = kXFix - e;
           // |x| >= 2^(e - 20) is exact in 30 bits below 2^e; each smaller nonzero
-          // element is truncated by less than 2^(e - 30): count them.  thr: the
-          // fp16 bits of 2^(e - 20), or 0 below the fp16 range (none truncated)
+          // element is truncated by less than 2^(e - 30): count them (rare: only
+          // when the smallest nonzero |x| is below thr).  thr: the fp16 bits of
+          // 2^(e - 20), or 0 below the fp16 range (none truncated)
           const int te = e - kXFix + 10;
           const uint32_t thr = te >= -14 ? (uint32_t)(te + 15) << 10
                                : te >= -24 ? 1u << (te + 24) : 0u;
           int ntr = 0;
+          if (__ballot(thr != 0u && tm < thr - 1u) != 0ull) {
 #pragma unroll
-          for (int ks = 0; ks < 2; ++ks)
+            for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-            for (int c = 0; c < 2; ++c)
+              for (int c = 0; c < 2; ++c)
 #pragma unroll
-              for (int q = 0; q < 4; ++q) {
-                const uint32_t wv = xv[ks][c][q];
-                ntr += ((wv & 0x7FFFu) - 1u < thr - 1u) ? 1 : 0;  // 0 < |x| < 2^(e - 20)
-                ntr += (((wv >> 16) & 0x7FFFu) - 1u < thr - 1u) ? 1 : 0;
-              }
-          ntr += __shfl_xor(ntr, 16);
-          ntr += __shfl_xor(ntr, 32);
+                for (int q = 0; q < 4; ++q) {
+                  const uint32_t wv = xv[ks][c][q];
+                  ntr += ((wv & 0x7FFFu) - 1u < thr - 1u) ? 1 : 0;  // 0 < |x| < 2^(e - 20)
+                  ntr += (((wv >> 16) & 0x7FFFu) - 1u < thr - 1u) ? 1 : 0;
+                }
+            ntr += __shfl_xor(ntr, 16);
+            ntr += __shfl_xor(ntr, 32);
+          }
 #pragma unroll
           for (int ks = 0; ks < 2; ++ks) {
             uint32_t dg[kXDigits][4];
@@ -561,7 +573,7 @@ void prefill_kernel(CompressLaunch a) {
         // disagree (about 1 in 10^3) get the exact certification.  One half
         // (4 tokens) of tile o per call; returns the open elements as bits.
         // (one element: register v of a lane's half tile, dyc the P truncation
-        // bound of its column; returns 1 when open)
+        // bound of its column; true when open)
         auto to_row = [&](int o, int T, const i32x4 (&acc)[2][kLevels], int v, float dyc) {
           const int col = 16 * o + m16;
           const double y = result(acc, T, v);
@@ -569,15 +581,15 @@ void prefill_kernel(CompressLaunch a) {
           const uint32_t lo = f16_via_f32(y - E1), hi = f16_via_f32(y + E1);
           const int tok = 16 * (2 * tp + T) + 4 * g4 + v;
           ((uint16_t*)rows)[tok * kRowHalves + col] = (uint16_t)lo;
-          return lo != hi ? 1u : 0u;
+          return lo != hi;
         };
         // the exact certification of the elements the fast check left open
-        auto fix_rows = [&](int o, int T, const i32x4 (&acc)[2][kLevels], uint32_t need) {
+        auto fix_rows = [&](int o, int T, const i32x4 (&acc)[2][kLevels], const bool (&need)[4]) {
           const int col = 16 * o + m16;
           const float dyc = colDY[col];
 #pragma unroll
           for (int v = 0; v < 4; ++v)
-            if (need & (1u << v)) {
+            if (need[v]) {
               const double y = result(acc, T, v);
               const double E = (double)fmaf(dyc, Ey[T][v], Eb[T][v]);
               const uint32_t hb = certified_f16(y, E);
@@ -602,11 +614,11 @@ void prefill_kernel(CompressLaunch a) {
           const float dyc = j >= 2 ? colDY[16 * (o - 1) + m16] : 0.f;
           if (j + 1 < 16) load_b(j + 1, Bq[(j + 1) & 1]);
           if (j < 16 && ks == 0) zero_acc(acc[o & 1]);
-          uint32_t need = 0u;
+          bool need[4] = {false, false, false, false};
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             if (j < 16) mfma_part(j, acc[o & 1], Bq[j & 1], q);
-            if (j >= 2) need |= to_row(o - 1, ks, acc[(o - 1) & 1], q, dyc) << q;
+            if (j >= 2) need[q] = to_row(o - 1, ks, acc[(o - 1) & 1], q, dyc);
             if (q == 0) {  // DS reads: the column bound, then the next step's P digits
               if (j >= 2 && j + 1 < 16)
                 __builtin_amdgcn_sched_group_barrier(0x100, kPDigits + 1, 0);
@@ -624,7 +636,8 @@ void prefill_kernel(CompressLaunch a) {
             }
             __builtin_amdgcn_sched_barrier(0);
           }
-          if (j >= 2 && __ballot(need != 0u) != 0u) fix_rows(o - 1, ks, acc[(o - 1) & 1], need);
+          if (j >= 2 && __ballot(need[0] | need[1] | need[2] | need[3]) != 0u)
+            fix_rows(o - 1, ks, acc[(o - 1) & 1], need);
         }
       }
     } else {

@@ -61,8 +61,9 @@ def test_calibrate_constructed_basis(gpu_device):
 # compress-append: indices and values bit-exact
 # --------------------------------------------------------------------------- #
 def _build(swan_mod, torch_mod, device, *, B, Hq, Hkv, L, b, k_active, dtype, chunks=None,
-           seed=0, capacity=None, wid=99, values="same", k_value=None):
-    """GPU cache + oracle caches for synthetic rows of the recipe."""
+           seed=0, capacity=None, wid=99, values="same", k_value=None, kv_hook=None):
+    """GPU cache + oracle caches for synthetic rows of the recipe (kv_hook(K, V)
+    may rewrite the rows in place first)."""
     torch = torch_mod
     np_dt = si.np_dtype(dtype)
     Pqk = np.stack([si.random_orthogonal(seed * 100 + h, 128) for h in range(Hkv)]).astype(
@@ -78,6 +79,8 @@ def _build(swan_mod, torch_mod, device, *, B, Hq, Hkv, L, b, k_active, dtype, ch
             R = si.haar_orthogonal(si.rng_for(wid, seed, h), 128)
             K[bi, h] = si.lowrank_rows(si.rng_for(wid, seed, bi, h, 0), Lmax, R).astype(np_dt)
             V[bi, h] = si.lowrank_rows(si.rng_for(wid, seed, bi, h, 1), Lmax, R).astype(np_dt)
+    if kv_hook is not None:
+        kv_hook(K, V)
     cap = capacity if capacity is not None else max(Lmax - b, 1)
     cache = swan_mod.SwanCache(B, Hq, Hkv, b, cap, k_active, C.torch_dtype(dtype), device,
                                sparse_values=values, k_value=k_value)
@@ -123,6 +126,51 @@ def test_compress_prefill_bit_exact(gpu_device, swan_mod, torch_mod, dtype, L, b
     for bi in range(2):
         for h in range(2):
             C.compare_unit(cache, oc[bi][h], bi, h, L, si.np_dtype(dtype))
+
+
+def _extreme_rows(K, V):
+    """Rows that reach the rotation's edge cases: elements far below the row's
+    largest (they fall below its fixed-point resolution), fp16 subnormals, zeros,
+    rows of small or large magnitude, all-zero rows and single-element rows."""
+    rng = si.rng_for(4242)
+    for X in (K, V):
+        B, H, L, D = X.shape
+        for bi in range(B):
+            for h in range(H):
+                x = X[bi, h].astype(np.float64)
+                for t in range(L):
+                    kind = t % 8
+                    row = x[t]
+                    m = np.max(np.abs(row))
+                    if kind == 1:    # a few elements 2^-21 .. 2^-26 of the largest
+                        idx = rng.choice(D, 6, replace=False)
+                        row[idx] = m * np.ldexp(1.0, -rng.integers(21, 27, 6)) * rng.choice([-1, 1], 6)
+                    elif kind == 2:  # fp16 subnormals and zeros
+                        idx = rng.choice(D, 10, replace=False)
+                        row[idx[:6]] = np.ldexp(rng.integers(1, 1024, 6).astype(np.float64), -24)
+                        row[idx[6:]] = 0.0
+                    elif kind == 3:  # small row: largest below 2^-8
+                        row *= np.ldexp(1.0, -10) / max(m, 1e-30)
+                    elif kind == 4:  # large row: rotated components up to ~3e4
+                        row *= 3.0e4 / max(np.linalg.norm(row), 1e-30)
+                    elif kind == 5 and t % 16 == 5:
+                        row[:] = 0.0
+                    elif kind == 6:  # one nonzero element
+                        j = int(rng.integers(0, D))
+                        v = row[j]
+                        row[:] = 0.0
+                        row[j] = v if v != 0 else 1.0
+                X[bi, h] = x.astype(X.dtype)
+
+
+@pytest.mark.parametrize("L,b,k", [(300, 16, 48), (200, 0, 13), (130, 64, 96)])
+def test_compress_prefill_extreme_rows(gpu_device, swan_mod, torch_mod, L, b, k):
+    _log(f"compress prefill extreme rows L={L} b={b} k={k}")
+    cache, oc, *_ = _build(swan_mod, torch_mod, gpu_device, B=2, Hq=2, Hkv=2, L=L, b=b,
+                           k_active=[k, k], dtype="f16", kv_hook=_extreme_rows)
+    for bi in range(2):
+        for h in range(2):
+            C.compare_unit(cache, oc[bi][h], bi, h, L, np.float16)
 
 
 @pytest.mark.parametrize("chunks", [[1] * 150, [7, 1, 64, 13, 65], [100, 1, 1, 1, 47]])
