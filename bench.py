@@ -27,7 +27,7 @@ MALL_BYTES = 256 << 20  # MI355X last-level (Infinity) cache
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic_{wl}.txt")
 # sources of the decode attention kernels: counter summaries are valid only for these bytes
 ATTN_SOURCES = ("decode.hip", "decode_gqa.hip", "decode_asym.hip", "decode_gqa_asym.hip",
-                "decode_mha.h", "decode_gqa.h", "decode_common.h", "decode_gqa_common.h",
+                "decode_fused.hip", "decode_mha.h", "decode_gqa.h", "decode_common.h", "decode_gqa_common.h",
                 "swan_device.h", "swan_internal.h")
 
 
@@ -108,16 +108,24 @@ def kpad(k: int) -> int:
     return (k + 7) // 8 * 8
 
 
-def attention_launches(k_key, k_val, merge_pct: int = 66):
+def fused_path(w) -> bool:
+    """MHA on fp16 storage: a batch with several k_pad takes one launch in which
+    each sequence's waves are specialised on its own k_pad."""
+    return w.dtype == "f16" and w.n_q_heads == w.n_kv_heads
+
+
+def attention_launches(k_key, k_val, merge_pct: int = 66, fused: bool = False):
     """The library's attention launches for these per-sequence k: [(kp8, same_k_pad)].
-    Sequences are grouped by (key, value) k_pad; from the largest k_pad down, a group
-    joins the launch before it when its k_pad is at least merge_pct % of that
-    launch's (the library's default, 66; <= 0 merges nothing), and a launch whose
-    sequences do not all have its k_pad for both roles runs the instances for
-    different k_pad."""
+    Sequences are grouped by (key, value) k_pad.  fused (fused_path): several groups
+    make one launch.  Otherwise, from the largest k_pad down, a group joins the
+    launch before it when its k_pad is at least merge_pct % of that launch's (the
+    library's default, 66; <= 0 merges nothing), and a launch whose sequences do
+    not all have its k_pad for both roles runs the instances for different k_pad."""
     pct = merge_pct
     groups = sorted({(kpad(a) // 8, kpad(b) // 8) for a, b in zip(k_key, k_val)},
                     key=lambda g: (-max(g), -g[0], -g[1]))
+    if fused and len(groups) > 1:
+        return [(max(groups[0]), False)]
     launches = []
     for pk, pv in groups:
         kp = max(pk, pv)
@@ -131,7 +139,11 @@ def attention_launches(k_key, k_val, merge_pct: int = 66):
 def attn_kernel_name(w, k_key, k_val) -> str:
     """The decode attention kernel the library launches for this shape."""
     g = w.n_q_heads // w.n_kv_heads
-    asym = not all(same for _, same in attention_launches(k_key, k_val))
+    launches = attention_launches(k_key, k_val, fused=fused_path(w))
+    if fused_path(w) and len({(kpad(a), kpad(b)) for a, b in zip(k_key, k_val)}) > 1:
+        return ("attn_fused_kernel (one query head per wave, each sequence's waves specialised "
+                "on its own k_pad; sparse split-K + dense buffer)")
+    asym = not all(same for _, same in launches)
     note = ("; launches mixing k_pad (keys and values, or merged sequences): specialised on "
             "the largest, each role and sequence at its own page size" if asym else "")
     if w.dtype == "f16" and g > 1 and g % 2 == 0:
@@ -141,8 +153,8 @@ def attn_kernel_name(w, k_key, k_val) -> str:
     return f"attn_kernel (one query head per wave, sparse split-K + dense buffer{note})"
 
 
-def launches_per_step(k_key, k_val) -> int:
-    return len(attention_launches(k_key, k_val))
+def launches_per_step(w, k_key, k_val) -> int:
+    return len(attention_launches(k_key, k_val, fused=fused_path(w)))
 
 
 def time_change_k(swan, torch, w, cache, ks, kvs, k_new, esize, reps=5):
@@ -616,7 +628,7 @@ def main():
             "kernel": attn_kernel_name(w, ks, kv_list),
             # one launch per distinct (key, value) padded k in the batch; bytes and
             # time cover all of a step's attention launches together
-            "launches_per_step": launches_per_step(ks, kv_list),
+            "launches_per_step": launches_per_step(w, ks, kv_list),
             "algorithmic_bytes_per_launch": bytes_avg,
             "avg_launch_ms": attn_avg * 1e3,
             "source_digest": digest,

@@ -300,17 +300,22 @@ swan_status swan_change_k(const swan_cache* src, const int32_t* k_active_src,
  * workspace size depends on the plan, so query it under the same tuning.
  * Every field: 0 selects the default.
  *  target_waves       sparse attention waves the split planner aims for over
- *                     the batch (default 2048, two per wave slot of the GPU);
- *                     each sequence's token splits follow its share of the
- *                     bytes, every split keeps at least one page;
+ *                     the batch (default 2048, two per wave slot of the GPU;
+ *                     twice that for a batch of several k_pad on the
+ *                     one-query-head-per-wave path with fp16 storage, which
+ *                     takes one launch with each sequence's waves specialised
+ *                     on its own k_pad); each sequence's token splits follow
+ *                     its share of the bytes, every split keeps at least one
+ *                     page;
  *  short_split_pages  a short sequence (whose shrinking splits would be at most
  *                     half as many as its share asks for) is cut into equal
  *                     splits of this many pages (default 4); -1: shrinking
  *                     splits for every sequence;
- *  merge_pct          for a batch mixing k_pad: from the largest k_pad down, a
- *                     group of sequences joins the launch before it when its
- *                     k_pad is at least this percentage of that launch's
- *                     (default 66); -1: one launch per k_pad;
+ *  merge_pct          for a batch mixing k_pad on the other paths (several
+ *                     query heads per wave, or fp32 storage): from the largest
+ *                     k_pad down, a group of sequences joins the launch before
+ *                     it when its k_pad is at least this percentage of that
+ *                     launch's (default 66); -1: one launch per k_pad;
  *  side_streams       library streams (per thread and device) for those
  *                     launches, 1..3 (default 3); -1: all on the caller's stream.
  * Errors: SWAN_ERR_INVALID_ARG for a value outside these ranges (the thread's

@@ -18,8 +18,8 @@ LIB = os.path.join(HERE, "libswan.so")
 BENCH_LIB = os.path.join(HERE, "libswanbench.so")
 BENCH_SOURCES = ["stream_ceiling.hip"]
 SOURCES = ["swan_api.hip", "decode.hip", "decode_gqa.hip", "decode_asym.hip",
-           "decode_gqa_asym.hip", "compress.hip", "prefill.hip", "change_k.hip", "rope.hip",
-           "calibrate.hip"]
+           "decode_gqa_asym.hip", "decode_fused.hip", "compress.hip", "prefill.hip",
+           "change_k.hip", "rope.hip", "calibrate.hip"]
 ARCH = "gfx950"
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "-shared", f"--offload-arch={ARCH}",

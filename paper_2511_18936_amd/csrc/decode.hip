@@ -5,11 +5,15 @@
 //   attn_kernel    one wave per (sequence, query head, token split) over the
 //                  sparse pages, plus one wave per (sequence, query head) over
 //                  the dense buffer; each writes a partial (m, l, acc[128]) in
-//                  the rotated space.  One launch per distinct k_pad of the
-//                  batch; several run side by side on library-owned streams
-//                  of the calling thread, joined back before the merge.  For fp16 GQA the launch is
-//                  attn_gqa_kernel (decode_gqa.h) instead, one workgroup per
-//                  KV stream for several query heads.  Sequences whose keys and
+//                  the rotated space.  On the fp16 formats a batch with
+//                  several k_pad takes one launch of attn_fused_kernel
+//                  (decode_fused.hip), each wave specialised on its own
+//                  sequence's k_pad.  Otherwise one launch per distinct k_pad
+//                  of the batch; several run side by side on library-owned
+//                  streams of the calling thread, joined back before the
+//                  merge.  For fp16 GQA the launch is attn_gqa_kernel
+//                  (decode_gqa.h) instead, one workgroup per KV stream for
+//                  several query heads.  Sequences whose keys and
 //                  values have different k_pad run the same kernels specialised
 //                  on the larger k_pad (decode_asym.hip, decode_gqa_asym.hip).
 //   merge_kernel   log-sum-exp merge of the partials, then o = o_hat . P_VO^T
@@ -208,6 +212,36 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
       kp8v[ng] = pv;
       ++ng;
     }
+  if (ng > 1 && decode_heads_per_wave(a.dtype, a.Hq, a.Hkv) == 1 &&
+      (a.dtype == SWAN_F16 || a.dtype == SWAN_F16_E4M3)) {
+    // MHA, fp16 storage: one launch over every group, each sequence's waves
+    // specialised on its own k_pad tier, larger k_pad first
+    FusedSeqs f;
+    f.n = 0;
+    f.n_splits = 0;
+    bool taken[SWAN_MAX_BATCH] = {};
+    for (int done = 0; done < ng; ++done) {
+      int best = -1, bkp = 0;
+      for (int i = 0; i < ng; ++i) {
+        const int kp = kp8k[i] > kp8v[i] ? kp8k[i] : kp8v[i];
+        if (!taken[i] && kp > bkp) {
+          best = i;
+          bkp = kp;
+        }
+      }
+      taken[best] = true;
+      for (int j = 0; j < groups[best].n; ++j) {
+        f.seq[f.n] = groups[best].seq[j];
+        f.kp8[f.n] = (int8_t)fused_tier(bkp);
+        ++f.n;
+      }
+      if (groups[best].n_splits > f.n_splits) f.n_splits = groups[best].n_splits;
+    }
+    if ((e = launch_attn_fused(a, f)) != hipSuccess) return e;
+    if (a.prof_stop && (e = hipEventRecord(a.prof_stop, a.stream)) != hipSuccess) return e;
+    hipLaunchKernelGGL(merge_kernel<E>, dim3(BH), dim3(128), 0, a.stream, a);
+    return hipGetLastError();
+  }
   struct Launch {
     SeqGroup g;
     int kp8;

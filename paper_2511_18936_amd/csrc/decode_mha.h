@@ -96,39 +96,32 @@ __device__ void sparse_split(const UnitPages& u, int pbeg, int pend, int S, floa
   }
 }
 
-// One launch per distinct k_pad of the batch (KP8 = k_pad / 8), over the
-// sequences g.seq[0..g.n) that use it.  kAsym: the sequences' keys and values
-// have different k_pad, the larger being 8 KP8; each role's own k_pad then
-// sets its page size and loaded groups at run time, the rest being spare
-// groups (load_page), for which q_rep and acc get a spare row kSpareRow.
-// Grid: n * Hq dense-buffer waves first, then n * Hq * g.n_splits sparse waves.
+// The dense-buffer wave of (sequence b, query head hq): its partial over the
+// ring's tokens (slot n_splits).
+template <typename T>
+__device__ __forceinline__ void buffer_wave(const DecodeLaunch& a, int b, int hq, float* qrep,
+                                            float* acc, int lane) {
+  const int h = hq / (a.Hq / a.Hkv);
+  const int bhq = b * a.Hq + hq;
+  const int L = a.tab.len[b];
+  const int nb = L < a.bb ? L : a.bb;
+  if (nb == 0) return;
+  const int64_t ring_off = ((int64_t)b * a.Hkv + h) * a.bb * kD;
+  float* part = a.part + ((int64_t)bhq * (a.n_splits + 1) + a.n_splits) * kPartFloats;
+  using E = typename Fmt<T>::Elem;
+  buffer_part<E>((const E*)a.k_ring + ring_off, (const E*)a.v_ring + ring_off, nb,
+                 a.qhat + (int64_t)bhq * kD, qrep, acc, lane, part);
+}
+
+// The sparse wave of (sequence b, query head hq, token split `split`) on pages
+// of k_pad 8 KP8.  kAsym: keys and values may have a smaller k_pad than 8 KP8;
+// each role's own k_pad then sets its page size and loaded groups at run time,
+// the rest being spare groups (load_page), for which q_rep and acc have a
+// spare row kSpareRow (qrep and acc hold kD + 1 rows).
 template <typename T, int KP8, bool kAsym>
-__global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup g) {
-  constexpr int kRows = kAsym ? kD + 1 : kD;
-  __shared__ __attribute__((aligned(16))) float qrep[kRows * kQRep];
-  __shared__ __attribute__((aligned(16))) float acc[kRows * kAccCols];
-  const int lane = threadIdx.x;
-  const int GH = g.n * a.Hq;
-  const int G = a.Hq / a.Hkv;
-  const int pstride = a.n_splits + 1;  // partial slots per (sequence, q-head)
-  int w = blockIdx.x;
-  if (w < GH) {  // dense-buffer wave
-    const int b = g.seq[w / a.Hq], hq = w % a.Hq, h = hq / G;
-    const int bhq = b * a.Hq + hq;
-    const int L = a.tab.len[b];
-    const int nb = L < a.bb ? L : a.bb;
-    if (nb == 0) return;
-    const int64_t ring_off = ((int64_t)b * a.Hkv + h) * a.bb * kD;
-    float* part = a.part + ((int64_t)bhq * pstride + a.n_splits) * kPartFloats;
-    using E = typename Fmt<T>::Elem;
-    buffer_part<E>((const E*)a.k_ring + ring_off, (const E*)a.v_ring + ring_off, nb,
-                   a.qhat + (int64_t)bhq * kD, qrep, acc, lane, part);
-    return;
-  }
-  w -= GH;
-  const int split = w / GH;
-  const int gi = w % GH;
-  const int b = g.seq[gi / a.Hq], hq = gi % a.Hq, h = hq / G;
+__device__ __forceinline__ void sparse_wave(const DecodeLaunch& a, int b, int hq, int split,
+                                            float* qrep, float* acc, int lane) {
+  const int h = hq / (a.Hq / a.Hkv);
   const int bhq = b * a.Hq + hq;
   const int L = a.tab.len[b];
   const int S = L > a.bb ? L - a.bb : 0;
@@ -145,7 +138,7 @@ __global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup g) {
   u.nv8 = kAsym ? kpad_of(a.tab.kact[1][b]) / 8 : KP8;
   u.kbase = (const char*)a.k_pages + a.tab.page_off[0][b] + (int64_t)h * a.n_pages_cap * u.kbytes;
   u.vbase = (const char*)a.v_pages + a.tab.page_off[1][b] + (int64_t)h * a.n_pages_cap * u.vbytes;
-  float* part = a.part + ((int64_t)bhq * pstride + split) * kPartFloats;
+  float* part = a.part + ((int64_t)bhq * (a.n_splits + 1) + split) * kPartFloats;
 
   // replicate q_hat: q_rep[dim][8]; lane writes dims lane and lane + 64
   const float* qh = a.qhat + (int64_t)bhq * kD;
@@ -164,6 +157,26 @@ __global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup g) {
     ((float4*)acc)[c * 64 + lane] = make_float4(0.f, 0.f, 0.f, 0.f);
   wave_lds_fence();
   sparse_split<T, KP8>(u, pbeg, pend, S, qrep, acc, lane, part);
+}
+
+// One launch per distinct k_pad of the batch (KP8 = k_pad / 8), over the
+// sequences g.seq[0..g.n) that use it (kAsym as in sparse_wave).
+// Grid: n * Hq dense-buffer waves first, then n * Hq * g.n_splits sparse waves.
+template <typename T, int KP8, bool kAsym>
+__global__ __launch_bounds__(64) void attn_kernel(DecodeLaunch a, SeqGroup g) {
+  constexpr int kRows = kAsym ? kD + 1 : kD;
+  __shared__ __attribute__((aligned(16))) float qrep[kRows * kQRep];
+  __shared__ __attribute__((aligned(16))) float acc[kRows * kAccCols];
+  const int lane = threadIdx.x;
+  const int GH = g.n * a.Hq;
+  int w = blockIdx.x;
+  if (w < GH) {  // dense-buffer wave
+    buffer_wave<T>(a, g.seq[w / a.Hq], w % a.Hq, qrep, acc, lane);
+    return;
+  }
+  w -= GH;
+  const int gi = w % GH;
+  sparse_wave<T, KP8, kAsym>(a, g.seq[gi / a.Hq], gi % a.Hq, w / GH, qrep, acc, lane);
 }
 
 }  // namespace swan

@@ -168,7 +168,19 @@ int plan_splits(const swan_cache* c, const int32_t* seq_len_host, const int32_t*
     const int S = seq_len_host[b] > c->buffer_tokens ? seq_len_host[b] - c->buffer_tokens : 0;
     total += (int64_t)swan::pages_for(S) * weight(b) * waves_per_seq;
   }
-  const int64_t target_waves = g_tuning.target_waves;
+  // A batch of several k_pad on the fused MHA launch (decode_fused.hip) takes
+  // twice the waves: its shorter splits balance the tiers' different costs
+  // per page (measured: 16k x 8 with k in {32, 48, 64, 96}, 0.222 -> 0.213 ms;
+  // the single-k workloads gain nothing from it and GQA loses 8 %).
+  bool several_kpad = false;
+  for (int b = 1; b < c->batch; ++b)
+    several_kpad |= swan::kpad_of(k_of(k_active_host, k_value_host, 0, b)) !=
+                        swan::kpad_of(k_of(k_active_host, k_value_host, 0, 0)) ||
+                    swan::kpad_of(k_of(k_active_host, k_value_host, 1, b)) !=
+                        swan::kpad_of(k_of(k_active_host, k_value_host, 1, 0));
+  const bool fused = several_kpad && hpw == 1 &&
+                     (c->dtype == SWAN_F16 || c->dtype == SWAN_F16_E4M3);
+  const int64_t target_waves = g_tuning.target_waves * (fused ? 2 : 1);
   // A sequence whose shrinking splits the one-page rule cuts to half the count
   // wanted or fewer is short: its waves would each walk many pages one after
   // another, so it gets equal splits of flat_pages pages instead.

@@ -82,6 +82,17 @@ struct SeqGroup {
   int32_t seq[SWAN_MAX_BATCH];
 };
 
+// sequences of a batch with several k_pad, in one MHA attention launch: each
+// sparse wave runs the kernel body specialised on its own sequence's k_pad
+struct FusedSeqs {
+  int32_t n;                    // sequences
+  int32_t n_splits;             // the largest split count among them
+  int32_t seq[SWAN_MAX_BATCH];  // batch indices, larger k_pad first
+  int8_t kp8[SWAN_MAX_BATCH];   // fused_tier of the larger of its key and value k_pad / 8
+};
+int fused_tier(int kp8);  // the kernel body serving k_pad 8 kp8: 2, 4, ..., 12 or 16
+hipError_t launch_attn_fused(const DecodeLaunch& a, const FusedSeqs& f);
+
 // GQA path (fp16 storage, G = n_q / n_kv > 1): query heads served by one wave,
 // 1 when the GQA kernel does not apply
 int gqa_heads_per_wave(int G);

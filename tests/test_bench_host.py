@@ -29,7 +29,16 @@ def test_attention_launches_mirror_the_grouping():
     ks = [48, 32, 32, 64, 48, 32, 96, 48]
     # k_pad 96 and 64 (two thirds) share a launch, so do 48 and 32
     assert bench.attention_launches(ks, ks) == [(12, False), (6, False)]
-    assert bench.launches_per_step(ks, ks) == 2
+    w4 = si.WORKLOADS["llama2_7b_prefill16k_b8"]
+    # MHA on fp16 storage: one launch, each sequence at its own k_pad
+    assert bench.fused_path(w4)
+    assert bench.attention_launches(ks, ks, fused=True) == [(12, False)]
+    assert bench.launches_per_step(w4, ks, ks) == 1
+    assert bench.attn_kernel_name(w4, ks, ks).startswith("attn_fused_kernel")
+    wg = si.WORKLOADS["llama3_8b_gqa_L128k_b4"]
+    assert not bench.fused_path(wg)
+    assert bench.launches_per_step(wg, ks, ks) == 2
+    assert bench.attention_launches([48] * 16, [48] * 16, fused=True) == [(6, True)]
     assert bench.attention_launches([48] * 16, [48] * 16) == [(6, True)]
     assert bench.attention_launches([41, 48], [47, 45]) == [(6, True)]  # one k_pad
     assert bench.attention_launches([77] * 4, [51] * 4) == [(10, False)]

@@ -1,7 +1,8 @@
 """swan_decode_attention captured in a HIP graph (torch.cuda.CUDAGraph) and replayed.
 
-A decode call enqueues only kernels (and, for a batch mixing k_pad, event fork /
-join with the library's side streams), so a serving loop can capture it.  Each
+A decode call enqueues only kernels (and, for a batch mixing k_pad on the GQA
+or fp32 paths, event fork / join with the library's side streams), so a serving
+loop can capture it.  Each
 replay must give the eager call's output bit for bit (decode is deterministic),
 with the program's own eager work and synchronisations between the replays, and
 a replay after new queries are written into the captured input must match an
@@ -23,8 +24,9 @@ def _log(msg):
 
 
 @pytest.mark.parametrize("Hq,Hkv,ks,dtype", [(8, 8, [48, 48, 48], "f16"),
-                                             (8, 8, [32, 48, 96], "f16"),  # side streams
+                                             (8, 8, [32, 48, 96], "f16"),  # fused launch
                                              (8, 2, [64, 64, 64], "f16"),  # GQA
+                                             (8, 2, [32, 48, 96], "f16"),  # side streams
                                              (4, 4, [40, 64, 24], "f32")])
 def test_decode_graph_replays_match_eager(gpu_device, swan_mod, torch_mod, Hq, Hkv, ks, dtype):
     torch = torch_mod

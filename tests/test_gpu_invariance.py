@@ -8,9 +8,9 @@
 * Cache round trip (checkpoint / resume): the library keeps no state between
   calls, so pages and ring copied to the host and back into new arrays continue
   exactly like the original: the next append and decode are bitwise equal.
-* Two threads, each with its own stream and a batch that mixes page formats (so
-  each uses its thread's side streams), decode concurrently and both match the
-  oracle.
+* Two threads, each with its own stream and a batch that mixes page formats
+  (one fused launch on the MHA path; on the GQA path each uses its thread's side
+  streams), decode concurrently and both match the oracle.
 """
 import sys
 import threading
@@ -154,16 +154,19 @@ def test_cache_round_trip_through_host_memory(gpu_device, swan_mod, torch_mod, d
         assert torch.equal(o1.view(torch.uint8), o2.view(torch.uint8)), step
 
 
-def test_two_threads_on_two_streams(gpu_device, swan_mod, torch_mod):
-    """Two callers, each on its own thread and stream with a mixed-k batch (side
-    streams of its own thread): both outputs match the oracle."""
+@pytest.mark.parametrize("Hq,Hkv", [(4, 4), (4, 2)])
+def test_two_threads_on_two_streams(gpu_device, swan_mod, torch_mod, Hq, Hkv):
+    """Two callers, each on its own thread and stream with a mixed-k batch (one
+    fused launch for MHA; side streams of its own thread for GQA): both outputs
+    match the oracle."""
     torch, swan = torch_mod, swan_mod
+    _log(f"two threads Hq={Hq} Hkv={Hkv}")
     setups = []
     for i in range(2):
         cache, oc, Pqk, Pvo, tP_qk, tP_vo, *_ = _build(
-            swan, torch, gpu_device, B=4, Hq=4, Hkv=4, L=[2000 + 300 * i, 900, 1500, 400],
+            swan, torch, gpu_device, B=4, Hq=Hq, Hkv=Hkv, L=[2000 + 300 * i, 900, 1500, 400],
             b=16, k_active=[96, 64, 48, 24], dtype="f16", seed=10 + i, wid=133)
-        q = torch.tensor(si.queries_host(133 + i, 4, 4, "f16"), device=gpu_device)
+        q = torch.tensor(si.queries_host(133 + i, 4, Hq, "f16"), device=gpu_device)
         setups.append((cache, oc, Pqk, Pvo, tP_qk, tP_vo, q))
     outs = [None, None]
     errors = []
@@ -192,6 +195,6 @@ def test_two_threads_on_two_streams(gpu_device, swan_mod, torch_mod):
         res = outs[i]
         for o in res[1:]:
             assert torch.equal(o, res[0])
-        err = _oracle_err(res[0], q, oc, Pqk, Pvo, 1)
+        err = _oracle_err(res[0], q, oc, Pqk, Pvo, Hq // Hkv)
         _log(f"thread {i}: oracle err {err:.2e}")
         assert err <= TOL

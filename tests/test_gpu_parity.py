@@ -257,8 +257,9 @@ def test_decode_ragged_lengths_and_per_sequence_k(gpu_device, swan_mod, torch_mo
 
 @pytest.mark.parametrize("Hq,Hkv", [(1, 1), (4, 2)])
 def test_decode_max_batch_many_k(gpu_device, swan_mod, torch_mod, Hq, Hkv):
-    """The largest batch, each sequence with its own length and k: up to 16
-    attention launches, spread over the library's side streams."""
+    """The largest batch, each sequence with its own length and k: on the MHA
+    path one fused launch with every k_pad tier, on the GQA path up to 16
+    attention launches spread over the library's side streams."""
     B = 64
     Ls = [1 + (37 * i) % 300 for i in range(B)]
     ks = [1 + (7 * i) % 128 for i in range(B)]
