@@ -21,6 +21,12 @@ SOURCES = ["swan_api.hip", "decode.hip", "decode_gqa.hip", "decode_asym.hip",
            "decode_gqa_asym.hip", "decode_fused.hip", "compress.hip", "prefill.hip",
            "change_k.hip", "rope.hip", "calibrate.hip"]
 ARCH = "gfx950"
+# per-source flags: the GQA kernels keep their MFMA accumulators in VGPRs (the
+# default puts them in AGPRs and copies them across for the per-page VALU work)
+SOURCE_FLAGS = {
+    "decode_gqa.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "decode_gqa_asym.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+}
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "-shared", f"--offload-arch={ARCH}",
     # no packed-FP32 instructions in generated code
@@ -56,7 +62,8 @@ def build(verbose: bool = False, extra=()) -> str:
     jobs = []
     for src in SOURCES:
         obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
-        jobs.append(([hipcc(), *flags, *extra, f"-I{INCLUDE}", f"-I{CSRC}", "-c",
+        jobs.append(([hipcc(), *flags, *SOURCE_FLAGS.get(src, []), *extra, f"-I{INCLUDE}",
+                      f"-I{CSRC}", "-c",
                       os.path.join(CSRC, src), "-o", obj], obj))
     workers = max(1, min(len(jobs), os.cpu_count() or 1, 8))
     with ThreadPoolExecutor(max_workers=workers) as pool:

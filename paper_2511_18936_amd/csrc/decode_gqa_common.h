@@ -60,6 +60,14 @@ __device__ __forceinline__ void gather_scores(const PageRegs<T, KP8>& kr, const 
   }
 }
 
+// zero N 16-byte chunks, 64 per wave store (the last one partial)
+template <int N>
+__device__ __forceinline__ void zero_chunks(u32x4* z, int lane) {
+#pragma unroll
+  for (int i = 0; i < N / 64; ++i) z[64 * i + lane] = u32x4{0u, 0u, 0u, 0u};
+  if (N % 64 != 0 && lane < N % 64) z[64 * (N / 64) + lane] = u32x4{0u, 0u, 0u, 0u};
+}
+
 // value wave, one page: zero the value tile, scatter the kept components.
 // E4M3 values go into a byte tile V8[dims][tokens] of their codes (code 0 is +0),
 // half the bytes to zero and to read back; the MFMA operand read decodes them.
@@ -70,9 +78,7 @@ __device__ __forceinline__ void gqa_scatter(const PageRegs<T, KP8>& vr, bool val
   if constexpr (std::is_same<T, E4M3V>::value) {
     constexpr int kRows = sizeof(sh.vt) / (kVtStride * 2);  // 128, or 129 with the spare row
     constexpr int kChunks = (kRows * kVt8Stride + 15) / 16;
-    u32x4* z = (u32x4*)sh.vt;
-#pragma unroll
-    for (int c = lane; c < kChunks; c += 64) z[c] = u32x4{0u, 0u, 0u, 0u};
+    zero_chunks<kChunks>((u32x4*)sh.vt, lane);
     wave_lds_fence();
     if (valid) {
       uint8_t* vt8 = (uint8_t*)sh.vt + lane;
@@ -86,12 +92,7 @@ __device__ __forceinline__ void gqa_scatter(const PageRegs<T, KP8>& vr, bool val
     }
     return;
   }
-  {
-    u32x4* z = (u32x4*)sh.vt;
-    constexpr int kChunks = kD * kVtStride * 2 / 16;
-#pragma unroll
-    for (int c = lane; c < kChunks; c += 64) z[c] = u32x4{0u, 0u, 0u, 0u};
-  }
+  zero_chunks<kD * kVtStride * 2 / 16>((u32x4*)sh.vt, lane);
   wave_lds_fence();
   if (valid) {
     uint16_t* vt16 = (uint16_t*)sh.vt + lane;
