@@ -53,19 +53,32 @@ struct UnitPages {
 // compiler can keep one page in flight; past the split's last page that load
 // reads the small resident spare arrays instead (n8 = 0: value 0, index
 // kSpareRow), which stay in cache, and its registers are never used.
+// pipeline depth by the register footprint of a page (16-byte chunks per lane):
+// two register sets (one page in flight while one is consumed) up to 12
+template <typename T, int KP8>
+constexpr bool two_page_sets() {
+  return KP8 * PageRegs<T, KP8>::VCH <= 12;
+}
+
+// sparse_split's first key and value page, loaded before the caller fills its
+// LDS (q replicas, zeroed accumulators) so that the load latency overlaps that
+template <typename T, int KP8>
+struct FirstPage {
+  PageRegs<T, KP8> k, v;
+};
+
 template <typename T, int KP8>
 __device__ void sparse_split(const UnitPages& u, int pbeg, int pend, int S, float* qrep,
-                             float* acc, int lane, float* __restrict__ part) {
+                             float* acc, int lane, float* __restrict__ part,
+                             FirstPage<T, KP8>& first) {
   const float* qrep_l = qrep + (lane & (kQRep - 1));
   float* acc_l = acc + (lane & (kAccCols - 1));
   SoftmaxState st{0.f, 0.f, true};
-  // pipeline depth by the register footprint of a page (16-byte chunks per lane)
-  constexpr int kChunks = KP8 * PageRegs<T, KP8>::VCH;
-  if constexpr (kChunks <= 12) {  // two register sets: one page in flight
-    PageRegs<T, KP8> ka, va, kb, vb;
+  if constexpr (two_page_sets<T, KP8>()) {
+    PageRegs<T, KP8>& ka = first.k;
+    PageRegs<T, KP8>& va = first.v;
+    PageRegs<T, KP8> kb, vb;
     const int plast = pend - 1;
-    load_page<T, KP8>(ka, u.kbase + pbeg * u.kbytes, lane, u.nk8);
-    load_page<T, KP8>(va, u.vbase + pbeg * u.vbytes, lane, u.nv8);
     for (int p = pbeg; p < pend; p += 2) {
       const bool in1 = p + 1 <= plast;  // uniform
       const int p1 = in1 ? p + 1 : plast;
@@ -79,11 +92,14 @@ __device__ void sparse_split(const UnitPages& u, int pbeg, int pend, int S, floa
       if (p + 1 < pend)
         process_page<T, KP8>(kb, vb, (p + 1) * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
     }
-  } else {  // large pages: one page at a time
-    PageRegs<T, KP8> ka, va;
+  } else {  // large pages: one page at a time (the first one already loaded)
+    PageRegs<T, KP8>& ka = first.k;
+    PageRegs<T, KP8>& va = first.v;
     for (int p = pbeg; p < pend; ++p) {
-      load_page<T, KP8>(ka, u.kbase + p * u.kbytes, lane, u.nk8);
-      load_page<T, KP8>(va, u.vbase + p * u.vbytes, lane, u.nv8);
+      if (p > pbeg) {
+        load_page<T, KP8>(ka, u.kbase + p * u.kbytes, lane, u.nk8);
+        load_page<T, KP8>(va, u.vbase + p * u.vbytes, lane, u.nv8);
+      }
       process_page<T, KP8>(ka, va, p * kPage + lane < S, qrep_l, acc_l, acc, lane, st);
     }
   }
@@ -139,6 +155,9 @@ __device__ __forceinline__ void sparse_wave(const DecodeLaunch& a, int b, int hq
   u.kbase = (const char*)a.k_pages + a.tab.page_off[0][b] + (int64_t)h * a.n_pages_cap * u.kbytes;
   u.vbase = (const char*)a.v_pages + a.tab.page_off[1][b] + (int64_t)h * a.n_pages_cap * u.vbytes;
   float* part = a.part + ((int64_t)bhq * (a.n_splits + 1) + split) * kPartFloats;
+  FirstPage<T, KP8> first;
+  load_page<T, KP8>(first.k, u.kbase + pbeg * u.kbytes, lane, u.nk8);
+  load_page<T, KP8>(first.v, u.vbase + pbeg * u.vbytes, lane, u.nv8);
 
   // replicate q_hat: q_rep[dim][8]; lane writes dims lane and lane + 64
   const float* qh = a.qhat + (int64_t)bhq * kD;
@@ -156,7 +175,7 @@ __device__ __forceinline__ void sparse_wave(const DecodeLaunch& a, int b, int hq
   for (int c = 0; c < kAccCols / 2; ++c)
     ((float4*)acc)[c * 64 + lane] = make_float4(0.f, 0.f, 0.f, 0.f);
   wave_lds_fence();
-  sparse_split<T, KP8>(u, pbeg, pend, S, qrep, acc, lane, part);
+  sparse_split<T, KP8>(u, pbeg, pend, S, qrep, acc, lane, part, first);
 }
 
 // One launch per distinct k_pad of the batch (KP8 = k_pad / 8), over the
