@@ -309,7 +309,7 @@ swan_status swan_change_k(const swan_cache* src, const int32_t* k_active_src,
  *                     page;
  *  short_split_pages  a short sequence (whose shrinking splits would be at most
  *                     half as many as its share asks for) is cut into equal
- *                     splits of this many pages (default 4); -1: shrinking
+ *                     splits of this many pages (default 3); -1: shrinking
  *                     splits for every sequence;
  *  merge_pct          for a batch mixing k_pad on the other paths (several
  *                     query heads per wave, or fp32 storage): from the largest

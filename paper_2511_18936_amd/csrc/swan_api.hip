@@ -35,7 +35,7 @@ thread_local hipEvent_t g_prof_stop = nullptr;
 // thirds of the k_pad, three side streams.
 struct Tuning {
   int64_t target_waves = 256 * 4 * 2;
-  int short_split_pages = 4;  // 0: never
+  int short_split_pages = 3;  // 0: never
   int merge_pct = 66;         // 0: never
   int side_streams = swan::kSideStreams;
 };
