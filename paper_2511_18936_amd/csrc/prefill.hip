@@ -30,9 +30,9 @@
 //   rotation   per pair of 16-token tiles (their x rows loaded one pair
 //              ahead): x digits in registers (A operands); 16 steps (16
 //              output dims x 64 input dims) of 34 MFMAs on P digits read
-//              from LDS one step ahead (B operands), each MFMA followed by
-//              VALU work of the previous tile's conversion into the LDS row
-//              of its token
+//              from LDS one step ahead (B operands), issued in four parts,
+//              each interleaved with the VALU work of one element of the
+//              previous tile's conversion into the LDS row of its token
 //   selection  one token per lane on its 128 stored values: a radix select
 //              on bit planes of the magnitudes finds the kept dims (a 128-bit
 //              mask; ties at the k-th largest to the lower dim)
