@@ -246,6 +246,30 @@ swan_status swan_decode_attention_noalloc(const swan_cache* c, const int32_t* se
                                           void* out, void* stream);
 
 /*
+ * One decode step of Algorithm 1 (its compress part for one new token per
+ * sequence, then its attention part): the same as swan_compress_append with
+ * n_new = 1 (n_new_host NULL) followed by swan_decode_attention with lengths
+ * seq_len_host[b] + 1, on `stream`, with the same results bit for bit, in one
+ * launch fewer: for n_q_heads / n_kv_heads <= 4 the query rotation runs inside
+ * the append launch, where the wave that rotates a kv head's new key reads the
+ * same rows of P_qk (one launch less on a latency-bound step).
+ *  seq_len_host[batch]  tokens cached per sequence BEFORE the step (>= 0);
+ *  k_new, v_new         [batch][n_kv_heads][1][head_dim] storage type (un-rotated);
+ *  q, out               [batch][n_q_heads][head_dim] storage type;
+ *  workspace            at least swan_decode_workspace_bytes for the lengths after
+ *                       the step (seq_len_host[b] + 1), 256-byte aligned;
+ *  k_active_host, k_value_host, P_qk, P_vo, scale  as in the two calls.
+ * Every argument of both parts is checked before anything is enqueued, so an
+ * error leaves the cache as it was.  The caller then adds 1 to each seq_len.
+ * Errors: those of swan_compress_append and swan_decode_attention.
+ */
+swan_status swan_decode_step(const swan_cache* c, const int32_t* seq_len_host,
+                             const int32_t* k_active_host, const int32_t* k_value_host,
+                             const void* k_new, const void* v_new, const void* q,
+                             const float* P_qk, const float* P_vo, float scale, void* out,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Rotary position embedding, for the query and key rows of a layer before the
  * cache rotates them (the paper rotates post-RoPE queries and keys, Sec. 4.2).
  *  x, y          [batch][n_heads][n][head_dim] rows of the storage type of
@@ -330,11 +354,14 @@ typedef struct swan_decode_tuning {
 swan_status swan_set_decode_tuning(const swan_decode_tuning* tuning);
 
 /*
- * Profiling hook.  While both are non-NULL, swan_decode_attention on this
- * thread records start_event (a hipEvent_t) on its stream right before its
- * sparse/buffer attention launches and stop_event right after them, so that
- * hipEventElapsedTime gives the duration of those kernels alone.  NULL, NULL
- * (the default) disables it.  The events stay owned by the caller.
+ * Profiling hook.  While both are non-NULL, swan_decode_attention,
+ * swan_decode_attention_noalloc and swan_decode_step on this thread record
+ * start_event (a hipEvent_t) on their stream right before their sparse/buffer
+ * attention launches and stop_event right after them, so that
+ * hipEventElapsedTime gives the duration of those kernels alone.  Events made
+ * with hipEventReleaseToDevice cost the stream the least (no system-scope
+ * release at each record).  NULL, NULL (the default) disables it.  The events
+ * stay owned by the caller.
  */
 swan_status swan_set_profile_events(void* start_event, void* stop_event);
 

@@ -12,7 +12,12 @@
 //                  that step's eviction, else 8): rotation
 //                  x . P accumulated in float64 and rounded once to the storage
 //                  type; tokens still inside the buffer go to their ring slot,
-//                  the others are pruned and packed at once
+//                  the others are pruned and packed at once.  In a
+//                  decode step (swan_decode_step) the key wave of (sequence,
+//                  kv head) also rotates the step's queries of that head's
+//                  QG query heads with the same rows of P_QK: q_hat for the
+//                  attention that follows, with the summation order of the
+//                  separate query rotation (qrot_kernel), so the same bits
 //
 // Top-k (Sec. 4.3, ranking the stored values, ties to the lower index): each
 // lane holds dims 2l and 2l+1; the key (|x| bits << 8) | (255 - dim) is unique
@@ -130,11 +135,17 @@ __global__ __launch_bounds__(64) void evict_kernel(CompressLaunch a) {
   select_and_pack<F>(x0, x1, k, page, p % kPage, lane);
 }
 
-template <typename F, int TPW>
+// QG > 0 (decode steps): the key wave also rotates QG query rows, q_hat = q .
+// P_QK[h] * qmult in float32.  Each output sums 4 quarters of 32 rows, each
+// quarter in two accumulators (even and odd rows) that are added, and the
+// quarters meet as (q0 + q1) + (q2 + q3): the order of qrot_kernel.
+template <typename F, int TPW, int QG>
 __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
   using T = typename Fmt<F>::Elem;
   using St = Store<T>;
+  static_assert(QG == 0 || TPW == 1, "query rotation: decode steps only");
   __shared__ __attribute__((aligned(16))) double xs[kD][TPW];
+  __shared__ float qs[QG > 0 ? QG : 1][kD];
   const int lane = threadIdx.x;
   const int ngroups = (a.n_new + TPW - 1) / TPW;
   int w = blockIdx.x;
@@ -159,6 +170,15 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
     xs[2 * lane][t] = v0;
     xs[2 * lane + 1][t] = v1;
   }
+  const bool with_q = QG > 0 && role == 0;  // uniform
+  const int64_t q0 = ((int64_t)b * a.Hq + (int64_t)h * QG) * kD;  // first query row
+  if (with_q) {
+#pragma unroll
+    for (int g = 0; g < QG; ++g) {
+      qs[g][2 * lane] = (float)((const T*)a.q)[q0 + g * kD + 2 * lane];
+      qs[g][2 * lane + 1] = (float)((const T*)a.q)[q0 + g * kD + 2 * lane + 1];
+    }
+  }
   __syncthreads();
   double acc0[TPW], acc1[TPW];
   const float* Prole = role ? a.P_vo : a.P_qk;
@@ -173,17 +193,52 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
 #pragma unroll
     for (int t = 0; t < TPW; ++t) acc0[t] = acc1[t] = 0.0;
     // 32 rows of P in flight per batch: the loads are the latency of this kernel
-#pragma unroll 32
-    for (int i = 0; i < kD; ++i) {
-      const float2 pr = P[i * (kD / 2)];
-      const double p0 = (double)pr.x, p1 = (double)pr.y;
+    auto rows = [&](auto wq) {
+      constexpr bool kQ = decltype(wq)::value && QG > 0;
+      constexpr int NQ = kQ ? QG : 1;
+      float qa[NQ][2][8];  // [query head][output dim 2 lane + o][2 quarter + row parity]
 #pragma unroll
-      for (int t = 0; t < TPW; ++t) {
-        const double xv = xs[i][t];
-        acc0[t] = fma(xv, p0, acc0[t]);
-        acc1[t] = fma(xv, p1, acc1[t]);
+      for (int g = 0; g < NQ; ++g)
+#pragma unroll
+        for (int c = 0; c < 8; ++c) qa[g][0][c] = qa[g][1][c] = 0.f;
+#pragma unroll
+      for (int qt = 0; qt < 4; ++qt) {
+#pragma unroll 32
+        for (int u = 0; u < 32; ++u) {
+          const int i = 32 * qt + u;
+          const float2 pr = P[i * (kD / 2)];
+          const double p0 = (double)pr.x, p1 = (double)pr.y;
+#pragma unroll
+          for (int t = 0; t < TPW; ++t) {
+            const double xv = xs[i][t];
+            acc0[t] = fma(xv, p0, acc0[t]);
+            acc1[t] = fma(xv, p1, acc1[t]);
+          }
+          if constexpr (kQ) {
+#pragma unroll
+            for (int g = 0; g < QG; ++g) {
+              const float qv = qs[g][i];
+              qa[g][0][2 * qt + (u & 1)] = fmaf(qv, pr.x, qa[g][0][2 * qt + (u & 1)]);
+              qa[g][1][2 * qt + (u & 1)] = fmaf(qv, pr.y, qa[g][1][2 * qt + (u & 1)]);
+            }
+          }
+        }
       }
-    }
+      if constexpr (kQ) {
+#pragma unroll
+        for (int g = 0; g < QG; ++g)
+#pragma unroll
+          for (int o = 0; o < 2; ++o) {
+            const float s0 = qa[g][o][0] + qa[g][o][1], s1 = qa[g][o][2] + qa[g][o][3];
+            const float s2 = qa[g][o][4] + qa[g][o][5], s3 = qa[g][o][6] + qa[g][o][7];
+            a.qhat[q0 + g * kD + 2 * lane + o] = ((s0 + s1) + (s2 + s3)) * a.qmult;
+          }
+      }
+    };
+    if (with_q)
+      rows(std::true_type{});
+    else
+      rows(std::false_type{});
   }
   const int len_old = a.tab.len[b];
   const int len_new = len_old + nnew;
@@ -225,7 +280,25 @@ template <typename F>
 static hipError_t launch_compress_t(const CompressLaunch& a) {
   const int units = a.B * a.Hkv * 2;
   if (a.n_new == 1) {  // a decode step: eviction and insertion in one launch
-    hipLaunchKernelGGL((insert_kernel<F, 1>), dim3(units), dim3(64), 0, a.stream, a);
+    switch (a.q ? a.Hq / a.Hkv : 0) {
+      case 0:
+        hipLaunchKernelGGL((insert_kernel<F, 1, 0>), dim3(units), dim3(64), 0, a.stream, a);
+        break;
+      case 1:
+        hipLaunchKernelGGL((insert_kernel<F, 1, 1>), dim3(units), dim3(64), 0, a.stream, a);
+        break;
+      case 2:
+        hipLaunchKernelGGL((insert_kernel<F, 1, 2>), dim3(units), dim3(64), 0, a.stream, a);
+        break;
+      case 3:
+        hipLaunchKernelGGL((insert_kernel<F, 1, 3>), dim3(units), dim3(64), 0, a.stream, a);
+        break;
+      case 4:
+        hipLaunchKernelGGL((insert_kernel<F, 1, 4>), dim3(units), dim3(64), 0, a.stream, a);
+        break;
+      default:
+        return hipErrorInvalidValue;  // the caller rotates more query heads per kv head itself
+    }
     return hipGetLastError();
   }
   if (a.max_evict > 0) {
@@ -236,7 +309,7 @@ static hipError_t launch_compress_t(const CompressLaunch& a) {
   if (a.n_new >= kPrefillMinTokens && sizeof(typename Fmt<F>::Elem) == 2) return launch_prefill(a);
   if (a.n_new > 0) {
     const int ngroups = (a.n_new + kTPW - 1) / kTPW;
-    hipLaunchKernelGGL((insert_kernel<F, kTPW>), dim3((int64_t)units * ngroups), dim3(64), 0,
+    hipLaunchKernelGGL((insert_kernel<F, kTPW, 0>), dim3((int64_t)units * ngroups), dim3(64), 0,
                        a.stream, a);
     return hipGetLastError();
   }

@@ -175,14 +175,13 @@ template <typename T>
 static hipError_t launch_decode_t(const DecodeLaunch& a) {
   const int BH = a.B * a.Hq;
   using E = typename Fmt<T>::Elem;
-  hipLaunchKernelGGL(qrot_kernel<E>, dim3(BH), dim3(kD * kRotQuarters), 0, a.stream,
-                     (const E*)a.q, a.P_qk, a.qhat, a.Hq, a.Hq / a.Hkv, a.qmult);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  if (a.prof_start) {
-    e = hipEventRecord(a.prof_start, a.stream);
-    if (e != hipSuccess) return e;
+  hipError_t e;
+  if (!a.qhat_ready) {
+    hipLaunchKernelGGL(qrot_kernel<E>, dim3(BH), dim3(kD * kRotQuarters), 0, a.stream,
+                       (const E*)a.q, a.P_qk, a.qhat, a.Hq, a.Hq / a.Hkv, a.qmult);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
   }
+  if (a.prof_start && (e = hipEventRecord(a.prof_start, a.stream)) != hipSuccess) return e;
   // sequences grouped by (k_pad of the keys, k_pad of the values); then, from
   // the largest k_pad down, a group joins the launch before it when its k_pad
   // is at least kMergePct % of that launch's (two thirds: the spare groups then
@@ -300,10 +299,7 @@ static hipError_t launch_decode_t(const DecodeLaunch& a) {
       if ((e = hipStreamWaitEvent(a.stream, ss->join[j], 0)) != hipSuccess) return e;
     }
   }
-  if (a.prof_stop) {
-    e = hipEventRecord(a.prof_stop, a.stream);
-    if (e != hipSuccess) return e;
-  }
+  if (a.prof_stop && (e = hipEventRecord(a.prof_stop, a.stream)) != hipSuccess) return e;
   hipLaunchKernelGGL(merge_kernel<E>, dim3(BH), dim3(128), 0, a.stream, a);
   return hipGetLastError();
 }

@@ -258,14 +258,80 @@ swan_status scratch_for_stream(hipStream_t stream, void** ptr) {
   return SWAN_OK;
 }
 
-// Both decode entry points: validation, split plan, launches.  no_alloc: the
-// workspace is this library's scratch array (looked up after every host check
-// has passed), a plan that needs more than the array is rejected, and the
-// launches stay on `stream` (creating the side streams could allocate).
-swan_status decode_impl(const swan_cache* c, const int32_t* seq_len_host,
+// swan_compress_append's validation, into `a` (nothing is enqueued); any_new:
+// some sequence appends a token
+swan_status compress_prep(const swan_cache* c, const int32_t* seq_len_host,
+                          const int32_t* k_active_host, const int32_t* k_value_host,
+                          const void* k_new, const void* v_new, int32_t n_new,
+                          const int32_t* n_new_host, const float* P_qk, const float* P_vo,
+                          void* stream, swan::CompressLaunch& a, bool& any_new) {
+  swan_status st = check_cache_shape(c);
+  if (st != SWAN_OK) return st;
+  if ((st = check_k(c, k_active_host, k_value_host)) != SWAN_OK) return st;
+  if ((st = check_cache_ptrs(c)) != SWAN_OK) return st;
+  if (!seq_len_host) return fail(SWAN_ERR_INVALID_ARG, "seq_len_host is NULL");
+  if (n_new < 0) return fail(SWAN_ERR_INVALID_ARG, "n_new %d < 0", n_new);
+  if (n_new > 0 && (!k_new || !v_new)) return fail(SWAN_ERR_INVALID_ARG, "k_new / v_new is NULL");
+  if (!P_qk) return fail(SWAN_ERR_INVALID_ARG, "P_qk is NULL");
+  if ((((uintptr_t)P_qk | (uintptr_t)P_vo) & 15) != 0)
+    return fail(SWAN_ERR_INVALID_ARG, "P_qk / P_vo must be 16-byte aligned");
+  if ((((uintptr_t)k_new | (uintptr_t)v_new) & 15) != 0)
+    return fail(SWAN_ERR_INVALID_ARG, "k_new / v_new must be 16-byte aligned");
+  int max_evict = 0;
+  any_new = false;
+  for (int b = 0; b < c->batch; ++b) {
+    const int64_t L0 = seq_len_host[b];
+    if (L0 < 0) return fail(SWAN_ERR_INVALID_ARG, "seq_len[%d] = %lld < 0", b, (long long)L0);
+    const int nb_new = n_new_host ? n_new_host[b] : n_new;
+    if (nb_new < 0 || nb_new > n_new)
+      return fail(SWAN_ERR_INVALID_ARG, "n_new_host[%d] = %d outside 0..%d", b, nb_new, n_new);
+    any_new |= nb_new != 0;
+    const int64_t L1 = L0 + nb_new;
+    if (L1 > INT32_MAX / 2)
+      return fail(SWAN_ERR_INVALID_ARG, "seq_len[%d] + n_new too large", b);
+    if (L1 - c->buffer_tokens > c->sparse_capacity)
+      return fail(SWAN_ERR_CAPACITY, "sequence %d needs %lld sparse tokens, capacity %d", b,
+                  (long long)(L1 - c->buffer_tokens), c->sparse_capacity);
+    const int64_t p0 = L0 > c->buffer_tokens ? L0 - c->buffer_tokens : 0;
+    const int64_t p1 = L0 < L1 - c->buffer_tokens ? L0 : L1 - c->buffer_tokens;
+    if (p1 - p0 > max_evict) max_evict = (int)(p1 - p0);
+  }
+  int64_t role_bytes[2];
+  fill_layout(c, k_active_host, k_value_host, a.tab, role_bytes);
+  for (int b = 0; b < c->batch; ++b) {
+    a.tab.len[b] = seq_len_host[b];
+    a.tab.nnew[b] = n_new_host ? n_new_host[b] : n_new;
+  }
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.P_qk = P_qk;
+  a.P_vo = P_vo;
+  a.k_pages = c->k_pages;
+  a.v_pages = c->v_pages;
+  a.k_ring = c->k_ring;
+  a.v_ring = c->v_ring;
+  a.B = c->batch;
+  a.Hkv = c->n_kv_heads;
+  a.bb = c->buffer_tokens;
+  a.n_pages_cap = swan::pages_for(c->sparse_capacity);
+  a.n_new = n_new;
+  a.max_evict = max_evict;
+  a.prefill_groups = swan::prefill_groups(n_new, 0);
+  a.dtype = c->dtype;
+  a.stream = (hipStream_t)stream;
+  return SWAN_OK;
+}
+
+// The decode entry points' validation and split plan, into `a` (nothing is
+// enqueued).  no_alloc: the workspace is this library's scratch array (looked
+// up after every host check has passed), a plan that needs more than the
+// array is rejected, and the launches stay on `stream` (creating the side
+// streams could allocate).
+swan_status decode_prep(const swan_cache* c, const int32_t* seq_len_host,
                         const int32_t* k_active_host, const int32_t* k_value_host, const void* q,
                         const float* P_qk, const float* P_vo, float scale, void* out,
-                        void* workspace, size_t workspace_bytes, void* stream, bool no_alloc) {
+                        void* workspace, size_t workspace_bytes, void* stream, bool no_alloc,
+                        swan::DecodeLaunch& a) {
   swan_status st = check_cache_shape(c);
   if (st != SWAN_OK) return st;
   if ((st = check_k(c, k_active_host, k_value_host)) != SWAN_OK) return st;
@@ -282,7 +348,6 @@ swan_status decode_impl(const swan_cache* c, const int32_t* seq_len_host,
                   (long long)(L - c->buffer_tokens), c->sparse_capacity);
   }
   if (!(scale == scale) || isinf(scale)) return fail(SWAN_ERR_INVALID_ARG, "scale is not finite");
-  swan::DecodeLaunch a;
   int64_t role_bytes[2];
   fill_layout(c, k_active_host, k_value_host, a.tab, role_bytes);
   const int ns = plan_splits(c, seq_len_host, k_active_host, k_value_host, a.tab.nsplit,
@@ -327,6 +392,19 @@ swan_status decode_impl(const swan_cache* c, const int32_t* seq_len_host,
   a.prof_stop = g_prof_stop;
   a.merge_pct = g_tuning.merge_pct;
   a.side_streams = no_alloc ? 0 : g_tuning.side_streams;
+  return SWAN_OK;
+}
+
+// Both decode entry points: validation, split plan, launches.
+swan_status decode_impl(const swan_cache* c, const int32_t* seq_len_host,
+                        const int32_t* k_active_host, const int32_t* k_value_host, const void* q,
+                        const float* P_qk, const float* P_vo, float scale, void* out,
+                        void* workspace, size_t workspace_bytes, void* stream, bool no_alloc) {
+  swan::DecodeLaunch a;
+  const swan_status st = decode_prep(c, seq_len_host, k_active_host, k_value_host, q, P_qk,
+                                     P_vo, scale, out, workspace, workspace_bytes, stream,
+                                     no_alloc, a);
+  if (st != SWAN_OK) return st;
   return hip_status(swan::launch_decode(a), "decode launch");
 }
 
@@ -336,7 +414,7 @@ extern "C" {
 
 const char* swan_last_error(void) { return g_last_error.c_str(); }
 
-int32_t swan_version(void) { return 204; }
+int32_t swan_version(void) { return 205; }
 
 swan_status swan_page_bytes(int32_t dtype, int32_t k_active, size_t* bytes) {
   if (!bytes) return fail(SWAN_ERR_INVALID_ARG, "bytes is NULL");
@@ -413,60 +491,11 @@ swan_status swan_compress_append(const swan_cache* c, const int32_t* seq_len_hos
                                  const void* k_new, const void* v_new, int32_t n_new,
                                  const int32_t* n_new_host, const float* P_qk, const float* P_vo,
                                  void* stream) {
-  swan_status st = check_cache_shape(c);
-  if (st != SWAN_OK) return st;
-  if ((st = check_k(c, k_active_host, k_value_host)) != SWAN_OK) return st;
-  if ((st = check_cache_ptrs(c)) != SWAN_OK) return st;
-  if (!seq_len_host) return fail(SWAN_ERR_INVALID_ARG, "seq_len_host is NULL");
-  if (n_new < 0) return fail(SWAN_ERR_INVALID_ARG, "n_new %d < 0", n_new);
-  if (n_new > 0 && (!k_new || !v_new)) return fail(SWAN_ERR_INVALID_ARG, "k_new / v_new is NULL");
-  if (!P_qk) return fail(SWAN_ERR_INVALID_ARG, "P_qk is NULL");
-  if ((((uintptr_t)P_qk | (uintptr_t)P_vo) & 15) != 0)
-    return fail(SWAN_ERR_INVALID_ARG, "P_qk / P_vo must be 16-byte aligned");
-  if ((((uintptr_t)k_new | (uintptr_t)v_new) & 15) != 0)
-    return fail(SWAN_ERR_INVALID_ARG, "k_new / v_new must be 16-byte aligned");
-  int max_evict = 0, any_new = 0;
-  for (int b = 0; b < c->batch; ++b) {
-    const int64_t L0 = seq_len_host[b];
-    if (L0 < 0) return fail(SWAN_ERR_INVALID_ARG, "seq_len[%d] = %lld < 0", b, (long long)L0);
-    const int nb_new = n_new_host ? n_new_host[b] : n_new;
-    if (nb_new < 0 || nb_new > n_new)
-      return fail(SWAN_ERR_INVALID_ARG, "n_new_host[%d] = %d outside 0..%d", b, nb_new, n_new);
-    any_new |= nb_new;
-    const int64_t L1 = L0 + nb_new;
-    if (L1 > INT32_MAX / 2)
-      return fail(SWAN_ERR_INVALID_ARG, "seq_len[%d] + n_new too large", b);
-    if (L1 - c->buffer_tokens > c->sparse_capacity)
-      return fail(SWAN_ERR_CAPACITY, "sequence %d needs %lld sparse tokens, capacity %d", b,
-                  (long long)(L1 - c->buffer_tokens), c->sparse_capacity);
-    const int64_t p0 = L0 > c->buffer_tokens ? L0 - c->buffer_tokens : 0;
-    const int64_t p1 = L0 < L1 - c->buffer_tokens ? L0 : L1 - c->buffer_tokens;
-    if (p1 - p0 > max_evict) max_evict = (int)(p1 - p0);
-  }
   swan::CompressLaunch a;
-  int64_t role_bytes[2];
-  fill_layout(c, k_active_host, k_value_host, a.tab, role_bytes);
-  for (int b = 0; b < c->batch; ++b) {
-    a.tab.len[b] = seq_len_host[b];
-    a.tab.nnew[b] = n_new_host ? n_new_host[b] : n_new;
-  }
-  a.k_new = k_new;
-  a.v_new = v_new;
-  a.P_qk = P_qk;
-  a.P_vo = P_vo;
-  a.k_pages = c->k_pages;
-  a.v_pages = c->v_pages;
-  a.k_ring = c->k_ring;
-  a.v_ring = c->v_ring;
-  a.B = c->batch;
-  a.Hkv = c->n_kv_heads;
-  a.bb = c->buffer_tokens;
-  a.n_pages_cap = swan::pages_for(c->sparse_capacity);
-  a.n_new = n_new;
-  a.max_evict = max_evict;
-  a.prefill_groups = swan::prefill_groups(n_new, 0);
-  a.dtype = c->dtype;
-  a.stream = (hipStream_t)stream;
+  bool any_new = false;
+  const swan_status st = compress_prep(c, seq_len_host, k_active_host, k_value_host, k_new, v_new,
+                                       n_new, n_new_host, P_qk, P_vo, stream, a, any_new);
+  if (st != SWAN_OK) return st;
   if (!any_new) return ok();
   return hip_status(swan::launch_compress(a), "compress launch");
 }
@@ -498,6 +527,35 @@ swan_status swan_decode_attention_noalloc(const swan_cache* c, const int32_t* se
                                           void* out, void* stream) {
   return decode_impl(c, seq_len_host, k_active_host, k_value_host, q, P_qk, P_vo, scale, out,
                      nullptr, 0, stream, true);
+}
+
+swan_status swan_decode_step(const swan_cache* c, const int32_t* seq_len_host,
+                             const int32_t* k_active_host, const int32_t* k_value_host,
+                             const void* k_new, const void* v_new, const void* q,
+                             const float* P_qk, const float* P_vo, float scale, void* out,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  // every check of both halves before anything is enqueued
+  swan::CompressLaunch ca;
+  bool any_new = false;
+  swan_status st = compress_prep(c, seq_len_host, k_active_host, k_value_host, k_new, v_new, 1,
+                                 nullptr, P_qk, P_vo, stream, ca, any_new);
+  if (st != SWAN_OK) return st;
+  int32_t len1[SWAN_MAX_BATCH];
+  for (int b = 0; b < c->batch; ++b) len1[b] = seq_len_host[b] + 1;
+  swan::DecodeLaunch da;
+  st = decode_prep(c, len1, k_active_host, k_value_host, q, P_qk, P_vo, scale, out, workspace,
+                   workspace_bytes, stream, false, da);
+  if (st != SWAN_OK) return st;
+  if (c->n_q_heads / c->n_kv_heads <= swan::kStepQG) {  // the key waves rotate the queries
+    ca.q = q;
+    ca.qhat = da.qhat;
+    ca.Hq = da.Hq;
+    ca.qmult = da.qmult;
+    da.qhat_ready = 1;
+  }
+  const hipError_t e = swan::launch_compress(ca);
+  if (e != hipSuccess) return hip_status(e, "compress launch");
+  return hip_status(swan::launch_decode(da), "decode launch");
 }
 
 swan_status swan_change_k(const swan_cache* src, const int32_t* k_active_src,

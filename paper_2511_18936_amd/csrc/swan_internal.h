@@ -70,6 +70,7 @@ struct DecodeLaunch {
   hipEvent_t prof_stop;
   int merge_pct;          // launch grouping of a mixed-k batch (<= 0: none)
   int side_streams;       // library streams for those launches, 0..kSideStreams
+  int qhat_ready = 0;     // 1: qhat already holds the rotated queries (decode steps)
 };
 hipError_t launch_decode(const DecodeLaunch& a);
 constexpr int kSideStreams = 3;  // extra streams for the launches of a mixed-k batch
@@ -121,7 +122,15 @@ struct CompressLaunch {
   int dtype;
   SeqTab tab;     // len = tokens cached before the call
   hipStream_t stream;
+  // decode steps (n_new == 1) only: q != nullptr makes the key waves also
+  // write q_hat = q . P_qk * qmult for the Hq / Hkv (at most kStepQG) query
+  // heads of their kv head, q [B][Hq][128] storage type, qhat [B][Hq][128]
+  const void* q = nullptr;
+  float* qhat = nullptr;
+  int Hq = 0;
+  float qmult = 0.f;
 };
+constexpr int kStepQG = 4;
 hipError_t launch_compress(const CompressLaunch& a);
 // prefill path (fp16, many tokens): float64 MFMA rotation + lane-per-token top-k
 constexpr int kPrefillMinTokens = 64;

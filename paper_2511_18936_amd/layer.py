@@ -9,9 +9,10 @@ leaves it rotated, straight into W_O_hat (Lemma 2).
 One call with n new tokens per sequence, on the current stream:
   [q | k | v_hat] = x . [W_Q | W_K | W_V_hat]    one dense GEMM (torch: the GEMM library)
   swan_rope on q and k at each sequence's next positions
-  swan_compress_append(k, v_hat, P_QK, P_VO = NULL)
-  for a decode step (n = 1): swan_decode_attention(q, P_QK, P_VO = NULL) -> o_hat,
-  and y = o_hat . W_O_hat                         dense GEMM
+  a prompt (n > 1): swan_compress_append(k, v_hat, P_QK, P_VO = NULL)
+  a decode step (n = 1): swan_decode_step(k, v_hat, q, P_QK, P_VO = NULL) -> o_hat
+  (the append, then the attention, in one call), and
+  y = o_hat . W_O_hat                             dense GEMM
 The SWAN steps run in libswan's kernels; attention over a prompt is the dense,
 standard kind and is not part of this layer (a prompt call only fills the cache).
 Weights are [in][out] row-major, x . W.
@@ -108,9 +109,9 @@ class SwanAttentionLayer:
         """x [B][n][hidden]: append the n rows of every sequence to the cache; for a
         decode step (n = 1) return y [B][hidden], the layer's attention output."""
         q, k, v = self.project(x)
-        self.cache.append(k, v, self.P_qk, None)
         if x.shape[1] != 1:
+            self.cache.append(k, v, self.P_qk, None)
             return None
         B = x.shape[0]
-        o_hat = self.cache.decode(q[:, :, 0].contiguous(), self.P_qk, None)
+        o_hat = self.cache.step(k, v, q[:, :, 0].contiguous(), self.P_qk, None)
         return o_hat.view(B, self.n_heads * HEAD_DIM) @ self.W_o_hat

@@ -33,7 +33,7 @@ EXPORTED = (
     "swan_last_error", "swan_version", "swan_page_bytes", "swan_cache_bytes",
     "swan_calibrate_workspace_bytes", "swan_calibrate_rotation", "swan_compress_append",
     "swan_decode_workspace_bytes", "swan_decode_attention", "swan_decode_attention_noalloc",
-    "swan_change_k", "swan_rope", "swan_set_decode_tuning", "swan_set_profile_events",
+    "swan_decode_step", "swan_change_k", "swan_rope", "swan_set_decode_tuning", "swan_set_profile_events",
 )
 NOALLOC_SCRATCH_BYTES = 16 << 20
 
@@ -97,6 +97,8 @@ def _load() -> ctypes.CDLL:
                                   vp],
         "swan_decode_attention_noalloc": [pdesc, pi32, pi32, pi32, vp, vp, vp, ctypes.c_float,
                                           vp, vp],
+        "swan_decode_step": [pdesc, pi32, pi32, pi32, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp,
+                             sz, vp],
         "swan_change_k": [pdesc, pi32, pi32, pdesc, pi32, pi32, pi32, vp],
         "swan_rope": [vp, vp, i32, i32, i32, i32, i32, pi32, ctypes.c_double, vp],
         "swan_set_decode_tuning": [ctypes.POINTER(DecodeTuning)],
@@ -306,6 +308,26 @@ def decode_attention_noalloc(desc: CacheDesc, seq_len: Sequence[int], k_active: 
                                               _ptr(out), _stream(stream, q.get_device())))
 
 
+def decode_step(desc: CacheDesc, seq_len: Sequence[int], k_active: Sequence[int], k_new, v_new,
+                q, P_qk, P_vo, out, workspace, scale: float = 0.0, stream=None,
+                k_value: Optional[Sequence[int]] = None) -> None:
+    """swan_decode_step: append one token per sequence (seq_len: lengths before it), then
+    decode q over the cache with it; workspace sized for the lengths after the step."""
+    et = _elem_torch_dtype(desc.dtype)
+    shape = (desc.batch, desc.n_kv_heads, 1, desc.head_dim)
+    _tensor(k_new, "k_new", et, shape)
+    _tensor(v_new, "v_new", et, shape)
+    _decode_tensors(desc, q, P_qk, P_vo, out)
+    _on_gpu(k_new=k_new, v_new=v_new)
+    if workspace is None or not workspace.is_cuda or not workspace.is_contiguous():
+        raise SwanError(SWAN_ERR_WORKSPACE, "workspace must be a contiguous GPU tensor")
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(_lib.swan_decode_step(ctypes.byref(desc), _i32_array(seq_len), _i32_array(k_active),
+                                 _opt_i32_array(k_value), _ptr(k_new), _ptr(v_new), _ptr(q),
+                                 _ptr(P_qk), _ptr(P_vo), float(scale), _ptr(out),
+                                 _ptr(workspace), ws_bytes, _stream(stream, q.get_device())))
+
+
 def change_k(src: CacheDesc, k_active_src: Sequence[int], k_value_src: Optional[Sequence[int]],
              dst: CacheDesc, k_active_dst: Sequence[int], k_value_dst: Optional[Sequence[int]],
              seq_len: Sequence[int], stream=None) -> None:
@@ -340,8 +362,9 @@ def set_decode_tuning(target_waves: int = 0, short_split_pages: int = 0, merge_p
 
 
 def set_profile_events(start=None, stop=None) -> None:
-    """Record torch.cuda.Event start/stop around the attention kernels of the next
-    decode calls on this thread (None, None disables)."""
+    """Record start/stop (events with a .cuda_event HIP handle: torch.cuda.Event, or one
+    made for timing only) around the attention kernels of the next decode calls on
+    this thread (None, None disables)."""
     _check(_lib.swan_set_profile_events(None if start is None else start.cuda_event,
                                         None if stop is None else stop.cuda_event))
 
@@ -441,4 +464,20 @@ class SwanCache:
             out = torch.empty_like(q)
         decode_attention(self.desc, self.seq_len, self.k_active, q, P_qk, P_vo, out,
                          self.workspace(), scale, stream, self.k_value)
+        return out
+
+    def step(self, k_new, v_new, q, P_qk, P_vo, out=None, scale: float = 0.0, stream=None):
+        """One decode step (swan_decode_step): append k_new / v_new ([B][H_kv][1][d]),
+        advance the lengths, and return the attention of q ([B][H_q][d]) over the cache."""
+        import torch
+
+        if out is None:
+            out = torch.empty_like(q)
+        after = [L + 1 for L in self.seq_len]
+        need = decode_workspace_bytes(self.desc, after, self.k_active, self.k_value)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(need, dtype=torch.uint8, device=self.device)
+        decode_step(self.desc, self.seq_len, self.k_active, k_new, v_new, q, P_qk, P_vo, out,
+                    self._ws, scale, stream, self.k_value)
+        self.seq_len = after
         return out

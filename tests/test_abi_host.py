@@ -22,7 +22,7 @@ def _declared_functions():
 
 def test_header_and_binding_agree_on_exports():
     declared = _declared_functions()
-    assert len(declared) == 14
+    assert len(declared) == 15
     assert sorted(swan.EXPORTED) == declared
     lib = swan.lib()
     for name in declared:
@@ -32,7 +32,7 @@ def test_header_and_binding_agree_on_exports():
 def test_version_is_the_current_abi():
     """2.04: swan_set_decode_tuning; 2.03: swan_decode_attention_noalloc; 2.02: swan_change_k, swan_rope; 2.00: keys
     and values with their own k."""
-    assert swan.lib().swan_version() == 204
+    assert swan.lib().swan_version() == 205
 
 
 def test_nm_shows_exported_symbols():
@@ -153,6 +153,34 @@ def test_decode_rejects_bad_arguments():
     for bad in ([48, 0], [129, 48]):
         assert lib.swan_decode_attention(ctypes.byref(d), seq, ok_k, swan._i32_array(bad), FAKE,
                                          FAKE, FAKE, 0.0, FAKE, FAKE, 1 << 30, None) == E
+
+
+def test_decode_step_checks_both_parts_on_the_host():
+    """swan_decode_step rejects whatever the append or the decode would, before
+    anything is enqueued; its workspace is sized for the lengths after the step."""
+    lib = swan.lib()
+    d = _desc()
+    ok_k = swan._i32_array([48, 64])
+    need = swan.decode_workspace_bytes(d, [101, 201], [48, 64])
+    E = swan.SWAN_ERR_INVALID_ARG
+
+    def step(seq=(100, 200), k_new=FAKE, q=FAKE, P_qk=FAKE, scale=0.0, ws=FAKE, wsb=need,
+             k_value=None):
+        return lib.swan_decode_step(ctypes.byref(d), swan._i32_array(list(seq)), ok_k, k_value,
+                                    k_new, FAKE, q, P_qk, FAKE, scale, FAKE, ws, wsb, None)
+
+    assert step(k_new=None) == E                    # append part
+    assert step(k_new=FAKE + 8) == E                # misaligned new rows
+    assert step(seq=(-1, 0)) == E
+    assert step(seq=(1016, 0)) == swan.SWAN_ERR_CAPACITY  # 1017 - 16 sparse tokens > 1000
+    assert step(P_qk=None) == E
+    assert step(q=None) == E                        # decode part
+    assert step(scale=float("inf")) == E
+    assert step(ws=None) == swan.SWAN_ERR_WORKSPACE
+    assert step(wsb=need - 1) == swan.SWAN_ERR_WORKSPACE
+    assert step(ws=FAKE + 16) == E                  # misaligned workspace
+    assert step(k_value=swan._i32_array([48, 0])) == E
+    assert swan.last_error()
 
 
 def test_calibrate_rejects_bad_arguments():
