@@ -11,6 +11,7 @@ swan_inputs), already resident in HBM before the timed region.
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
 import argparse
+import ctypes
 import hashlib
 import json
 import math
@@ -54,6 +55,46 @@ def parse_args():
     ap.add_argument("--probe-copy", type=int, default=0,
                     help="also run a device copy of this many bytes (HBM counter calibration)")
     return ap.parse_args()
+
+
+class TimingEvent:
+    """A HIP event made for timing only (hipEventDisableSystemFence): the library's
+    record of it before and after the attention launches then adds no system-scope
+    release to the step, which torch's events do (a few microseconds per record on
+    a short step).  The same .cuda_event / elapsed_time(end) as torch.cuda.Event."""
+    FLAGS = 0x20000000  # hipEventDisableSystemFence
+    _hip = None
+
+    @classmethod
+    def _runtime(cls):
+        if cls._hip is None:  # the HIP runtime this process (torch, the library) runs on
+            path = next(ln.split()[-1] for ln in open("/proc/self/maps") if "libamdhip64" in ln)
+            hip = ctypes.CDLL(path)
+            hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p),
+                                                    ctypes.c_uint]
+            hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                ctypes.c_void_p]
+            hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            cls._hip = hip
+        return cls._hip
+
+    def __init__(self):
+        self._ev = ctypes.c_void_p()
+        st = self._runtime().hipEventCreateWithFlags(ctypes.byref(self._ev), self.FLAGS)
+        if st != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({st})")
+        self.cuda_event = self._ev.value
+
+    def elapsed_time(self, end) -> float:
+        ms = ctypes.c_float()
+        st = self._runtime().hipEventElapsedTime(ctypes.byref(ms), self._ev, end._ev)
+        if st != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({st})")
+        return ms.value
+
+    def __del__(self):
+        if self._hip is not None and self._ev.value:
+            self._hip.hipEventDestroy(self._ev)
 
 
 def source_digest() -> str:
@@ -497,34 +538,37 @@ def main():
     out = torch.empty((w.batch, w.n_q_heads, 128), dtype=tdt, device=dev)
 
     def step(i, evs=None, breakdown=False):
-        """One decode step on replica i % n_rep; evs[2] / evs[3] bracket the attention
-        launches (recorded by the library on their stream), and with breakdown evs[0],
-        [1], [4] bracket the compress-append and the whole decode call."""
+        """One decode step on replica i % n_rep: one swan_decode_step call (the
+        compress-append of the new token, then decode attention); evs[2] / evs[3]
+        bracket the attention launches (recorded by the library on their stream).
+        With breakdown the step is the two calls it stands for instead, evs[0], [1],
+        [4] bracketing the compress-append and the whole decode call."""
         cache = caches[i % n_rep]
-        if breakdown:
-            evs[0].record()
-        cache.append(step_k[i], step_v[i], Pqk, Pvo)
-        if breakdown:
-            evs[1].record()
         if evs is not None:
             swan.set_profile_events(evs[2], evs[3])
-        swan.decode_attention(cache.desc, cache.seq_len, ks, qs[i], Pqk, Pvo, out, ws,
-                              k_value=kvs)
+        if breakdown:
+            evs[0].record()
+            cache.append(step_k[i], step_v[i], Pqk, Pvo)
+            evs[1].record()
+            swan.decode_attention(cache.desc, cache.seq_len, ks, qs[i], Pqk, Pvo, out, ws,
+                                  k_value=kvs)
+            evs[4].record()
+        else:
+            swan.decode_step(cache.desc, cache.seq_len, ks, step_k[i], step_v[i], qs[i], Pqk,
+                             Pvo, out, ws, k_value=kvs)
+            cache.seq_len = [L + 1 for L in cache.seq_len]
         if evs is not None:
             swan.set_profile_events(None, None)
-        if breakdown:
-            evs[4].record()
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
 
     def events(n):
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(n)]
-        for e in evs:  # torch creates its events on first record; the library re-records these
-            e[2].record()
-            e[3].record()
-        return evs
+        """Per step: [0], [1], [4] recorded here (torch), [2], [3] by the library."""
+        return [[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+                 TimingEvent(), TimingEvent(), torch.cuda.Event(enable_timing=True)]
+                for _ in range(n)]
 
     evs = events(args.steps)
     lens = []
