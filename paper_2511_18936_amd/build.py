@@ -21,11 +21,13 @@ SOURCES = ["swan_api.hip", "decode.hip", "decode_gqa.hip", "decode_asym.hip",
            "decode_gqa_asym.hip", "decode_fused.hip", "compress.hip", "prefill.hip",
            "change_k.hip", "rope.hip", "calibrate.hip"]
 ARCH = "gfx950"
-# per-source flags: the GQA kernels keep their MFMA accumulators in VGPRs (the
-# default puts them in AGPRs and copies them across for the per-page VALU work)
+# per-source flags: the GQA kernels and the prefill rotation keep their MFMA
+# accumulators in VGPRs (the default puts them in AGPRs and copies them across
+# for the VALU work on them: the per-page rescale, the per-element conversion)
 SOURCE_FLAGS = {
     "decode_gqa.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "decode_gqa_asym.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "prefill.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "-shared", f"--offload-arch={ARCH}",
