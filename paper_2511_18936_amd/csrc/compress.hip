@@ -3,21 +3,21 @@
 //
 // Several new tokens per sequence: two launches on the caller's stream, so
 // that every vector leaving the ring is read before a new token overwrites its
-// slot.  One new token (a decode step): one launch, insert_kernel<F, 1>, whose
-// wave evicts the slot's old vector before it writes the new one.
+// slot.  One new token (a decode step): one launch, step_kernel, which evicts
+// the slot's old vector before it writes the new one.
 //   evict_kernel   one wave per ring vector that leaves the buffer: top-k of
 //                  its stored values, packed into its page slot
-//   insert_kernel  one wave per group of TPW new tokens of one (sequence, kv
-//                  head, role) (TPW = 1 for a decode step, which also does
-//                  that step's eviction, else 8): rotation
-//                  x . P accumulated in float64 and rounded once to the storage
-//                  type; tokens still inside the buffer go to their ring slot,
-//                  the others are pruned and packed at once.  In a
-//                  decode step (swan_decode_step) the key wave of (sequence,
-//                  kv head) also rotates the step's queries of that head's
-//                  QG query heads with the same rows of P_QK: q_hat for the
-//                  attention that follows, with the summation order of the
-//                  separate query rotation (qrot_kernel), so the same bits
+//   insert_kernel  one wave per group of kTPW new tokens of one (sequence, kv
+//                  head, role): rotation x . P accumulated in float64 and
+//                  rounded once to the storage type; tokens still inside the
+//                  buffer go to their ring slot, the others are pruned and
+//                  packed at once
+//   step_kernel    a decode step: one workgroup of four waves per (sequence,
+//                  kv head, role), each wave a quarter of P's rows; the same
+//                  rounding, ring write or pruning, and the eviction.  In
+//                  swan_decode_step the key workgroup also rotates the step's
+//                  queries of its kv head (q_hat for the attention that
+//                  follows) with the same rows of P_QK
 //
 // Top-k (Sec. 4.3, ranking the stored values, ties to the lower index): each
 // lane holds dims 2l and 2l+1; the key (|x| bits << 8) | (255 - dim) is unique
@@ -135,17 +135,11 @@ __global__ __launch_bounds__(64) void evict_kernel(CompressLaunch a) {
   select_and_pack<F>(x0, x1, k, page, p % kPage, lane);
 }
 
-// QG > 0 (decode steps): the key wave also rotates QG query rows, q_hat = q .
-// P_QK[h] * qmult in float32.  Each output sums 4 quarters of 32 rows, each
-// quarter in two accumulators (even and odd rows) that are added, and the
-// quarters meet as (q0 + q1) + (q2 + q3): the order of qrot_kernel.
-template <typename F, int TPW, int QG>
+template <typename F, int TPW>
 __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
   using T = typename Fmt<F>::Elem;
   using St = Store<T>;
-  static_assert(QG == 0 || TPW == 1, "query rotation: decode steps only");
   __shared__ __attribute__((aligned(16))) double xs[kD][TPW];
-  __shared__ float qs[QG > 0 ? QG : 1][kD];
   const int lane = threadIdx.x;
   const int ngroups = (a.n_new + TPW - 1) / TPW;
   int w = blockIdx.x;
@@ -170,15 +164,6 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
     xs[2 * lane][t] = v0;
     xs[2 * lane + 1][t] = v1;
   }
-  const bool with_q = QG > 0 && role == 0;  // uniform
-  const int64_t q0 = ((int64_t)b * a.Hq + (int64_t)h * QG) * kD;  // first query row
-  if (with_q) {
-#pragma unroll
-    for (int g = 0; g < QG; ++g) {
-      qs[g][2 * lane] = (float)((const T*)a.q)[q0 + g * kD + 2 * lane];
-      qs[g][2 * lane + 1] = (float)((const T*)a.q)[q0 + g * kD + 2 * lane + 1];
-    }
-  }
   __syncthreads();
   double acc0[TPW], acc1[TPW];
   const float* Prole = role ? a.P_vo : a.P_qk;
@@ -193,52 +178,17 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
 #pragma unroll
     for (int t = 0; t < TPW; ++t) acc0[t] = acc1[t] = 0.0;
     // 32 rows of P in flight per batch: the loads are the latency of this kernel
-    auto rows = [&](auto wq) {
-      constexpr bool kQ = decltype(wq)::value && QG > 0;
-      constexpr int NQ = kQ ? QG : 1;
-      float qa[NQ][2][8];  // [query head][output dim 2 lane + o][2 quarter + row parity]
-#pragma unroll
-      for (int g = 0; g < NQ; ++g)
-#pragma unroll
-        for (int c = 0; c < 8; ++c) qa[g][0][c] = qa[g][1][c] = 0.f;
-#pragma unroll
-      for (int qt = 0; qt < 4; ++qt) {
 #pragma unroll 32
-        for (int u = 0; u < 32; ++u) {
-          const int i = 32 * qt + u;
-          const float2 pr = P[i * (kD / 2)];
-          const double p0 = (double)pr.x, p1 = (double)pr.y;
+    for (int i = 0; i < kD; ++i) {
+      const float2 pr = P[i * (kD / 2)];
+      const double p0 = (double)pr.x, p1 = (double)pr.y;
 #pragma unroll
-          for (int t = 0; t < TPW; ++t) {
-            const double xv = xs[i][t];
-            acc0[t] = fma(xv, p0, acc0[t]);
-            acc1[t] = fma(xv, p1, acc1[t]);
-          }
-          if constexpr (kQ) {
-#pragma unroll
-            for (int g = 0; g < QG; ++g) {
-              const float qv = qs[g][i];
-              qa[g][0][2 * qt + (u & 1)] = fmaf(qv, pr.x, qa[g][0][2 * qt + (u & 1)]);
-              qa[g][1][2 * qt + (u & 1)] = fmaf(qv, pr.y, qa[g][1][2 * qt + (u & 1)]);
-            }
-          }
-        }
+      for (int t = 0; t < TPW; ++t) {
+        const double xv = xs[i][t];
+        acc0[t] = fma(xv, p0, acc0[t]);
+        acc1[t] = fma(xv, p1, acc1[t]);
       }
-      if constexpr (kQ) {
-#pragma unroll
-        for (int g = 0; g < QG; ++g)
-#pragma unroll
-          for (int o = 0; o < 2; ++o) {
-            const float s0 = qa[g][o][0] + qa[g][o][1], s1 = qa[g][o][2] + qa[g][o][3];
-            const float s2 = qa[g][o][4] + qa[g][o][5], s3 = qa[g][o][6] + qa[g][o][7];
-            a.qhat[q0 + g * kD + 2 * lane + o] = ((s0 + s1) + (s2 + s3)) * a.qmult;
-          }
-      }
-    };
-    if (with_q)
-      rows(std::true_type{});
-    else
-      rows(std::false_type{});
+    }
   }
   const int len_old = a.tab.len[b];
   const int len_new = len_old + nnew;
@@ -248,18 +198,6 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
                 (int64_t)h * a.n_pages_cap * pbytes;
   typename St::Bits* ring = (typename St::Bits*)(role ? a.v_ring : a.k_ring) +
                             ((int64_t)b * a.Hkv + h) * a.bb * kD;
-  if constexpr (TPW == 1) {
-    // one new token: the vector that leaves the buffer (if any) sits in the
-    // ring slot the new token takes; prune and pack it first (each lane reads
-    // the two elements it overwrites below)
-    const int p0 = evict_begin(len_old, a.bb);
-    if (p0 < evict_end(len_old, nnew, a.bb)) {
-      const typename St::Bits* old = ring + (int64_t)(p0 % a.bb) * kD;
-      const typename St::Bits o0 = old[2 * lane];
-      const typename St::Bits o1 = old[2 * lane + 1];
-      select_and_pack<F>(o0, o1, k, pages + (int64_t)(p0 / kPage) * pbytes, p0 % kPage, lane);
-    }
-  }
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
     if (t >= nt) break;
@@ -276,25 +214,140 @@ __global__ __launch_bounds__(64) void insert_kernel(CompressLaunch a) {
   }
 }
 
+// A decode step's append, one new token per sequence: one workgroup of four
+// waves per (sequence, kv head, role).  Wave s rotates with rows 32 s .. 32 s
+// + 31 of P, its 32 row loads issued together, so the rotation costs one
+// memory latency rather than a wave's walk over all 128 rows; the four
+// float64 partials meet in LDS as (s0 + s1) + (s2 + s3), and wave 0 rounds the
+// sum once and writes the ring slot (or, with no buffer, prunes and packs the
+// token), after it has pruned and packed the vector that leaves the buffer
+// from that same slot.  QG > 0 (swan_decode_step): the key workgroup also
+// rotates the QG query rows of its kv head, q_hat = q . P_QK[h] * qmult in
+// float32, quarter s in wave s with even and odd rows in two accumulators
+// that are added, the quarters meeting as (q0 + q1) + (q2 + q3): the order of
+// qrot_kernel, so q_hat has the same bits as from that kernel.
+template <typename F, int QG>
+__global__ __launch_bounds__(256) void step_kernel(CompressLaunch a) {
+  using T = typename Fmt<F>::Elem;
+  using St = Store<T>;
+  constexpr int NQ = QG > 0 ? QG : 1;
+  __shared__ double xs[kD];
+  __shared__ double part[4][kD];
+  __shared__ float qs[NQ][kD];
+  __shared__ float qpart[NQ][4][kD];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int w = blockIdx.x;
+  const int role = w & 1;
+  w >>= 1;
+  const int h = w % a.Hkv;
+  const int b = w / a.Hkv;
+  if (a.tab.nnew[b] == 0) return;  // uniform over the workgroup
+  const bool with_q = QG > 0 && role == 0;
+  const T* x = (const T*)(role ? a.v_new : a.k_new) + ((int64_t)b * a.Hkv + h) * a.n_new * kD;
+  const int64_t q0 = ((int64_t)b * a.Hq + (int64_t)h * NQ) * kD;  // first query row
+  if (tid < kD) xs[tid] = (double)(float)x[tid];
+  if (with_q)
+    for (int i = tid; i < NQ * kD; i += 256) qs[i / kD][i % kD] = (float)((const T*)a.q)[q0 + i];
+  const int len_old = a.tab.len[b];
+  const int k = a.tab.kact[role][b];
+  const int64_t pbytes = page_bytes_of(Fmt<F>::kValBytes, k);
+  char* pages = (char*)(role ? a.v_pages : a.k_pages) + a.tab.page_off[role][b] +
+                (int64_t)h * a.n_pages_cap * pbytes;
+  typename St::Bits* ring = (typename St::Bits*)(role ? a.v_ring : a.k_ring) +
+                            ((int64_t)b * a.Hkv + h) * a.bb * kD;
+  const float* Prole = role ? a.P_vo : a.P_qk;
+  float2 pr[32];
+  if (Prole) {  // this wave's quarter of P: 32 rows in flight
+    const float2* P = (const float2*)(Prole + (int64_t)h * kD * kD + (int64_t)(32 * wave) * kD) +
+                      lane;
+#pragma unroll
+    for (int u = 0; u < 32; ++u) pr[u] = P[u * (kD / 2)];
+  }
+  // the vector that leaves the buffer (if any) sits in the ring slot the new
+  // token takes: wave 0 prunes and packs it first (each lane reads the two
+  // elements it overwrites below)
+  const int p0 = evict_begin(len_old, a.bb);
+  if (wave == 0 && p0 < evict_end(len_old, 1, a.bb)) {
+    const typename St::Bits* old = ring + (int64_t)(p0 % a.bb) * kD;
+    const typename St::Bits o0 = old[2 * lane];
+    const typename St::Bits o1 = old[2 * lane + 1];
+    select_and_pack<F>(o0, o1, k, pages + (int64_t)(p0 / kPage) * pbytes, p0 % kPage, lane);
+  }
+  __syncthreads();  // xs and qs
+  if (Prole) {
+    double acc0 = 0.0, acc1 = 0.0;
+#pragma unroll
+    for (int u = 0; u < 32; ++u) {
+      const double xv = xs[32 * wave + u];
+      acc0 = fma(xv, (double)pr[u].x, acc0);
+      acc1 = fma(xv, (double)pr[u].y, acc1);
+    }
+    part[wave][2 * lane] = acc0;
+    part[wave][2 * lane + 1] = acc1;
+    if (with_q) {
+#pragma unroll
+      for (int g = 0; g < NQ; ++g) {
+        float e0 = 0.f, o0 = 0.f, e1 = 0.f, o1 = 0.f;  // [even / odd rows][output 2 lane + 0 / 1]
+#pragma unroll
+        for (int u = 0; u < 32; u += 2) {
+          e0 = fmaf(qs[g][32 * wave + u], pr[u].x, e0);
+          o0 = fmaf(qs[g][32 * wave + u + 1], pr[u + 1].x, o0);
+          e1 = fmaf(qs[g][32 * wave + u], pr[u].y, e1);
+          o1 = fmaf(qs[g][32 * wave + u + 1], pr[u + 1].y, o1);
+        }
+        qpart[g][wave][2 * lane] = e0 + o0;
+        qpart[g][wave][2 * lane + 1] = e1 + o1;
+      }
+    }
+  }
+  __syncthreads();  // the partials
+  if (wave == 0) {
+    double y0 = xs[2 * lane], y1 = xs[2 * lane + 1];  // values already rotated (P_VO absorbed)
+    if (Prole) {
+      y0 = (part[0][2 * lane] + part[1][2 * lane]) + (part[2][2 * lane] + part[3][2 * lane]);
+      y1 = (part[0][2 * lane + 1] + part[1][2 * lane + 1]) +
+           (part[2][2 * lane + 1] + part[3][2 * lane + 1]);
+    }
+    const typename St::Bits v0 = St::from_f64(y0);
+    const typename St::Bits v1 = St::from_f64(y1);
+    const int pos = len_old;
+    if (a.bb > 0) {  // stays dense: ring slot pos % b
+      typename St::Bits* r = ring + (int64_t)(pos % a.bb) * kD;
+      r[2 * lane] = v0;
+      r[2 * lane + 1] = v1;
+    } else {  // no buffer: pruned on arrival
+      select_and_pack<F>(v0, v1, k, pages + (int64_t)(pos / kPage) * pbytes, pos % kPage, lane);
+    }
+  } else if (wave == 1 && with_q) {
+    for (int i = lane; i < NQ * kD; i += 64) {
+      const int g = i / kD, j = i % kD;
+      a.qhat[q0 + i] =
+          ((qpart[g][0][j] + qpart[g][1][j]) + (qpart[g][2][j] + qpart[g][3][j])) * a.qmult;
+    }
+  }
+}
+
 template <typename F>
 static hipError_t launch_compress_t(const CompressLaunch& a) {
   const int units = a.B * a.Hkv * 2;
   if (a.n_new == 1) {  // a decode step: eviction and insertion in one launch
+    const dim3 grid(units), block(256);
     switch (a.q ? a.Hq / a.Hkv : 0) {
       case 0:
-        hipLaunchKernelGGL((insert_kernel<F, 1, 0>), dim3(units), dim3(64), 0, a.stream, a);
+        hipLaunchKernelGGL((step_kernel<F, 0>), grid, block, 0, a.stream, a);
         break;
       case 1:
-        hipLaunchKernelGGL((insert_kernel<F, 1, 1>), dim3(units), dim3(64), 0, a.stream, a);
+        hipLaunchKernelGGL((step_kernel<F, 1>), grid, block, 0, a.stream, a);
         break;
       case 2:
-        hipLaunchKernelGGL((insert_kernel<F, 1, 2>), dim3(units), dim3(64), 0, a.stream, a);
+        hipLaunchKernelGGL((step_kernel<F, 2>), grid, block, 0, a.stream, a);
         break;
       case 3:
-        hipLaunchKernelGGL((insert_kernel<F, 1, 3>), dim3(units), dim3(64), 0, a.stream, a);
+        hipLaunchKernelGGL((step_kernel<F, 3>), grid, block, 0, a.stream, a);
         break;
       case 4:
-        hipLaunchKernelGGL((insert_kernel<F, 1, 4>), dim3(units), dim3(64), 0, a.stream, a);
+        hipLaunchKernelGGL((step_kernel<F, 4>), grid, block, 0, a.stream, a);
         break;
       default:
         return hipErrorInvalidValue;  // the caller rotates more query heads per kv head itself
@@ -309,7 +362,7 @@ static hipError_t launch_compress_t(const CompressLaunch& a) {
   if (a.n_new >= kPrefillMinTokens && sizeof(typename Fmt<F>::Elem) == 2) return launch_prefill(a);
   if (a.n_new > 0) {
     const int ngroups = (a.n_new + kTPW - 1) / kTPW;
-    hipLaunchKernelGGL((insert_kernel<F, kTPW, 0>), dim3((int64_t)units * ngroups), dim3(64), 0,
+    hipLaunchKernelGGL((insert_kernel<F, kTPW>), dim3((int64_t)units * ngroups), dim3(64), 0,
                        a.stream, a);
     return hipGetLastError();
   }
