@@ -3,8 +3,10 @@
  * runtime's C API for device memory): the boundary as a C caller sees it.
  *
  *   swan_c_example sizes   host only: size queries and argument checks
- *   swan_c_example run     GPU: compress + decode through the C ABI, checked
- *                          against a reference computed here in double
+ *   swan_c_example run     GPU: compress of the context, then one decode step
+ *                          (swan_decode_step: the last token's append and the
+ *                          attention) through the C ABI, checked against a
+ *                          reference computed here in double
  *
  * The reference restates Algorithm 1 for this case: fp32 storage, rotations that
  * are signed permutations (so the rotated vectors are exact in fp32), tokens older
@@ -157,19 +159,27 @@ static int gpu_run(void) {
   const int32_t kact[B] = {K, K};
   size_t kb, vb, rb;
   if (swan_cache_bytes(&c, kact, NULL, &kb, &vb, &rb) != SWAN_OK) return 1;
-  void *kp, *vp, *kr, *vr, *kn, *vn, *q, *out, *Pd, *ws;
+  void *kp, *vp, *kr, *vr, *kn, *vn, *kl, *vl, *q, *out, *Pd, *ws;
   HIP(hipMalloc(&kp, kb));
   HIP(hipMalloc(&vp, vb));
   HIP(hipMalloc(&kr, rb));
   HIP(hipMalloc(&vr, rb));
   HIP(hipMalloc(&kn, sizeof(float) * nkv));
   HIP(hipMalloc(&vn, sizeof(float) * nkv));
+  HIP(hipMalloc(&kl, sizeof(float) * B * HKV * D));
+  HIP(hipMalloc(&vl, sizeof(float) * B * HKV * D));
   HIP(hipMalloc(&q, sizeof(float) * B * HQ * D));
   HIP(hipMalloc(&out, sizeof(float) * B * HQ * D));
   HIP(hipMalloc(&Pd, sizeof(float) * 2 * HKV * D * D));
   HIP(hipMemcpy(kn, kh, sizeof(float) * nkv, hipMemcpyHostToDevice));
   HIP(hipMemcpy(vn, vh, sizeof(float) * nkv, hipMemcpyHostToDevice));
   HIP(hipMemcpy(q, qh, sizeof(float) * B * HQ * D, hipMemcpyHostToDevice));
+  /* the last token of every (sequence, kv head): the decode step's new key and value */
+  for (int bh = 0; bh < B * HKV; ++bh) {
+    const size_t src = ((size_t)bh * L + (L - 1)) * D;
+    HIP(hipMemcpy((float*)kl + (size_t)bh * D, kh + src, sizeof(float) * D, hipMemcpyHostToDevice));
+    HIP(hipMemcpy((float*)vl + (size_t)bh * D, vh + src, sizeof(float) * D, hipMemcpyHostToDevice));
+  }
   HIP(hipMemcpy(Pd, P, sizeof(float) * 2 * HKV * D * D, hipMemcpyHostToDevice));
   c.k_pages = kp;
   c.v_pages = vp;
@@ -177,14 +187,16 @@ static int gpu_run(void) {
   c.v_ring = vr;
   const float* Pqk = (const float*)Pd;
   const float* Pvo = (const float*)Pd + (size_t)HKV * D * D;
-  const int32_t zero[B] = {0, 0}, lens[B] = {L, L};
-  swan_status st = swan_compress_append(&c, zero, kact, NULL, kn, vn, L, NULL, Pqk, Pvo, NULL);
+  /* the context: the first L - 1 rows of each sequence's L; then the decode step appends the
+     last token and attends in one call */
+  const int32_t zero[B] = {0, 0}, first[B] = {L - 1, L - 1}, lens[B] = {L, L};
+  swan_status st = swan_compress_append(&c, zero, kact, NULL, kn, vn, L, first, Pqk, Pvo, NULL);
   CHECK(st == SWAN_OK, "compress: %s", swan_last_error());
   size_t wsb = 0;
   CHECK(swan_decode_workspace_bytes(&c, lens, kact, NULL, &wsb) == SWAN_OK, "ws bytes");
   HIP(hipMalloc(&ws, wsb));
-  st = swan_decode_attention(&c, lens, kact, NULL, q, Pqk, Pvo, 0.f, out, ws, wsb, NULL);
-  CHECK(st == SWAN_OK, "decode: %s", swan_last_error());
+  st = swan_decode_step(&c, first, kact, NULL, kl, vl, q, Pqk, Pvo, 0.f, out, ws, wsb, NULL);
+  CHECK(st == SWAN_OK, "decode step: %s", swan_last_error());
   HIP(hipDeviceSynchronize());
   float* got = malloc(sizeof(float) * B * HQ * D);
   HIP(hipMemcpy(got, out, sizeof(float) * B * HQ * D, hipMemcpyDeviceToHost));
@@ -237,6 +249,8 @@ static int gpu_run(void) {
   HIP(hipFree(vr));
   HIP(hipFree(kn));
   HIP(hipFree(vn));
+  HIP(hipFree(kl));
+  HIP(hipFree(vl));
   HIP(hipFree(q));
   HIP(hipFree(out));
   HIP(hipFree(Pd));
