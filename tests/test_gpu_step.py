@@ -3,6 +3,7 @@ rotation runs inside the append launch), against the two calls it stands for
 (compress-append of one token, then decode attention): outputs, pages and ring
 bit for bit at every step, then the cache and the last output against the
 oracle."""
+import os
 import sys
 
 import numpy as np
@@ -48,12 +49,9 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("Hq,Hkv,dtype,values,b,L0,ks,kv", CASES)
-def test_decode_step_equals_append_then_decode(gpu_device, swan_mod, torch_mod, Hq, Hkv, dtype,
-                                               values, b, L0, ks, kv):
-    _log(f"decode_step Hq={Hq} Hkv={Hkv} {dtype}/{values} b={b} L0={L0} k={ks} kv={kv}")
+def _steps_against_two_calls(gpu_device, swan_mod, torch_mod, Hq, Hkv, dtype, values, b, L0, ks,
+                             kv, steps=3):
     torch = torch_mod
-    steps = 3
     B, L = len(ks), L0 + steps
     np_dt = si.np_dtype(dtype)
     # the rows, rotations and oracle caches at the final length
@@ -85,6 +83,14 @@ def test_decode_step_equals_append_then_decode(gpu_device, swan_mod, torch_mod, 
     err = C.max_rel_err(out_one.cpu().numpy().astype(np.float64), ref)
     _log(f"  last step vs oracle: max rel err {err:.3e}")
     assert err <= TOL
+
+
+@pytest.mark.parametrize("Hq,Hkv,dtype,values,b,L0,ks,kv", CASES)
+def test_decode_step_equals_append_then_decode(gpu_device, swan_mod, torch_mod, Hq, Hkv, dtype,
+                                               values, b, L0, ks, kv):
+    _log(f"decode_step Hq={Hq} Hkv={Hkv} {dtype}/{values} b={b} L0={L0} k={ks} kv={kv}")
+    _steps_against_two_calls(gpu_device, swan_mod, torch_mod, Hq, Hkv, dtype, values, b, L0, ks,
+                             kv)
 
 
 def test_decode_step_error_leaves_the_cache(gpu_device, swan_mod, torch_mod):
@@ -152,3 +158,30 @@ def test_profile_events_time_the_attention(gpu_device, swan_mod, torch_mod, Hq, 
     err = C.max_rel_err(out.cpu().numpy().astype(np.float64),
                         O.decode_batch(q.cpu().numpy().astype(np.float64), Pqk, Pvo, oc))
     assert err <= TOL
+
+
+N_RANDOM = int(os.environ.get("SWAN_RANDOM_STEPS", "24"))  # a wider sweep on request
+
+
+def _random_case(i):
+    r = si.rng_for(42421, i)
+    Hkv = int(r.choice([1, 2, 3]))
+    G = int(r.choice([1, 2, 3, 4, 5, 8]))
+    dtype = "f32" if r.random() < 0.2 else "f16"
+    values = "e4m3" if (dtype == "f16" and r.random() < 0.4) else "same"
+    B = int(r.integers(1, 5))
+    b = int(r.choice([0, 1, 2, 7, 16, 64]))
+    L0 = int(r.integers(0, 400))
+    ks = [int(x) for x in r.integers(1, 129, B)]
+    kv = [int(x) for x in r.integers(1, 129, B)] if r.random() < 0.3 else None
+    return dict(Hq=Hkv * G, Hkv=Hkv, dtype=dtype, values=values, b=b, L0=L0, ks=ks, kv=kv)
+
+
+@pytest.mark.parametrize("i", range(N_RANDOM))
+def test_random_decode_steps(gpu_device, swan_mod, torch_mod, i):
+    """Seeded random shapes: swan_decode_step against append + decode bit for bit over
+    four steps (lengths crossing the buffer size on the way), then the oracle."""
+    c = _random_case(i)
+    _log(f"random decode steps {i}: {c}")
+    _steps_against_two_calls(gpu_device, swan_mod, torch_mod, c["Hq"], c["Hkv"], c["dtype"],
+                             c["values"], c["b"], c["L0"], c["ks"], c["kv"], steps=4)
