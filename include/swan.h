@@ -250,7 +250,7 @@ swan_status swan_decode_attention_noalloc(const swan_cache* c, const int32_t* se
  * sequence, then its attention part): the same as swan_compress_append with
  * n_new = 1 (n_new_host NULL) followed by swan_decode_attention with lengths
  * seq_len_host[b] + 1, on `stream`, with the same results bit for bit, in one
- * launch fewer: for n_q_heads / n_kv_heads <= 4 the query rotation runs inside
+ * launch fewer: for n_q_heads / n_kv_heads <= 8 the query rotation runs inside
  * the append launch, where the workgroup that rotates a kv head's new key reads
  * the same rows of P_qk (one launch less on a latency-bound step).
  *  seq_len_host[batch]  tokens cached per sequence BEFORE the step (>= 0);

@@ -349,6 +349,18 @@ static hipError_t launch_compress_t(const CompressLaunch& a) {
       case 4:
         hipLaunchKernelGGL((step_kernel<F, 4>), grid, block, 0, a.stream, a);
         break;
+      case 5:
+        hipLaunchKernelGGL((step_kernel<F, 5>), grid, block, 0, a.stream, a);
+        break;
+      case 6:
+        hipLaunchKernelGGL((step_kernel<F, 6>), grid, block, 0, a.stream, a);
+        break;
+      case 7:
+        hipLaunchKernelGGL((step_kernel<F, 7>), grid, block, 0, a.stream, a);
+        break;
+      case 8:
+        hipLaunchKernelGGL((step_kernel<F, 8>), grid, block, 0, a.stream, a);
+        break;
       default:
         return hipErrorInvalidValue;  // the caller rotates more query heads per kv head itself
     }

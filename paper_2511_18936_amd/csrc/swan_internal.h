@@ -130,7 +130,7 @@ struct CompressLaunch {
   int Hq = 0;
   float qmult = 0.f;
 };
-constexpr int kStepQG = 4;
+constexpr int kStepQG = 8;
 hipError_t launch_compress(const CompressLaunch& a);
 // prefill path (fp16, many tokens): float64 MFMA rotation + lane-per-token top-k
 constexpr int kPrefillMinTokens = 64;

@@ -38,7 +38,8 @@ CASES = [
     (8, 2, "f16", "same", 16, 200, [32, 32], None),      # GQA, G = 4
     (6, 2, "f16", "same", 16, 150, [64, 40], None),      # G = 3
     (4, 2, "f16", "same", 16, 150, [1, 128], None),      # G = 2, extreme k
-    (16, 2, "f16", "same", 16, 150, [48, 48], None),     # G = 8: the separate query rotation
+    (16, 2, "f16", "same", 16, 150, [48, 48], None),     # G = 8
+    (32, 2, "f16", "same", 16, 150, [48, 40], None),     # G = 16: the separate query rotation
     (4, 4, "f32", "same", 8, 130, [48, 17], None),
     (8, 2, "f16", "e4m3", 16, 200, [64, 64], None),
     (4, 4, "f16", "e4m3", 16, 200, [48, 24], None),
